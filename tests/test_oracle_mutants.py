@@ -1,0 +1,50 @@
+"""Plant plausible mistakes in a copy of the C oracle and check that the pin
+suite (test_oracle_pins.py) rejects every one of them.
+
+Each mutant is compiled from a text edit of kvx_oracle.c into a temporary
+library and the pins run against it in a child process (a mutant that reads or
+writes out of bounds may crash the child; that also counts as caught).
+"""
+import os
+import subprocess
+import sys
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+SRC = os.path.join(ROOT, "oracle", "kvx_oracle.c")
+
+GATHER_KV = "const uint8_t* base = (const uint8_t*)(kv == 0 ? k[l] : v[l]);"
+SCATTER_KV = "uint8_t* base = (uint8_t*)(kv == 0 ? k[l] : v[l]);"
+
+MUTANTS = {
+    "gather_swaps_k_and_v": (GATHER_KV, GATHER_KV.replace("k[l] : v[l]", "v[l] : k[l]")),
+    "scatter_swaps_k_and_v": (SCATTER_KV, SCATTER_KV.replace("k[l] : v[l]", "v[l] : k[l]")),
+    "layer_index_not_rebased": ("out + c * S + ((l - l0) * 2 + kv)", "out + c * S + (l * 2 + kv)"),
+    "kv_major_instead_of_layer_major": ("out + c * S + ((l - l0) * 2 + kv) * Tc",
+                                        "out + c * S + (kv * (l1 - l0) + (l - l0)) * Tc"),
+    "block_index_ignores_chunk_stride": ("const int64_t id = bt[c * bpc + j];\n          memcpy(out",
+                                         "const int64_t id = bt[c + j];\n          memcpy(out"),
+    "chunk_stride_counts_all_layers": ("const int64_t S = (l1 - l0) * 2 * chunk_tokens * row;",
+                                       "const int64_t S = l1 * 2 * chunk_tokens * row;"),
+    "last_chunk_strided_as_full": ("((l - l0) * 2 + kv) * Tc * row + j * slab, base",
+                                   "((l - l0) * 2 + kv) * chunk_tokens * row + j * slab, base"),
+    "scatter_block_off_by_one": ("memcpy(base + id * slab, in", "memcpy(base + (id ^ 1) * slab, in"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_pins_reject_mutant(name, tmp_path):
+    old, new = MUTANTS[name]
+    text = open(SRC).read()
+    assert text.count(old) >= 1, f"mutation anchor for {name} not found"
+    mutated = text.replace(old, new, 1)
+    c = tmp_path / "mutant.c"
+    c.write_text(mutated)
+    lib = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O1", "-fPIC", "-shared", "-o", str(lib), str(c)], check=True)
+    env = dict(os.environ, KVX_ORACLE_LIB=str(lib), KVX_NO_AUTOBUILD="1")
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
+                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+                       env=env, cwd=ROOT, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
