@@ -1,0 +1,226 @@
+/*
+ * kvx.h -- C ABI of libkvx.so: moving prefix KV state between a paged GPU KV
+ * cache and contiguous transfer chunks on one MI355X (gfx950).
+ *
+ * What the operations are (from the paper's statement of the problem):
+ *   - The serving engine keeps KV in fixed-size token blocks; the blocks of
+ *     one prompt are not adjacent in memory (Sec. 2.1, "KV Cache in LLM
+ *     Serving"). Size model: bytes per token = layers x 2 x KV heads x head
+ *     dim x dtype size (Sec. 2.1).
+ *   - The external cache transfers "storage blocks" that each group several
+ *     GPU blocks (Sec. 6.4); a batched block copy moves data between the GPU
+ *     KV tensors and contiguous staging slots (Secs. 6.2, 6.4). Here that copy
+ *     is a gather (paged -> packed chunks, for offload) and a scatter (packed
+ *     chunks -> paged, for load).
+ *   - Staging is one contiguous, aligned, pinned host allocation cut into
+ *     fixed slots; a transfer larger than the pool goes through it piece by
+ *     piece, and a slot is reused only after the GPU copy that read it has
+ *     completed, as reported by a device event (Sec. 6.4). That is
+ *     kvx_restore_from_staging.
+ *
+ * Layouts (the paper gives none; these are this library's definitions):
+ *   Cache   per layer l, separate K and V device tensors, each contiguous
+ *           [num_blocks][block_size][num_kv_heads][head_dim] of elem_bytes-byte
+ *           words. A slab is one (layer, K|V, block):
+ *           slab = block_size * num_kv_heads * head_dim * elem_bytes bytes.
+ *   Chunk   chunk_tokens must be a positive multiple of block_size; a chunk
+ *           holds bpc = chunk_tokens / block_size consecutive entries of the
+ *           block table. Inside a chunk the order is [layer l0..l1-1][K, V]
+ *           [token][head][dim]: for each (layer, K|V) the chunk's slabs are
+ *           adjacent, in block-table order.
+ *   Image   the packed image of n blocks over layers [l0, l1) is the chunks
+ *           back to back. The last chunk may hold fewer than bpc blocks and
+ *           is compact, so the image is exactly
+ *           n * (l1 - l0) * 2 * slab bytes with no padding.
+ *
+ * Asynchrony: gather and scatter validate, enqueue on the caller's stream and
+ * return; results are defined once that stream has completed. Block ids live
+ * in device memory and are checked by the kernels: a unit whose id is outside
+ * [0, num_blocks) is skipped (nothing is written for it) and a sticky
+ * per-device flag is set, which kvx_check() reports as KVX_EBADBLOCK.
+ * Scatter destinations must be distinct; duplicates make the result depend
+ * on execution order (not checked).
+ *
+ * Ownership: the caller owns every cache tensor, block table, packed buffer,
+ * landing buffer, host source and stream passed in. The library never frees
+ * caller memory and keeps no pointer to kvx_cache's arrays after a call
+ * returns (kvx_ring_bind copies what it needs). A ring owns its pinned slot
+ * allocation, its side stream, its events and its fill threads.
+ *
+ * Threading: gather, scatter and kvx_check may be called from any thread. A
+ * ring is used by one thread at a time.
+ *
+ * No C++ exception crosses this interface.
+ */
+#ifndef KVX_H_
+#define KVX_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum kvx_status {
+  KVX_OK = 0,
+  KVX_EINVAL = -1,     /* bad argument (detected on the host, nothing enqueued) */
+  KVX_ENOMEM = -2,     /* a host or device allocation failed */
+  KVX_EHIP = -3,       /* a HIP runtime call failed */
+  KVX_EBADBLOCK = -4,  /* a kernel met a block id outside [0, num_blocks) */
+  KVX_ECLOSED = -5,    /* the ring was aborted while a restore was running */
+  KVX_EINTERNAL = -6   /* invariant violated inside the library */
+} kvx_status;
+
+/* Largest layer range a single call may cover. */
+#define KVX_MAX_LAYERS 128
+
+/* Description of a paged cache. k and v are host arrays of num_layers device
+ * pointers (16-byte aligned); they are read during the call only. */
+typedef struct kvx_cache {
+  void* const* k;
+  void* const* v;
+  int32_t num_layers;
+  int32_t num_blocks;
+  int32_t block_size;    /* tokens per GPU block */
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t elem_bytes;    /* 1, 2, 4 or 8; the path copies raw words */
+} kvx_cache;
+
+/* Size model of Sec. 2.1: layers * 2 * kv_heads * head_dim * elem_bytes.
+ * Returns -1 if any argument is not positive. */
+int64_t kvx_bytes_per_token(int32_t layers, int32_t kv_heads, int32_t head_dim,
+                            int32_t elem_bytes);
+
+/* Bytes of the packed image of n_blocks blocks over layers [l0, l1):
+ * n_blocks * (l1 - l0) * 2 * slab. Returns -1 on an invalid shape or range. */
+int64_t kvx_packed_bytes(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t n_blocks);
+
+/* Gather (offload side): for every chunk c, layer l in [l0, l1), K|V and block
+ * j of the chunk, copy slab cache[l][K|V][block_table[c*bpc + j]] to its place
+ * in the packed image at dst (layout above).
+ *   block_table  device int32[n_blocks]; ids may repeat (read-only side)
+ *   dst          device, 16-byte aligned, kvx_packed_bytes(...) bytes; must
+ *                not overlap any cache tensor
+ *   stream       HIP stream to enqueue on (0 = the null stream)
+ * n_blocks == 0 or l0 == l1 is a no-op returning KVX_OK.
+ * Errors: KVX_EINVAL for a null or misaligned pointer, l0 < 0, l1 < l0,
+ * l1 > num_layers, l1 - l0 > KVX_MAX_LAYERS, chunk_tokens not a positive
+ * multiple of block_size, slab not a multiple of 16 bytes, or dst overlapping
+ * the cache; KVX_EHIP if the launch fails. Bad block ids: see kvx_check. */
+kvx_status kvx_gather_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
+                             const int32_t* block_table, int32_t n_blocks, int32_t chunk_tokens,
+                             void* dst, hipStream_t stream);
+
+/* Scatter (load side): the inverse of kvx_gather_blocks. Every slab the image
+ * names is written; no other cache byte changes. block_table holds distinct
+ * destination ids. Arguments and errors as for kvx_gather_blocks, with src
+ * (device, 16-byte aligned, kvx_packed_bytes(...) bytes) read instead of dst
+ * written. */
+kvx_status kvx_scatter_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
+                              const int32_t* block_table, int32_t n_blocks, int32_t chunk_tokens,
+                              const void* src, hipStream_t stream);
+
+/* Wait for `stream`, then read and clear the calling device's sticky error
+ * flag: KVX_EBADBLOCK if any kernel since the last check met a bad block id,
+ * KVX_EHIP if the stream reported an error, else KVX_OK. */
+kvx_status kvx_check(hipStream_t stream);
+
+const char* kvx_strerror(kvx_status status);
+
+/* ---- staging ring (Sec. 6.4) ---------------------------------------------- */
+
+/* One piece of a staged transfer: the image bytes [src_offset, src_offset +
+ * bytes) hold the packed image of blocks block_table[bt_first ..
+ * bt_first + n_blocks) over layers [l_begin, l_end) with chunk size
+ * chunk_tokens (a piece is either a run of whole chunks or a layer range of
+ * one chunk). */
+typedef struct kvx_piece {
+  int64_t src_offset;
+  int64_t bytes;
+  int32_t bt_first;
+  int32_t n_blocks;
+  int32_t l_begin;
+  int32_t l_end;
+  int32_t chunk_tokens;
+  int32_t reserved;
+} kvx_piece;
+
+/* Split the packed image of (cache shape, [l0, l1), n_blocks, chunk_tokens)
+ * into pieces of at most slot_bytes: as many whole chunks per piece as fit;
+ * a chunk larger than a slot is split into contiguous layer ranges, as many
+ * layers per piece as fit. Pure host computation (no HIP call). Writes at
+ * most max_pieces entries to out (out may be NULL to count) and the total
+ * count to *n_pieces. KVX_EINVAL if a single layer of a chunk exceeds
+ * slot_bytes or the arguments are invalid (cache pointers are not read). */
+kvx_status kvx_plan_pieces(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t n_blocks,
+                           int32_t chunk_tokens, int64_t slot_bytes, kvx_piece* out,
+                           int32_t max_pieces, int32_t* n_pieces);
+
+typedef struct kvx_ring kvx_ring;
+
+/* Create a ring on `device` with n_slots (>= 1) slots of slot_bytes (a
+ * positive multiple of 4096): one hipHostMalloc allocation of
+ * n_slots * slot_bytes pinned bytes, one non-blocking side stream at default
+ * priority, and per-slot events. device_landing is the device buffer that
+ * H2D copies land in (n_slots * slot_bytes bytes, 16-byte aligned, owned by
+ * the caller); NULL makes the ring allocate its own. */
+kvx_status kvx_ring_create(int device, int32_t n_slots, int64_t slot_bytes, void* device_landing,
+                           kvx_ring** out);
+
+/* Bind the next restores to a transfer: cache (pointers copied), layer
+ * range, prefix length, chunk size, the host image (packed layout,
+ * kvx_packed_bytes(...) bytes; it stands in for the storage tier and is read
+ * only) and the number of host fill threads (1..64) that copy image pieces
+ * into staging slots. fill_threads == 0 skips staging: the H2D copies then
+ * read the image directly, which must be pinned (the preloaded case, where
+ * the data already sits in pinned memory). Plans the pieces (see
+ * kvx_plan_pieces). */
+kvx_status kvx_ring_bind(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int32_t l1,
+                         int32_t n_blocks, int32_t chunk_tokens, const void* host_source,
+                         int32_t fill_threads);
+
+/* Restore the bound image into the blocks named by block_table (device
+ * int32[n_blocks], distinct destination ids). For piece i on slot s = i mod
+ * n_slots: fill threads copy the piece into host slot s once the H2D copy of
+ * piece i - n_slots has completed; the side stream waits until the scatter of
+ * piece i - n_slots has finished reading device slot s, copies host slot s
+ * to device slot s and records an event; `stream` waits on that event and
+ * runs the scatter of the piece. Returns once every piece is enqueued (the
+ * host thread waits for fill threads, never for the device); all scatters
+ * are ordered on `stream`. The cache equals the scatter of the whole image
+ * once `stream` completes. KVX_ECLOSED if kvx_ring_abort was called; pieces
+ * already enqueued still complete. */
+kvx_status kvx_restore_from_staging(kvx_ring* ring, const int32_t* block_table,
+                                    hipStream_t stream);
+
+typedef struct kvx_ring_stats {
+  int64_t pieces;         /* pieces moved by the last restore */
+  int64_t bytes;          /* image bytes moved by the last restore */
+  double fill_ms;         /* summed fill-thread copy time */
+  double wait_fill_ms;    /* time the enqueuing thread waited for fills */
+  double enqueue_ms;      /* wall time of the last kvx_restore_from_staging */
+} kvx_ring_stats;
+
+kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out);
+
+/* Make a running or later restore on this ring return KVX_ECLOSED. Safe to
+ * call from another thread. */
+kvx_status kvx_ring_abort(kvx_ring* ring);
+
+/* Wait for the ring's side stream and last restore, then free everything the
+ * ring owns. */
+kvx_status kvx_ring_destroy(kvx_ring* ring);
+
+/* Pinned host memory of exactly `bytes` (hipHostMalloc), for host images. */
+kvx_status kvx_pinned_alloc(int64_t bytes, void** out);
+kvx_status kvx_pinned_free(void* p);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVX_H_ */

@@ -41,6 +41,10 @@ def _host_lib():
         lib.kvs_word.argtypes = [ctypes.c_uint64, ctypes.c_uint64]
         lib.kvs_normal_table.restype = ctypes.POINTER(ctypes.c_uint16)
         lib.kvs_normal_table.argtypes = []
+        lib.kvs_fill_ranges.restype = ctypes.c_int
+        lib.kvs_fill_ranges.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_uint64,
+                                        ctypes.c_uint64, ctypes.c_uint64, ctypes.c_uint64,
+                                        ctypes.c_int, ctypes.c_int]
         lib.kvs_fill_host.restype = ctypes.c_int
         lib.kvs_fill_host.argtypes = [ctypes.c_void_p, ctypes.c_uint64, ctypes.c_uint64,
                                       ctypes.c_uint64, ctypes.c_uint64, ctypes.c_int, ctypes.c_int]
@@ -101,6 +105,20 @@ def fill_host(buf: np.ndarray, seed: int, stream: int, byte_offset: int = 0,
                                    stream & (2**64 - 1), byte_offset, mode, threads)
     if rc != 0:
         raise ValueError(f"kvs_fill_host rejected nbytes={buf.nbytes} offset={byte_offset}")
+
+
+def fill_ranges(buf: np.ndarray, offsets, length: int, seed: int, stream: int,
+                mode: int = MODE_NORMAL_BF16, threads: int = 8) -> None:
+    """For each offset o: buf[o:o+length] = stream bytes [o, o+length)."""
+    offs = np.ascontiguousarray(np.asarray(offsets, dtype=np.uint64))
+    if offs.size and int(offs.max()) + length > buf.nbytes:
+        raise ValueError("range past the end of the buffer")
+    if not buf.flags["C_CONTIGUOUS"]:
+        raise ValueError("fill_ranges needs a C-contiguous array")
+    rc = _host_lib().kvs_fill_ranges(buf.ctypes.data, offs.ctypes.data, offs.size, length,
+                                     seed & (2**64 - 1), stream & (2**64 - 1), mode, threads)
+    if rc != 0:
+        raise ValueError("kvs_fill_ranges rejected its arguments")
 
 
 def host_bytes(nbytes: int, seed: int, stream: int, byte_offset: int = 0,

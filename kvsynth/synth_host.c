@@ -167,3 +167,46 @@ int kvs_fill_host(void* out, uint64_t nbytes, uint64_t seed, uint64_t stream,
     if (created[t]) pthread_join(th[t], 0);
   return 0;
 }
+
+/* Fill many equal-length ranges of one stream: for i < n,
+ * out_base[offsets[i], offsets[i] + len) = stream bytes [offsets[i], +len).
+ * Offsets and len must be multiples of 8. Ranges are split over threads. */
+typedef struct {
+  uint8_t* base;
+  const uint64_t* offsets;
+  uint64_t n, len, key;
+  int mode, stride, start;
+  const uint16_t* tab;
+} ranges_job;
+
+static void* ranges_thread(void* arg) {
+  ranges_job* j = (ranges_job*)arg;
+  for (uint64_t i = (uint64_t)j->start; i < j->n; i += (uint64_t)j->stride)
+    fill_words(j->base + j->offsets[i], j->key, j->offsets[i] / 8, j->len / 8, j->mode, j->tab);
+  return 0;
+}
+
+int kvs_fill_ranges(void* out_base, const uint64_t* offsets, uint64_t n, uint64_t len,
+                    uint64_t seed, uint64_t stream, int mode, int threads) {
+  if ((len & 7) || (mode != KVS_MODE_NORMAL_BF16 && mode != KVS_MODE_RAW)) return -1;
+  if (n == 0 || len == 0) return 0;
+  if (!out_base || !offsets) return -1;
+  for (uint64_t i = 0; i < n; ++i)
+    if (offsets[i] & 7) return -1;
+  const uint16_t* tab = kvs_normal_table();
+  uint64_t key = kvs_stream_key(seed, stream);
+  if (threads < 1) threads = 1;
+  if (threads > 64) threads = 64;
+  if ((uint64_t)threads > n) threads = (int)n;
+  pthread_t th[64];
+  int created[64];
+  ranges_job jobs[64];
+  for (int t = 0; t < threads; ++t) {
+    jobs[t] = (ranges_job){(uint8_t*)out_base, offsets, n, len, key, mode, threads, t, tab};
+    created[t] = threads > 1 && pthread_create(&th[t], 0, ranges_thread, &jobs[t]) == 0;
+    if (!created[t]) ranges_thread(&jobs[t]);
+  }
+  for (int t = 0; t < threads; ++t)
+    if (created[t]) pthread_join(th[t], 0);
+  return 0;
+}

@@ -1,0 +1,293 @@
+"""Paged-KV gather / scatter / staged restore on MI355X (gfx950).
+
+Thin Python binding over the C ABI of ``libkvx.so`` (include/kvx.h): the
+functions below marshal arguments and call the library; every byte of the
+path is moved by the library's HIP kernels and HIP copies. PyTorch provides
+device memory and streams only. There is no CPU fallback: importing works
+without a GPU, but any call that moves data needs the built library and a GPU.
+
+Operations (sections of the paper they follow):
+  * kvx_gather_blocks  -- pack paged KV blocks into contiguous transfer chunks
+    (offload side of the batched block copy, Secs. 6.2 and 6.4);
+  * kvx_scatter_blocks -- unpack chunks into paged blocks (load side);
+  * kvx_restore_from_staging -- feed scatters through a bounded pinned
+    staging ring with H2D copies on a side stream (Sec. 6.4).
+"""
+from __future__ import annotations
+
+import ctypes
+
+from . import _native
+from ._native import KvxCache, KvxPiece, KvxRingStats
+
+KVX_OK, KVX_EINVAL, KVX_ENOMEM, KVX_EHIP, KVX_EBADBLOCK, KVX_ECLOSED, KVX_EINTERNAL = (
+    0, -1, -2, -3, -4, -5, -6)
+KVX_MAX_LAYERS = 128
+
+
+class KvxError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        msg = _native.lib().kvx_strerror(status).decode()
+        super().__init__(f"{where}: {msg} (status {status})")
+        self.status = status
+
+
+def _ok(status: int, where: str) -> None:
+    if status != KVX_OK:
+        raise KvxError(status, where)
+
+
+def _stream_handle(stream):
+    import torch
+
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+_ELEM = None
+
+
+def _elem_bytes(dtype) -> int:
+    import torch
+
+    return torch.empty((), dtype=dtype).element_size()
+
+
+class PagedKVCache:
+    """A paged KV cache: per layer, K and V device tensors of shape
+    [num_blocks, block_size, num_kv_heads, head_dim] (contiguous)."""
+
+    def __init__(self, k, v):
+        if len(k) != len(v) or not k:
+            raise ValueError("need the same positive number of K and V layers")
+        shape = tuple(k[0].shape)
+        if len(shape) != 4:
+            raise ValueError("cache tensors are [num_blocks, block_size, kv_heads, head_dim]")
+        for t in list(k) + list(v):
+            if tuple(t.shape) != shape or t.dtype != k[0].dtype or not t.is_contiguous():
+                raise ValueError("all cache tensors must share shape and dtype and be contiguous")
+            if t.device != k[0].device:
+                raise ValueError("all cache tensors must be on one device")
+        self.k, self.v = list(k), list(v)
+        self.num_blocks, self.block_size, self.num_kv_heads, self.head_dim = shape
+        self.num_layers = len(k)
+        self.dtype = k[0].dtype
+        self.device = k[0].device
+        self.elem_bytes = k[0].element_size()
+        self._kp = (ctypes.c_void_p * self.num_layers)(*[t.data_ptr() for t in self.k])
+        self._vp = (ctypes.c_void_p * self.num_layers)(*[t.data_ptr() for t in self.v])
+        self._c = KvxCache(self._kp, self._vp, self.num_layers, self.num_blocks, self.block_size,
+                           self.num_kv_heads, self.head_dim, self.elem_bytes)
+
+    @property
+    def slab_bytes(self) -> int:
+        return self.block_size * self.num_kv_heads * self.head_dim * self.elem_bytes
+
+    @classmethod
+    def allocate(cls, num_layers, num_blocks, block_size, num_kv_heads, head_dim, dtype, device):
+        import torch
+
+        mk = lambda: torch.empty((num_blocks, block_size, num_kv_heads, head_dim),  # noqa: E731
+                                 dtype=dtype, device=device)
+        return cls([mk() for _ in range(num_layers)], [mk() for _ in range(num_layers)])
+
+    @classmethod
+    def from_host(cls, k_bytes, v_bytes, num_blocks, block_size, num_kv_heads, head_dim, dtype,
+                  device):
+        """Upload per-layer host byte arrays (numpy uint8) into a new cache."""
+        import torch
+
+        def up(b):
+            t = torch.from_numpy(b).to(device)
+            return t.view(dtype).view(num_blocks, block_size, num_kv_heads, head_dim)
+
+        return cls([up(b) for b in k_bytes], [up(b) for b in v_bytes])
+
+    def c_struct(self) -> KvxCache:
+        return self._c
+
+
+def shape_only_cache(num_layers, num_blocks, block_size, num_kv_heads, head_dim, elem_bytes):
+    """A kvx_cache description with no tensors (for planning on the host)."""
+    return KvxCache(None, None, num_layers, num_blocks, block_size, num_kv_heads, head_dim,
+                    elem_bytes)
+
+
+def _cstruct(cache):
+    return cache.c_struct() if isinstance(cache, PagedKVCache) else cache
+
+
+def kvx_bytes_per_token(layers, kv_heads, head_dim, elem_bytes) -> int:
+    return int(_native.lib().kvx_bytes_per_token(layers, kv_heads, head_dim, elem_bytes))
+
+
+def kvx_packed_bytes(cache, l0, l1, n_blocks) -> int:
+    c = _cstruct(cache)
+    return int(_native.lib().kvx_packed_bytes(ctypes.byref(c), l0, l1, n_blocks))
+
+
+def _table_ptr(cache, block_table, n_blocks):
+    import torch
+
+    if n_blocks == 0:
+        return block_table.data_ptr() if block_table is not None else None
+    if block_table.dtype != torch.int32 or not block_table.is_contiguous():
+        raise ValueError("block_table must be a contiguous int32 tensor")
+    if block_table.device != cache.device:
+        raise ValueError("block_table must be on the cache's device")
+    if block_table.numel() < n_blocks:
+        raise ValueError("block_table shorter than n_blocks")
+    return block_table.data_ptr()
+
+
+def _buffer_ptr(cache, buf, need):
+    if need <= 0:
+        return buf.data_ptr() if buf is not None else None
+    if buf.device != cache.device or not buf.is_contiguous():
+        raise ValueError("packed buffer must be contiguous on the cache's device")
+    if buf.numel() * buf.element_size() < need:
+        raise ValueError(f"packed buffer holds {buf.numel() * buf.element_size()} bytes, "
+                         f"needs {need}")
+    return buf.data_ptr()
+
+
+def kvx_gather_blocks(cache: PagedKVCache, l0, l1, block_table, n_blocks, chunk_tokens, dst,
+                      stream=None) -> None:
+    need = max(kvx_packed_bytes(cache, l0, l1, n_blocks), 0)
+    st = _native.lib().kvx_gather_blocks(
+        ctypes.byref(cache.c_struct()), l0, l1, _table_ptr(cache, block_table, n_blocks),
+        n_blocks, chunk_tokens, _buffer_ptr(cache, dst, need), _stream_handle(stream))
+    _ok(st, "kvx_gather_blocks")
+
+
+def kvx_scatter_blocks(cache: PagedKVCache, l0, l1, block_table, n_blocks, chunk_tokens, src,
+                       stream=None) -> None:
+    need = max(kvx_packed_bytes(cache, l0, l1, n_blocks), 0)
+    st = _native.lib().kvx_scatter_blocks(
+        ctypes.byref(cache.c_struct()), l0, l1, _table_ptr(cache, block_table, n_blocks),
+        n_blocks, chunk_tokens, _buffer_ptr(cache, src, need), _stream_handle(stream))
+    _ok(st, "kvx_scatter_blocks")
+
+
+def kvx_check(stream=None) -> None:
+    _ok(_native.lib().kvx_check(_stream_handle(stream)), "kvx_check")
+
+
+def kvx_plan_pieces(cache, l0, l1, n_blocks, chunk_tokens, slot_bytes):
+    """Staging pieces as a list of dicts (pure host computation)."""
+    c = _cstruct(cache)
+    n = ctypes.c_int32(0)
+    _ok(_native.lib().kvx_plan_pieces(ctypes.byref(c), l0, l1, n_blocks, chunk_tokens,
+                                      slot_bytes, None, 0, ctypes.byref(n)), "kvx_plan_pieces")
+    arr = (KvxPiece * max(n.value, 1))()
+    _ok(_native.lib().kvx_plan_pieces(ctypes.byref(c), l0, l1, n_blocks, chunk_tokens,
+                                      slot_bytes, arr, n.value, ctypes.byref(n)),
+        "kvx_plan_pieces")
+    return [{f: getattr(arr[i], f) for f, _ in KvxPiece._fields_ if f != "reserved"}
+            for i in range(n.value)]
+
+
+class PinnedBuffer:
+    """Exactly-sized pinned host memory (kvx_pinned_alloc), with a numpy view."""
+
+    def __init__(self, nbytes: int):
+        import numpy as np
+
+        p = ctypes.c_void_p()
+        _ok(_native.lib().kvx_pinned_alloc(nbytes, ctypes.byref(p)), "kvx_pinned_alloc")
+        self.ptr = p.value
+        self.nbytes = nbytes
+        self.array = np.ctypeslib.as_array((ctypes.c_uint8 * nbytes).from_address(self.ptr))
+
+    def free(self):
+        if self.ptr:
+            self.array = None
+            _native.lib().kvx_pinned_free(self.ptr)
+            self.ptr = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+class StagingRing:
+    """A bounded pinned staging ring (kvx_ring_*)."""
+
+    def __init__(self, device, n_slots: int, slot_bytes: int, landing=None):
+        import torch
+
+        dev = torch.device(device)
+        idx = dev.index if dev.index is not None else torch.cuda.current_device()
+        if landing is not None:
+            if landing.numel() * landing.element_size() < n_slots * slot_bytes:
+                raise ValueError("landing buffer too small")
+            lp = landing.data_ptr()
+        else:
+            lp = None
+        self._landing = landing
+        h = ctypes.c_void_p()
+        _ok(_native.lib().kvx_ring_create(idx, n_slots, slot_bytes, lp, ctypes.byref(h)),
+            "kvx_ring_create")
+        self.handle = h.value
+        self.n_slots, self.slot_bytes = n_slots, slot_bytes
+        self._source = None
+        self._cache = None
+        self.n_blocks = 0
+
+    def bind(self, cache: PagedKVCache, l0, l1, n_blocks, chunk_tokens, host_source,
+             fill_threads=4):
+        """host_source: numpy uint8 array, PinnedBuffer or pinned CPU tensor."""
+        need = max(kvx_packed_bytes(cache, l0, l1, n_blocks), 0)
+        if isinstance(host_source, PinnedBuffer):
+            ptr, size = host_source.ptr, host_source.nbytes
+        elif hasattr(host_source, "ctypes"):
+            if not host_source.flags["C_CONTIGUOUS"]:
+                raise ValueError("host image must be contiguous")
+            ptr, size = host_source.ctypes.data, host_source.nbytes
+        else:
+            ptr, size = host_source.data_ptr(), host_source.numel() * host_source.element_size()
+        if size < need:
+            raise ValueError(f"host image holds {size} bytes, needs {need}")
+        _ok(_native.lib().kvx_ring_bind(self.handle, ctypes.byref(cache.c_struct()), l0, l1,
+                                        n_blocks, chunk_tokens, ptr, fill_threads),
+            "kvx_ring_bind")
+        self._source = host_source  # keep alive while bound
+        self._cache = cache
+        self.n_blocks = n_blocks
+
+    def stats(self) -> dict:
+        s = KvxRingStats()
+        _ok(_native.lib().kvx_ring_stats_get(self.handle, ctypes.byref(s)), "kvx_ring_stats_get")
+        return {f: getattr(s, f) for f, _ in KvxRingStats._fields_}
+
+    def abort(self):
+        _ok(_native.lib().kvx_ring_abort(self.handle), "kvx_ring_abort")
+
+    def close(self):
+        if self.handle:
+            _native.lib().kvx_ring_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def kvx_restore_from_staging(ring: StagingRing, block_table, stream=None) -> None:
+    ptr = _table_ptr(ring._cache, block_table, ring.n_blocks) if ring._cache is not None else None
+    st = _native.lib().kvx_restore_from_staging(ring.handle, ptr, _stream_handle(stream))
+    _ok(st, "kvx_restore_from_staging")
+
+
+__all__ = [
+    "KvxError", "PagedKVCache", "PinnedBuffer", "StagingRing", "kvx_bytes_per_token",
+    "kvx_packed_bytes", "kvx_gather_blocks", "kvx_scatter_blocks", "kvx_check",
+    "kvx_plan_pieces", "kvx_restore_from_staging", "shape_only_cache", "KVX_MAX_LAYERS",
+]

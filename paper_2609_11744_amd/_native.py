@@ -1,0 +1,70 @@
+"""ctypes declarations for libkvx.so (include/kvx.h). Marshalling only."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libkvx.so")
+
+c_i32, c_i64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
+
+
+class KvxCache(ctypes.Structure):
+    _fields_ = [("k", ctypes.POINTER(c_vp)), ("v", ctypes.POINTER(c_vp)),
+                ("num_layers", c_i32), ("num_blocks", c_i32), ("block_size", c_i32),
+                ("num_kv_heads", c_i32), ("head_dim", c_i32), ("elem_bytes", c_i32)]
+
+
+class KvxPiece(ctypes.Structure):
+    _fields_ = [("src_offset", c_i64), ("bytes", c_i64), ("bt_first", c_i32),
+                ("n_blocks", c_i32), ("l_begin", c_i32), ("l_end", c_i32),
+                ("chunk_tokens", c_i32), ("reserved", c_i32)]
+
+
+class KvxRingStats(ctypes.Structure):
+    _fields_ = [("pieces", c_i64), ("bytes", c_i64), ("fill_ms", ctypes.c_double),
+                ("wait_fill_ms", ctypes.c_double), ("enqueue_ms", ctypes.c_double)]
+
+
+# name -> (restype, argtypes); every symbol include/kvx.h declares.
+SIGNATURES = {
+    "kvx_bytes_per_token": (c_i64, [c_i32, c_i32, c_i32, c_i32]),
+    "kvx_packed_bytes": (c_i64, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32]),
+    "kvx_gather_blocks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
+                                         c_i32, c_vp, c_vp]),
+    "kvx_scatter_blocks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
+                                          c_i32, c_vp, c_vp]),
+    "kvx_check": (ctypes.c_int, [c_vp]),
+    "kvx_strerror": (ctypes.c_char_p, [ctypes.c_int]),
+    "kvx_plan_pieces": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32, c_i32,
+                                       c_i64, ctypes.POINTER(KvxPiece), c_i32,
+                                       ctypes.POINTER(c_i32)]),
+    "kvx_ring_create": (ctypes.c_int, [ctypes.c_int, c_i32, c_i64, c_vp, ctypes.POINTER(c_vp)]),
+    "kvx_ring_bind": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32, c_i32,
+                                     c_vp, c_i32]),
+    "kvx_restore_from_staging": (ctypes.c_int, [c_vp, c_vp, c_vp]),
+    "kvx_ring_stats_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxRingStats)]),
+    "kvx_ring_abort": (ctypes.c_int, [c_vp]),
+    "kvx_ring_destroy": (ctypes.c_int, [c_vp]),
+    "kvx_pinned_alloc": (ctypes.c_int, [c_i64, ctypes.POINTER(c_vp)]),
+    "kvx_pinned_free": (ctypes.c_int, [c_vp]),
+}
+
+_lib = None
+
+
+def lib():
+    """Load libkvx.so; raise if it is not built (there is no fallback path)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"libkvx.so not found at {LIB_PATH}; build it with "
+                               "__graft_entry__.build() (there is no non-HIP fallback)")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(handle, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = handle
+    return _lib

@@ -1,0 +1,160 @@
+// HIP kernels for gfx950: paged-KV gather (paged slabs -> packed image) and
+// scatter (packed image -> paged slabs).
+//
+// The work is pure data movement, bound by HBM bandwidth, so the kernels use
+// no MFMA and no LDS (the chunk layout keeps every slab contiguous on both
+// sides, so nothing is transposed). One workgroup moves one unit, a whole
+// slab (layer, K|V, block) of `slab` bytes:
+//   * the unit's decode (chunk, layer, K|V, block) and its block-table read
+//     depend on blockIdx only, so they run on the scalar unit once per
+//     workgroup;
+//   * the slab moves as 16-byte vectors, consecutive lanes on consecutive
+//     addresses, so every wave instruction reads or writes 1 KiB contiguous;
+//   * each thread issues all of its loads before its stores, so a 256-thread
+//     workgroup has a whole 32 KiB slab in flight;
+//   * both streams are touched once, so loads and stores are non-temporal.
+// The packed-side address of unit u is u * slab (see Geometry), so only the
+// paged side goes through the block table.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+
+#include "kvx_internal.h"
+
+namespace kvx {
+namespace {
+
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+constexpr int kThreads = 256;
+constexpr int kErrBadBlock = 1;
+
+// Device pointers of the call's layers, in image order: p[2 * (l - l0) + kv].
+// Passed by value as a kernel argument (2 KiB for KVX_MAX_LAYERS = 128).
+struct LayerPtrs {
+  char* p[2 * KVX_MAX_LAYERS];
+};
+
+struct UnitGeom {
+  uint32_t units_per_chunk;  // (l1 - l0) * 2 * bpc
+  uint32_t bpc;
+  uint32_t n_blocks;
+  uint32_t num_blocks;       // pool size
+  uint32_t n16;              // 16-byte vectors per slab
+  uint32_t pad;
+  uint64_t slab;
+};
+
+// Sticky error word, one per device. Host code reaches it only through the
+// address that hipGetSymbolAddress returns (device_error_word()).
+__device__ int g_error_word;
+
+template <int V>
+__device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __restrict__ d,
+                                          uint32_t n16) {
+  uint32_t i = threadIdx.x;
+  // Main body: V vectors per thread per pass, loads first.
+  for (; i + (V - 1) * kThreads < n16; i += V * kThreads) {
+    v4u r[V];
+#pragma unroll
+    for (int q = 0; q < V; ++q) r[q] = __builtin_nontemporal_load(s + i + q * kThreads);
+#pragma unroll
+    for (int q = 0; q < V; ++q) __builtin_nontemporal_store(r[q], d + i + q * kThreads);
+  }
+  for (; i < n16; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+}
+
+template <bool kToPacked, int V>
+__global__ void __launch_bounds__(kThreads)
+    copy_units_kernel(LayerPtrs layers, const int32_t* __restrict__ block_table, UnitGeom g,
+                      uint32_t unit_base, char* __restrict__ packed, int* __restrict__ err) {
+  const uint32_t u = unit_base + blockIdx.x;
+  const uint32_t c = u / g.units_per_chunk;
+  const uint32_t r = u - c * g.units_per_chunk;
+  const uint32_t first = c * g.bpc;
+  const uint32_t left = g.n_blocks - first;
+  const uint32_t nc = left < g.bpc ? left : g.bpc;  // blocks in this chunk
+  const uint32_t lk = r / nc;                       // 2 * (l - l0) + kv
+  const uint32_t j = r - lk * nc;
+  const int32_t id = block_table[first + j];
+  if ((uint32_t)id >= g.num_blocks) {
+    if (threadIdx.x == 0) atomicOr(err, kErrBadBlock);
+    return;
+  }
+  char* paged = layers.p[lk] + (uint64_t)(uint32_t)id * g.slab;
+  char* pk = packed + (uint64_t)u * g.slab;
+  if (kToPacked)
+    move_slab<V>(reinterpret_cast<const v4u*>(paged), reinterpret_cast<v4u*>(pk), g.n16);
+  else
+    move_slab<V>(reinterpret_cast<const v4u*>(pk), reinterpret_cast<v4u*>(paged), g.n16);
+}
+
+// A dispatch's grid is counted in work-items in 32 bits, so one launch covers
+// at most kMaxUnitsPerLaunch workgroups; larger calls are split.
+constexpr uint32_t kMaxUnitsPerLaunch = 1u << 22;
+
+template <bool kToPacked>
+hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, uint32_t n_units,
+                  char* packed, int* err, hipStream_t stream) {
+  for (uint32_t base = 0; base < n_units; base += kMaxUnitsPerLaunch) {
+    const uint32_t cnt = n_units - base < kMaxUnitsPerLaunch ? n_units - base : kMaxUnitsPerLaunch;
+    const dim3 grid(cnt), block(kThreads);
+    if (ug.n16 % (8 * kThreads) == 0)
+      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 8>), grid, block, 0, stream, lp, bt, ug,
+                         base, packed, err);
+    else if (ug.n16 % (4 * kThreads) == 0)
+      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 4>), grid, block, 0, stream, lp, bt, ug,
+                         base, packed, err);
+    else
+      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 1>), grid, block, 0, stream, lp, bt, ug,
+                         base, packed, err);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+}  // namespace
+
+int* device_error_word() {
+  static std::mutex mu;
+  static int* addr[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(g_error_word)) == hipSuccess) addr[dev] = (int*)p;
+  }
+  return addr[dev];
+}
+
+kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
+                       const int32_t* block_table, const Geometry& g, void* packed,
+                       hipStream_t stream) {
+  if (g.n_units == 0) return KVX_OK;
+  if (g.n_units > 0x7FFFFFFF || g.slab % 16 != 0) return KVX_EINTERNAL;
+  int* err = device_error_word();
+  if (!err) return KVX_EHIP;
+  LayerPtrs lp = {};
+  for (int32_t l = l0; l < l1; ++l) {
+    lp.p[2 * (l - l0)] = static_cast<char*>(cache->k[l]);
+    lp.p[2 * (l - l0) + 1] = static_cast<char*>(cache->v[l]);
+  }
+  UnitGeom ug;
+  ug.units_per_chunk = (uint32_t)(2 * g.lr * g.bpc);
+  ug.bpc = (uint32_t)g.bpc;
+  ug.n_blocks = (uint32_t)g.n_blocks;
+  ug.num_blocks = (uint32_t)g.num_blocks;
+  ug.n16 = (uint32_t)(g.slab / 16);
+  ug.pad = 0;
+  ug.slab = (uint64_t)g.slab;
+  hipError_t e = to_packed
+                     ? launch<true>(lp, block_table, ug, (uint32_t)g.n_units, (char*)packed, err,
+                                    stream)
+                     : launch<false>(lp, block_table, ug, (uint32_t)g.n_units, (char*)packed, err,
+                                     stream);
+  return e == hipSuccess ? KVX_OK : KVX_EHIP;
+}
+
+}  // namespace kvx

@@ -1,0 +1,169 @@
+"""Host-side checks of the C ABI (no GPU): the library loads and exports every
+function kvx.h declares, host validation rejects bad arguments before any
+HIP call, and the staging-piece planner tiles the image so that scattering
+the pieces one by one equals scattering the whole image (checked with the
+oracle)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import kvsynth
+import oracle
+import paper_2609_11744_amd as kvx
+from paper_2609_11744_amd import _native
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "kvx.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvx_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_three_path_calls():
+    names = _declared_functions()
+    for n in ("kvx_gather_blocks", "kvx_scatter_blocks", "kvx_restore_from_staging"):
+        assert n in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = ctypes.CDLL(_native.LIB_PATH)
+    for name in _declared_functions():
+        assert hasattr(lib, name), name
+    assert set(_declared_functions()) == set(_native.SIGNATURES)
+
+
+def test_bytes_per_token_matches_oracle_and_paper():
+    assert kvx.kvx_bytes_per_token(28, 8, 128, 2) == 114688
+    assert kvx.kvx_bytes_per_token(0, 8, 128, 2) == -1
+    for args in [(32, 8, 128, 2), (80, 8, 128, 2), (2, 2, 64, 2)]:
+        assert kvx.kvx_bytes_per_token(*args) == oracle.bytes_per_token(*args)
+
+
+def _fake_cache(L=4, NB=100, BS=16, H=8, D=128, e=2, base=0x10000000):
+    tensor = NB * BS * H * D * e
+    kp = (ctypes.c_void_p * L)(*[base + (2 * l) * tensor for l in range(L)])
+    vp = (ctypes.c_void_p * L)(*[base + (2 * l + 1) * tensor for l in range(L)])
+    c = _native.KvxCache(kp, vp, L, NB, BS, H, D, e)
+    c._keep = (kp, vp)
+    return c, base, tensor
+
+
+def _gather(c, l0, l1, bt, n, ct, dst):
+    return _native.lib().kvx_gather_blocks(ctypes.byref(c), l0, l1, bt, n, ct, dst, None)
+
+
+@pytest.mark.parametrize("args", [
+    dict(l0=-1), dict(l1=5), dict(l0=3, l1=2), dict(n=-1), dict(ct=0), dict(ct=24), dict(ct=-16),
+    dict(bt=None), dict(dst=None), dict(dst=0x7000_0000_0008),
+])
+def test_validation_rejects_before_any_hip_call(args):
+    c, base, tensor = _fake_cache()
+    a = dict(l0=0, l1=4, bt=0x5000_0000_0000, n=10, ct=32, dst=0x7000_0000_0000)
+    a.update(args)
+    st = _gather(c, a["l0"], a["l1"], a["bt"], a["n"], a["ct"], a["dst"])
+    assert st == kvx.KVX_EINVAL
+
+
+def test_validation_rejects_dst_overlapping_cache():
+    c, base, tensor = _fake_cache()
+    assert _gather(c, 0, 4, 0x5000_0000_0000, 10, 32, base + tensor + 4096) == kvx.KVX_EINVAL
+
+
+def test_validation_rejects_misaligned_cache_and_bad_shapes():
+    c, base, tensor = _fake_cache(base=0x10000008)
+    assert _gather(c, 0, 4, 0x5000_0000_0000, 1, 16, 0x7000_0000_0000) == kvx.KVX_EINVAL
+    c, _, _ = _fake_cache(e=3)
+    assert _gather(c, 0, 4, 0x5000_0000_0000, 1, 16, 0x7000_0000_0000) == kvx.KVX_EINVAL
+    c, _, _ = _fake_cache(H=1, D=3, BS=1, e=2)  # 6-byte slab, not a multiple of 16
+    assert _gather(c, 0, 4, 0x5000_0000_0000, 1, 1, 0x7000_0000_0000) == kvx.KVX_EINVAL
+    c, _, _ = _fake_cache(L=200)
+    assert _gather(c, 0, 200, 0x5000_0000_0000, 1, 16, 0x7000_0000_0000) == kvx.KVX_EINVAL
+
+
+def test_noops_return_ok_without_touching_the_device():
+    c, _, _ = _fake_cache()
+    assert _gather(c, 0, 4, None, 0, 32, None) == kvx.KVX_OK
+    assert _gather(c, 2, 2, 0x5000_0000_0000, 10, 32, 0x7000_0000_0000) == kvx.KVX_OK
+
+
+def test_packed_bytes_matches_oracle():
+    for L, NB, BS, H, D, e in [(32, 20000, 16, 8, 128, 2), (2, 64, 16, 2, 64, 2),
+                               (80, 1000, 16, 8, 128, 2), (3, 7, 4, 1, 8, 4)]:
+        c = kvx.shape_only_cache(L, NB, BS, H, D, e)
+        s = oracle.Shape(L, NB, BS, H, D, e)
+        for l0, l1, n in [(0, L, 5), (1, L, 0), (0, 1, 13)]:
+            assert kvx.kvx_packed_bytes(c, l0, l1, n) == oracle.packed_bytes(s, l0, l1, n)
+
+
+# ---- staging piece planner ---------------------------------------------------
+
+PLAN_CASES = [
+    # (layers, heads, dim, block_size, n_blocks, chunk_tokens, slot_bytes)
+    (32, 8, 128, 16, 5000, 256, 64 << 20),    # 80k prefix, 4 x 64 MiB ring
+    (32, 8, 128, 16, 2048, 16, 64 << 20),
+    (32, 8, 128, 16, 2048, 1024, 64 << 20),   # chunk larger than a slot: layer split
+    (80, 8, 128, 16, 1000, 256, 64 << 20),    # 70B chunk 80 MiB -> 64 + 16 layers
+    (3, 1, 8, 4, 17, 12, 4096),
+    (5, 2, 8, 2, 9, 6, 640),
+]
+
+
+@pytest.mark.parametrize("case", PLAN_CASES)
+def test_plan_tiles_image_exactly_and_fits_slots(case):
+    L, H, D, BS, n, ct, slot = case
+    c = kvx.shape_only_cache(L, 4 * n + 8, BS, H, D, 2)
+    pieces = kvx.kvx_plan_pieces(c, 0, L, n, ct, slot)
+    total = kvx.kvx_packed_bytes(c, 0, L, n)
+    at = 0
+    for p in pieces:
+        assert p["src_offset"] == at and 0 < p["bytes"] <= slot
+        slab = BS * H * D * 2
+        assert p["bytes"] == p["n_blocks"] * (p["l_end"] - p["l_begin"]) * 2 * slab
+        at += p["bytes"]
+    assert at == total
+
+
+def test_plan_80k_prefix_has_157_pieces():
+    c = kvx.shape_only_cache(32, 20000, 16, 8, 128, 2)
+    pieces = kvx.kvx_plan_pieces(c, 0, 32, 5000, 256, 64 << 20)
+    assert len(pieces) == 157
+    assert pieces[-1]["bytes"] == 16 << 20 and pieces[-1]["n_blocks"] == 8
+
+
+def test_plan_70b_chunk_splits_64_plus_16_layers():
+    c = kvx.shape_only_cache(80, 2000, 16, 8, 128, 2)
+    pieces = kvx.kvx_plan_pieces(c, 0, 80, 32, 256, 64 << 20)
+    assert [(p["l_begin"], p["l_end"]) for p in pieces] == [(0, 64), (64, 80)] * 2
+
+
+def test_plan_rejects_slot_smaller_than_one_layer():
+    c = kvx.shape_only_cache(4, 100, 16, 8, 128, 2)
+    with pytest.raises(kvx.KvxError):
+        # one layer (K and V) of a 16-block chunk is 2 * 16 * 32 KiB = 1 MiB
+        kvx.kvx_plan_pieces(c, 0, 4, 16, 256, (1 << 20) - 4096)
+
+
+@pytest.mark.parametrize("case", PLAN_CASES[4:] + [(4, 2, 8, 4, 23, 16, 2048), (6, 1, 8, 2, 13, 8, 256)])
+def test_scattering_pieces_equals_scattering_image(case):
+    """Every piece is a plain scatter of its bytes; together they reproduce the
+    oracle's scatter of the whole image (restore transparency, on the CPU)."""
+    L, H, D, BS, n, ct, slot = case
+    NB = 3 * n + 5
+    s = oracle.Shape(L, NB, BS, H, D, 2)
+    c = kvx.shape_only_cache(L, NB, BS, H, D, 2)
+    bt = np.random.default_rng(n).permutation(NB)[:n].astype(np.int32)
+    img = kvsynth.host_bytes(oracle.packed_bytes(s, 0, L, n), 5, 123, mode=kvsynth.MODE_RAW)
+    whole = oracle.new_mirror(s)
+    oracle.scatter(s, *whole, 0, L, bt, ct, img)
+    by_piece = oracle.new_mirror(s)
+    for p in kvx.kvx_plan_pieces(c, 0, L, n, ct, slot):
+        part = img[p["src_offset"]:p["src_offset"] + p["bytes"]]
+        oracle.scatter(s, *by_piece, p["l_begin"], p["l_end"],
+                       bt[p["bt_first"]:p["bt_first"] + p["n_blocks"]], p["chunk_tokens"], part)
+    for a, b in zip(whole[0] + whole[1], by_piece[0] + by_piece[1]):
+        assert np.array_equal(a, b)

@@ -50,3 +50,16 @@ def test_rejects_unaligned():
         kvsynth.fill_host(np.zeros(12, np.uint8), 1, 1)
     with pytest.raises(ValueError):
         kvsynth.fill_host(np.zeros(16, np.uint8), 1, 1, byte_offset=4)
+
+
+def test_fill_ranges_matches_whole_fill():
+    whole = kvsynth.host_bytes(1 << 20, 9, 77, mode=kvsynth.MODE_RAW)
+    buf = np.zeros(1 << 20, np.uint8)
+    offs = [0, 4096 * 3, 4096 * 17, (1 << 20) - 4096]
+    kvsynth.fill_ranges(buf, offs, 4096, 9, 77, mode=kvsynth.MODE_RAW, threads=3)
+    for o in offs:
+        assert np.array_equal(buf[o:o + 4096], whole[o:o + 4096])
+    mask = np.ones(1 << 20, bool)
+    for o in offs:
+        mask[o:o + 4096] = False
+    assert not buf[mask].any()
