@@ -206,7 +206,7 @@ def main():
                                  "enqueue_wait_for_fill": round(med["wait_fill_ms"], 2),
                                  "device_span": round(med["restore_dev_ms"], 2)},
         "probes": {k: round(v, 2) for k, v in probe.items()},
-        "roofline": {"bound": "hbm", "kernel": "gather (copy_units_kernel<true,8>)",
+        "roofline": {"bound": "hbm", "kernel": "gather (copy_units_kernel<true, 1024, 2>)",
                      "achieved": round(gather_GBps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(gather_GBps / HBM_PEAK_GBPS, 4),
                      "traffic": None},

@@ -10,9 +10,14 @@
 //     workgroup;
 //   * the slab moves as 16-byte vectors, consecutive lanes on consecutive
 //     addresses, so every wave instruction reads or writes 1 KiB contiguous;
-//   * each thread issues all of its loads before its stores, so a 256-thread
-//     workgroup has a whole 32 KiB slab in flight;
-//   * both streams are touched once, so loads and stores are non-temporal.
+//   * each thread issues all of its loads before its stores, so a workgroup
+//     has its whole slab in flight (32 KiB slabs: 1024 threads x 2 vectors);
+//   * both streams are touched once, so loads and stores are non-temporal;
+//   * workgroups are dispatched round-robin over the 8 XCDs, so workgroup b
+//     is mapped to a unit such that each XCD walks one contiguous range of
+//     units. The packed side of an XCD's work is then one sequential stream,
+//     which HBM serves measurably better than 8 interleaved ones (the write
+//     side of a copy is what bounds it).
 // The packed-side address of unit u is u * slab (see Geometry), so only the
 // paged side goes through the block table.
 #include <hip/hip_runtime.h>
@@ -26,8 +31,8 @@ namespace {
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 256;
 constexpr int kErrBadBlock = 1;
+constexpr unsigned kXcds = 8;  // MI355X: 8 XCDs, workgroups dispatched round-robin
 
 // Device pointers of the call's layers, in image order: p[2 * (l - l0) + kv].
 // Passed by value as a kernel argument (2 KiB for KVX_MAX_LAYERS = 128).
@@ -49,26 +54,36 @@ struct UnitGeom {
 // address that hipGetSymbolAddress returns (device_error_word()).
 __device__ int g_error_word;
 
-template <int V>
+// Workgroup b of a launch over n units -> unit index. XCD x = b % kXcds runs
+// the workgroups b = x, x + kXcds, ...; they get the contiguous range
+// [x*q + min(x, r), ...) of q or q + 1 units (q = n / kXcds, r = n % kXcds).
+// A bijection on [0, n) for every n.
+__device__ __forceinline__ uint32_t xcd_contiguous(uint32_t b, uint32_t n) {
+  const uint32_t q = n / kXcds, r = n % kXcds, x = b % kXcds, k = b / kXcds;
+  return x * q + (x < r ? x : r) + k;
+}
+
+template <int T, int V>
 __device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __restrict__ d,
                                           uint32_t n16) {
   uint32_t i = threadIdx.x;
   // Main body: V vectors per thread per pass, loads first.
-  for (; i + (V - 1) * kThreads < n16; i += V * kThreads) {
+  for (; i + (V - 1) * T < n16; i += V * T) {
     v4u r[V];
 #pragma unroll
-    for (int q = 0; q < V; ++q) r[q] = __builtin_nontemporal_load(s + i + q * kThreads);
+    for (int q = 0; q < V; ++q) r[q] = __builtin_nontemporal_load(s + i + q * T);
 #pragma unroll
-    for (int q = 0; q < V; ++q) __builtin_nontemporal_store(r[q], d + i + q * kThreads);
+    for (int q = 0; q < V; ++q) __builtin_nontemporal_store(r[q], d + i + q * T);
   }
-  for (; i < n16; i += kThreads) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+  for (; i < n16; i += T) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
 }
 
-template <bool kToPacked, int V>
-__global__ void __launch_bounds__(kThreads)
+template <bool kToPacked, int T, int V>
+__global__ void __launch_bounds__(T)
     copy_units_kernel(LayerPtrs layers, const int32_t* __restrict__ block_table, UnitGeom g,
-                      uint32_t unit_base, char* __restrict__ packed, int* __restrict__ err) {
-  const uint32_t u = unit_base + blockIdx.x;
+                      uint32_t unit_base, uint32_t unit_count, char* __restrict__ packed,
+                      int* __restrict__ err) {
+  const uint32_t u = unit_base + xcd_contiguous(blockIdx.x, unit_count);
   const uint32_t c = u / g.units_per_chunk;
   const uint32_t r = u - c * g.units_per_chunk;
   const uint32_t first = c * g.bpc;
@@ -84,9 +99,9 @@ __global__ void __launch_bounds__(kThreads)
   char* paged = layers.p[lk] + (uint64_t)(uint32_t)id * g.slab;
   char* pk = packed + (uint64_t)u * g.slab;
   if (kToPacked)
-    move_slab<V>(reinterpret_cast<const v4u*>(paged), reinterpret_cast<v4u*>(pk), g.n16);
+    move_slab<T, V>(reinterpret_cast<const v4u*>(paged), reinterpret_cast<v4u*>(pk), g.n16);
   else
-    move_slab<V>(reinterpret_cast<const v4u*>(pk), reinterpret_cast<v4u*>(paged), g.n16);
+    move_slab<T, V>(reinterpret_cast<const v4u*>(pk), reinterpret_cast<v4u*>(paged), g.n16);
 }
 
 // A dispatch's grid is counted in work-items in 32 bits, so one launch covers
@@ -98,16 +113,19 @@ hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, ui
                   char* packed, int* err, hipStream_t stream) {
   for (uint32_t base = 0; base < n_units; base += kMaxUnitsPerLaunch) {
     const uint32_t cnt = n_units - base < kMaxUnitsPerLaunch ? n_units - base : kMaxUnitsPerLaunch;
-    const dim3 grid(cnt), block(kThreads);
-    if (ug.n16 % (8 * kThreads) == 0)
-      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 8>), grid, block, 0, stream, lp, bt, ug,
-                         base, packed, err);
-    else if (ug.n16 % (4 * kThreads) == 0)
-      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 4>), grid, block, 0, stream, lp, bt, ug,
-                         base, packed, err);
+    const dim3 grid(cnt);
+    // Slabs of a multiple of 32 KiB: 1024 threads x 2 vectors per pass (the
+    // shape that measured fastest for 32 KiB slabs). Smaller slabs: 256
+    // threads, so that fewer lanes sit idle.
+    if (ug.n16 % (2 * 1024) == 0)
+      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 1024, 2>), grid, dim3(1024), 0, stream, lp,
+                         bt, ug, base, cnt, packed, err);
+    else if (ug.n16 % (4 * 256) == 0)
+      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 256, 4>), grid, dim3(256), 0, stream, lp,
+                         bt, ug, base, cnt, packed, err);
     else
-      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 1>), grid, block, 0, stream, lp, bt, ug,
-                         base, packed, err);
+      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 256, 1>), grid, dim3(256), 0, stream, lp,
+                         bt, ug, base, cnt, packed, err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
