@@ -20,6 +20,13 @@
 //     side of a copy is what bounds it).
 // The packed-side address of unit u is u * slab (see Geometry), so only the
 // paged side goes through the block table.
+//
+// Large scatters write to caller-chosen (typically random) blocks. HBM takes
+// writes faster when each XCD's write stream ascends through memory, so a
+// large scatter first ranks the destination ids (rank_kernel, into stream-
+// ordered scratch) and then visits units layer by layer in ascending
+// destination order; the packed side is then read out of order, which costs
+// less than unordered writes.
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -78,19 +85,36 @@ __device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __rest
   for (; i < n16; i += T) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
 }
 
-template <bool kToPacked, int T, int V>
+// kOrdered = false: units in image order (u -> chunk, layer|K|V, block).
+// kOrdered = true: unit v -> lk = v / n_blocks, k = v % n_blocks, block index
+// i = order[k] (the block holding the k-th smallest destination id); the
+// image position u of (chunk i / bpc, lk, block i % bpc) follows.
+template <bool kToPacked, bool kOrdered, int T, int V>
 __global__ void __launch_bounds__(T)
     copy_units_kernel(LayerPtrs layers, const int32_t* __restrict__ block_table, UnitGeom g,
-                      uint32_t unit_base, uint32_t unit_count, char* __restrict__ packed,
+                      uint32_t unit_base, uint32_t unit_count,
+                      const uint32_t* __restrict__ order, char* __restrict__ packed,
                       int* __restrict__ err) {
-  const uint32_t u = unit_base + xcd_contiguous(blockIdx.x, unit_count);
-  const uint32_t c = u / g.units_per_chunk;
-  const uint32_t r = u - c * g.units_per_chunk;
-  const uint32_t first = c * g.bpc;
-  const uint32_t left = g.n_blocks - first;
-  const uint32_t nc = left < g.bpc ? left : g.bpc;  // blocks in this chunk
-  const uint32_t lk = r / nc;                       // 2 * (l - l0) + kv
-  const uint32_t j = r - lk * nc;
+  uint32_t u = unit_base + xcd_contiguous(blockIdx.x, unit_count);
+  uint32_t c, first, nc, lk, j;
+  if (kOrdered) {
+    lk = u / g.n_blocks;
+    const uint32_t i = order[u - lk * g.n_blocks];  // < n_blocks (a permutation)
+    c = i / g.bpc;
+    first = c * g.bpc;
+    j = i - first;
+    const uint32_t left = g.n_blocks - first;
+    nc = left < g.bpc ? left : g.bpc;
+    u = c * g.units_per_chunk + lk * nc + j;
+  } else {
+    c = u / g.units_per_chunk;
+    const uint32_t r = u - c * g.units_per_chunk;
+    first = c * g.bpc;
+    const uint32_t left = g.n_blocks - first;
+    nc = left < g.bpc ? left : g.bpc;  // blocks in this chunk
+    lk = r / nc;                       // 2 * (l - l0) + kv
+    j = r - lk * nc;
+  }
   const int32_t id = block_table[first + j];
   if ((uint32_t)id >= g.num_blocks) {
     if (threadIdx.x == 0) atomicOr(err, kErrBadBlock);
@@ -104,13 +128,45 @@ __global__ void __launch_bounds__(T)
     move_slab<T, V>(reinterpret_cast<const v4u*>(pk), reinterpret_cast<v4u*>(paged), g.n16);
 }
 
+// order[rank(i)] = i, where rank orders the pairs (id as unsigned, index i)
+// lexicographically: a permutation of [0, n) for any table, duplicates and
+// out-of-range ids included. Each thread counts the pairs below its own,
+// reading the table through LDS tiles: n^2 comparisons, a few microseconds
+// for the few thousand blocks of a long prefix.
+constexpr int kRankThreads = 256;
+constexpr int kRankTile = 2048;
+
+__global__ void __launch_bounds__(kRankThreads)
+    rank_kernel(const int32_t* __restrict__ block_table, uint32_t n,
+                uint32_t* __restrict__ order) {
+  __shared__ uint32_t tile[kRankTile];
+  const uint32_t i = blockIdx.x * kRankThreads + threadIdx.x;
+  const uint32_t key = i < n ? (uint32_t)block_table[i] : 0u;
+  uint32_t below = 0;
+  for (uint32_t t0 = 0; t0 < n; t0 += kRankTile) {
+    const uint32_t cnt = n - t0 < (uint32_t)kRankTile ? n - t0 : (uint32_t)kRankTile;
+    __syncthreads();
+    for (uint32_t q = threadIdx.x; q < cnt; q += kRankThreads)
+      tile[q] = (uint32_t)block_table[t0 + q];
+    __syncthreads();
+    for (uint32_t q = 0; q < cnt; ++q) {
+      const uint32_t kj = tile[q], jj = t0 + q;
+      below += (kj < key) | ((kj == key) & (jj < i));
+    }
+  }
+  if (i < n) order[below] = i;
+}
+
 // A dispatch's grid is counted in work-items in 32 bits, so one launch covers
 // at most kMaxUnitsPerLaunch workgroups; larger calls are split.
 constexpr uint32_t kMaxUnitsPerLaunch = 1u << 22;
 
-template <bool kToPacked>
+// Scatters of at least this many blocks run in destination order.
+constexpr int32_t kOrderedScatterMinBlocks = 1024;
+
+template <bool kToPacked, bool kOrdered>
 hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, uint32_t n_units,
-                  char* packed, int* err, hipStream_t stream) {
+                  const uint32_t* order, char* packed, int* err, hipStream_t stream) {
   for (uint32_t base = 0; base < n_units; base += kMaxUnitsPerLaunch) {
     const uint32_t cnt = n_units - base < kMaxUnitsPerLaunch ? n_units - base : kMaxUnitsPerLaunch;
     const dim3 grid(cnt);
@@ -118,14 +174,14 @@ hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, ui
     // shape that measured fastest for 32 KiB slabs). Smaller slabs: 256
     // threads, so that fewer lanes sit idle.
     if (ug.n16 % (2 * 1024) == 0)
-      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 1024, 2>), grid, dim3(1024), 0, stream, lp,
-                         bt, ug, base, cnt, packed, err);
+      hipLaunchKernelGGL((copy_units_kernel<kToPacked, kOrdered, 1024, 2>), grid, dim3(1024), 0,
+                         stream, lp, bt, ug, base, cnt, order, packed, err);
     else if (ug.n16 % (4 * 256) == 0)
-      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 256, 4>), grid, dim3(256), 0, stream, lp,
-                         bt, ug, base, cnt, packed, err);
+      hipLaunchKernelGGL((copy_units_kernel<kToPacked, kOrdered, 256, 4>), grid, dim3(256), 0,
+                         stream, lp, bt, ug, base, cnt, order, packed, err);
     else
-      hipLaunchKernelGGL((copy_units_kernel<kToPacked, 256, 1>), grid, dim3(256), 0, stream, lp,
-                         bt, ug, base, cnt, packed, err);
+      hipLaunchKernelGGL((copy_units_kernel<kToPacked, kOrdered, 256, 1>), grid, dim3(256), 0,
+                         stream, lp, bt, ug, base, cnt, order, packed, err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -167,11 +223,33 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.n16 = (uint32_t)(g.slab / 16);
   ug.pad = 0;
   ug.slab = (uint64_t)g.slab;
-  hipError_t e = to_packed
-                     ? launch<true>(lp, block_table, ug, (uint32_t)g.n_units, (char*)packed, err,
-                                    stream)
-                     : launch<false>(lp, block_table, ug, (uint32_t)g.n_units, (char*)packed, err,
-                                     stream);
+  const uint32_t n_units = (uint32_t)g.n_units;
+  if (to_packed) {
+    hipError_t e = launch<true, false>(lp, block_table, ug, n_units, nullptr, (char*)packed, err,
+                                       stream);
+    return e == hipSuccess ? KVX_OK : KVX_EHIP;
+  }
+  // Destination-ordered scatter for large calls; the order lives in
+  // stream-ordered scratch. If that allocation fails, fall back to image
+  // order (same result, slower).
+  uint32_t* order = nullptr;
+  if (g.n_blocks >= kOrderedScatterMinBlocks &&
+      hipMallocAsync((void**)&order, (size_t)g.n_blocks * sizeof(uint32_t), stream) != hipSuccess)
+    order = nullptr;
+  (void)hipGetLastError();
+  hipError_t e;
+  if (order) {
+    const uint32_t nb = (uint32_t)g.n_blocks;
+    hipLaunchKernelGGL(rank_kernel, dim3((nb + kRankThreads - 1) / kRankThreads),
+                       dim3(kRankThreads), 0, stream, block_table, nb, order);
+    e = hipGetLastError();
+    if (e == hipSuccess)
+      e = launch<false, true>(lp, block_table, ug, n_units, order, (char*)packed, err, stream);
+    const hipError_t ef = hipFreeAsync(order, stream);
+    if (e == hipSuccess) e = ef;
+  } else {
+    e = launch<false, false>(lp, block_table, ug, n_units, nullptr, (char*)packed, err, stream);
+  }
   return e == hipSuccess ? KVX_OK : KVX_EHIP;
 }
 

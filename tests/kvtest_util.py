@@ -100,6 +100,14 @@ def to_host(t) -> np.ndarray:
     return t.contiguous().view(torch.uint8).cpu().numpy().ravel()
 
 
-def first_mismatch(a: np.ndarray, b: np.ndarray):
-    d = np.flatnonzero(a != b)
-    return None if d.size == 0 else int(d[0])
+def first_mismatch(a: np.ndarray, b: np.ndarray, step: int = 1 << 28):
+    """Index of the first differing byte of two equal-length arrays, or None.
+    Compares in bounded pieces so multi-GB images need no full-size temporaries."""
+    a, b = a.ravel(), b.ravel()
+    if a.size != b.size:
+        return min(a.size, b.size)
+    for s in range(0, a.size, step):
+        x, y = a[s:s + step], b[s:s + step]
+        if not np.array_equal(x, y):
+            return s + int(np.flatnonzero(x != y)[0])
+    return None
