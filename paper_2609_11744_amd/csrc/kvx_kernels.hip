@@ -23,8 +23,8 @@
 //
 // Large scatters write to caller-chosen (typically random) blocks. HBM takes
 // writes faster when each XCD's write stream ascends through memory, so a
-// large scatter first ranks the destination ids (rank_kernel, into stream-
-// ordered scratch) and then visits units layer by layer in ascending
+// large scatter first buckets the destination ids (order_kernel, into
+// stream-ordered scratch) and then visits units layer by layer in ascending
 // destination order; the packed side is then read out of order, which costs
 // less than unordered writes.
 #include <hip/hip_runtime.h>
@@ -87,8 +87,8 @@ __device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __rest
 
 // kOrdered = false: units in image order (u -> chunk, layer|K|V, block).
 // kOrdered = true: unit v -> lk = v / n_blocks, k = v % n_blocks, block index
-// i = order[k] (the block holding the k-th smallest destination id); the
-// image position u of (chunk i / bpc, lk, block i % bpc) follows.
+// i = order[k] (destinations ascending by bucket); the image position u of
+// (chunk i / bpc, lk, block i % bpc) follows.
 template <bool kToPacked, bool kOrdered, int T, int V>
 __global__ void __launch_bounds__(T)
     copy_units_kernel(LayerPtrs layers, const int32_t* __restrict__ block_table, UnitGeom g,
@@ -128,33 +128,61 @@ __global__ void __launch_bounds__(T)
     move_slab<T, V>(reinterpret_cast<const v4u*>(pk), reinterpret_cast<v4u*>(paged), g.n16);
 }
 
-// order[rank(i)] = i, where rank orders the pairs (id as unsigned, index i)
-// lexicographically: a permutation of [0, n) for any table, duplicates and
-// out-of-range ids included. Each thread counts the pairs below its own,
-// reading the table through LDS tiles: n^2 comparisons, a few microseconds
-// for the few thousand blocks of a long prefix.
-constexpr int kRankThreads = 256;
-constexpr int kRankTile = 2048;
+// Destination order for a scatter: order[] lists the block-table indexes
+// bucketed by destination id, buckets ascending. The id range [0, num_blocks)
+// is cut into kBins equal bins (ids outside it go to the last bin; the copy
+// kernel skips them). One workgroup counts bin sizes in LDS, scans them into
+// bin starts and places each index with an LDS atomic, so order[] is a
+// permutation of [0, n) for any table (within a bin the order is
+// unspecified, which only matters if destinations repeat, and a scatter's
+// destinations must be distinct).
+constexpr int kOrderThreads = 1024;
+constexpr uint32_t kBins = 4096;  // 4 bins per thread
 
-__global__ void __launch_bounds__(kRankThreads)
-    rank_kernel(const int32_t* __restrict__ block_table, uint32_t n,
-                uint32_t* __restrict__ order) {
-  __shared__ uint32_t tile[kRankTile];
-  const uint32_t i = blockIdx.x * kRankThreads + threadIdx.x;
-  const uint32_t key = i < n ? (uint32_t)block_table[i] : 0u;
-  uint32_t below = 0;
-  for (uint32_t t0 = 0; t0 < n; t0 += kRankTile) {
-    const uint32_t cnt = n - t0 < (uint32_t)kRankTile ? n - t0 : (uint32_t)kRankTile;
-    __syncthreads();
-    for (uint32_t q = threadIdx.x; q < cnt; q += kRankThreads)
-      tile[q] = (uint32_t)block_table[t0 + q];
-    __syncthreads();
-    for (uint32_t q = 0; q < cnt; ++q) {
-      const uint32_t kj = tile[q], jj = t0 + q;
-      below += (kj < key) | ((kj == key) & (jj < i));
-    }
+__device__ __forceinline__ uint32_t bin_of(int32_t id, uint32_t num_blocks, uint32_t bins) {
+  const uint32_t u = (uint32_t)id;
+  return u >= num_blocks ? bins - 1 : (uint32_t)(((uint64_t)u * bins) / num_blocks);
+}
+
+__global__ void __launch_bounds__(kOrderThreads)
+    order_kernel(const int32_t* __restrict__ block_table, uint32_t n, uint32_t num_blocks,
+                 uint32_t* __restrict__ order) {
+  __shared__ uint32_t cnt[kBins];
+  __shared__ uint32_t wave_total[kOrderThreads / 64];
+  const uint32_t t = threadIdx.x, lane = t % 64, wave = t / 64;
+  const uint32_t bins = num_blocks < kBins ? num_blocks : kBins;
+  for (uint32_t b = t; b < kBins; b += kOrderThreads) cnt[b] = 0;
+  __syncthreads();
+  for (uint32_t i = t; i < n; i += kOrderThreads)
+    atomicAdd(&cnt[bin_of(block_table[i], num_blocks, bins)], 1u);
+  __syncthreads();
+  // exclusive scan of the kBins counts: 4 per thread, then waves, then workgroup
+  const uint32_t c0 = cnt[4 * t], c1 = cnt[4 * t + 1], c2 = cnt[4 * t + 2], c3 = cnt[4 * t + 3];
+  const uint32_t mine = c0 + c1 + c2 + c3;
+  uint32_t incl = mine;
+  for (uint32_t off = 1; off < 64; off <<= 1) {
+    const uint32_t y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
   }
-  if (i < n) order[below] = i;
+  if (lane == 63) wave_total[wave] = incl;
+  __syncthreads();
+  if (wave == 0) {
+    uint32_t w = lane < kOrderThreads / 64 ? wave_total[lane] : 0;
+    for (uint32_t off = 1; off < kOrderThreads / 64; off <<= 1) {
+      const uint32_t y = __shfl_up(w, off, 64);
+      if (lane >= off) w += y;
+    }
+    if (lane < kOrderThreads / 64) wave_total[lane] = w;  // inclusive over waves
+  }
+  __syncthreads();
+  const uint32_t base = (wave > 0 ? wave_total[wave - 1] : 0u) + incl - mine;
+  cnt[4 * t] = base;
+  cnt[4 * t + 1] = base + c0;
+  cnt[4 * t + 2] = base + c0 + c1;
+  cnt[4 * t + 3] = base + c0 + c1 + c2;
+  __syncthreads();
+  for (uint32_t i = t; i < n; i += kOrderThreads)
+    order[atomicAdd(&cnt[bin_of(block_table[i], num_blocks, bins)], 1u)] = i;
 }
 
 // A dispatch's grid is counted in work-items in 32 bits, so one launch covers
@@ -239,9 +267,8 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   (void)hipGetLastError();
   hipError_t e;
   if (order) {
-    const uint32_t nb = (uint32_t)g.n_blocks;
-    hipLaunchKernelGGL(rank_kernel, dim3((nb + kRankThreads - 1) / kRankThreads),
-                       dim3(kRankThreads), 0, stream, block_table, nb, order);
+    hipLaunchKernelGGL(order_kernel, dim3(1), dim3(kOrderThreads), 0, stream, block_table,
+                       (uint32_t)g.n_blocks, (uint32_t)g.num_blocks, order);
     e = hipGetLastError();
     if (e == hipSuccess)
       e = launch<false, true>(lp, block_table, ug, n_units, order, (char*)packed, err, stream);

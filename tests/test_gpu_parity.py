@@ -262,3 +262,51 @@ def test_aborted_ring_reports_closed():
         assert ei.value.status == kvx.KVX_ECLOSED
     finally:
         ring.close()
+
+
+# ---- destination-ordered scatter (1024..8192 blocks) --------------------------
+
+@pytest.mark.parametrize("n", [1024, 1500, 8192])
+def test_ordered_scatter_bit_exact(n):
+    s = oracle.Shape(2, 3 * 8192, 16, 2, 64, 2)  # 4 KiB slabs
+    seed = 40 + n
+    bt_src, bt_dst = seeded_ids(seed, s.num_blocks, n, n)
+    cache = device_cache(s, SRC(seed, kvsynth.MODE_RAW), DEV)
+    mirror = host_mirror(s, SRC(seed, kvsynth.MODE_RAW), np.concatenate([bt_src, bt_dst]))
+    expect = oracle.gather(s, *mirror, 0, 2, bt_src, 48)
+    dst = _packed(expect.size)
+    kvx.kvx_gather_blocks(cache, 0, 2, _bt(bt_src), n, 48, dst)
+    _sync_check()
+    assert np.array_equal(to_host(dst)[:expect.size], expect)
+    before = _clone(cache)
+    kvx.kvx_scatter_blocks(cache, 0, 2, _bt(bt_dst), n, 48, dst)
+    _sync_check()
+    oracle.scatter(s, *mirror, 0, 2, bt_dst, 48, expect)
+    _compare_paged(cache, s, mirror, range(2), bt_dst, "ordered scatter")
+    _untouched_equal(cache, before, s, {0, 1}, bt_dst, "ordered scatter")
+
+
+def test_ordered_scatter_with_bad_ids_skips_only_those():
+    s = oracle.Shape(2, 6000, 16, 2, 64, 2)
+    n = 2000
+    bt, spare = seeded_ids(9, s.num_blocks, n, 3)
+    bad_pos = [5, 777, 1999]
+    bad = bt.copy()
+    bad[bad_pos] = [6000, -3, 2**31 - 1]
+    cache = device_cache(s, BKG(9), DEV)
+    before = _clone(cache)
+    img = kvsynth.host_bytes(oracle.packed_bytes(s, 0, 2, n), 9, 11)
+    kvx.kvx_scatter_blocks(cache, 0, 2, _bt(bad), n, 32, torch.from_numpy(img).to(DEV))
+    torch.cuda.synchronize()
+    with pytest.raises(kvx.KvxError) as ei:
+        kvx.kvx_check()
+    assert ei.value.status == kvx.KVX_EBADBLOCK
+    good = np.delete(bt, bad_pos)
+    _untouched_equal(cache, before, s, {0, 1}, good, "bad-id ordered scatter")
+    # Oracle: the same scatter with each bad id replaced by a spare block; the
+    # valid destinations must match it (the spares' units were skipped on the GPU).
+    mirror = host_mirror(s, BKG(9), range(s.num_blocks))
+    subst = bt.copy()
+    subst[bad_pos] = spare
+    oracle.scatter(s, *mirror, 0, 2, subst, 32, img)
+    _compare_paged(cache, s, mirror, range(2), good, "bad-id ordered scatter")
