@@ -124,9 +124,48 @@ kvx_status kvx_scatter_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
                               const int32_t* block_table, int32_t n_blocks, int32_t chunk_tokens,
                               const void* src, hipStream_t stream);
 
+/* ---- batched chunk lists (several requests in one launch) ------------------ */
+
+/* One chunk of a batch: the packed image of blocks block_table[bt_offset ..
+ * bt_offset + n_blocks) over the call's layer range, laid out as one chunk
+ * (1 <= n_blocks <= chunk_tokens / block_size), at byte packed_offset of the
+ * packed buffer (16-byte aligned). Chunks may come from different requests
+ * and sit anywhere in the packed buffer; they must not overlap there. */
+typedef struct kvx_chunk_ref {
+  int64_t packed_offset;
+  int32_t bt_offset;
+  int32_t n_blocks;
+} kvx_chunk_ref;
+
+/* Batched gather: every chunk of `chunks` (a device array of n_chunks refs) is
+ * gathered into the packed buffer in one launch. This is the paper's fused
+ * batched block copy: the ready mappings of several requests moved by a single
+ * launch (Sec. 6.4).
+ *   block_table  device int32[table_len]
+ *   packed       device, 16-byte aligned, packed_bytes bytes; must not
+ *                overlap any cache tensor
+ * Host-checkable errors as for kvx_gather_blocks (KVX_EINVAL), plus a launch
+ * too large for 32-bit unit indexes (n_chunks * (l1 - l0) * 2 * blocks per
+ * chunk >= 2^31). The refs live on the device and are checked by the kernel:
+ * a ref with n_blocks out of range, a block-table slice past table_len, or an
+ * image that is misaligned or does not fit in packed_bytes is skipped and
+ * makes kvx_check return KVX_EINVAL. Bad block ids: KVX_EBADBLOCK. */
+kvx_status kvx_gather_chunks(const kvx_cache* cache, int32_t l0, int32_t l1,
+                             const int32_t* block_table, int32_t table_len,
+                             const kvx_chunk_ref* chunks, int32_t n_chunks, int32_t chunk_tokens,
+                             void* packed, int64_t packed_bytes, hipStream_t stream);
+
+/* Batched scatter: the inverse of kvx_gather_chunks. Destinations of all
+ * chunks must be distinct. */
+kvx_status kvx_scatter_chunks(const kvx_cache* cache, int32_t l0, int32_t l1,
+                              const int32_t* block_table, int32_t table_len,
+                              const kvx_chunk_ref* chunks, int32_t n_chunks, int32_t chunk_tokens,
+                              const void* packed, int64_t packed_bytes, hipStream_t stream);
+
 /* Wait for `stream`, then read and clear the calling device's sticky error
- * flag: KVX_EBADBLOCK if any kernel since the last check met a bad block id,
- * KVX_EHIP if the stream reported an error, else KVX_OK. */
+ * flag: KVX_EINVAL if a kernel met an invalid device-resident chunk
+ * reference, else KVX_EBADBLOCK if one met a bad block id, KVX_EHIP if the
+ * stream reported an error, else KVX_OK. */
 kvx_status kvx_check(hipStream_t stream);
 
 const char* kvx_strerror(kvx_status status);
@@ -197,12 +236,54 @@ kvx_status kvx_ring_bind(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int
 kvx_status kvx_restore_from_staging(kvx_ring* ring, const int32_t* block_table,
                                     hipStream_t stream);
 
+/* A chunk image in host memory: the packed image of one chunk (layout above,
+ * over the binding's layer range) of the blocks block_table[bt_offset ..
+ * bt_offset + n_blocks), 1 <= n_blocks <= chunk_tokens / block_size. For a
+ * restore, host is the source (stands in for the storage read); for an
+ * offload, the destination (stands in for the storage write). */
+typedef struct kvx_host_chunk {
+  void* host;
+  int32_t bt_offset;
+  int32_t n_blocks;
+} kvx_host_chunk;
+
+/* Bind the next restores to a list of chunk images, each at its own host
+ * address (the deduplicated chunks of several requests, Sec. 6.5: identical
+ * prefixes share one read). Pieces pack consecutive chunks into slots; every
+ * piece is scattered by one fused chunk-list launch. The block table passed to
+ * kvx_restore_from_staging must hold at least max(bt_offset + n_blocks)
+ * entries. fill_threads as for kvx_ring_bind (0: the chunk images must be
+ * pinned). Waits until the ring's previous transfer has finished on the
+ * device (its chunk table is replaced). */
+kvx_status kvx_ring_bind_chunks(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int32_t l1,
+                                int32_t chunk_tokens, const kvx_host_chunk* chunks,
+                                int32_t n_chunks, int32_t fill_threads);
+
+/* Bind the next offloads: the store path, the mirror of a restore (Sec. 6.4,
+ * stores use the reverse pipeline). Each chunk's blocks are gathered and its
+ * image written to the chunk's host address. drain_threads (1..64) copy
+ * staging slots to the destinations; 0 copies device slots straight into the
+ * destinations, which must then be pinned. */
+kvx_status kvx_ring_bind_offload(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int32_t l1,
+                                 int32_t chunk_tokens, const kvx_host_chunk* chunks,
+                                 int32_t n_chunks, int32_t drain_threads);
+
+/* Offload the bound chunks, reading the blocks named by block_table (device).
+ * For piece i on slot s = i mod n_slots: `stream` waits until device slot s is
+ * no longer read by the copy of piece i - n_slots, gathers the piece into it
+ * (one fused launch) and records an event; the side stream waits on it and
+ * copies device slot s to host slot s once the drain threads have emptied
+ * host slot s; drain threads copy host slot s to the chunks' destinations once
+ * that copy has completed. Returns when every destination holds its image (it
+ * waits for the device). KVX_ECLOSED after kvx_ring_abort. */
+kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hipStream_t stream);
+
 typedef struct kvx_ring_stats {
-  int64_t pieces;         /* pieces moved by the last restore */
-  int64_t bytes;          /* image bytes moved by the last restore */
-  double fill_ms;         /* summed fill-thread copy time */
-  double wait_fill_ms;    /* time the enqueuing thread waited for fills */
-  double enqueue_ms;      /* wall time of the last kvx_restore_from_staging */
+  int64_t pieces;         /* pieces moved by the last restore or offload */
+  int64_t bytes;          /* image bytes moved by it */
+  double fill_ms;         /* summed fill (restore) or drain (offload) thread copy time */
+  double wait_fill_ms;    /* time the enqueuing thread waited for fill or drain threads */
+  double enqueue_ms;      /* wall time of the last restore or offload call */
 } kvx_ring_stats;
 
 kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out);
@@ -214,6 +295,23 @@ kvx_status kvx_ring_abort(kvx_ring* ring);
 /* Wait for the ring's side stream and last restore, then free everything the
  * ring owns. */
 kvx_status kvx_ring_destroy(kvx_ring* ring);
+
+/* ---- step planning (host) ---------------------------------------------------- */
+
+/* Prefix-hash chain (Sec. 2.1): out[b] = hash of full block b of `tokens`,
+ * covering that block's block_size tokens and the hash of block b - 1
+ * (parent_hash for block 0, e.g. 0 at the start of a prompt). Equal hashes mean
+ * equal token prefixes through that block, so the hash of a chunk's last block
+ * identifies the chunk. A trailing partial block gets no hash (partial blocks
+ * are never cached). Returns the number of full blocks (n_tokens / block_size)
+ * written to out, or -1 on a bad argument. Pure host code. */
+int64_t kvx_block_hashes(const int32_t* tokens, int64_t n_tokens, int32_t block_size,
+                         uint64_t parent_hash, uint64_t* out);
+
+/* Chunk dedupe (Sec. 6.5: identical prefixes share one read): first_of[i] =
+ * the smallest j with keys[j] == keys[i]; chunk i is restored itself iff
+ * first_of[i] == i. Pure host code. */
+kvx_status kvx_dedupe_keys(const uint64_t* keys, int32_t n, int32_t* first_of);
 
 /* Pinned host memory of exactly `bytes` (hipHostMalloc), for host images. */
 kvx_status kvx_pinned_alloc(int64_t bytes, void** out);

@@ -18,7 +18,7 @@ from __future__ import annotations
 import ctypes
 
 from . import _native
-from ._native import KvxCache, KvxPiece, KvxRingStats
+from ._native import KvxCache, KvxChunkRef, KvxHostChunk, KvxPiece, KvxRingStats
 
 KVX_OK, KVX_EINVAL, KVX_ENOMEM, KVX_EHIP, KVX_EBADBLOCK, KVX_ECLOSED, KVX_EINTERNAL = (
     0, -1, -2, -3, -4, -5, -6)
@@ -172,6 +172,52 @@ def kvx_scatter_blocks(cache: PagedKVCache, l0, l1, block_table, n_blocks, chunk
     _ok(st, "kvx_scatter_blocks")
 
 
+CHUNK_REF_DTYPE = [("packed_offset", "<i8"), ("bt_offset", "<i4"), ("n_blocks", "<i4")]
+
+
+def chunk_refs(refs, device):
+    """Device array of kvx_chunk_ref from (packed_offset, bt_offset, n_blocks) rows."""
+    import numpy as np
+    import torch
+
+    a = np.zeros(len(refs), dtype=CHUNK_REF_DTYPE)
+    for i, (off, bt0, nb) in enumerate(refs):
+        a[i] = (off, bt0, nb)
+    return torch.from_numpy(a.view(np.uint8).copy()).to(device)
+
+
+def _chunks_call(fn, cache, l0, l1, block_table, table_len, refs_dev, n_chunks, chunk_tokens,
+                 packed, stream, where):
+    import torch
+
+    if n_chunks > 0:
+        if refs_dev.device != cache.device or refs_dev.numel() * refs_dev.element_size() < 16 * n_chunks:
+            raise ValueError("chunk refs must be a device buffer of n_chunks kvx_chunk_ref")
+        if block_table.dtype != torch.int32 or block_table.numel() < table_len:
+            raise ValueError("block_table must be int32 with at least table_len entries")
+        if packed.device != cache.device or not packed.is_contiguous():
+            raise ValueError("packed buffer must be contiguous on the cache's device")
+    nbytes = packed.numel() * packed.element_size() if packed is not None else 0
+    st = fn(ctypes.byref(cache.c_struct()), l0, l1,
+            block_table.data_ptr() if block_table is not None else None, table_len,
+            refs_dev.data_ptr() if refs_dev is not None else None, n_chunks, chunk_tokens,
+            packed.data_ptr() if packed is not None else None, nbytes, _stream_handle(stream))
+    _ok(st, where)
+
+
+def kvx_gather_chunks(cache, l0, l1, block_table, table_len, refs_dev, n_chunks, chunk_tokens,
+                      packed, stream=None) -> None:
+    """Fused batched gather of a chunk list (refs_dev from chunk_refs())."""
+    _chunks_call(_native.lib().kvx_gather_chunks, cache, l0, l1, block_table, table_len,
+                 refs_dev, n_chunks, chunk_tokens, packed, stream, "kvx_gather_chunks")
+
+
+def kvx_scatter_chunks(cache, l0, l1, block_table, table_len, refs_dev, n_chunks, chunk_tokens,
+                       packed, stream=None) -> None:
+    _chunks_call(_native.lib().kvx_scatter_chunks, cache, l0, l1, block_table, table_len,
+                 refs_dev, n_chunks, chunk_tokens, packed, stream, "kvx_scatter_chunks")
+
+
 def kvx_check(stream=None) -> None:
     _ok(_native.lib().kvx_check(_stream_handle(stream)), "kvx_check")
 
@@ -260,6 +306,41 @@ class StagingRing:
         self._cache = cache
         self.n_blocks = n_blocks
 
+    def _host_chunks(self, chunks):
+        arr = (KvxHostChunk * max(len(chunks), 1))()
+        keep = []
+        for i, (buf, bt0, nb) in enumerate(chunks):
+            if isinstance(buf, int):
+                ptr = buf
+            elif isinstance(buf, PinnedBuffer):
+                ptr = buf.ptr
+            else:
+                if not buf.flags["C_CONTIGUOUS"]:
+                    raise ValueError("host chunk buffers must be contiguous")
+                ptr = buf.ctypes.data
+            keep.append(buf)
+            arr[i] = KvxHostChunk(ptr, bt0, nb)
+        return arr, keep
+
+    def bind_chunks(self, cache, l0, l1, chunk_tokens, chunks, fill_threads=4):
+        """Restore binding over a chunk list [(host image, bt_offset, n_blocks)];
+        a host image is a numpy uint8 array, a PinnedBuffer or a raw address."""
+        arr, keep = self._host_chunks(chunks)
+        _ok(_native.lib().kvx_ring_bind_chunks(self.handle, ctypes.byref(cache.c_struct()), l0, l1,
+                                               chunk_tokens, arr, len(chunks), fill_threads),
+            "kvx_ring_bind_chunks")
+        self._source, self._cache = keep, cache
+        self.n_blocks = max((bt0 + nb for _, bt0, nb in chunks), default=0)
+
+    def bind_offload(self, cache, l0, l1, chunk_tokens, chunks, drain_threads=4):
+        """Offload binding over a chunk list [(host destination, bt_offset, n_blocks)]."""
+        arr, keep = self._host_chunks(chunks)
+        _ok(_native.lib().kvx_ring_bind_offload(self.handle, ctypes.byref(cache.c_struct()), l0,
+                                                l1, chunk_tokens, arr, len(chunks), drain_threads),
+            "kvx_ring_bind_offload")
+        self._source, self._cache = keep, cache
+        self.n_blocks = max((bt0 + nb for _, bt0, nb in chunks), default=0)
+
     def stats(self) -> dict:
         s = KvxRingStats()
         _ok(_native.lib().kvx_ring_stats_get(self.handle, ctypes.byref(s)), "kvx_ring_stats_get")
@@ -286,8 +367,40 @@ def kvx_restore_from_staging(ring: StagingRing, block_table, stream=None) -> Non
     _ok(st, "kvx_restore_from_staging")
 
 
+def kvx_block_hashes(tokens, block_size, parent_hash=0):
+    """Prefix-hash chain over the full blocks of `tokens` (numpy int32 array)."""
+    import numpy as np
+
+    t = np.ascontiguousarray(tokens, dtype=np.int32)
+    out = np.empty(max(t.size // block_size, 1), dtype=np.uint64)
+    n = _native.lib().kvx_block_hashes(t.ctypes.data if t.size else None, t.size, block_size,
+                                       parent_hash & (2**64 - 1), out.ctypes.data)
+    if n < 0:
+        raise KvxError(KVX_EINVAL, "kvx_block_hashes")
+    return out[:n]
+
+
+def kvx_dedupe_keys(keys):
+    """first_of[i] = index of the first occurrence of keys[i]."""
+    import numpy as np
+
+    k = np.ascontiguousarray(keys, dtype=np.uint64)
+    first = np.empty(max(k.size, 1), dtype=np.int32)
+    _ok(_native.lib().kvx_dedupe_keys(k.ctypes.data if k.size else None, k.size, first.ctypes.data),
+        "kvx_dedupe_keys")
+    return first[:k.size]
+
+
+def kvx_offload_to_staging(ring: StagingRing, block_table, stream=None) -> None:
+    ptr = _table_ptr(ring._cache, block_table, ring.n_blocks) if ring._cache is not None else None
+    st = _native.lib().kvx_offload_to_staging(ring.handle, ptr, _stream_handle(stream))
+    _ok(st, "kvx_offload_to_staging")
+
+
 __all__ = [
     "KvxError", "PagedKVCache", "PinnedBuffer", "StagingRing", "kvx_bytes_per_token",
     "kvx_packed_bytes", "kvx_gather_blocks", "kvx_scatter_blocks", "kvx_check",
     "kvx_plan_pieces", "kvx_restore_from_staging", "shape_only_cache", "KVX_MAX_LAYERS",
+    "kvx_gather_chunks", "kvx_scatter_chunks", "chunk_refs", "kvx_offload_to_staging",
+    "kvx_block_hashes", "kvx_dedupe_keys",
 ]

@@ -22,6 +22,14 @@ class KvxPiece(ctypes.Structure):
                 ("chunk_tokens", c_i32), ("reserved", c_i32)]
 
 
+class KvxChunkRef(ctypes.Structure):
+    _fields_ = [("packed_offset", c_i64), ("bt_offset", c_i32), ("n_blocks", c_i32)]
+
+
+class KvxHostChunk(ctypes.Structure):
+    _fields_ = [("host", c_vp), ("bt_offset", c_i32), ("n_blocks", c_i32)]
+
+
 class KvxRingStats(ctypes.Structure):
     _fields_ = [("pieces", c_i64), ("bytes", c_i64), ("fill_ms", ctypes.c_double),
                 ("wait_fill_ms", ctypes.c_double), ("enqueue_ms", ctypes.c_double)]
@@ -35,6 +43,10 @@ SIGNATURES = {
                                          c_i32, c_vp, c_vp]),
     "kvx_scatter_blocks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
                                           c_i32, c_vp, c_vp]),
+    "kvx_gather_chunks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
+                                         c_vp, c_i32, c_i32, c_vp, c_i64, c_vp]),
+    "kvx_scatter_chunks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
+                                          c_vp, c_i32, c_i32, c_vp, c_i64, c_vp]),
     "kvx_check": (ctypes.c_int, [c_vp]),
     "kvx_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "kvx_plan_pieces": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32, c_i32,
@@ -44,9 +56,16 @@ SIGNATURES = {
     "kvx_ring_bind": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32, c_i32,
                                      c_vp, c_i32]),
     "kvx_restore_from_staging": (ctypes.c_int, [c_vp, c_vp, c_vp]),
+    "kvx_ring_bind_chunks": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32,
+                                            ctypes.POINTER(KvxHostChunk), c_i32, c_i32]),
+    "kvx_ring_bind_offload": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32,
+                                             ctypes.POINTER(KvxHostChunk), c_i32, c_i32]),
+    "kvx_offload_to_staging": (ctypes.c_int, [c_vp, c_vp, c_vp]),
     "kvx_ring_stats_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxRingStats)]),
     "kvx_ring_abort": (ctypes.c_int, [c_vp]),
     "kvx_ring_destroy": (ctypes.c_int, [c_vp]),
+    "kvx_block_hashes": (c_i64, [c_vp, c_i64, c_i32, ctypes.c_uint64, c_vp]),
+    "kvx_dedupe_keys": (ctypes.c_int, [c_vp, c_i32, c_vp]),
     "kvx_pinned_alloc": (ctypes.c_int, [c_i64, ctypes.POINTER(c_vp)]),
     "kvx_pinned_free": (ctypes.c_int, [c_vp]),
 }

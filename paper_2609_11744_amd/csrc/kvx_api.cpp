@@ -86,6 +86,30 @@ static kvx_status copy_entry(bool to_packed, const kvx_cache* cache, int32_t l0,
   return launch_copy(to_packed, cache, l0, l1, block_table, g, const_cast<void*>(packed), stream);
 }
 
+static kvx_status chunks_entry(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
+                               const int32_t* block_table, int32_t table_len,
+                               const kvx_chunk_ref* chunks, int32_t n_chunks,
+                               int32_t chunk_tokens, const void* packed, int64_t packed_bytes,
+                               hipStream_t stream) {
+  Geometry g;
+  kvx_status st = validate(cache, l0, l1, 0, chunk_tokens, false, &g);
+  if (st != KVX_OK) return st;
+  if (n_chunks < 0 || table_len < 0) return KVX_EINVAL;
+  if (n_chunks == 0 || l0 == l1) return KVX_OK;
+  if (!chunks || !packed || ((uintptr_t)packed & 15) || packed_bytes <= 0) return KVX_EINVAL;
+  if (table_len > 0 && !block_table) return KVX_EINVAL;
+  if (!cache->k || !cache->v) return KVX_EINVAL;
+  for (int32_t l = l0; l < l1; ++l) {
+    if (!cache->k[l] || !cache->v[l]) return KVX_EINVAL;
+    if (((uintptr_t)cache->k[l] | (uintptr_t)cache->v[l]) & 15) return KVX_EINVAL;
+  }
+  const int64_t units = (int64_t)n_chunks * (l1 - l0) * 2 * (chunk_tokens / cache->block_size);
+  if (units > INT32_MAX) return KVX_EINVAL;
+  if (overlaps_cache(cache, l0, l1, packed, packed_bytes)) return KVX_EINVAL;
+  return launch_copy_chunks(to_packed, cache, l0, l1, block_table, table_len, chunks, n_chunks,
+                            chunk_tokens, const_cast<void*>(packed), packed_bytes, stream);
+}
+
 }  // namespace kvx
 
 extern "C" {
@@ -123,6 +147,30 @@ kvx_status kvx_scatter_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
   }
 }
 
+kvx_status kvx_gather_chunks(const kvx_cache* cache, int32_t l0, int32_t l1,
+                             const int32_t* block_table, int32_t table_len,
+                             const kvx_chunk_ref* chunks, int32_t n_chunks, int32_t chunk_tokens,
+                             void* packed, int64_t packed_bytes, hipStream_t stream) {
+  try {
+    return kvx::chunks_entry(true, cache, l0, l1, block_table, table_len, chunks, n_chunks,
+                             chunk_tokens, packed, packed_bytes, stream);
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}
+
+kvx_status kvx_scatter_chunks(const kvx_cache* cache, int32_t l0, int32_t l1,
+                              const int32_t* block_table, int32_t table_len,
+                              const kvx_chunk_ref* chunks, int32_t n_chunks, int32_t chunk_tokens,
+                              const void* packed, int64_t packed_bytes, hipStream_t stream) {
+  try {
+    return kvx::chunks_entry(false, cache, l0, l1, block_table, table_len, chunks, n_chunks,
+                             chunk_tokens, packed, packed_bytes, stream);
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}
+
 kvx_status kvx_check(hipStream_t stream) {
   if (hipStreamSynchronize(stream) != hipSuccess) return KVX_EHIP;
   int* w = kvx::device_error_word();
@@ -132,7 +180,7 @@ kvx_status kvx_check(hipStream_t stream) {
   if (v != 0) {
     const int zero = 0;
     if (hipMemcpy(w, &zero, sizeof(int), hipMemcpyHostToDevice) != hipSuccess) return KVX_EHIP;
-    return KVX_EBADBLOCK;
+    return (v & 2) ? KVX_EINVAL : KVX_EBADBLOCK;  // bit 1: bad chunk ref, bit 0: bad block id
   }
   return KVX_OK;
 }

@@ -42,10 +42,51 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
                        const int32_t* block_table, const Geometry& g, void* packed,
                        hipStream_t stream);
 
-// Cut the image described by g (over layers [l0, l1)) into staging pieces of
-// at most slot_bytes each (kvx_plan_pieces).
-kvx_status plan_pieces(const Geometry& g, int32_t l0, int32_t l1, int32_t block_size,
-                       int64_t slot_bytes, std::vector<kvx_piece>* out);
+// Enqueue the chunk-list gather (to_packed) or scatter on `stream`: refs is a
+// device array of n_chunks references, validated by the kernel against
+// table_len and packed_bytes. Host-checkable arguments must already be valid.
+kvx_status launch_copy_chunks(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
+                              const int32_t* block_table, int32_t table_len,
+                              const kvx_chunk_ref* refs, int32_t n_chunks, int32_t chunk_tokens,
+                              void* packed, int64_t packed_bytes, hipStream_t stream);
+
+// A chunk image in host memory (restore source or offload destination) and the
+// block-table slice it belongs to.
+struct HostChunk {
+  uint8_t* host;
+  int32_t bt_offset;
+  int32_t n_blocks;
+};
+
+// Host memory <-> staging-slot bytes [slot_off, slot_off + bytes).
+struct Span {
+  uint8_t* host;
+  int64_t bytes;
+  int64_t slot_off;
+};
+
+// One staging piece: a fused chunk-list copy over layers [l_begin, l_end) of
+// the chunk references refs[ref_first, ref_first + ref_count) (packed offsets
+// relative to the slot), filled from / drained to `spans`.
+struct Piece {
+  int32_t l_begin = 0, l_end = 0;
+  int64_t bytes = 0;
+  int32_t ref_first = 0, ref_count = 0;
+  std::vector<Span> spans;
+};
+
+struct Plan {
+  std::vector<Piece> pieces;
+  std::vector<kvx_chunk_ref> refs;
+  int32_t table_len = 0;  // block-table entries the chunks reference
+};
+
+// Cut a chunk list into staging pieces of at most slot_bytes (see kvx_plan.cpp).
+kvx_status plan_chunks(const std::vector<HostChunk>& chunks, int32_t l0, int32_t l1, int64_t slab,
+                       int32_t bpc, int64_t slot_bytes, Plan* out);
+
+// The chunks of one contiguous packed image at `base` (geometry g).
+std::vector<HostChunk> image_chunks(uint8_t* base, const Geometry& g);
 
 // Device address of the calling device's sticky error word (resolved once per
 // device with hipGetSymbolAddress). Null on failure.

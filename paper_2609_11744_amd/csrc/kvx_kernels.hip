@@ -39,6 +39,7 @@ namespace {
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
 constexpr int kErrBadBlock = 1;
+constexpr int kErrBadChunk = 2;
 constexpr unsigned kXcds = 8;  // MI355X: 8 XCDs, workgroups dispatched round-robin
 
 // Device pointers of the call's layers, in image order: p[2 * (l - l0) + kv].
@@ -122,6 +123,60 @@ __global__ void __launch_bounds__(T)
   }
   char* paged = layers.p[lk] + (uint64_t)(uint32_t)id * g.slab;
   char* pk = packed + (uint64_t)u * g.slab;
+  if (kToPacked)
+    move_slab<T, V>(reinterpret_cast<const v4u*>(paged), reinterpret_cast<v4u*>(pk), g.n16);
+  else
+    move_slab<T, V>(reinterpret_cast<const v4u*>(pk), reinterpret_cast<v4u*>(paged), g.n16);
+}
+
+// Chunk-list copy: a batch of chunks, each with its own block-table slice and
+// its own place in the packed buffer (the fused block copy of several
+// requests' chunks in one launch). Unit space is padded: chunk c owns units
+// [c * upc, (c + 1) * upc) with upc = (l1 - l0) * 2 * bpc, unit r of a chunk
+// is (lk = r / bpc, j = r % bpc), and units with j >= the chunk's n_blocks
+// exit at once. So a workgroup finds its chunk by one division, with no
+// search. Each reference is validated here (it lives in device memory): a bad
+// one sets kErrBadChunk and its units are skipped.
+struct ChunkGeom {
+  uint32_t upc;          // (l1 - l0) * 2 * bpc
+  uint32_t bpc;
+  uint32_t lr2;          // (l1 - l0) * 2
+  uint32_t num_blocks;   // pool size
+  uint32_t n16;
+  int32_t table_len;
+  uint64_t slab;
+  int64_t packed_bytes;
+};
+
+template <bool kToPacked, int T, int V>
+__global__ void __launch_bounds__(T)
+    copy_chunks_kernel(LayerPtrs layers, const int32_t* __restrict__ block_table,
+                       const kvx_chunk_ref* __restrict__ refs, ChunkGeom g, uint32_t unit_base,
+                       uint32_t unit_count, char* __restrict__ packed, int* __restrict__ err) {
+  const uint32_t u = unit_base + xcd_contiguous(blockIdx.x, unit_count);
+  const uint32_t c = u / g.upc;
+  const uint32_t r = u - c * g.upc;
+  const uint32_t lk = r / g.bpc;
+  const uint32_t j = r - lk * g.bpc;
+  const kvx_chunk_ref ref = refs[c];
+  const bool ok = ref.n_blocks >= 1 && (uint32_t)ref.n_blocks <= g.bpc && ref.bt_offset >= 0 &&
+                  (int64_t)ref.bt_offset + ref.n_blocks <= (int64_t)g.table_len &&
+                  ref.packed_offset >= 0 && (ref.packed_offset & 15) == 0 &&
+                  ref.packed_offset + (int64_t)g.lr2 * ref.n_blocks * (int64_t)g.slab <=
+                      g.packed_bytes;
+  if (!ok) {
+    if (r == 0 && threadIdx.x == 0) atomicOr(err, kErrBadChunk);
+    return;
+  }
+  const uint32_t nc = (uint32_t)ref.n_blocks;
+  if (j >= nc) return;  // padding unit
+  const int32_t id = block_table[ref.bt_offset + j];
+  if ((uint32_t)id >= g.num_blocks) {
+    if (threadIdx.x == 0) atomicOr(err, kErrBadBlock);
+    return;
+  }
+  char* paged = layers.p[lk] + (uint64_t)(uint32_t)id * g.slab;
+  char* pk = packed + ref.packed_offset + (uint64_t)(lk * nc + j) * g.slab;
   if (kToPacked)
     move_slab<T, V>(reinterpret_cast<const v4u*>(paged), reinterpret_cast<v4u*>(pk), g.n16);
   else
@@ -216,6 +271,28 @@ hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, ui
   return hipSuccess;
 }
 
+template <bool kToPacked>
+hipError_t launch_chunks(const LayerPtrs& lp, const int32_t* bt, const kvx_chunk_ref* refs,
+                         const ChunkGeom& cg, uint32_t n_units, char* packed, int* err,
+                         hipStream_t stream) {
+  for (uint32_t base = 0; base < n_units; base += kMaxUnitsPerLaunch) {
+    const uint32_t cnt = n_units - base < kMaxUnitsPerLaunch ? n_units - base : kMaxUnitsPerLaunch;
+    const dim3 grid(cnt);
+    if (cg.n16 % (2 * 1024) == 0)
+      hipLaunchKernelGGL((copy_chunks_kernel<kToPacked, 1024, 2>), grid, dim3(1024), 0, stream,
+                         lp, bt, refs, cg, base, cnt, packed, err);
+    else if (cg.n16 % (4 * 256) == 0)
+      hipLaunchKernelGGL((copy_chunks_kernel<kToPacked, 256, 4>), grid, dim3(256), 0, stream, lp,
+                         bt, refs, cg, base, cnt, packed, err);
+    else
+      hipLaunchKernelGGL((copy_chunks_kernel<kToPacked, 256, 1>), grid, dim3(256), 0, stream, lp,
+                         bt, refs, cg, base, cnt, packed, err);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
 }  // namespace
 
 int* device_error_word() {
@@ -277,6 +354,40 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   } else {
     e = launch<false, false>(lp, block_table, ug, n_units, nullptr, (char*)packed, err, stream);
   }
+  return e == hipSuccess ? KVX_OK : KVX_EHIP;
+}
+
+kvx_status launch_copy_chunks(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
+                              const int32_t* block_table, int32_t table_len,
+                              const kvx_chunk_ref* refs, int32_t n_chunks, int32_t chunk_tokens,
+                              void* packed, int64_t packed_bytes, hipStream_t stream) {
+  if (n_chunks <= 0 || l1 <= l0) return KVX_OK;
+  int* err = device_error_word();
+  if (!err) return KVX_EHIP;
+  const int64_t slab = (int64_t)cache->block_size * cache->num_kv_heads * cache->head_dim *
+                       cache->elem_bytes;
+  const int64_t bpc = chunk_tokens / cache->block_size;
+  const int64_t upc = (int64_t)(l1 - l0) * 2 * bpc;
+  const int64_t n_units = upc * n_chunks;
+  if (bpc <= 0 || n_units > 0x7FFFFFFF || slab % 16 != 0) return KVX_EINTERNAL;
+  LayerPtrs lp = {};
+  for (int32_t l = l0; l < l1; ++l) {
+    lp.p[2 * (l - l0)] = static_cast<char*>(cache->k[l]);
+    lp.p[2 * (l - l0) + 1] = static_cast<char*>(cache->v[l]);
+  }
+  ChunkGeom cg;
+  cg.upc = (uint32_t)upc;
+  cg.bpc = (uint32_t)bpc;
+  cg.lr2 = (uint32_t)(2 * (l1 - l0));
+  cg.num_blocks = (uint32_t)cache->num_blocks;
+  cg.n16 = (uint32_t)(slab / 16);
+  cg.table_len = table_len;
+  cg.slab = (uint64_t)slab;
+  cg.packed_bytes = packed_bytes;
+  hipError_t e = to_packed ? launch_chunks<true>(lp, block_table, refs, cg, (uint32_t)n_units,
+                                                 (char*)packed, err, stream)
+                           : launch_chunks<false>(lp, block_table, refs, cg, (uint32_t)n_units,
+                                                  (char*)packed, err, stream);
   return e == hipSuccess ? KVX_OK : KVX_EHIP;
 }
 

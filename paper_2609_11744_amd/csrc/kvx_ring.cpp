@@ -1,19 +1,28 @@
-// Bounded pinned staging ring and the staged restore (Sec. 6.4: one
-// contiguous, aligned, pinned host allocation cut into fixed slots; a
-// transfer larger than the pool moves piece by piece; a slot is reused only
-// after the device event of the copy that read it has completed).
+// Bounded pinned staging ring: the staged restore (load) and the staged
+// offload (store) of Sec. 6.4. The pool is one contiguous, aligned, pinned
+// host allocation cut into fixed slots; a transfer larger than the pool moves
+// piece by piece; a slot is reused only after the device event of the copy
+// that last used it has completed. Stores use the reverse pipeline.
 //
-// Pipeline for piece i on slot s = i mod n_slots:
-//   fill   host threads copy image bytes into host slot s, after the H2D copy
-//          of piece i - n_slots (which read host slot s) has completed;
-//   H2D    the side stream waits until the scatter of piece i - n_slots has
-//          read device slot s, copies host slot s to device slot s, records
-//          h2d_done[s];
-//   scatter the caller's stream waits on h2d_done[s], runs the scatter kernel
-//          from device slot s, records scatter_done[s].
-// So the fill of piece i + 2, the H2D of piece i + 1 and the scatter of piece
-// i overlap. The enqueuing thread never waits for the device; fill threads
-// wait on h2d_done events (blocking-sync events, so they sleep).
+// Restore, piece i on slot s = i mod n_slots:
+//   fill    host threads copy the piece's chunk images into host slot s, after
+//           the H2D copy of piece i - n_slots (which read host slot s) is done;
+//   H2D     the side stream waits until device slot s is free (the scatter of
+//           piece i - n_slots has read it), copies host slot s to device slot
+//           s and records copy_done[s];
+//   scatter the caller's stream waits on copy_done[s], runs one fused
+//           chunk-list scatter from device slot s, records dev_done[s].
+// Offload, piece i on slot s:
+//   gather  the caller's stream waits on copy_done[s] (the D2H copy of piece
+//           i - n_slots has read device slot s), runs one fused chunk-list
+//           gather into device slot s, records dev_done[s];
+//   D2H     once the drain threads have emptied host slot s, the side stream
+//           waits on dev_done[s], copies device slot s to host slot s and
+//           records copy_done[s];
+//   drain   host threads wait on copy_done[s] and copy host slot s to the
+//           chunks' destinations.
+// The enqueuing thread never waits for the device in a restore; fill and
+// drain threads wait on copy_done events (blocking-sync events: they sleep).
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -30,6 +39,10 @@
 #include "kvx.h"
 #include "kvx_internal.h"
 
+namespace {
+enum class Dir { kNone, kRestore, kOffload };
+}
+
 struct kvx_ring {
   int device = 0;
   int32_t n_slots = 0;
@@ -38,28 +51,29 @@ struct kvx_ring {
   uint8_t* landing = nullptr;  // n_slots * slot_bytes device bytes
   bool owns_landing = false;
   hipStream_t side = nullptr;
-  std::vector<hipEvent_t> h2d_done;
-  std::vector<hipEvent_t> scatter_done;
+  std::vector<hipEvent_t> copy_done;  // H2D / D2H of the slot's last piece (host waits)
+  std::vector<hipEvent_t> dev_done;   // scatter / gather of the slot's last piece
 
   // binding
-  bool bound = false;
+  Dir dir = Dir::kNone;
   std::vector<void*> kptr, vptr;
   kvx_cache cache{};
-  int32_t l0 = 0, l1 = 0, n_blocks = 0, chunk_tokens = 0;
-  const uint8_t* source = nullptr;
-  int32_t fill_threads = 0;
-  std::vector<kvx_piece> pieces;
+  int32_t chunk_tokens = 0;
+  int32_t threads = 0;  // fill (restore) or drain (offload) threads
+  kvx::Plan plan;
+  kvx_chunk_ref* d_refs = nullptr;  // device copy of plan.refs
+  size_t d_refs_cap = 0;
 
-  // restore state: `closed` is set by kvx_ring_abort and stays set; `stop`
-  // ends the current restore (closed, or an internal failure).
+  // transfer state: `closed` is set by kvx_ring_abort and stays set; `stop`
+  // ends the current transfer (closed, or an internal failure).
   std::atomic<bool> closed{false};
   std::atomic<bool> stop{false};
   std::atomic<int> worker_error{0};
   std::mutex mu;
-  std::condition_variable cv_filled, cv_enqueued;
-  int64_t enqueued = 0;
-  std::vector<int32_t> parts_done;
-  std::atomic<int64_t> fill_ns{0};
+  std::condition_variable cv_host, cv_enqueued;
+  int64_t enqueued = 0;               // pieces whose slot copy is enqueued
+  std::vector<int32_t> parts_done;    // per piece: fill / drain parts finished
+  std::atomic<int64_t> busy_ns{0};
   kvx_ring_stats stats{};
 };
 
@@ -83,72 +97,130 @@ struct DeviceGuard {
   }
 };
 
-void destroy_resources(kvx_ring* r) {
+// Wait until nothing the ring enqueued can still touch its slots or tables.
+void drain_device(kvx_ring* r) {
   if (r->side) (void)hipStreamSynchronize(r->side);
-  for (hipEvent_t e : r->scatter_done)
-    if (e) { (void)hipEventSynchronize(e); (void)hipEventDestroy(e); }
-  for (hipEvent_t e : r->h2d_done)
-    if (e) { (void)hipEventSynchronize(e); (void)hipEventDestroy(e); }
-  r->scatter_done.clear();
-  r->h2d_done.clear();
+  for (hipEvent_t e : r->dev_done)
+    if (e) (void)hipEventSynchronize(e);
+  for (hipEvent_t e : r->copy_done)
+    if (e) (void)hipEventSynchronize(e);
+}
+
+void destroy_resources(kvx_ring* r) {
+  drain_device(r);
+  for (hipEvent_t e : r->dev_done)
+    if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : r->copy_done)
+    if (e) (void)hipEventDestroy(e);
+  r->dev_done.clear();
+  r->copy_done.clear();
   if (r->side) (void)hipStreamDestroy(r->side);
   r->side = nullptr;
   if (r->host) (void)hipHostFree(r->host);
   r->host = nullptr;
   if (r->owns_landing && r->landing) (void)hipFree(r->landing);
   r->landing = nullptr;
+  if (r->d_refs) (void)hipFree(r->d_refs);
+  r->d_refs = nullptr;
+  r->d_refs_cap = 0;
 }
 
-// Fill thread w of t: copies its share of every piece into the piece's slot.
+// Copy share w of T of a piece between host slot s and its spans.
+void copy_share(kvx_ring* r, const kvx::Piece& p, int32_t s, int w, int T, bool to_slot) {
+  int64_t per = (p.bytes + T - 1) / T;
+  per = (per + 4095) & ~(int64_t)4095;
+  const int64_t a = std::min<int64_t>(p.bytes, per * w);
+  const int64_t b = std::min<int64_t>(p.bytes, a + per);
+  uint8_t* slot = r->host + (int64_t)s * r->slot_bytes;
+  for (const kvx::Span& sp : p.spans) {
+    const int64_t lo = std::max<int64_t>(a, sp.slot_off);
+    const int64_t hi = std::min<int64_t>(b, sp.slot_off + sp.bytes);
+    if (hi <= lo) continue;
+    uint8_t* h = sp.host + (lo - sp.slot_off);
+    if (to_slot)
+      std::memcpy(slot + lo, h, (size_t)(hi - lo));
+    else
+      std::memcpy(h, slot + lo, (size_t)(hi - lo));
+  }
+}
+
+void signal_stop(kvx_ring* r) {
+  r->stop.store(true);
+  std::lock_guard<std::mutex> lock(r->mu);
+  r->cv_host.notify_all();
+  r->cv_enqueued.notify_all();
+}
+
+// Restore fill thread w: copies its share of every piece into the piece's slot.
 void fill_worker(kvx_ring* r, int w) {
-  const int32_t S = r->n_slots;
-  const int32_t T = r->fill_threads;
-  const int64_t P = (int64_t)r->pieces.size();
-  int64_t busy_ns = 0;
+  const int32_t S = r->n_slots, T = r->threads;
+  const int64_t P = (int64_t)r->plan.pieces.size();
+  int64_t busy = 0;
   for (int64_t i = 0; i < P; ++i) {
     const int32_t s = (int32_t)(i % S);
     if (i >= S) {
-      // h2d_done[s] must hold the record of piece i - S before we wait on it.
+      // copy_done[s] must hold the record of piece i - S before we wait on it.
       std::unique_lock<std::mutex> lock(r->mu);
       r->cv_enqueued.wait(lock, [&] { return r->enqueued > i - S || r->stop.load(); });
     }
     if (r->stop.load()) break;
-    if (hipEventSynchronize(r->h2d_done[s]) != hipSuccess) {
+    if (hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
       r->worker_error.store(1);
-      r->stop.store(true);
-      std::lock_guard<std::mutex> lock(r->mu);
-      r->cv_filled.notify_all();
-      r->cv_enqueued.notify_all();
+      signal_stop(r);
       break;
     }
-    const kvx_piece& p = r->pieces[(size_t)i];
-    int64_t per = (p.bytes + T - 1) / T;
-    per = (per + 4095) & ~(int64_t)4095;
-    const int64_t a = std::min<int64_t>(p.bytes, per * w);
-    const int64_t b = std::min<int64_t>(p.bytes, a + per);
-    if (b > a) {
-      auto t0 = clk::now();
-      std::memcpy(r->host + (int64_t)s * r->slot_bytes + a, r->source + p.src_offset + a,
-                  (size_t)(b - a));
-      busy_ns += std::chrono::duration_cast<std::chrono::nanoseconds>(clk::now() - t0).count();
-    }
+    auto t0 = clk::now();
+    copy_share(r, r->plan.pieces[(size_t)i], s, w, T, true);
+    busy += std::chrono::duration_cast<std::chrono::nanoseconds>(clk::now() - t0).count();
     std::lock_guard<std::mutex> lock(r->mu);
-    if (++r->parts_done[(size_t)i] == T) r->cv_filled.notify_all();
+    if (++r->parts_done[(size_t)i] == T) r->cv_host.notify_all();
   }
-  r->fill_ns.fetch_add(busy_ns);
+  r->busy_ns.fetch_add(busy);
 }
 
-kvx_status restore(kvx_ring* r, const int32_t* bt, hipStream_t stream) {
-  if (!r->bound) return KVX_EINVAL;
+// Offload drain thread w: copies its share of every piece out of its slot.
+void drain_worker(kvx_ring* r, int w) {
+  const int32_t S = r->n_slots, T = r->threads;
+  const int64_t P = (int64_t)r->plan.pieces.size();
+  int64_t busy = 0;
+  for (int64_t i = 0; i < P; ++i) {
+    const int32_t s = (int32_t)(i % S);
+    {
+      std::unique_lock<std::mutex> lock(r->mu);
+      r->cv_enqueued.wait(lock, [&] { return r->enqueued > i || r->stop.load(); });
+    }
+    if (r->stop.load()) break;
+    if (hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
+      r->worker_error.store(1);
+      signal_stop(r);
+      break;
+    }
+    auto t0 = clk::now();
+    copy_share(r, r->plan.pieces[(size_t)i], s, w, T, false);
+    busy += std::chrono::duration_cast<std::chrono::nanoseconds>(clk::now() - t0).count();
+    std::lock_guard<std::mutex> lock(r->mu);
+    if (++r->parts_done[(size_t)i] == T) r->cv_host.notify_all();
+  }
+  r->busy_ns.fetch_add(busy);
+}
+
+kvx_status launch_piece(kvx_ring* r, bool to_packed, const kvx::Piece& p, const int32_t* bt,
+                        uint8_t* dslot, hipStream_t stream) {
+  return kvx::launch_copy_chunks(to_packed, &r->cache, p.l_begin, p.l_end, bt, r->plan.table_len,
+                                 r->d_refs + p.ref_first, p.ref_count, r->chunk_tokens, dslot,
+                                 r->slot_bytes, stream);
+}
+
+kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
+  if (r->dir != dir) return KVX_EINVAL;
   if (r->closed.load()) return KVX_ECLOSED;
-  if (r->pieces.empty()) return KVX_OK;
+  if (r->plan.pieces.empty()) return KVX_OK;
   if (!bt) return KVX_EINVAL;
   DeviceGuard dg(r->device);
   if (!dg.ok) return KVX_EHIP;
   const auto t_start = clk::now();
-  const int32_t S = r->n_slots;
-  const int32_t T = r->fill_threads;
-  const int64_t P = (int64_t)r->pieces.size();
+  const int32_t S = r->n_slots, T = r->threads;
+  const int64_t P = (int64_t)r->plan.pieces.size();
   {
     std::lock_guard<std::mutex> lock(r->mu);
     r->enqueued = 0;
@@ -156,72 +228,200 @@ kvx_status restore(kvx_ring* r, const int32_t* bt, hipStream_t stream) {
   }
   r->worker_error.store(0);
   r->stop.store(false);
-  r->fill_ns.store(0);
+  r->busy_ns.store(0);
   std::vector<std::thread> workers;
   kvx_status st = KVX_OK;
   double wait_ms = 0;
   try {
-    for (int w = 0; w < T; ++w) workers.emplace_back(fill_worker, r, w);
+    for (int w = 0; w < T; ++w)
+      workers.emplace_back(dir == Dir::kRestore ? fill_worker : drain_worker, r, w);
   } catch (...) {
     st = KVX_ENOMEM;
   }
+  auto wait_parts = [&](int64_t i) {
+    auto t0 = clk::now();
+    std::unique_lock<std::mutex> lock(r->mu);
+    r->cv_host.wait(lock, [&] { return r->parts_done[(size_t)i] == T || r->stop.load(); });
+    wait_ms += ms_since(t0);
+  };
   for (int64_t i = 0; st == KVX_OK && i < P; ++i) {
     const int32_t s = (int32_t)(i % S);
-    const kvx_piece& p = r->pieces[(size_t)i];
-    if (T > 0) {
-      auto t0 = clk::now();
-      std::unique_lock<std::mutex> lock(r->mu);
-      r->cv_filled.wait(lock, [&] { return r->parts_done[(size_t)i] == T || r->stop.load(); });
-      wait_ms += ms_since(t0);
-    }
-    if (r->stop.load() || r->closed.load()) {
-      st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
-      break;
-    }
+    const kvx::Piece& p = r->plan.pieces[(size_t)i];
     uint8_t* dslot = r->landing + (int64_t)s * r->slot_bytes;
-    const uint8_t* hsrc = T > 0 ? r->host + (int64_t)s * r->slot_bytes : r->source + p.src_offset;
-    if (hipStreamWaitEvent(r->side, r->scatter_done[s], 0) != hipSuccess ||
-        hipMemcpyAsync(dslot, hsrc, (size_t)p.bytes, hipMemcpyHostToDevice, r->side) !=
-            hipSuccess ||
-        hipEventRecord(r->h2d_done[s], r->side) != hipSuccess) {
-      st = KVX_EHIP;
-      break;
-    }
-    {
-      std::lock_guard<std::mutex> lock(r->mu);
-      r->enqueued = i + 1;
-    }
-    r->cv_enqueued.notify_all();
-    if (hipStreamWaitEvent(stream, r->h2d_done[s], 0) != hipSuccess) {
-      st = KVX_EHIP;
-      break;
-    }
-    kvx::Geometry g;
-    st = kvx::validate(&r->cache, p.l_begin, p.l_end, p.n_blocks, p.chunk_tokens, true, &g);
-    if (st != KVX_OK) break;
-    st = kvx::launch_copy(false, &r->cache, p.l_begin, p.l_end, bt + p.bt_first, g, dslot, stream);
-    if (st != KVX_OK) break;
-    if (hipEventRecord(r->scatter_done[s], stream) != hipSuccess) {
-      st = KVX_EHIP;
-      break;
+    uint8_t* hslot = r->host + (int64_t)s * r->slot_bytes;
+    if (dir == Dir::kRestore) {
+      if (T > 0) wait_parts(i);
+      if (r->stop.load() || r->closed.load()) {
+        st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
+        break;
+      }
+      bool ok = hipStreamWaitEvent(r->side, r->dev_done[s], 0) == hipSuccess;
+      if (T > 0) {
+        ok = ok && hipMemcpyAsync(dslot, hslot, (size_t)p.bytes, hipMemcpyHostToDevice, r->side) ==
+                       hipSuccess;
+      } else {
+        for (const kvx::Span& sp : p.spans)
+          ok = ok && hipMemcpyAsync(dslot + sp.slot_off, sp.host, (size_t)sp.bytes,
+                                    hipMemcpyHostToDevice, r->side) == hipSuccess;
+      }
+      ok = ok && hipEventRecord(r->copy_done[s], r->side) == hipSuccess;
+      if (!ok) {
+        st = KVX_EHIP;
+        break;
+      }
+      {
+        std::lock_guard<std::mutex> lock(r->mu);
+        r->enqueued = i + 1;
+      }
+      r->cv_enqueued.notify_all();
+      if (hipStreamWaitEvent(stream, r->copy_done[s], 0) != hipSuccess) {
+        st = KVX_EHIP;
+        break;
+      }
+      st = launch_piece(r, false, p, bt, dslot, stream);
+      if (st != KVX_OK) break;
+      if (hipEventRecord(r->dev_done[s], stream) != hipSuccess) st = KVX_EHIP;
+    } else {
+      if (r->closed.load()) {
+        st = KVX_ECLOSED;
+        break;
+      }
+      if (hipStreamWaitEvent(stream, r->copy_done[s], 0) != hipSuccess) {
+        st = KVX_EHIP;
+        break;
+      }
+      st = launch_piece(r, true, p, bt, dslot, stream);
+      if (st != KVX_OK) break;
+      if (hipEventRecord(r->dev_done[s], stream) != hipSuccess) {
+        st = KVX_EHIP;
+        break;
+      }
+      if (T > 0 && i >= S) wait_parts(i - S);  // host slot s emptied by the drains
+      if (r->stop.load()) {
+        st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
+        break;
+      }
+      bool ok = hipStreamWaitEvent(r->side, r->dev_done[s], 0) == hipSuccess;
+      if (T > 0) {
+        ok = ok && hipMemcpyAsync(hslot, dslot, (size_t)p.bytes, hipMemcpyDeviceToHost, r->side) ==
+                       hipSuccess;
+      } else {
+        for (const kvx::Span& sp : p.spans)
+          ok = ok && hipMemcpyAsync(sp.host, dslot + sp.slot_off, (size_t)sp.bytes,
+                                    hipMemcpyDeviceToHost, r->side) == hipSuccess;
+      }
+      ok = ok && hipEventRecord(r->copy_done[s], r->side) == hipSuccess;
+      if (!ok) {
+        st = KVX_EHIP;
+        break;
+      }
+      {
+        std::lock_guard<std::mutex> lock(r->mu);
+        r->enqueued = i + 1;
+      }
+      r->cv_enqueued.notify_all();
     }
   }
-  if (st != KVX_OK) {
-    r->stop.store(true);
-    std::lock_guard<std::mutex> lock(r->mu);
-    r->cv_filled.notify_all();
-    r->cv_enqueued.notify_all();
+  if (st == KVX_OK && dir == Dir::kOffload) {
+    // The destinations are complete once the last drains (or, without drain
+    // threads, the last device-to-host copies) have finished.
+    if (T > 0) {
+      for (int64_t i = std::max<int64_t>(0, P - S); i < P && !r->stop.load(); ++i) wait_parts(i);
+      if (r->stop.load()) st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
+    } else if (hipStreamSynchronize(r->side) != hipSuccess) {
+      st = KVX_EHIP;
+    }
   }
+  if (st != KVX_OK) signal_stop(r);
   for (auto& th : workers) th.join();
   r->stop.store(false);
   r->stats.pieces = st == KVX_OK ? P : 0;
   r->stats.bytes = 0;
   if (st == KVX_OK)
-    for (const auto& p : r->pieces) r->stats.bytes += p.bytes;
-  r->stats.fill_ms = (double)r->fill_ns.load() / 1e6;
+    for (const auto& p : r->plan.pieces) r->stats.bytes += p.bytes;
+  r->stats.fill_ms = (double)r->busy_ns.load() / 1e6;
   r->stats.wait_fill_ms = wait_ms;
   r->stats.enqueue_ms = ms_since(t_start);
   return st;
+}
+
+bool is_pinned(const void* p) {
+  hipPointerAttribute_t attr{};
+  return hipPointerGetAttributes(&attr, p) == hipSuccess && attr.type == hipMemoryTypeHost;
+}
+
+// Common part of every bind: validate, plan, upload the chunk table.
+kvx_status bind(kvx_ring* r, Dir dir, const kvx_cache* cache, int32_t l0, int32_t l1,
+                int32_t chunk_tokens, std::vector<kvx::HostChunk> chunks, int32_t threads) {
+  if (threads < 0 || threads > 64) return KVX_EINVAL;
+  kvx::Geometry g;
+  kvx_status st = kvx::validate(cache, l0, l1, 0, chunk_tokens, false, &g);
+  if (st != KVX_OK) return st;
+  if (!cache->k || !cache->v) return KVX_EINVAL;
+  for (int32_t l = l0; l < l1; ++l) {
+    if (!cache->k[l] || !cache->v[l]) return KVX_EINVAL;
+    if (((uintptr_t)cache->k[l] | (uintptr_t)cache->v[l]) & 15) return KVX_EINVAL;
+  }
+  if (kvx::overlaps_cache(cache, l0, l1, r->landing, (int64_t)r->n_slots * r->slot_bytes))
+    return KVX_EINVAL;
+  int32_t bpc = chunk_tokens / cache->block_size;
+  // A chunk's layout depends only on its own block count, so the launches only
+  // need blocks-per-chunk up to the largest chunk (keeps padded unit counts small).
+  int32_t most = 1;
+  for (const auto& c : chunks) most = std::max(most, c.n_blocks);
+  for (const auto& c : chunks)
+    if (c.n_blocks > bpc) return KVX_EINVAL;
+  bpc = std::min(bpc, most);
+  kvx::Plan plan;
+  st = kvx::plan_chunks(chunks, l0, l1, g.slab, bpc, r->slot_bytes, &plan);
+  if (st != KVX_OK) return st;
+  if (threads == 0)
+    for (const auto& p : plan.pieces)
+      for (const auto& sp : p.spans)
+        if (!is_pinned(sp.host)) return KVX_EINVAL;  // direct copies need pinned memory
+  DeviceGuard dg(r->device);
+  if (!dg.ok) return KVX_EHIP;
+  drain_device(r);  // the previous transfer may still read d_refs
+  const size_t need = std::max<size_t>(plan.refs.size(), 1);
+  if (need > r->d_refs_cap) {
+    if (r->d_refs) (void)hipFree(r->d_refs);
+    r->d_refs = nullptr;
+    r->d_refs_cap = 0;
+    if (hipMalloc((void**)&r->d_refs, need * sizeof(kvx_chunk_ref)) != hipSuccess) {
+      r->d_refs = nullptr;
+      r->dir = Dir::kNone;
+      return KVX_ENOMEM;
+    }
+    r->d_refs_cap = need;
+  }
+  if (!plan.refs.empty() &&
+      hipMemcpy(r->d_refs, plan.refs.data(), plan.refs.size() * sizeof(kvx_chunk_ref),
+                hipMemcpyHostToDevice) != hipSuccess) {
+    r->dir = Dir::kNone;
+    return KVX_EHIP;
+  }
+  r->kptr.assign(cache->k, cache->k + cache->num_layers);
+  r->vptr.assign(cache->v, cache->v + cache->num_layers);
+  r->cache = *cache;
+  r->cache.k = r->kptr.data();
+  r->cache.v = r->vptr.data();
+  r->chunk_tokens = bpc * cache->block_size;
+  r->threads = threads;
+  r->plan.pieces.swap(plan.pieces);
+  r->plan.refs.swap(plan.refs);
+  r->plan.table_len = plan.table_len;
+  r->dir = dir;
+  return KVX_OK;
+}
+
+kvx_status host_chunks(const kvx_host_chunk* chunks, int32_t n,
+                       std::vector<kvx::HostChunk>* out) {
+  if (n < 0 || (n > 0 && !chunks)) return KVX_EINVAL;
+  out->clear();
+  for (int32_t i = 0; i < n; ++i)
+    out->push_back(kvx::HostChunk{(uint8_t*)chunks[i].host, chunks[i].bt_offset,
+                                  chunks[i].n_blocks});
+  return KVX_OK;
 }
 
 }  // namespace
@@ -264,12 +464,12 @@ kvx_status kvx_ring_create(int device, int32_t n_slots, int64_t slot_bytes, void
     }
     if (st == KVX_OK && hipStreamCreateWithFlags(&r->side, hipStreamNonBlocking) != hipSuccess)
       st = KVX_EHIP;
-    r->h2d_done.assign((size_t)n_slots, nullptr);
-    r->scatter_done.assign((size_t)n_slots, nullptr);
+    r->copy_done.assign((size_t)n_slots, nullptr);
+    r->dev_done.assign((size_t)n_slots, nullptr);
     for (int32_t s = 0; st == KVX_OK && s < n_slots; ++s) {
-      if (hipEventCreateWithFlags(&r->h2d_done[s], hipEventDisableTiming | hipEventBlockingSync) !=
+      if (hipEventCreateWithFlags(&r->copy_done[s], hipEventDisableTiming | hipEventBlockingSync) !=
               hipSuccess ||
-          hipEventCreateWithFlags(&r->scatter_done[s], hipEventDisableTiming) != hipSuccess)
+          hipEventCreateWithFlags(&r->dev_done[s], hipEventDisableTiming) != hipSuccess)
         st = KVX_EHIP;
     }
     if (st != KVX_OK) {
@@ -290,38 +490,43 @@ kvx_status kvx_ring_bind(kvx_ring* r, const kvx_cache* cache, int32_t l0, int32_
                          int32_t n_blocks, int32_t chunk_tokens, const void* host_source,
                          int32_t fill_threads) {
   if (!r || !cache) return KVX_EINVAL;
-  if (fill_threads < 0 || fill_threads > 64) return KVX_EINVAL;
   try {
     kvx::Geometry g;
-    kvx_status st = kvx::validate(cache, l0, l1, n_blocks, chunk_tokens, true, &g);
+    kvx_status st = kvx::validate(cache, l0, l1, n_blocks, chunk_tokens, false, &g);
     if (st != KVX_OK) return st;
     if (g.n_units > 0 && !host_source) return KVX_EINVAL;
-    if (g.n_units > 0 && kvx::overlaps_cache(cache, l0, l1, r->landing,
-                                             (int64_t)r->n_slots * r->slot_bytes))
-      return KVX_EINVAL;
-    if (g.n_units > 0 && fill_threads == 0) {
-      hipPointerAttribute_t attr{};
-      if (hipPointerGetAttributes(&attr, host_source) != hipSuccess ||
-          attr.type != hipMemoryTypeHost)
-        return KVX_EINVAL;  // direct H2D needs pinned memory
-    }
-    std::vector<kvx_piece> pieces;
-    st = kvx::plan_pieces(g, l0, l1, cache->block_size, r->slot_bytes, &pieces);
+    std::vector<kvx::HostChunk> chunks;
+    if (g.n_units > 0) chunks = kvx::image_chunks((uint8_t*)host_source, g);
+    return bind(r, Dir::kRestore, cache, l0, l1, g.bpc * cache->block_size, std::move(chunks),
+                fill_threads);
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}
+
+kvx_status kvx_ring_bind_chunks(kvx_ring* r, const kvx_cache* cache, int32_t l0, int32_t l1,
+                                int32_t chunk_tokens, const kvx_host_chunk* chunks,
+                                int32_t n_chunks, int32_t fill_threads) {
+  if (!r || !cache) return KVX_EINVAL;
+  try {
+    std::vector<kvx::HostChunk> v;
+    kvx_status st = host_chunks(chunks, n_chunks, &v);
     if (st != KVX_OK) return st;
-    r->kptr.assign(cache->k, cache->k + cache->num_layers);
-    r->vptr.assign(cache->v, cache->v + cache->num_layers);
-    r->cache = *cache;
-    r->cache.k = r->kptr.data();
-    r->cache.v = r->vptr.data();
-    r->l0 = l0;
-    r->l1 = l1;
-    r->n_blocks = n_blocks;
-    r->chunk_tokens = chunk_tokens;
-    r->source = (const uint8_t*)host_source;
-    r->fill_threads = fill_threads;
-    r->pieces.swap(pieces);
-    r->bound = true;
-    return KVX_OK;
+    return bind(r, Dir::kRestore, cache, l0, l1, chunk_tokens, std::move(v), fill_threads);
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}
+
+kvx_status kvx_ring_bind_offload(kvx_ring* r, const kvx_cache* cache, int32_t l0, int32_t l1,
+                                 int32_t chunk_tokens, const kvx_host_chunk* chunks,
+                                 int32_t n_chunks, int32_t drain_threads) {
+  if (!r || !cache) return KVX_EINVAL;
+  try {
+    std::vector<kvx::HostChunk> v;
+    kvx_status st = host_chunks(chunks, n_chunks, &v);
+    if (st != KVX_OK) return st;
+    return bind(r, Dir::kOffload, cache, l0, l1, chunk_tokens, std::move(v), drain_threads);
   } catch (...) {
     return KVX_EINTERNAL;
   }
@@ -331,7 +536,16 @@ kvx_status kvx_restore_from_staging(kvx_ring* ring, const int32_t* block_table,
                                     hipStream_t stream) {
   if (!ring) return KVX_EINVAL;
   try {
-    return restore(ring, block_table, stream);
+    return run(ring, Dir::kRestore, block_table, stream);
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}
+
+kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hipStream_t stream) {
+  if (!ring) return KVX_EINVAL;
+  try {
+    return run(ring, Dir::kOffload, block_table, stream);
   } catch (...) {
     return KVX_EINTERNAL;
   }
@@ -346,10 +560,7 @@ kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out) {
 kvx_status kvx_ring_abort(kvx_ring* ring) {
   if (!ring) return KVX_EINVAL;
   ring->closed.store(true);
-  ring->stop.store(true);
-  std::lock_guard<std::mutex> lock(ring->mu);
-  ring->cv_filled.notify_all();
-  ring->cv_enqueued.notify_all();
+  signal_stop(ring);
   return KVX_OK;
 }
 

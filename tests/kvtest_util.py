@@ -39,7 +39,7 @@ def seeded_ids(seed: int, pool: int, *counts):
 class Filled:
     seed: int
     role: int
-    mode: int
+    mode: int = kvsynth.MODE_NORMAL_BF16
 
 
 def torch_dtype(elem_bytes: int):
