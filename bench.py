@@ -1,10 +1,10 @@
 #!/usr/bin/env python3
 """Benchmark: paged-KV gather / scatter / staged restore on one MI355X.
 
-Workload (default): Llama-3-8B-shaped KV cache (32 layers, K and V each
-[20000 blocks, 16 tokens, 8 KV heads, head dim 128] bf16, N(0,1) from a seed),
-an 80,000-token prefix = 5,000 blocks at seeded random block ids, 256-token
-transfer chunks (all layers per chunk, layer-major).
+Default workload (--workload 8b-80k): Llama-3-8B-shaped KV cache (32 layers,
+K and V each [20000 blocks, 16 tokens, 8 KV heads, head dim 128] bf16, N(0,1)
+from a seed), an 80,000-token prefix = 5,000 blocks at seeded random block
+ids, 256-token transfer chunks (all layers per chunk, layer-major).
 
 One step = the whole hot path once over that prefix:
   1. gather the 5,000 blocks into packed chunks (HBM -> HBM),
@@ -13,25 +13,46 @@ One step = the whole hot path once over that prefix:
      through a 4 x 64 MiB pinned staging ring (fill -> H2D on a side stream ->
      scatter kernel, overlapped through HIP events) into another 5,000 blocks.
 Inputs are resident (cache in HBM, image in pinned host memory) before the
-timed region starts.
+timed region starts. Prints ONE JSON line. `value` is the gather/scatter HBM
+throughput (bytes read plus bytes written by the two kernels, per second of
+their event-timed device time); the restore time is reported next to it.
 
-Prints ONE JSON line. `value` is the gather/scatter HBM throughput (bytes read
-plus bytes written by the two kernels, per second of their event-timed
-device time); the restore time is reported next to it.
+Other workloads print one JSON line each with their own metric:
+  --workload 8b-32k-sweep  32,768-token prefix, chunks of 16/64/256/1024
+                           tokens (gather, scatter) and rings of 2/4/8 slots
+                           (staged restore), 20,000-block pool;
+  --workload 70b-batch     64 requests on a seeded prefix tree over a
+                           70B-shaped cache (80 layers): the distinct missing
+                           chunks restored through one ring while the new
+                           blocks are offloaded through another.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import statistics
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
+KERNELS_SRC = os.path.join(ROOT, "paper_2609_11744_amd", "csrc", "kvx_kernels.hip")
+
+# HBM bytes of one gather launch on the 80k workload, from two rocprofv3 --pmc
+# runs (FETCH_SIZE, then WRITE_SIZE; profiles/copy_units_8b_80k_pmc.md), each
+# scaled by what the same counter reads for a 4 GiB plain device copy. Valid
+# only for the kernel source they were taken on (sha256 below); otherwise the
+# bench reports traffic as null.
+GATHER_TRAFFIC = {
+    "kernels_sha256": "c82c36ebddb94cb8100ac59963a175ff0a802e1f7120e1e1a6541af55195efb5",
+    "fetch_bytes": 10488342792,   # FETCH_SIZE 5,121,313.9 KiB x 1.99998 (copy calibration)
+    "write_bytes": 10489107264,   # WRITE_SIZE 10,243,268.8 KiB x 1.0
+}
 
 
 def log(msg):
@@ -43,6 +64,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="8b-80k", choices=["8b-80k", "8b-32k-sweep", "70b-batch"])
     ap.add_argument("--num-blocks", type=int, default=20000)
     ap.add_argument("--prefix-blocks", type=int, default=5000)
     ap.add_argument("--chunk-tokens", type=int, default=256)
@@ -56,12 +78,74 @@ def parse():
     return ap.parse_args()
 
 
-def main():
-    args = parse()
-    if args.gpus != 1:
-        print("bench.py measures one GPU only: this path needs no collective, and the "
-              "multi-GPU sharding is described, not built. Run with --gpus 1.", file=sys.stderr)
-        sys.exit(2)
+def kernels_sha256() -> str:
+    with open(KERNELS_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def probes(dev, reps):
+    """Same-run link and copy probes: 1 GiB pinned H2D / D2H, 4 GiB D2D."""
+    import torch
+
+    def timed_copy(dst, src, n):
+        out = []
+        for _ in range(n):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            dst.copy_(src, non_blocking=True)
+            b.record()
+            b.synchronize()
+            out.append(a.elapsed_time(b))
+        return statistics.median(out)
+
+    p = {}
+    h = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
+    d = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+    p["h2d_GBps"] = (1 << 30) / timed_copy(d, h, reps) / 1e6
+    p["d2h_GBps"] = (1 << 30) / timed_copy(h, d, reps) / 1e6
+    del h, d
+    dd = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
+    ds = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
+    p["d2d_copy_GBps_rw"] = 2 * (4 << 30) / timed_copy(dd, ds, 5) / 1e6
+    del dd, ds
+    torch.cuda.empty_cache()
+    log(f"probes: {p}")
+    return p
+
+
+def event_ms(fn, reps):
+    import torch
+
+    out = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        fn()
+        b.record()
+        b.synchronize()
+        out.append(a.elapsed_time(b))
+    return out
+
+
+def fill_cache(cache, seed, role):
+    import kvsynth
+
+    for l in range(cache.num_layers):
+        kvsynth.fill_device(cache.k[l], seed, kvsynth.cache_stream(role, l, 0))
+        kvsynth.fill_device(cache.v[l], seed, kvsynth.cache_stream(role, l, 1))
+
+
+def base_record(args, metric, unit, value, ms_per_step, config, higher=True):
+    return {"metric": metric, "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps,
+            "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": higher,
+            "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+            "data": "synthetic (seeded N(0,1) bf16 KV, seeded random block ids)",
+            "config": config}
+
+
+# ---- default: 8B-shaped cache, 80,000-token prefix ------------------------------------
+
+def run_80k(args):
     import numpy as np
     import torch
 
@@ -69,9 +153,6 @@ def main():
     import paper_2609_11744_amd as kvx
 
     dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
-    stream = torch.cuda.current_stream()
-
     L, BS, H, D, E = 32, 16, 8, 128, 2
     NB, n, ct = args.num_blocks, args.prefix_blocks, args.chunk_tokens
     if 3 * n > NB:
@@ -81,11 +162,8 @@ def main():
     log(f"workload: 8B-shaped cache {NB} blocks ({NB * L * 2 * slab / 1e9:.1f} GB), "
         f"prefix {n} blocks = {n * BS} tokens, payload {payload / 1e9:.3f} GB")
 
-    # ---- inputs -----------------------------------------------------------
     cache = kvx.PagedKVCache.allocate(L, NB, BS, H, D, torch.bfloat16, dev)
-    for l in range(L):
-        kvsynth.fill_device(cache.k[l], args.seed, kvsynth.cache_stream(kvsynth.ROLE_SRC, l, 0))
-        kvsynth.fill_device(cache.v[l], args.seed, kvsynth.cache_stream(kvsynth.ROLE_SRC, l, 1))
+    fill_cache(cache, args.seed, kvsynth.ROLE_SRC)
     perm = np.random.default_rng(args.seed).permutation(NB).astype(np.int32)
     bt_src = torch.from_numpy(perm[:n].copy()).to(dev)
     bt_dst = torch.from_numpy(perm[n:2 * n].copy()).to(dev)
@@ -98,35 +176,8 @@ def main():
     ring = kvx.StagingRing(dev, args.slots, args.slot_mib << 20)
     ring.bind(cache, 0, L, n, ct, image, fill_threads=args.fill_threads)
     torch.cuda.synchronize()
+    probe = probes(dev, args.probe_reps)
 
-    # ---- same-run probes ----------------------------------------------------
-    probe = {}
-    h = torch.empty(1 << 30, dtype=torch.uint8, pin_memory=True)
-    d = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
-
-    def timed_copy(dst, src, reps):
-        out = []
-        for _ in range(reps):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            dst.copy_(src, non_blocking=True)
-            b.record()
-            b.synchronize()
-            out.append(a.elapsed_time(b))
-        return statistics.median(out)
-
-    probe["h2d_GBps"] = (1 << 30) / timed_copy(d, h, args.probe_reps) / 1e6
-    probe["d2h_GBps"] = (1 << 30) / timed_copy(h, d, args.probe_reps) / 1e6
-    del h
-    dd = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
-    ds = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
-    ms = timed_copy(dd, ds, 5)
-    probe["d2d_copy_GBps_rw"] = 2 * (4 << 30) / ms / 1e6
-    del dd, ds, d
-    torch.cuda.empty_cache()
-    log(f"probes: {probe}")
-
-    # ---- steps --------------------------------------------------------------
     def step(record):
         e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
         e[0].record()
@@ -170,30 +221,21 @@ def main():
     gather_GBps = rw / mean_g / 1e6
     scatter_GBps = rw / mean_s / 1e6
     restore_GBps = payload / med["restore_ms"] / 1e6
+    cpu = None if args.no_cpu_baseline else cpu_baseline(args, L, BS, H, D, E, perm)
+    traffic = None
+    if GATHER_TRAFFIC["kernels_sha256"] == kernels_sha256() and \
+            (args.num_blocks, args.prefix_blocks, args.chunk_tokens) == (20000, 5000, 256):
+        traffic = GATHER_TRAFFIC["fetch_bytes"] + GATHER_TRAFFIC["write_bytes"]
 
-    # ---- CPU baseline: the oracle on a bounded sample ------------------------
-    cpu = None
-    if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args, L, BS, H, D, E, perm)
-
-    out = {
-        "metric": "KV gather/scatter GB/s & % HBM peak; 80k-token prefix restore ms",
-        "value": round(gs_GBps, 1),
-        "unit": "GB/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(wall_ms / args.steps, 3),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic (seeded N(0,1) bf16 KV, seeded random block ids)",
-        "config": {"workload": "llama-3-8b-shaped paged KV, 80k-token prefix (5000 blocks), "
-                               "256-token chunks, 4 x 64 MiB pinned staging ring",
-                   "num_blocks": NB, "prefix_tokens": n * BS, "chunk_tokens": ct,
-                   "slots": args.slots, "slot_mib": args.slot_mib,
-                   "fill_threads": args.fill_threads, "parallelism": "single GPU"},
+    out = base_record(
+        args, "KV gather/scatter GB/s & % HBM peak; 80k-token prefix restore ms",
+        "GB/s", round(gs_GBps, 1), round(wall_ms / args.steps, 3),
+        {"workload": "llama-3-8b-shaped paged KV, 80k-token prefix (5000 blocks), "
+                     "256-token chunks, 4 x 64 MiB pinned staging ring",
+         "num_blocks": NB, "prefix_tokens": n * BS, "chunk_tokens": ct,
+         "slots": args.slots, "slot_mib": args.slot_mib,
+         "fill_threads": args.fill_threads, "parallelism": "single GPU"})
+    out.update({
         "pct_hbm_peak": round(100 * gs_GBps / HBM_PEAK_GBPS, 2),
         "gather_GBps_rw": round(gather_GBps, 1),
         "scatter_GBps_rw": round(scatter_GBps, 1),
@@ -206,12 +248,12 @@ def main():
                                  "enqueue_wait_for_fill": round(med["wait_fill_ms"], 2),
                                  "device_span": round(med["restore_dev_ms"], 2)},
         "probes": {k: round(v, 2) for k, v in probe.items()},
-        "roofline": {"bound": "hbm", "kernel": "gather (copy_units_kernel<true, 1024, 2>)",
+        "roofline": {"bound": "hbm", "kernel": "gather (copy_units_kernel<true, false, 1024, 2>)",
                      "achieved": round(gather_GBps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(gather_GBps / HBM_PEAK_GBPS, 4),
-                     "traffic": None},
+                     "traffic": traffic, "algorithmic_bytes": rw},
         "cpu_baseline": cpu,
-    }
+    })
     print(json.dumps(out), flush=True)
     ring.close()
     image.free()
@@ -251,6 +293,175 @@ def cpu_baseline(args, L, BS, H, D, E, perm):
             "sample": f"gather + scatter of {m} of the {args.prefix_blocks} prefix blocks "
                       f"({out.nbytes / 1e9:.2f} GB payload each way), median of 3, "
                       f"single-threaded C slab memcpy"}
+
+
+# ---- 32k-token granularity sweep --------------------------------------------------------
+
+def run_sweep(args):
+    import numpy as np
+    import torch
+
+    import kvsynth
+    import paper_2609_11744_amd as kvx
+
+    dev = torch.device("cuda:0")
+    L, BS, H, D, E = 32, 16, 8, 128, 2
+    NB, n = args.num_blocks, 2048
+    slab = BS * H * D * E
+    payload = n * L * 2 * slab
+    cache = kvx.PagedKVCache.allocate(L, NB, BS, H, D, torch.bfloat16, dev)
+    fill_cache(cache, args.seed, kvsynth.ROLE_SRC)
+    perm = np.random.default_rng(args.seed).permutation(NB).astype(np.int32)
+    bt_src = torch.from_numpy(perm[:n].copy()).to(dev)
+    bt_dst = torch.from_numpy(perm[n:2 * n].copy()).to(dev)
+    packed = torch.empty(payload, dtype=torch.uint8, device=dev)
+    image = kvx.PinnedBuffer(payload)
+    kvsynth.fill_host(image.array, args.seed, kvsynth.image_stream(2), threads=16)
+    probe = probes(dev, args.probe_reps)
+    reps = max(args.steps, 3)
+    rows = []
+    t_begin = time.perf_counter()
+    for ct in (16, 64, 256, 1024):
+        g = event_ms(lambda: kvx.kvx_gather_blocks(cache, 0, L, bt_src, n, ct, packed), reps)
+        s = event_ms(lambda: kvx.kvx_scatter_blocks(cache, 0, L, bt_dst, n, ct, packed), reps)
+        row = {"chunk_tokens": ct, "gather_GBps_rw": round(2 * payload / statistics.median(g) / 1e6, 1),
+               "scatter_GBps_rw": round(2 * payload / statistics.median(s) / 1e6, 1), "restore": []}
+        for slots in (2, 4, 8):
+            ring = kvx.StagingRing(dev, slots, args.slot_mib << 20)
+            ring.bind(cache, 0, L, n, ct, image, fill_threads=args.fill_threads)
+            times = []
+            for i in range(reps + 1):
+                t0 = time.perf_counter()
+                kvx.kvx_restore_from_staging(ring, bt_dst)
+                torch.cuda.synchronize()
+                if i:
+                    times.append((time.perf_counter() - t0) * 1e3)
+            ms = statistics.median(times)
+            row["restore"].append({"slots": slots, "ms": round(ms, 3),
+                                   "GBps": round(payload / ms / 1e6, 2),
+                                   "frac_of_h2d": round(payload / ms / 1e6 / probe["h2d_GBps"], 4),
+                                   "pieces": ring.stats()["pieces"]})
+            ring.close()
+        rows.append(row)
+        log(f"chunk {ct}: {row}")
+    kvx.kvx_check()
+    wall = (time.perf_counter() - t_begin) * 1e3
+    best = max(min(r["gather_GBps_rw"], r["scatter_GBps_rw"]) for r in rows)
+    out = base_record(args, "KV gather/scatter GB/s across transfer chunk sizes (32k-token prefix)",
+                      "GB/s", best, round(wall, 1),
+                      {"workload": "llama-3-8b-shaped paged KV, 32k-token prefix (2048 blocks) of "
+                                   "a 20000-block pool; chunks 16/64/256/1024; rings 2/4/8 x 64 MiB",
+                       "num_blocks": NB, "prefix_tokens": n * BS, "parallelism": "single GPU"})
+    out["ms_per_step_note"] = "wall time of the whole sweep"
+    out.update({"sweep": rows, "probes": {k: round(v, 2) for k, v in probe.items()}})
+    print(json.dumps(out), flush=True)
+    image.free()
+
+
+# ---- 70B-shaped batched step -------------------------------------------------------
+
+def run_batch(args):
+    import numpy as np
+    import torch
+
+    import kvsynth
+    import kvsynth.prefix_tree as pt
+    import paper_2609_11744_amd as kvx
+    from paper_2609_11744_amd import step
+
+    dev = torch.device("cuda:0")
+    L, BS, H, D, E = 80, 16, 8, 128, 2
+    reqs = pt.make_requests(5, n=64)
+    plan = step.plan_step(reqs, BS, 256)
+    NB = plan.restore_blocks + plan.offload_blocks + 64
+    per_block = L * 2 * BS * H * D * E
+    rb, ob = plan.restore_blocks * per_block, plan.offload_blocks * per_block
+    log(f"70B batch: {len(plan.restore)} distinct missing chunks ({rb / 1e9:.1f} GB), "
+        f"{plan.resident_hits} resident chunks, {plan.offload_blocks} new blocks "
+        f"({ob / 1e9:.1f} GB); pool {NB} blocks")
+    ids = np.random.default_rng(5).permutation(NB).astype(np.int32)
+    rbt = torch.from_numpy(ids[:plan.restore_blocks].copy()).to(dev)
+    obt = torch.from_numpy(ids[plan.restore_blocks:plan.restore_blocks + plan.offload_blocks]
+                           .copy()).to(dev)
+    cache = kvx.PagedKVCache.allocate(L, NB, BS, H, D, torch.bfloat16, dev)
+    fill_cache(cache, 5, kvsynth.ROLE_NEW)
+    store = np.empty(rb, dtype=np.uint8)
+    chunks = []
+    for c in plan.restore:
+        view = store[c.bt_offset * per_block:(c.bt_offset + c.n_blocks) * per_block]
+        kvsynth.fill_host(view, 5, pt.chunk_stream(reqs[c.origin[0]].chunk_owner[c.origin[1]]),
+                          threads=16)
+        chunks.append((view, c.bt_offset, c.n_blocks))
+    sink = np.ones(ob, dtype=np.uint8)  # touched up front: no page faults while draining
+    sinks = [(sink[c.bt_offset * per_block:(c.bt_offset + c.n_blocks) * per_block],
+              c.bt_offset, c.n_blocks) for c in plan.offload]
+    probe = probes(dev, args.probe_reps)
+    r_ring = kvx.StagingRing(dev, args.slots, args.slot_mib << 20)
+    o_ring = kvx.StagingRing(dev, args.slots, args.slot_mib << 20)
+    r_ring.bind_chunks(cache, 0, L, 256, chunks, fill_threads=args.fill_threads)
+    o_ring.bind_offload(cache, 0, L, 256, sinks, drain_threads=args.fill_threads)
+    s_r, s_o = torch.cuda.Stream(), torch.cuda.Stream()
+
+    def one_step():
+        t = {}
+
+        def restore():
+            t0 = time.perf_counter()
+            kvx.kvx_restore_from_staging(r_ring, rbt, stream=s_r)
+            s_r.synchronize()
+            t["restore"] = time.perf_counter() - t0
+
+        def offload():
+            t0 = time.perf_counter()
+            kvx.kvx_offload_to_staging(o_ring, obt, stream=s_o)
+            t["offload"] = time.perf_counter() - t0
+
+        th = [threading.Thread(target=restore), threading.Thread(target=offload)]
+        t0 = time.perf_counter()
+        for x in th:
+            x.start()
+        for x in th:
+            x.join()
+        t["step"] = time.perf_counter() - t0
+        return t
+
+    for _ in range(args.warmup):
+        one_step()
+    torch.cuda.synchronize()
+    recs = [one_step() for _ in range(args.steps)]
+    kvx.kvx_check()
+    med = {k: statistics.median(r[k] for r in recs) for k in recs[0]}
+    out = base_record(args, "KV staged restore GB/s (70B batched step, offload concurrent)", "GB/s",
+                      round(rb / med["restore"] / 1e9, 2), round(med["step"] * 1e3, 2),
+                      {"workload": "70b-shaped paged KV, 64 requests on a seeded prefix tree "
+                                   "(log-uniform 1k-32k tokens, branching 1-4, 50% resident), "
+                                   "256-token chunks, 2 rings of 4 x 64 MiB",
+                       "distinct_missing_chunks": len(plan.restore),
+                       "restore_blocks": plan.restore_blocks,
+                       "offload_blocks": plan.offload_blocks,
+                       "resident_chunks": plan.resident_hits, "parallelism": "single GPU"})
+    out.update({"restore_GBps": round(rb / med["restore"] / 1e9, 2),
+                "restore_frac_of_h2d": round(rb / med["restore"] / 1e9 / (probe["h2d_GBps"]), 4),
+                "offload_GBps": round(ob / med["offload"] / 1e9, 2),
+                "offload_frac_of_d2h": round(ob / med["offload"] / 1e9 / probe["d2h_GBps"], 4),
+                "restore_ms": round(med["restore"] * 1e3, 2),
+                "offload_ms": round(med["offload"] * 1e3, 2),
+                "probes": {k: round(v, 2) for k, v in probe.items()}})
+    print(json.dumps(out), flush=True)
+    r_ring.close()
+    o_ring.close()
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this path needs no collective, and the "
+              "multi-GPU sharding is described, not built. Run with --gpus 1.", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    torch.cuda.set_device(torch.device("cuda:0"))
+    {"8b-80k": run_80k, "8b-32k-sweep": run_sweep, "70b-batch": run_batch}[args.workload](args)
 
 
 if __name__ == "__main__":
