@@ -431,6 +431,18 @@ def run_batch(args):
     recs = [one_step() for _ in range(args.steps)]
     kvx.kvx_check()
     med = {k: statistics.median(r[k] for r in recs) for k in recs[0]}
+    # each leg alone, for comparison with the concurrent step
+    alone = {"restore": [], "offload": []}
+    for _ in range(2):
+        t0 = time.perf_counter()
+        kvx.kvx_restore_from_staging(r_ring, rbt, stream=s_r)
+        s_r.synchronize()
+        alone["restore"].append(time.perf_counter() - t0)
+        t0 = time.perf_counter()
+        kvx.kvx_offload_to_staging(o_ring, obt, stream=s_o)
+        alone["offload"].append(time.perf_counter() - t0)
+    alone = {k: min(v) for k, v in alone.items()}
+    o_stats = o_ring.stats()
     out = base_record(args, "KV staged restore GB/s (70B batched step, offload concurrent)", "GB/s",
                       round(rb / med["restore"] / 1e9, 2), round(med["step"] * 1e3, 2),
                       {"workload": "70b-shaped paged KV, 64 requests on a seeded prefix tree "
@@ -446,6 +458,10 @@ def run_batch(args):
                 "offload_frac_of_d2h": round(ob / med["offload"] / 1e9 / probe["d2h_GBps"], 4),
                 "restore_ms": round(med["restore"] * 1e3, 2),
                 "offload_ms": round(med["offload"] * 1e3, 2),
+                "alone": {"restore_GBps": round(rb / alone["restore"] / 1e9, 2),
+                          "offload_GBps": round(ob / alone["offload"] / 1e9, 2),
+                          "offload_drain_thread_ms": round(o_stats["fill_ms"], 2),
+                          "offload_wait_for_drain_ms": round(o_stats["wait_fill_ms"], 2)},
                 "probes": {k: round(v, 2) for k, v in probe.items()}})
     print(json.dumps(out), flush=True)
     r_ring.close()
