@@ -292,6 +292,15 @@ kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out);
  * call from another thread. */
 kvx_status kvx_ring_abort(kvx_ring* ring);
 
+/* Fault-injection hooks for testing the slot-reuse protocol from the host.
+ * max_delay_us > 0: each fill or drain thread pauses a pseudo-random 0 ..
+ * max_delay_us microseconds before every piece (varies the interleavings).
+ * poison != 0: a restore's fill threads overwrite their share of a released
+ * host slot with 0xA5 bytes (then pause) before refilling it, so a copy that
+ * still read a released slot would deliver the poison. Off by default; call
+ * between transfers. */
+kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t poison);
+
 /* Wait for the ring's side stream and last restore, then free everything the
  * ring owns. */
 kvx_status kvx_ring_destroy(kvx_ring* ring);

@@ -349,6 +349,11 @@ class StagingRing:
     def abort(self):
         _ok(_native.lib().kvx_ring_abort(self.handle), "kvx_ring_abort")
 
+    def set_test_hooks(self, max_delay_us=0, poison=False):
+        """Fault injection: random fill/drain pauses, poisoning of released slots."""
+        _ok(_native.lib().kvx_ring_set_test_hooks(self.handle, max_delay_us, int(poison)),
+            "kvx_ring_set_test_hooks")
+
     def close(self):
         if self.handle:
             _native.lib().kvx_ring_destroy(self.handle)

@@ -63,6 +63,7 @@ SIGNATURES = {
     "kvx_offload_to_staging": (ctypes.c_int, [c_vp, c_vp, c_vp]),
     "kvx_ring_stats_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxRingStats)]),
     "kvx_ring_abort": (ctypes.c_int, [c_vp]),
+    "kvx_ring_set_test_hooks": (ctypes.c_int, [c_vp, c_i32, c_i32]),
     "kvx_ring_destroy": (ctypes.c_int, [c_vp]),
     "kvx_block_hashes": (c_i64, [c_vp, c_i64, c_i32, ctypes.c_uint64, c_vp]),
     "kvx_dedupe_keys": (ctypes.c_int, [c_vp, c_i32, c_vp]),

@@ -75,6 +75,10 @@ struct kvx_ring {
   std::vector<int32_t> parts_done;    // per piece: fill / drain parts finished
   std::atomic<int64_t> busy_ns{0};
   kvx_ring_stats stats{};
+
+  // test hooks (kvx_ring_set_test_hooks)
+  int32_t hook_max_delay_us = 0;
+  bool hook_poison = false;
 };
 
 namespace {
@@ -151,12 +155,22 @@ void signal_stop(kvx_ring* r) {
   r->cv_enqueued.notify_all();
 }
 
+// Test hook: a deterministic pseudo-random pause of 0..max microseconds.
+void hook_pause(kvx_ring* r, uint64_t* state) {
+  if (r->hook_max_delay_us <= 0) return;
+  *state = *state * 6364136223846793005ULL + 1442695040888963407ULL;
+  const int64_t us = (int64_t)((*state >> 33) % (uint64_t)(r->hook_max_delay_us + 1));
+  std::this_thread::sleep_for(std::chrono::microseconds(us));
+}
+
 // Restore fill thread w: copies its share of every piece into the piece's slot.
 void fill_worker(kvx_ring* r, int w) {
   const int32_t S = r->n_slots, T = r->threads;
   const int64_t P = (int64_t)r->plan.pieces.size();
   int64_t busy = 0;
+  uint64_t rng = 0x9E3779B97F4A7C15ULL * (uint64_t)(w + 1);
   for (int64_t i = 0; i < P; ++i) {
+    hook_pause(r, &rng);
     const int32_t s = (int32_t)(i % S);
     if (i >= S) {
       // copy_done[s] must hold the record of piece i - S before we wait on it.
@@ -168,6 +182,17 @@ void fill_worker(kvx_ring* r, int w) {
       r->worker_error.store(1);
       signal_stop(r);
       break;
+    }
+    if (r->hook_poison) {
+      // The slot is released: overwrite this thread's share before refilling
+      // it, so a copy that still read it would carry the poison.
+      const kvx::Piece& p = r->plan.pieces[(size_t)i];
+      int64_t per = (p.bytes + T - 1) / T;
+      per = (per + 4095) & ~(int64_t)4095;
+      const int64_t a = std::min<int64_t>(p.bytes, per * w);
+      const int64_t b = std::min<int64_t>(p.bytes, a + per);
+      if (b > a) std::memset(r->host + (int64_t)s * r->slot_bytes + a, 0xA5, (size_t)(b - a));
+      hook_pause(r, &rng);
     }
     auto t0 = clk::now();
     copy_share(r, r->plan.pieces[(size_t)i], s, w, T, true);
@@ -183,8 +208,10 @@ void drain_worker(kvx_ring* r, int w) {
   const int32_t S = r->n_slots, T = r->threads;
   const int64_t P = (int64_t)r->plan.pieces.size();
   int64_t busy = 0;
+  uint64_t rng = 0xD1B54A32D192ED03ULL * (uint64_t)(w + 1);
   for (int64_t i = 0; i < P; ++i) {
     const int32_t s = (int32_t)(i % S);
+    hook_pause(r, &rng);
     {
       std::unique_lock<std::mutex> lock(r->mu);
       r->cv_enqueued.wait(lock, [&] { return r->enqueued > i || r->stop.load(); });
@@ -549,6 +576,13 @@ kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hi
   } catch (...) {
     return KVX_EINTERNAL;
   }
+}
+
+kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t poison) {
+  if (!ring || max_delay_us < 0 || max_delay_us > 1000000) return KVX_EINVAL;
+  ring->hook_max_delay_us = max_delay_us;
+  ring->hook_poison = poison != 0;
+  return KVX_OK;
 }
 
 kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out) {
