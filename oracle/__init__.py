@@ -39,9 +39,13 @@ LIB_PATH = os.environ.get("KVX_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so
 OK, EINVAL, EBADBLOCK = 0, -1, -4
 
 
+LAYOUT_NHD, LAYOUT_HND, LAYOUT_PAGED_ATTN = 0, 1, 2
+
+
 class _Shape(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in
-                ("num_layers", "num_blocks", "block_size", "kv_heads", "head_dim", "elem_bytes")]
+                ("num_layers", "num_blocks", "block_size", "kv_heads", "head_dim", "elem_bytes",
+                 "layout")]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -52,6 +56,7 @@ class Shape:
     kv_heads: int
     head_dim: int
     elem_bytes: int = 2
+    layout: int = LAYOUT_NHD
 
     @property
     def row_bytes(self) -> int:
@@ -63,7 +68,7 @@ class Shape:
 
     def _c(self) -> _Shape:
         return _Shape(self.num_layers, self.num_blocks, self.block_size, self.kv_heads,
-                      self.head_dim, self.elem_bytes)
+                      self.head_dim, self.elem_bytes, self.layout)
 
 
 _lib = None
@@ -165,7 +170,25 @@ def new_mirror(shape: Shape):
 
 
 def element_view(buf: np.ndarray, shape: Shape) -> np.ndarray:
-    """View a per-layer byte array as [num_blocks, block_size, kv_heads, head_dim] words."""
+    """View a per-layer byte array of the default layout as
+    [num_blocks, block_size, kv_heads, head_dim] words."""
     dt = {1: np.uint8, 2: np.uint16, 4: np.uint32, 8: np.uint64}[shape.elem_bytes]
     return buf.view(dt).reshape(shape.num_blocks, shape.block_size, shape.kv_heads,
                                 shape.head_dim)
+
+
+def canonical_view(buf: np.ndarray, shape: Shape, kv: int) -> np.ndarray:
+    """A per-layer K (kv=0) or V (kv=1) byte array of any layout, seen as
+    [num_blocks, block_size, kv_heads, head_dim] words (a numpy view built by
+    reshaping and transposing the layout's own axes)."""
+    dt = {1: np.uint8, 2: np.uint16, 4: np.uint32, 8: np.uint64}[shape.elem_bytes]
+    w = buf.view(dt)
+    NB, BS, H, D = shape.num_blocks, shape.block_size, shape.kv_heads, shape.head_dim
+    if shape.layout == LAYOUT_NHD:
+        return w.reshape(NB, BS, H, D)
+    if shape.layout == LAYOUT_HND:
+        return w.reshape(NB, H, BS, D).transpose(0, 2, 1, 3)
+    if kv == 1:  # [NB][H][D][BS]
+        return w.reshape(NB, H, D, BS).transpose(0, 3, 1, 2)
+    x = 16 // shape.elem_bytes  # [NB][H][D/x][BS][x]
+    return w.reshape(NB, H, D // x, BS, x).transpose(0, 3, 1, 2, 4).reshape(NB, BS, H, D)

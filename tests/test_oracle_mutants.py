@@ -23,13 +23,19 @@ MUTANTS = {
     "layer_index_not_rebased": ("out + c * S + ((l - l0) * 2 + kv)", "out + c * S + (l * 2 + kv)"),
     "kv_major_instead_of_layer_major": ("out + c * S + ((l - l0) * 2 + kv) * Tc",
                                         "out + c * S + (kv * (l1 - l0) + (l - l0)) * Tc"),
-    "block_index_ignores_chunk_stride": ("const int64_t id = bt[c * bpc + j];\n          memcpy(out",
-                                         "const int64_t id = bt[c + j];\n          memcpy(out"),
+    "block_index_ignores_chunk_stride": ("const int64_t id = bt[c * bpc + j];\n          move_slab(s, kv, out",
+                                         "const int64_t id = bt[c + j];\n          move_slab(s, kv, out"),
     "chunk_stride_counts_all_layers": ("const int64_t S = (l1 - l0) * 2 * chunk_tokens * row;",
                                        "const int64_t S = l1 * 2 * chunk_tokens * row;"),
-    "last_chunk_strided_as_full": ("((l - l0) * 2 + kv) * Tc * row + j * slab, base",
-                                   "((l - l0) * 2 + kv) * chunk_tokens * row + j * slab, base"),
-    "scatter_block_off_by_one": ("memcpy(base + id * slab, in", "memcpy(base + (id ^ 1) * slab, in"),
+    "last_chunk_strided_as_full": ("((l - l0) * 2 + kv) * Tc * row + j * slab,\n                    (uint8_t*)base",
+                                   "((l - l0) * 2 + kv) * chunk_tokens * row + j * slab,\n                    (uint8_t*)base"),
+    "scatter_block_off_by_one": ("base + id * slab, 0);", "base + (id ^ 1) * slab, 0);"),
+    "hnd_token_head_swapped": ("if (s->layout == KVO_LAYOUT_HND) return ((h * BS + t) * D + d) * e;",
+                               "if (s->layout == KVO_LAYOUT_HND) return ((t * H + h) * D + d) * e;"),
+    "paged_attn_v_dim_token_swapped": ("if (kv == 1) return ((h * D + d) * BS + t) * e;",
+                                       "if (kv == 1) return ((h * BS + t) * D + d) * e;"),
+    "paged_attn_k_split_swapped": ("return (((h * (D / x) + d / x) * BS + t) * x + d % x) * e;",
+                                   "return (((h * (D / x) + d % x) * BS + t) * x + d / x) * e;"),
 }
 
 

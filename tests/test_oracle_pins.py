@@ -320,3 +320,63 @@ def test_elementwise_equals_slab_tiny_config():
     o2 = oracle.gather(s, *src, 0, 2, ids[:16], 256)
     o1 = oracle.gather_elementwise(ev(src[0]), ev(src[1]), 0, 2, ids[:16], 256)
     assert np.array_equal(o2.view(np.uint16), o1)
+
+
+# ---- cache layouts other than the default ------------------------------------
+
+LAYOUTS = [oracle.LAYOUT_HND, oracle.LAYOUT_PAGED_ATTN]
+
+
+def _as_default_layout(shape, m):
+    """Copy a mirror of any layout into a default-layout mirror via numpy views."""
+    s0 = oracle.Shape(shape.num_layers, shape.num_blocks, shape.block_size, shape.kv_heads,
+                      shape.head_dim, shape.elem_bytes)
+    k0, v0 = oracle.new_mirror(s0)
+    for l in range(shape.num_layers):
+        oracle.element_view(k0[l], s0)[...] = oracle.canonical_view(m[0][l], shape, 0)
+        oracle.element_view(v0[l], s0)[...] = oracle.canonical_view(m[1][l], shape, 1)
+    return s0, (k0, v0)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+@pytest.mark.parametrize("e", [2, 4])
+def test_layout_gather_equals_default_after_numpy_transpose(layout, e):
+    s = Shape(3, 20, 4, 2, 16, e, layout)
+    m = _mirror(s, 81)
+    s0, m0 = _as_default_layout(s, m)
+    bt = _ids(np.random.default_rng(8), s.num_blocks, 9)
+    for ct in (4, 8, 16):
+        assert np.array_equal(oracle.gather(s, *m, 0, 3, bt, ct), oracle.gather(s0, *m0, 0, 3, bt, ct))
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_layout_elementwise_equals_slab(layout):
+    s = Shape(2, 12, 4, 2, 16, 2, layout)
+    m = _mirror(s, 82)
+    bt = _ids(np.random.default_rng(9), s.num_blocks, 5)
+    o1 = oracle.gather_elementwise([oracle.canonical_view(a, s, 0) for a in m[0]],
+                                   [oracle.canonical_view(a, s, 1) for a in m[1]], 0, 2, bt, 8)
+    assert np.array_equal(oracle.gather(s, *m, 0, 2, bt, 8).view(np.uint16), o1)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
+def test_layout_round_trip_and_untouched(layout):
+    s = Shape(2, 30, 4, 2, 16, 2, layout)
+    src = _mirror(s, 83)
+    dst = _mirror(s, 84, role=kvsynth.ROLE_DST)
+    before = _copy(dst)
+    ids = np.random.default_rng(10).permutation(s.num_blocks).astype(np.int32)
+    img = oracle.gather(s, *src, 0, 2, ids[:11], 8)
+    oracle.scatter(s, *dst, 0, 2, ids[11:22], 8, img)
+    assert np.array_equal(oracle.gather(s, *dst, 0, 2, ids[11:22], 8), img)
+    for side in range(2):
+        for l in range(2):
+            for b in np.setdiff1d(np.arange(s.num_blocks), ids[11:22]):
+                assert np.array_equal(_slab(dst[side][l], s, b), _slab(before[side][l], s, b))
+
+
+def test_layout_rejects_head_dim_not_a_whole_number_of_16_byte_groups():
+    s = Shape(1, 4, 4, 1, 12, 2, oracle.LAYOUT_PAGED_ATTN)  # x = 8 does not divide 12
+    k, v = oracle.new_mirror(s)
+    with pytest.raises(ValueError):
+        oracle.gather(s, k, v, 0, 1, [0], 4)
