@@ -72,6 +72,8 @@ def parse():
     ap.add_argument("--slot-mib", type=int, default=64)
     ap.add_argument("--fill-threads", type=int, default=8)
     ap.add_argument("--seed", type=int, default=3)
+    ap.add_argument("--layout", default="nhd", choices=["nhd", "hnd", "paged_attn"],
+                    help="cache tensor layout (8b-80k workload)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-blocks", type=int, default=1250)
     ap.add_argument("--probe-reps", type=int, default=10)
@@ -162,7 +164,9 @@ def run_80k(args):
     log(f"workload: 8B-shaped cache {NB} blocks ({NB * L * 2 * slab / 1e9:.1f} GB), "
         f"prefix {n} blocks = {n * BS} tokens, payload {payload / 1e9:.3f} GB")
 
-    cache = kvx.PagedKVCache.allocate(L, NB, BS, H, D, torch.bfloat16, dev)
+    layout = {"nhd": kvx.KVX_LAYOUT_NHD, "hnd": kvx.KVX_LAYOUT_HND,
+              "paged_attn": kvx.KVX_LAYOUT_PAGED_ATTN}[args.layout]
+    cache = kvx.PagedKVCache.allocate(L, NB, BS, H, D, torch.bfloat16, dev, layout=layout)
     fill_cache(cache, args.seed, kvsynth.ROLE_SRC)
     perm = np.random.default_rng(args.seed).permutation(NB).astype(np.int32)
     bt_src = torch.from_numpy(perm[:n].copy()).to(dev)
@@ -223,7 +227,7 @@ def run_80k(args):
     restore_GBps = payload / med["restore_ms"] / 1e6
     cpu = None if args.no_cpu_baseline else cpu_baseline(args, L, BS, H, D, E, perm)
     traffic = None
-    if GATHER_TRAFFIC["kernels_sha256"] == kernels_sha256() and \
+    if GATHER_TRAFFIC["kernels_sha256"] == kernels_sha256() and layout == kvx.KVX_LAYOUT_NHD and \
             (args.num_blocks, args.prefix_blocks, args.chunk_tokens) == (20000, 5000, 256):
         traffic = GATHER_TRAFFIC["fetch_bytes"] + GATHER_TRAFFIC["write_bytes"]
 
@@ -233,7 +237,7 @@ def run_80k(args):
         {"workload": "llama-3-8b-shaped paged KV, 80k-token prefix (5000 blocks), "
                      "256-token chunks, 4 x 64 MiB pinned staging ring",
          "num_blocks": NB, "prefix_tokens": n * BS, "chunk_tokens": ct,
-         "slots": args.slots, "slot_mib": args.slot_mib,
+         "cache_layout": args.layout, "slots": args.slots, "slot_mib": args.slot_mib,
          "fill_threads": args.fill_threads, "parallelism": "single GPU"})
     out.update({
         "pct_hbm_peak": round(100 * gs_GBps / HBM_PEAK_GBPS, 2),
@@ -248,7 +252,8 @@ def run_80k(args):
                                  "enqueue_wait_for_fill": round(med["wait_fill_ms"], 2),
                                  "device_span": round(med["restore_dev_ms"], 2)},
         "probes": {k: round(v, 2) for k, v in probe.items()},
-        "roofline": {"bound": "hbm", "kernel": "gather (copy_units_kernel<true, false, 1024, 2>)",
+        "roofline": {"bound": "hbm",
+                     "kernel": "gather (copy_units_kernel<true, false, layout %s>)" % args.layout,
                      "achieved": round(gather_GBps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(gather_GBps / HBM_PEAK_GBPS, 4),
                      "traffic": traffic, "algorithmic_bytes": rw},

@@ -77,6 +77,19 @@ typedef enum kvx_status {
 /* Largest layer range a single call may cover. */
 #define KVX_MAX_LAYERS 128
 
+/* Cache tensor layouts (per layer; the packed chunk layout is the same for
+ * all of them, [token][head][dim] inside each (layer, K|V)):
+ *   KVX_LAYOUT_NHD         K and V [num_blocks][block_size][num_kv_heads][head_dim]
+ *   KVX_LAYOUT_HND         K and V [num_blocks][num_kv_heads][block_size][head_dim]
+ *   KVX_LAYOUT_PAGED_ATTN  K [num_blocks][num_kv_heads][head_dim / x][block_size][x]
+ *                          with x = 16 / elem_bytes, V [num_blocks][num_kv_heads]
+ *                          [head_dim][block_size] (the paged-attention kernel layout)
+ * The two transposing layouts stage each slab through LDS and need
+ * head_dim * elem_bytes to be a multiple of 16 and a slab of at most 48 KiB. */
+#define KVX_LAYOUT_NHD 0
+#define KVX_LAYOUT_HND 1
+#define KVX_LAYOUT_PAGED_ATTN 2
+
 /* Description of a paged cache. k and v are host arrays of num_layers device
  * pointers (16-byte aligned); they are read during the call only. */
 typedef struct kvx_cache {
@@ -88,6 +101,7 @@ typedef struct kvx_cache {
   int32_t num_kv_heads;
   int32_t head_dim;
   int32_t elem_bytes;    /* 1, 2, 4 or 8; the path copies raw words */
+  int32_t layout;        /* KVX_LAYOUT_*; 0 is the default */
 } kvx_cache;
 
 /* Size model of Sec. 2.1: layers * 2 * kv_heads * head_dim * elem_bytes.

@@ -23,6 +23,7 @@ from ._native import KvxCache, KvxChunkRef, KvxHostChunk, KvxPiece, KvxRingStats
 KVX_OK, KVX_EINVAL, KVX_ENOMEM, KVX_EHIP, KVX_EBADBLOCK, KVX_ECLOSED, KVX_EINTERNAL = (
     0, -1, -2, -3, -4, -5, -6)
 KVX_MAX_LAYERS = 128
+KVX_LAYOUT_NHD, KVX_LAYOUT_HND, KVX_LAYOUT_PAGED_ATTN = 0, 1, 2
 
 
 class KvxError(RuntimeError):
@@ -56,64 +57,99 @@ def _elem_bytes(dtype) -> int:
     return torch.empty((), dtype=dtype).element_size()
 
 
-class PagedKVCache:
-    """A paged KV cache: per layer, K and V device tensors of shape
-    [num_blocks, block_size, num_kv_heads, head_dim] (contiguous)."""
+def layer_shapes(num_blocks, block_size, num_kv_heads, head_dim, elem_bytes,
+                 layout=KVX_LAYOUT_NHD):
+    """Per-layer (K shape, V shape) of a cache layout."""
+    if layout == KVX_LAYOUT_NHD:
+        s = (num_blocks, block_size, num_kv_heads, head_dim)
+        return s, s
+    if layout == KVX_LAYOUT_HND:
+        s = (num_blocks, num_kv_heads, block_size, head_dim)
+        return s, s
+    if layout == KVX_LAYOUT_PAGED_ATTN:
+        x = 16 // elem_bytes
+        if head_dim % x:
+            raise ValueError(f"head_dim must be a multiple of {x} for this layout")
+        return ((num_blocks, num_kv_heads, head_dim // x, block_size, x),
+                (num_blocks, num_kv_heads, head_dim, block_size))
+    raise ValueError(f"unknown layout {layout}")
 
-    def __init__(self, k, v):
+
+class PagedKVCache:
+    """A paged KV cache: per layer, K and V device tensors in one of the
+    layouts of kvx.h (default [num_blocks, block_size, num_kv_heads, head_dim])."""
+
+    def __init__(self, k, v, layout=KVX_LAYOUT_NHD):
         if len(k) != len(v) or not k:
             raise ValueError("need the same positive number of K and V layers")
-        shape = tuple(k[0].shape)
-        if len(shape) != 4:
-            raise ValueError("cache tensors are [num_blocks, block_size, kv_heads, head_dim]")
+        ks = tuple(k[0].shape)
+        if layout == KVX_LAYOUT_NHD and len(ks) == 4:
+            nb, bs, h, d = ks
+        elif layout == KVX_LAYOUT_HND and len(ks) == 4:
+            nb, h, bs, d = ks
+        elif layout == KVX_LAYOUT_PAGED_ATTN and len(ks) == 5:
+            nb, h, dx, bs, x = ks
+            d = dx * x
+        else:
+            raise ValueError("cache tensor shape does not match the layout")
+        elem = k[0].element_size()
+        kshape, vshape = layer_shapes(nb, bs, h, d, elem, layout)
+        for t in k:
+            if tuple(t.shape) != kshape:
+                raise ValueError("all K tensors must share the layout's shape")
+        for t in v:
+            if tuple(t.shape) != vshape:
+                raise ValueError("all V tensors must share the layout's shape")
         for t in list(k) + list(v):
-            if tuple(t.shape) != shape or t.dtype != k[0].dtype or not t.is_contiguous():
-                raise ValueError("all cache tensors must share shape and dtype and be contiguous")
-            if t.device != k[0].device:
-                raise ValueError("all cache tensors must be on one device")
+            if t.dtype != k[0].dtype or not t.is_contiguous() or t.device != k[0].device:
+                raise ValueError("all cache tensors must share dtype and device and be contiguous")
         self.k, self.v = list(k), list(v)
-        self.num_blocks, self.block_size, self.num_kv_heads, self.head_dim = shape
+        self.num_blocks, self.block_size, self.num_kv_heads, self.head_dim = nb, bs, h, d
         self.num_layers = len(k)
+        self.layout = layout
         self.dtype = k[0].dtype
         self.device = k[0].device
-        self.elem_bytes = k[0].element_size()
+        self.elem_bytes = elem
         self._kp = (ctypes.c_void_p * self.num_layers)(*[t.data_ptr() for t in self.k])
         self._vp = (ctypes.c_void_p * self.num_layers)(*[t.data_ptr() for t in self.v])
         self._c = KvxCache(self._kp, self._vp, self.num_layers, self.num_blocks, self.block_size,
-                           self.num_kv_heads, self.head_dim, self.elem_bytes)
+                           self.num_kv_heads, self.head_dim, self.elem_bytes, layout)
 
     @property
     def slab_bytes(self) -> int:
         return self.block_size * self.num_kv_heads * self.head_dim * self.elem_bytes
 
     @classmethod
-    def allocate(cls, num_layers, num_blocks, block_size, num_kv_heads, head_dim, dtype, device):
+    def allocate(cls, num_layers, num_blocks, block_size, num_kv_heads, head_dim, dtype, device,
+                 layout=KVX_LAYOUT_NHD):
         import torch
 
-        mk = lambda: torch.empty((num_blocks, block_size, num_kv_heads, head_dim),  # noqa: E731
-                                 dtype=dtype, device=device)
-        return cls([mk() for _ in range(num_layers)], [mk() for _ in range(num_layers)])
+        e = torch.empty((), dtype=dtype).element_size()
+        ks, vs = layer_shapes(num_blocks, block_size, num_kv_heads, head_dim, e, layout)
+        return cls([torch.empty(ks, dtype=dtype, device=device) for _ in range(num_layers)],
+                   [torch.empty(vs, dtype=dtype, device=device) for _ in range(num_layers)],
+                   layout)
 
     @classmethod
     def from_host(cls, k_bytes, v_bytes, num_blocks, block_size, num_kv_heads, head_dim, dtype,
-                  device):
+                  device, layout=KVX_LAYOUT_NHD):
         """Upload per-layer host byte arrays (numpy uint8) into a new cache."""
         import torch
 
-        def up(b):
-            t = torch.from_numpy(b).to(device)
-            return t.view(dtype).view(num_blocks, block_size, num_kv_heads, head_dim)
-
-        return cls([up(b) for b in k_bytes], [up(b) for b in v_bytes])
+        e = torch.empty((), dtype=dtype).element_size()
+        ks, vs = layer_shapes(num_blocks, block_size, num_kv_heads, head_dim, e, layout)
+        up = lambda b, shp: torch.from_numpy(b).to(device).view(dtype).view(shp)  # noqa: E731
+        return cls([up(b, ks) for b in k_bytes], [up(b, vs) for b in v_bytes], layout)
 
     def c_struct(self) -> KvxCache:
         return self._c
 
 
-def shape_only_cache(num_layers, num_blocks, block_size, num_kv_heads, head_dim, elem_bytes):
+def shape_only_cache(num_layers, num_blocks, block_size, num_kv_heads, head_dim, elem_bytes,
+                     layout=KVX_LAYOUT_NHD):
     """A kvx_cache description with no tensors (for planning on the host)."""
     return KvxCache(None, None, num_layers, num_blocks, block_size, num_kv_heads, head_dim,
-                    elem_bytes)
+                    elem_bytes, layout)
 
 
 def _cstruct(cache):
@@ -407,5 +443,6 @@ __all__ = [
     "kvx_packed_bytes", "kvx_gather_blocks", "kvx_scatter_blocks", "kvx_check",
     "kvx_plan_pieces", "kvx_restore_from_staging", "shape_only_cache", "KVX_MAX_LAYERS",
     "kvx_gather_chunks", "kvx_scatter_chunks", "chunk_refs", "kvx_offload_to_staging",
-    "kvx_block_hashes", "kvx_dedupe_keys",
+    "kvx_block_hashes", "kvx_dedupe_keys", "KVX_LAYOUT_NHD", "KVX_LAYOUT_HND",
+    "KVX_LAYOUT_PAGED_ATTN", "layer_shapes",
 ]

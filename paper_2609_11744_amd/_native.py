@@ -13,7 +13,8 @@ c_i32, c_i64, c_vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p
 class KvxCache(ctypes.Structure):
     _fields_ = [("k", ctypes.POINTER(c_vp)), ("v", ctypes.POINTER(c_vp)),
                 ("num_layers", c_i32), ("num_blocks", c_i32), ("block_size", c_i32),
-                ("num_kv_heads", c_i32), ("head_dim", c_i32), ("elem_bytes", c_i32)]
+                ("num_kv_heads", c_i32), ("head_dim", c_i32), ("elem_bytes", c_i32),
+                ("layout", c_i32)]
 
 
 class KvxPiece(ctypes.Structure):

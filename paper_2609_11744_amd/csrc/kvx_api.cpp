@@ -30,6 +30,14 @@ kvx_status validate(const kvx_cache* c, int32_t l0, int32_t l1, int32_t n_blocks
       !mul_ok(t, c->elem_bytes, &slab))
     return KVX_EINVAL;
   if (slab % 16 != 0) return KVX_EINVAL;
+  if (c->layout != KVX_LAYOUT_NHD && c->layout != KVX_LAYOUT_HND &&
+      c->layout != KVX_LAYOUT_PAGED_ATTN)
+    return KVX_EINVAL;
+  if (c->layout != KVX_LAYOUT_NHD) {
+    // staged through LDS: whole 16-byte vectors per row, a bounded slab
+    if (((int64_t)c->head_dim * c->elem_bytes) % 16 != 0 || slab > kMaxTransposedSlab)
+      return KVX_EINVAL;
+  }
   int64_t pool = 0;
   if (!mul_ok(slab, c->num_blocks, &pool)) return KVX_EINVAL;
   const int64_t lr = l1 - l0;

@@ -10,6 +10,10 @@
 
 namespace kvx {
 
+// Largest slab the LDS-staged (transposing) layouts accept: the padded image
+// of a slab must fit the workgroup's LDS allocation.
+constexpr int64_t kMaxTransposedSlab = 48 * 1024;
+
 // Geometry of one gather / scatter call, validated on the host.
 //
 // Units: one unit is one slab (layer, K|V, block) of the image. Enumerating

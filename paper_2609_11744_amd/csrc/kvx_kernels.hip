@@ -2,9 +2,11 @@
 // scatter (packed image -> paged slabs).
 //
 // The work is pure data movement, bound by HBM bandwidth, so the kernels use
-// no MFMA and no LDS (the chunk layout keeps every slab contiguous on both
-// sides, so nothing is transposed). One workgroup moves one unit, a whole
-// slab (layer, K|V, block) of `slab` bytes:
+// no MFMA. With the default cache layout every slab is contiguous and in the
+// same order on both sides, so nothing is transposed and no LDS is used; the
+// other cache layouts stage each slab through LDS (see move_slab_transposed).
+// One workgroup moves one unit, a whole slab (layer, K|V, block) of `slab`
+// bytes:
 //   * the unit's decode (chunk, layer, K|V, block) and its block-table read
 //     depend on blockIdx only, so they run on the scalar unit once per
 //     workgroup;
@@ -48,6 +50,16 @@ struct LayerPtrs {
   char* p[2 * KVX_MAX_LAYERS];
 };
 
+// Shape of one slab, for the transposing layouts.
+struct SlabGeom {
+  uint32_t bs;   // tokens per block
+  uint32_t h;    // KV heads
+  uint32_t d;    // head dim (elements)
+  uint32_t v16;  // 16-byte vectors per (token, head) row: d * elem_bytes / 16
+  uint32_t x;    // elements per 16-byte vector: 16 / elem_bytes
+  uint32_t pad;
+};
+
 struct UnitGeom {
   uint32_t units_per_chunk;  // (l1 - l0) * 2 * bpc
   uint32_t bpc;
@@ -56,6 +68,7 @@ struct UnitGeom {
   uint32_t n16;              // 16-byte vectors per slab
   uint32_t pad;
   uint64_t slab;
+  SlabGeom sg;
 };
 
 // Sticky error word, one per device. Host code reaches it only through the
@@ -86,11 +99,111 @@ __device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __rest
   for (; i < n16; i += T) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
 }
 
+// ---- cache layouts that reorder a slab ---------------------------------------
+//
+// The packed side is always [token][head][dim]. The cache side may be
+//   KVX_LAYOUT_HND         [head][token][dim] rows (K and V);
+//   KVX_LAYOUT_PAGED_ATTN  K [head][dim / x][token][x] (x = 16 / elem_bytes: the
+//                          16-byte vectors of a row are re-strided), V
+//                          [head][dim][token] (an element transpose).
+// Such a slab is staged through LDS: the workgroup loads it in source order
+// (16-byte vectors, consecutive lanes on consecutive addresses), then writes
+// it in destination order, each lane fetching what its output vector needs
+// from LDS. Both global sides stay coalesced; only LDS sees the transpose.
+// One pad vector after every 16 spreads strided LDS reads over the banks.
+
+extern __shared__ __attribute__((aligned(16))) unsigned char kvx_lds[];
+
+__device__ __forceinline__ uint32_t lds_slot(uint32_t v) { return v + (v >> 4); }
+
+// Source vector index of destination vector w for a vector permutation
+// (HND K/V, paged-attention K). Gather: destination = packed, source = cache.
+template <bool kToPacked, int kLayout>
+__device__ __forceinline__ uint32_t src_vector(uint32_t w, const SlabGeom& g) {
+  uint32_t t, h, dv;
+  if (kToPacked) {  // w = (t * h + hh) * v16 + dv in packed order
+    dv = w % g.v16;
+    const uint32_t th = w / g.v16;
+    h = th % g.h;
+    t = th / g.h;
+    return kLayout == KVX_LAYOUT_HND ? (h * g.bs + t) * g.v16 + dv : (h * g.v16 + dv) * g.bs + t;
+  }
+  if (kLayout == KVX_LAYOUT_HND) {  // w = (h * bs + t) * v16 + dv in cache order
+    dv = w % g.v16;
+    const uint32_t r = w / g.v16;
+    t = r % g.bs;
+    h = r / g.bs;
+  } else {  // w = (h * v16 + dv) * bs + t in cache order
+    t = w % g.bs;
+    const uint32_t r = w / g.bs;
+    dv = r % g.v16;
+    h = r / g.v16;
+  }
+  return (t * g.h + h) * g.v16 + dv;
+}
+
+// Destination vector w of a paged-attention V slab move, assembled element by
+// element from the LDS image of the source (Elem = the element type).
+template <bool kToPacked, typename Elem>
+__device__ __forceinline__ v4u gather_elements(uint32_t w, const SlabGeom& g) {
+  constexpr uint32_t kX = 16 / sizeof(Elem);
+  Elem out[kX];
+#pragma unroll
+  for (uint32_t i = 0; i < kX; ++i) {
+    const uint32_t e = w * kX + i;
+    uint32_t se;
+    if (kToPacked) {  // packed element (t, h, d) <- cache element (h, d, t)
+      const uint32_t d = e % g.d, th = e / g.d, h = th % g.h, t = th / g.h;
+      se = (h * g.d + d) * g.bs + t;
+    } else {          // cache element (h, d, t) <- packed element (t, h, d)
+      const uint32_t t = e % g.bs, r = e / g.bs, d = r % g.d, h = r / g.d;
+      se = (t * g.h + h) * g.d + d;
+    }
+    const uint32_t v = se / kX, lane = se % kX;
+    out[i] = reinterpret_cast<const Elem*>(kvx_lds + 16u * lds_slot(v))[lane];
+  }
+  return __builtin_bit_cast(v4u, out);
+}
+
+template <bool kToPacked, int kLayout, int kElem, int T>
+__device__ __forceinline__ void move_slab_transposed(const v4u* __restrict__ src,
+                                                     v4u* __restrict__ dst, uint32_t n16,
+                                                     const SlabGeom& g, uint32_t kv) {
+  v4u* lds = reinterpret_cast<v4u*>(kvx_lds);
+  for (uint32_t v = threadIdx.x; v < n16; v += T) lds[lds_slot(v)] = __builtin_nontemporal_load(src + v);
+  __syncthreads();
+  if (kLayout == KVX_LAYOUT_PAGED_ATTN && kv == 1) {
+    for (uint32_t w = threadIdx.x; w < n16; w += T) {
+      v4u val;
+      if (kElem == 1) val = gather_elements<kToPacked, uint8_t>(w, g);
+      else if (kElem == 2) val = gather_elements<kToPacked, uint16_t>(w, g);
+      else if (kElem == 4) val = gather_elements<kToPacked, uint32_t>(w, g);
+      else val = gather_elements<kToPacked, uint64_t>(w, g);
+      __builtin_nontemporal_store(val, dst + w);
+    }
+  } else {
+    for (uint32_t w = threadIdx.x; w < n16; w += T)
+      __builtin_nontemporal_store(lds[lds_slot(src_vector<kToPacked, kLayout>(w, g))], dst + w);
+  }
+}
+
+// Move one slab in the direction and layout of the kernel.
+template <bool kToPacked, int kLayout, int kElem, int T, int V>
+__device__ __forceinline__ void move_unit(char* paged, char* pk, uint32_t n16, const SlabGeom& g,
+                                          uint32_t kv) {
+  const v4u* s = reinterpret_cast<const v4u*>(kToPacked ? paged : pk);
+  v4u* d = reinterpret_cast<v4u*>(kToPacked ? pk : paged);
+  if (kLayout == KVX_LAYOUT_NHD)
+    move_slab<T, V>(s, d, n16);
+  else
+    move_slab_transposed<kToPacked, kLayout, kElem, T>(s, d, n16, g, kv);
+}
+
 // kOrdered = false: units in image order (u -> chunk, layer|K|V, block).
 // kOrdered = true: unit v -> lk = v / n_blocks, k = v % n_blocks, block index
 // i = order[k] (destinations ascending by bucket); the image position u of
 // (chunk i / bpc, lk, block i % bpc) follows.
-template <bool kToPacked, bool kOrdered, int T, int V>
+template <bool kToPacked, bool kOrdered, int kLayout, int kElem, int T, int V>
 __global__ void __launch_bounds__(T)
     copy_units_kernel(LayerPtrs layers, const int32_t* __restrict__ block_table, UnitGeom g,
                       uint32_t unit_base, uint32_t unit_count,
@@ -123,10 +236,7 @@ __global__ void __launch_bounds__(T)
   }
   char* paged = layers.p[lk] + (uint64_t)(uint32_t)id * g.slab;
   char* pk = packed + (uint64_t)u * g.slab;
-  if (kToPacked)
-    move_slab<T, V>(reinterpret_cast<const v4u*>(paged), reinterpret_cast<v4u*>(pk), g.n16);
-  else
-    move_slab<T, V>(reinterpret_cast<const v4u*>(pk), reinterpret_cast<v4u*>(paged), g.n16);
+  move_unit<kToPacked, kLayout, kElem, T, V>(paged, pk, g.n16, g.sg, lk & 1);
 }
 
 // Chunk-list copy: a batch of chunks, each with its own block-table slice and
@@ -146,9 +256,10 @@ struct ChunkGeom {
   int32_t table_len;
   uint64_t slab;
   int64_t packed_bytes;
+  SlabGeom sg;
 };
 
-template <bool kToPacked, int T, int V>
+template <bool kToPacked, int kLayout, int kElem, int T, int V>
 __global__ void __launch_bounds__(T)
     copy_chunks_kernel(LayerPtrs layers, const int32_t* __restrict__ block_table,
                        const kvx_chunk_ref* __restrict__ refs, ChunkGeom g, uint32_t unit_base,
@@ -177,10 +288,7 @@ __global__ void __launch_bounds__(T)
   }
   char* paged = layers.p[lk] + (uint64_t)(uint32_t)id * g.slab;
   char* pk = packed + ref.packed_offset + (uint64_t)(lk * nc + j) * g.slab;
-  if (kToPacked)
-    move_slab<T, V>(reinterpret_cast<const v4u*>(paged), reinterpret_cast<v4u*>(pk), g.n16);
-  else
-    move_slab<T, V>(reinterpret_cast<const v4u*>(pk), reinterpret_cast<v4u*>(paged), g.n16);
+  move_unit<kToPacked, kLayout, kElem, T, V>(paged, pk, g.n16, g.sg, lk & 1);
 }
 
 // Destination order for a scatter: order[] lists the block-table indexes
@@ -247,24 +355,54 @@ constexpr uint32_t kMaxUnitsPerLaunch = 1u << 22;
 // Scatters of at least this many blocks run in destination order.
 constexpr int32_t kOrderedScatterMinBlocks = 1024;
 
+// Dynamic LDS bytes for a transposing layout: the padded slab image.
+inline size_t lds_bytes(uint32_t n16) { return 16u * (size_t)(n16 + n16 / 16 + 1); }
+
+// Launch `cnt` workgroups of kernel K<..., layout, elem, T, V> for the slab
+// shape: the default layout picks the copy shape by slab size; the others use
+// 256 threads and the LDS-staged mover.
+#define KVX_DISPATCH(KERNEL, PREFIX, ...)                                                      \
+  do {                                                                                     \
+    if (layout == KVX_LAYOUT_NHD) {                                                        \
+      if (n16 % (2 * 1024) == 0)                                                           \
+        hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_NHD, 0, 1024, 2>), grid, dim3(1024), 0, \
+                           stream, __VA_ARGS__);                                           \
+      else if (n16 % (4 * 256) == 0)                                                       \
+        hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_NHD, 0, 256, 4>), grid, dim3(256), 0,   \
+                           stream, __VA_ARGS__);                                           \
+      else                                                                                 \
+        hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_NHD, 0, 256, 1>), grid, dim3(256), 0,   \
+                           stream, __VA_ARGS__);                                           \
+    } else if (layout == KVX_LAYOUT_HND) {                                                 \
+      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_HND, 0, 256, 1>), grid, dim3(256),        \
+                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+    } else if (elem == 1) {                                                                \
+      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 1, 256, 1>), grid, dim3(256), \
+                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+    } else if (elem == 2) {                                                                \
+      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 2, 256, 1>), grid, dim3(256), \
+                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+    } else if (elem == 4) {                                                                \
+      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 4, 256, 1>), grid, dim3(256), \
+                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+    } else {                                                                               \
+      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 8, 256, 1>), grid, dim3(256), \
+                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+    }                                                                                      \
+  } while (0)
+
+#define KVX_DIR_ORDER(D, O) D, O
+
 template <bool kToPacked, bool kOrdered>
 hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, uint32_t n_units,
-                  const uint32_t* order, char* packed, int* err, hipStream_t stream) {
+                  const uint32_t* order, char* packed, int* err, int layout, int elem,
+                  hipStream_t stream) {
+  const uint32_t n16 = ug.n16;
   for (uint32_t base = 0; base < n_units; base += kMaxUnitsPerLaunch) {
     const uint32_t cnt = n_units - base < kMaxUnitsPerLaunch ? n_units - base : kMaxUnitsPerLaunch;
     const dim3 grid(cnt);
-    // Slabs of a multiple of 32 KiB: 1024 threads x 2 vectors per pass (the
-    // shape that measured fastest for 32 KiB slabs). Smaller slabs: 256
-    // threads, so that fewer lanes sit idle.
-    if (ug.n16 % (2 * 1024) == 0)
-      hipLaunchKernelGGL((copy_units_kernel<kToPacked, kOrdered, 1024, 2>), grid, dim3(1024), 0,
-                         stream, lp, bt, ug, base, cnt, order, packed, err);
-    else if (ug.n16 % (4 * 256) == 0)
-      hipLaunchKernelGGL((copy_units_kernel<kToPacked, kOrdered, 256, 4>), grid, dim3(256), 0,
-                         stream, lp, bt, ug, base, cnt, order, packed, err);
-    else
-      hipLaunchKernelGGL((copy_units_kernel<kToPacked, kOrdered, 256, 1>), grid, dim3(256), 0,
-                         stream, lp, bt, ug, base, cnt, order, packed, err);
+    KVX_DISPATCH(copy_units_kernel, KVX_DIR_ORDER(kToPacked, kOrdered), lp, bt, ug, base, cnt,
+                 order, packed, err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -274,23 +412,27 @@ hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, ui
 template <bool kToPacked>
 hipError_t launch_chunks(const LayerPtrs& lp, const int32_t* bt, const kvx_chunk_ref* refs,
                          const ChunkGeom& cg, uint32_t n_units, char* packed, int* err,
-                         hipStream_t stream) {
+                         int layout, int elem, hipStream_t stream) {
+  const uint32_t n16 = cg.n16;
   for (uint32_t base = 0; base < n_units; base += kMaxUnitsPerLaunch) {
     const uint32_t cnt = n_units - base < kMaxUnitsPerLaunch ? n_units - base : kMaxUnitsPerLaunch;
     const dim3 grid(cnt);
-    if (cg.n16 % (2 * 1024) == 0)
-      hipLaunchKernelGGL((copy_chunks_kernel<kToPacked, 1024, 2>), grid, dim3(1024), 0, stream,
-                         lp, bt, refs, cg, base, cnt, packed, err);
-    else if (cg.n16 % (4 * 256) == 0)
-      hipLaunchKernelGGL((copy_chunks_kernel<kToPacked, 256, 4>), grid, dim3(256), 0, stream, lp,
-                         bt, refs, cg, base, cnt, packed, err);
-    else
-      hipLaunchKernelGGL((copy_chunks_kernel<kToPacked, 256, 1>), grid, dim3(256), 0, stream, lp,
-                         bt, refs, cg, base, cnt, packed, err);
+    KVX_DISPATCH(copy_chunks_kernel, kToPacked, lp, bt, refs, cg, base, cnt, packed, err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
+}
+
+SlabGeom slab_geom(const kvx_cache* c) {
+  SlabGeom sg;
+  sg.bs = (uint32_t)c->block_size;
+  sg.h = (uint32_t)c->num_kv_heads;
+  sg.d = (uint32_t)c->head_dim;
+  sg.v16 = (uint32_t)((int64_t)c->head_dim * c->elem_bytes / 16);
+  sg.x = (uint32_t)(16 / c->elem_bytes);
+  sg.pad = 0;
+  return sg;
 }
 
 }  // namespace
@@ -328,10 +470,12 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.n16 = (uint32_t)(g.slab / 16);
   ug.pad = 0;
   ug.slab = (uint64_t)g.slab;
+  ug.sg = slab_geom(cache);
+  const int layout = cache->layout, elem = cache->elem_bytes;
   const uint32_t n_units = (uint32_t)g.n_units;
   if (to_packed) {
     hipError_t e = launch<true, false>(lp, block_table, ug, n_units, nullptr, (char*)packed, err,
-                                       stream);
+                                       layout, elem, stream);
     return e == hipSuccess ? KVX_OK : KVX_EHIP;
   }
   // Destination-ordered scatter for large calls; the order lives in
@@ -348,11 +492,13 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
                        (uint32_t)g.n_blocks, (uint32_t)g.num_blocks, order);
     e = hipGetLastError();
     if (e == hipSuccess)
-      e = launch<false, true>(lp, block_table, ug, n_units, order, (char*)packed, err, stream);
+      e = launch<false, true>(lp, block_table, ug, n_units, order, (char*)packed, err, layout,
+                              elem, stream);
     const hipError_t ef = hipFreeAsync(order, stream);
     if (e == hipSuccess) e = ef;
   } else {
-    e = launch<false, false>(lp, block_table, ug, n_units, nullptr, (char*)packed, err, stream);
+    e = launch<false, false>(lp, block_table, ug, n_units, nullptr, (char*)packed, err, layout,
+                             elem, stream);
   }
   return e == hipSuccess ? KVX_OK : KVX_EHIP;
 }
@@ -384,10 +530,12 @@ kvx_status launch_copy_chunks(bool to_packed, const kvx_cache* cache, int32_t l0
   cg.table_len = table_len;
   cg.slab = (uint64_t)slab;
   cg.packed_bytes = packed_bytes;
+  cg.sg = slab_geom(cache);
+  const int layout = cache->layout, elem = cache->elem_bytes;
   hipError_t e = to_packed ? launch_chunks<true>(lp, block_table, refs, cg, (uint32_t)n_units,
-                                                 (char*)packed, err, stream)
+                                                 (char*)packed, err, layout, elem, stream)
                            : launch_chunks<false>(lp, block_table, refs, cg, (uint32_t)n_units,
-                                                  (char*)packed, err, stream);
+                                                  (char*)packed, err, layout, elem, stream);
   return e == hipSuccess ? KVX_OK : KVX_EHIP;
 }
 

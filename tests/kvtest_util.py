@@ -54,7 +54,7 @@ def device_cache(shape: Shape, fill: Filled | None, device):
 
     cache = kvx.PagedKVCache.allocate(shape.num_layers, shape.num_blocks, shape.block_size,
                                       shape.kv_heads, shape.head_dim,
-                                      torch_dtype(shape.elem_bytes), device)
+                                      torch_dtype(shape.elem_bytes), device, layout=shape.layout)
     if fill is not None:
         for l in range(shape.num_layers):
             kvsynth.fill_device(cache.k[l], fill.seed, kvsynth.cache_stream(fill.role, l, 0),

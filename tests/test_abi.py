@@ -167,3 +167,14 @@ def test_scattering_pieces_equals_scattering_image(case):
                        bt[p["bt_first"]:p["bt_first"] + p["n_blocks"]], p["chunk_tokens"], part)
     for a, b in zip(whole[0] + whole[1], by_piece[0] + by_piece[1]):
         assert np.array_equal(a, b)
+
+
+def test_layout_validation_on_the_host():
+    def call(layout, H=8, D=128, e=2, BS=16):
+        c, _, _ = _fake_cache(H=H, D=D, e=e, BS=BS)
+        c.layout = layout
+        return _gather(c, 0, 4, 0x5000_0000_0000, 1, BS, 0x7000_0000_0000)
+    assert call(3) == kvx.KVX_EINVAL                          # unknown layout
+    assert call(kvx.KVX_LAYOUT_HND, BS=32) == kvx.KVX_EINVAL  # 64 KiB slab > 48 KiB LDS image
+    assert call(kvx.KVX_LAYOUT_PAGED_ATTN, H=1, D=4, e=2) == kvx.KVX_EINVAL  # 8-byte rows
+    assert call(kvx.KVX_LAYOUT_HND, H=1, D=12, e=2) == kvx.KVX_EINVAL       # 24-byte rows
