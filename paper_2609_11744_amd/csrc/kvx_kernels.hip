@@ -32,6 +32,7 @@
 #include <hip/hip_runtime.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "kvx_internal.h"
 
@@ -50,14 +51,32 @@ struct LayerPtrs {
   char* p[2 * KVX_MAX_LAYERS];
 };
 
+// Division by a divisor known only at run time, as a multiply: for d >= 2,
+// m = ceil(2^32 / d) and n / d = umulhi(n, m) whenever n * d < 2^32 (the
+// rounding error of m, below d, then moves n * m / 2^32 by less than 1/d);
+// m = 0 stands for d = 1. Every numerator here is an element or vector index
+// inside one slab and every divisor a slab dimension; a transposed slab is at
+// most kMaxTransposedSlab (48 KiB) bytes, so both are below 2^16.
+struct FastDiv {
+  uint32_t d;
+  uint32_t m;
+};
+
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) {
+  return f.m ? __umulhi(n, f.m) : n;
+}
+
 // Shape of one slab, for the transposing layouts.
 struct SlabGeom {
-  uint32_t bs;   // tokens per block
-  uint32_t h;    // KV heads
-  uint32_t d;    // head dim (elements)
-  uint32_t v16;  // 16-byte vectors per (token, head) row: d * elem_bytes / 16
-  uint32_t x;    // elements per 16-byte vector: 16 / elem_bytes
-  uint32_t pad;
+  FastDiv bs;      // tokens per block
+  FastDiv h;       // KV heads
+  FastDiv d;       // head dim (elements)
+  FastDiv v16;     // 16-byte vectors per (token, head) row: d * elem_bytes / 16
+  FastDiv pad[2];  // LDS pad period of K and V slabs (see lds_slot)
+  uint32_t x;      // elements per 16-byte vector: 16 / elem_bytes
+  uint32_t ntv;    // V tile path: vectors per (head, dim) row, bs / x; 0 if bs % x != 0
+  uint32_t tiles;  // V tile path: x-by-x tiles per slab, n16 / x
+  uint32_t pad_;
 };
 
 struct UnitGeom {
@@ -106,15 +125,41 @@ __device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __rest
 //   KVX_LAYOUT_PAGED_ATTN  K [head][dim / x][token][x] (x = 16 / elem_bytes: the
 //                          16-byte vectors of a row are re-strided), V
 //                          [head][dim][token] (an element transpose).
-// Such a slab is staged through LDS: the workgroup loads it in source order
-// (16-byte vectors, consecutive lanes on consecutive addresses), then writes
-// it in destination order, each lane fetching what its output vector needs
-// from LDS. Both global sides stay coalesced; only LDS sees the transpose.
-// One pad vector after every 16 spreads strided LDS reads over the banks.
+// Such a slab is staged through LDS so that both global sides stay coalesced
+// (consecutive lanes on consecutive 16-byte vectors) and only LDS sees the
+// reordering:
+//   * vector permutations (HND, paged-attention K): load the slab in source
+//     order into LDS, then write it in destination order, each lane fetching
+//     the source vector its output vector is;
+//   * the V element transpose works on x-by-x tiles (x dims by x tokens of one
+//     head: x vectors on each side) transposed in registers. A gather reads a
+//     tile's x cache rows from LDS and writes its x packed vectors to global
+//     memory; a scatter reads a tile's x packed vectors from global memory and
+//     writes its x cache rows into LDS, which is then stored in cache order.
+//     If bs is not a multiple of x the tiles do not exist and each output
+//     vector is assembled element by element from LDS instead.
+// Each thread issues all of its global loads before it waits for any of them,
+// so the whole slab is in flight at once (a transposed slab is at most
+// kMaxSlabVectors vectors, kVecPerThread per thread).
+
+constexpr int kTransposeThreads = 256;
+constexpr uint32_t kMaxSlabVectors = 48 * 1024 / 16;
+constexpr int kVecPerThread = (int)(kMaxSlabVectors / kTransposeThreads);  // 12
 
 extern __shared__ __attribute__((aligned(16))) unsigned char kvx_lds[];
 
-__device__ __forceinline__ uint32_t lds_slot(uint32_t v) { return v + (v >> 4); }
+// LDS slot of vector v: one pad vector after every `pad` vectors. The pad
+// period is the stride at which the slab's strided LDS accesses walk (chosen
+// per layout and direction on the host), so a wave's 16-byte accesses at that
+// stride land on distinct banks.
+__device__ __forceinline__ uint32_t lds_slot(uint32_t v, FastDiv pad) { return v + fdiv(v, pad); }
+
+// Quotient and remainder.
+__device__ __forceinline__ uint32_t divmod(uint32_t n, FastDiv f, uint32_t& rem) {
+  const uint32_t q = fdiv(n, f);
+  rem = n - q * f.d;
+  return q;
+}
 
 // Source vector index of destination vector w for a vector permutation
 // (HND K/V, paged-attention K). Gather: destination = packed, source = cache.
@@ -122,69 +167,205 @@ template <bool kToPacked, int kLayout>
 __device__ __forceinline__ uint32_t src_vector(uint32_t w, const SlabGeom& g) {
   uint32_t t, h, dv;
   if (kToPacked) {  // w = (t * h + hh) * v16 + dv in packed order
-    dv = w % g.v16;
-    const uint32_t th = w / g.v16;
-    h = th % g.h;
-    t = th / g.h;
-    return kLayout == KVX_LAYOUT_HND ? (h * g.bs + t) * g.v16 + dv : (h * g.v16 + dv) * g.bs + t;
+    t = divmod(divmod(w, g.v16, dv), g.h, h);
+    return kLayout == KVX_LAYOUT_HND ? (h * g.bs.d + t) * g.v16.d + dv
+                                     : (h * g.v16.d + dv) * g.bs.d + t;
   }
-  if (kLayout == KVX_LAYOUT_HND) {  // w = (h * bs + t) * v16 + dv in cache order
-    dv = w % g.v16;
-    const uint32_t r = w / g.v16;
-    t = r % g.bs;
-    h = r / g.bs;
-  } else {  // w = (h * v16 + dv) * bs + t in cache order
-    t = w % g.bs;
-    const uint32_t r = w / g.bs;
-    dv = r % g.v16;
-    h = r / g.v16;
-  }
-  return (t * g.h + h) * g.v16 + dv;
+  if (kLayout == KVX_LAYOUT_HND)  // w = (h * bs + t) * v16 + dv in cache order
+    h = divmod(divmod(w, g.v16, dv), g.bs, t);
+  else                            // w = (h * v16 + dv) * bs + t in cache order
+    h = divmod(divmod(w, g.bs, t), g.v16, dv);
+  return (t * g.h.d + h) * g.v16.d + dv;
 }
 
-// Destination vector w of a paged-attention V slab move, assembled element by
-// element from the LDS image of the source (Elem = the element type).
-template <bool kToPacked, typename Elem>
-__device__ __forceinline__ v4u gather_elements(uint32_t w, const SlabGeom& g) {
-  constexpr uint32_t kX = 16 / sizeof(Elem);
-  Elem out[kX];
+// Load n16 source vectors in order into the padded LDS image.
+template <int T>
+__device__ __forceinline__ void stage_in(const v4u* __restrict__ src, uint32_t n16, FastDiv pad) {
+  v4u* lds = reinterpret_cast<v4u*>(kvx_lds);
+  v4u r[kVecPerThread];
 #pragma unroll
-  for (uint32_t i = 0; i < kX; ++i) {
-    const uint32_t e = w * kX + i;
-    uint32_t se;
-    if (kToPacked) {  // packed element (t, h, d) <- cache element (h, d, t)
-      const uint32_t d = e % g.d, th = e / g.d, h = th % g.h, t = th / g.h;
-      se = (h * g.d + d) * g.bs + t;
-    } else {          // cache element (h, d, t) <- packed element (t, h, d)
-      const uint32_t t = e % g.bs, r = e / g.bs, d = r % g.d, h = r / g.d;
-      se = (t * g.h + h) * g.d + d;
+  for (int q = 0; q < kVecPerThread; ++q) {
+    const uint32_t v = threadIdx.x + q * T;
+    if (v < n16) r[q] = __builtin_nontemporal_load(src + v);
+  }
+#pragma unroll
+  for (int q = 0; q < kVecPerThread; ++q) {
+    const uint32_t v = threadIdx.x + q * T;
+    if (v < n16) lds[lds_slot(v, pad)] = r[q];
+  }
+}
+
+// x-by-x transpose of elements E held as x 16-byte vectors: b[j] element i =
+// a[i] element j.
+template <typename E>
+struct ElemRow {
+  E e[16 / sizeof(E)];
+};
+
+template <typename E>
+__device__ __forceinline__ void transpose_tile(const v4u* a, v4u* b) {
+  constexpr int X = 16 / sizeof(E);
+  ElemRow<E> in[X];
+#pragma unroll
+  for (int i = 0; i < X; ++i) in[i] = __builtin_bit_cast(ElemRow<E>, a[i]);
+#pragma unroll
+  for (int j = 0; j < X; ++j) {
+    ElemRow<E> o;
+#pragma unroll
+    for (int i = 0; i < X; ++i) o.e[i] = in[i].e[j];
+    b[j] = __builtin_bit_cast(v4u, o);
+  }
+}
+
+// Tile k of a V slab -> (head, dim vector dv, token vector tv). Tiles are
+// numbered dv fastest, then head, then tv, so for each of a tile's x packed
+// vectors consecutive lanes address consecutive packed vectors.
+struct Tile {
+  uint32_t cache0;   // cache vector of (head, dim dv * x, token vector tv)
+  uint32_t packed0;  // packed vector of (token tv * x, head, dim vector dv)
+};
+
+__device__ __forceinline__ Tile tile_of(uint32_t k, const SlabGeom& g) {
+  uint32_t dv, h;
+  const uint32_t tv = divmod(divmod(k, g.v16, dv), g.h, h);
+  Tile t;
+  t.cache0 = (h * g.v16.d + dv) * g.x * g.ntv + tv;
+  t.packed0 = (tv * g.x * g.h.d + h) * g.v16.d + dv;
+  return t;
+}
+
+// Paged-attention V gather through x-by-x tiles (the cache image is in LDS).
+// Cache row i of a tile is at stride ntv, packed vector j at stride h * v16.
+template <typename E, int T>
+__device__ __forceinline__ void tiles_to_packed(v4u* __restrict__ dst, const SlabGeom& g,
+                                                FastDiv pad) {
+  constexpr int X = 16 / sizeof(E);
+  const v4u* lds = reinterpret_cast<const v4u*>(kvx_lds);
+  const uint32_t prow = g.h.d * g.v16.d;
+  for (uint32_t k = threadIdx.x; k < g.tiles; k += T) {
+    const Tile t = tile_of(k, g);
+    v4u a[X], b[X];
+#pragma unroll
+    for (int i = 0; i < X; ++i) a[i] = lds[lds_slot(t.cache0 + i * g.ntv, pad)];
+    transpose_tile<E>(a, b);
+#pragma unroll
+    for (int j = 0; j < X; ++j) __builtin_nontemporal_store(b[j], dst + t.packed0 + j * prow);
+  }
+}
+
+// Paged-attention V scatter through x-by-x tiles: read each tile's packed
+// vectors from global memory (all of a thread's tiles in flight at once),
+// transpose, and place the cache rows in LDS.
+template <typename E, int T>
+__device__ __forceinline__ void tiles_from_packed(const v4u* __restrict__ src, const SlabGeom& g,
+                                                  FastDiv pad) {
+  constexpr int X = 16 / sizeof(E);
+  constexpr int kTiles = (kVecPerThread + X - 1) / X;  // tiles per thread at most
+  v4u* lds = reinterpret_cast<v4u*>(kvx_lds);
+  const uint32_t prow = g.h.d * g.v16.d;
+  v4u a[kTiles][X];
+#pragma unroll
+  for (int m = 0; m < kTiles; ++m) {
+    const uint32_t k = threadIdx.x + m * T;
+    if (k < g.tiles) {
+      const Tile t = tile_of(k, g);
+#pragma unroll
+      for (int j = 0; j < X; ++j) a[m][j] = __builtin_nontemporal_load(src + t.packed0 + j * prow);
     }
-    const uint32_t v = se / kX, lane = se % kX;
-    out[i] = reinterpret_cast<const Elem*>(kvx_lds + 16u * lds_slot(v))[lane];
+  }
+#pragma unroll
+  for (int m = 0; m < kTiles; ++m) {
+    const uint32_t k = threadIdx.x + m * T;
+    if (k < g.tiles) {
+      const Tile t = tile_of(k, g);
+      v4u b[X];
+      transpose_tile<E>(a[m], b);
+#pragma unroll
+      for (int i = 0; i < X; ++i) lds[lds_slot(t.cache0 + i * g.ntv, pad)] = b[i];
+    }
+  }
+}
+
+// Paged-attention V when bs is not a multiple of x: destination vector w
+// assembled element by element from the LDS image of the source.
+template <bool kToPacked, typename E>
+__device__ __forceinline__ v4u gather_elements(uint32_t w, const SlabGeom& g, FastDiv pad) {
+  constexpr uint32_t kX = 16 / sizeof(E);
+  ElemRow<E> out;
+  uint32_t se, step;  // source element of output element 0, and per-element stride
+  uint32_t t, d, h;
+  if (kToPacked) {  // packed (t, h, d0 + i) <- cache element (h, d0 + i, t): stride bs
+    uint32_t dv;
+    t = divmod(divmod(w, g.v16, dv), g.h, h);
+    se = (h * g.d.d + dv * kX) * g.bs.d + t;
+    step = g.bs.d;
+#pragma unroll
+    for (uint32_t i = 0; i < kX; ++i) {
+      const uint32_t e = se + i * step;
+      out.e[i] = reinterpret_cast<const E*>(kvx_lds + 16u * lds_slot(e / kX, pad))[e % kX];
+    }
+  } else {          // cache element (h, d, t) <- packed element (t, h, d); t runs fastest
+    h = divmod(divmod(w * kX, g.bs, t), g.d, d);
+#pragma unroll
+    for (uint32_t i = 0; i < kX; ++i) {
+      const uint32_t e = (t * g.h.d + h) * g.d.d + d;
+      out.e[i] = reinterpret_cast<const E*>(kvx_lds + 16u * lds_slot(e / kX, pad))[e % kX];
+      if (++t == g.bs.d) {
+        t = 0;
+        if (++d == g.d.d) { d = 0; ++h; }
+      }
+    }
   }
   return __builtin_bit_cast(v4u, out);
+}
+
+// Write n16 destination vectors in order, each produced by f(w).
+template <int T, typename F>
+__device__ __forceinline__ void stage_out(v4u* __restrict__ dst, uint32_t n16, F f) {
+  v4u r[kVecPerThread];
+#pragma unroll
+  for (int q = 0; q < kVecPerThread; ++q) {
+    const uint32_t w = threadIdx.x + q * T;
+    if (w < n16) r[q] = f(w);
+  }
+#pragma unroll
+  for (int q = 0; q < kVecPerThread; ++q) {
+    const uint32_t w = threadIdx.x + q * T;
+    if (w < n16) __builtin_nontemporal_store(r[q], dst + w);
+  }
 }
 
 template <bool kToPacked, int kLayout, int kElem, int T>
 __device__ __forceinline__ void move_slab_transposed(const v4u* __restrict__ src,
                                                      v4u* __restrict__ dst, uint32_t n16,
                                                      const SlabGeom& g, uint32_t kv) {
-  v4u* lds = reinterpret_cast<v4u*>(kvx_lds);
-  for (uint32_t v = threadIdx.x; v < n16; v += T) lds[lds_slot(v)] = __builtin_nontemporal_load(src + v);
-  __syncthreads();
-  if (kLayout == KVX_LAYOUT_PAGED_ATTN && kv == 1) {
-    for (uint32_t w = threadIdx.x; w < n16; w += T) {
-      v4u val;
-      if (kElem == 1) val = gather_elements<kToPacked, uint8_t>(w, g);
-      else if (kElem == 2) val = gather_elements<kToPacked, uint16_t>(w, g);
-      else if (kElem == 4) val = gather_elements<kToPacked, uint32_t>(w, g);
-      else val = gather_elements<kToPacked, uint64_t>(w, g);
-      __builtin_nontemporal_store(val, dst + w);
+  typedef typename std::conditional<
+      kElem == 1, uint8_t,
+      typename std::conditional<kElem == 2, uint16_t,
+                                typename std::conditional<kElem == 4, uint32_t,
+                                                          uint64_t>::type>::type>::type E;
+  const FastDiv pad = g.pad[kv];
+  const v4u* lds = reinterpret_cast<const v4u*>(kvx_lds);
+  if (kLayout == KVX_LAYOUT_PAGED_ATTN && kv == 1 && g.tiles != 0) {
+    if (kToPacked) {
+      stage_in<T>(src, n16, pad);
+      __syncthreads();
+      tiles_to_packed<E, T>(dst, g, pad);
+    } else {
+      tiles_from_packed<E, T>(src, g, pad);
+      __syncthreads();
+      stage_out<T>(dst, n16, [&](uint32_t w) { return lds[lds_slot(w, pad)]; });
     }
-  } else {
-    for (uint32_t w = threadIdx.x; w < n16; w += T)
-      __builtin_nontemporal_store(lds[lds_slot(src_vector<kToPacked, kLayout>(w, g))], dst + w);
+    return;
   }
+  stage_in<T>(src, n16, pad);
+  __syncthreads();
+  if (kLayout == KVX_LAYOUT_PAGED_ATTN && kv == 1)
+    stage_out<T>(dst, n16, [&](uint32_t w) { return gather_elements<kToPacked, E>(w, g, pad); });
+  else
+    stage_out<T>(dst, n16, [&](uint32_t w) {
+      return lds[lds_slot(src_vector<kToPacked, kLayout>(w, g), pad)];
+    });
 }
 
 // Move one slab in the direction and layout of the kernel.
@@ -356,7 +537,10 @@ constexpr uint32_t kMaxUnitsPerLaunch = 1u << 22;
 constexpr int32_t kOrderedScatterMinBlocks = 1024;
 
 // Dynamic LDS bytes for a transposing layout: the padded slab image.
-inline size_t lds_bytes(uint32_t n16) { return 16u * (size_t)(n16 + n16 / 16 + 1); }
+inline size_t lds_bytes(uint32_t n16, const SlabGeom& sg) {
+  const uint32_t pad = sg.pad[0].d < sg.pad[1].d ? sg.pad[0].d : sg.pad[1].d;
+  return 16u * (size_t)(n16 + n16 / pad + 1);
+}
 
 // Launch `cnt` workgroups of kernel K<..., layout, elem, T, V> for the slab
 // shape: the default layout picks the copy shape by slab size; the others use
@@ -375,19 +559,19 @@ inline size_t lds_bytes(uint32_t n16) { return 16u * (size_t)(n16 + n16 / 16 + 1
                            stream, __VA_ARGS__);                                           \
     } else if (layout == KVX_LAYOUT_HND) {                                                 \
       hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_HND, 0, 256, 1>), grid, dim3(256),        \
-                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
     } else if (elem == 1) {                                                                \
       hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 1, 256, 1>), grid, dim3(256), \
-                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
     } else if (elem == 2) {                                                                \
       hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 2, 256, 1>), grid, dim3(256), \
-                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
     } else if (elem == 4) {                                                                \
       hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 4, 256, 1>), grid, dim3(256), \
-                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
     } else {                                                                               \
       hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 8, 256, 1>), grid, dim3(256), \
-                         lds_bytes(n16), stream, __VA_ARGS__);                             \
+                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
     }                                                                                      \
   } while (0)
 
@@ -398,6 +582,7 @@ hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, ui
                   const uint32_t* order, char* packed, int* err, int layout, int elem,
                   hipStream_t stream) {
   const uint32_t n16 = ug.n16;
+  const SlabGeom& sg = ug.sg;
   for (uint32_t base = 0; base < n_units; base += kMaxUnitsPerLaunch) {
     const uint32_t cnt = n_units - base < kMaxUnitsPerLaunch ? n_units - base : kMaxUnitsPerLaunch;
     const dim3 grid(cnt);
@@ -414,6 +599,7 @@ hipError_t launch_chunks(const LayerPtrs& lp, const int32_t* bt, const kvx_chunk
                          const ChunkGeom& cg, uint32_t n_units, char* packed, int* err,
                          int layout, int elem, hipStream_t stream) {
   const uint32_t n16 = cg.n16;
+  const SlabGeom& sg = cg.sg;
   for (uint32_t base = 0; base < n_units; base += kMaxUnitsPerLaunch) {
     const uint32_t cnt = n_units - base < kMaxUnitsPerLaunch ? n_units - base : kMaxUnitsPerLaunch;
     const dim3 grid(cnt);
@@ -424,14 +610,42 @@ hipError_t launch_chunks(const LayerPtrs& lp, const int32_t* bt, const kvx_chunk
   return hipSuccess;
 }
 
-SlabGeom slab_geom(const kvx_cache* c) {
+FastDiv fast_div(uint32_t d) {
+  FastDiv f;
+  f.d = d;
+  f.m = d == 1 ? 0u : (uint32_t)(((1ull << 32) + d - 1) / d);
+  return f;
+}
+
+// Slab shape and LDS pad periods for a transposing layout. The pad period of
+// a slab kind is the stride (in vectors) of its strided LDS accesses:
+//   gather (cache image in LDS): HND reads head rows, stride bs * v16;
+//     paged-attention K and V read token / dim rows, stride bs;
+//   scatter (packed image in LDS): HND and paged-attention K read token rows,
+//     stride h * v16; paged-attention V tiles write dim rows, stride bs, and
+//     the element fallback reads token rows of elements, stride h * d.
+SlabGeom slab_geom(const kvx_cache* c, bool to_packed) {
+  const uint32_t bs = (uint32_t)c->block_size, h = (uint32_t)c->num_kv_heads,
+                 d = (uint32_t)c->head_dim, x = (uint32_t)(16 / c->elem_bytes),
+                 v16 = (uint32_t)((int64_t)c->head_dim * c->elem_bytes / 16);
   SlabGeom sg;
-  sg.bs = (uint32_t)c->block_size;
-  sg.h = (uint32_t)c->num_kv_heads;
-  sg.d = (uint32_t)c->head_dim;
-  sg.v16 = (uint32_t)((int64_t)c->head_dim * c->elem_bytes / 16);
-  sg.x = (uint32_t)(16 / c->elem_bytes);
-  sg.pad = 0;
+  sg.bs = fast_div(bs);
+  sg.h = fast_div(h);
+  sg.d = fast_div(d);
+  sg.v16 = fast_div(v16 ? v16 : 1);
+  sg.x = x;
+  sg.ntv = bs % x == 0 ? bs / x : 0;
+  sg.tiles = sg.ntv * h * v16;  // n16 / x (0 without tiles)
+  sg.pad_ = 0;
+  uint32_t pk, pv;
+  if (c->layout == KVX_LAYOUT_HND) {
+    pk = pv = to_packed ? bs * v16 : h * v16;
+  } else {
+    pk = to_packed ? bs : h * v16;
+    pv = (to_packed || sg.ntv) ? bs : h * d;
+  }
+  sg.pad[0] = fast_div(pk < 8 ? 8 : pk);
+  sg.pad[1] = fast_div(pv < 8 ? 8 : pv);
   return sg;
 }
 
@@ -470,7 +684,7 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.n16 = (uint32_t)(g.slab / 16);
   ug.pad = 0;
   ug.slab = (uint64_t)g.slab;
-  ug.sg = slab_geom(cache);
+  ug.sg = slab_geom(cache, to_packed);
   const int layout = cache->layout, elem = cache->elem_bytes;
   const uint32_t n_units = (uint32_t)g.n_units;
   if (to_packed) {
@@ -530,7 +744,7 @@ kvx_status launch_copy_chunks(bool to_packed, const kvx_cache* cache, int32_t l0
   cg.table_len = table_len;
   cg.slab = (uint64_t)slab;
   cg.packed_bytes = packed_bytes;
-  cg.sg = slab_geom(cache);
+  cg.sg = slab_geom(cache, to_packed);
   const int layout = cache->layout, elem = cache->elem_bytes;
   hipError_t e = to_packed ? launch_chunks<true>(lp, block_table, refs, cg, (uint32_t)n_units,
                                                  (char*)packed, err, layout, elem, stream)

@@ -38,6 +38,12 @@ CASES = [
     (PA, 2, 16, 2, 32, 1, 1, 2, 5, 48),       # 1-byte elements (x = 16)
     (PA, 2, 4, 1, 16, 8, 0, 2, 6, 8),         # 8-byte elements (x = 2)
     (PA, 2, 5, 2, 16, 2, 0, 2, 7, 15),        # block size not a multiple of x
+    (PA, 2, 16, 12, 128, 2, 0, 2, 5, 32),     # 48 KiB slabs, the largest transposed
+    (HND, 2, 16, 12, 128, 2, 0, 2, 5, 32),
+    (PA, 2, 32, 4, 128, 2, 0, 2, 6, 64),      # 4 token vectors per value row
+    (PA, 2, 16, 16, 96, 1, 0, 2, 5, 32),      # 1-byte elements, 24 KiB slabs
+    (PA, 2, 1, 8, 64, 2, 0, 2, 9, 3),         # one token per block
+    (PA, 2, 3, 5, 40, 2, 0, 2, 7, 9),         # odd block size and head count
 ]
 
 
