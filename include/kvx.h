@@ -336,6 +336,50 @@ int64_t kvx_block_hashes(const int32_t* tokens, int64_t n_tokens, int32_t block_
  * first_of[i] == i. Pure host code. */
 kvx_status kvx_dedupe_keys(const uint64_t* keys, int32_t n, int32_t* first_of);
 
+/* ---- break-even gate (host) --------------------------------------------------- */
+
+/* A timing curve from an offline calibration sweep (Sec. 4.1, Pareto capture):
+ * seconds[i] measured at a document (or prefix) of tokens[i] tokens. tokens
+ * strictly ascending, n >= 2, every value finite; the caller owns both arrays.
+ * Between points the curve is linear; beyond either end it continues the end
+ * segment's line. Any invalid curve makes the calls below return KVX_EINVAL. */
+typedef struct {
+  const double* tokens;
+  const double* seconds;
+  int32_t n;
+} kvx_curve;
+
+/* *out = the curve at `tokens`. */
+kvx_status kvx_curve_eval(const kvx_curve* c, double tokens, double* out);
+
+/* *out = 1 when loading a cached prefix of prefix_tokens of a doc_tokens
+ * document beats recomputing it (Sec. 4.1): hit(P) + cold(D - P) < cold(D),
+ * with cold the full-prefill TTFT curve and hit the cache-hit TTFT curve;
+ * else 0. Requires 0 <= prefix_tokens <= doc_tokens. */
+kvx_status kvx_load_beats_recompute(const kvx_curve* cold, const kvx_curve* hit,
+                                    int64_t doc_tokens, int64_t prefix_tokens, int32_t* out);
+
+/* The break-even frontier at one document size (Sec. 5.2): *out = the
+ * smallest P in {g, 2g, ...} (g = granularity, e.g. the chunk size), P <=
+ * doc_tokens, for which loading beats recomputing; -1 if none does. */
+kvx_status kvx_break_even_prefix(const kvx_curve* cold, const kvx_curve* hit, int64_t doc_tokens,
+                                 int32_t granularity, int64_t* out);
+
+/* The gate's threshold for one source tier (Sec. 6.6): *out = the smallest x
+ * in {g, 2g, ...}, x <= max_tokens, such that a fully cached prompt of every
+ * grid size from x through max_tokens loads faster than it recomputes
+ * (hit(y) < cold(y)); -1 if even max_tokens does not. A reusable prefix below
+ * the threshold is recomputed instead of loaded. */
+kvx_status kvx_break_even_tokens(const kvx_curve* cold, const kvx_curve* hit, int64_t max_tokens,
+                                 int32_t granularity, int64_t* out);
+
+/* The transfer budget of a fully cached document (Sec. 5.2): *out_seconds =
+ * cold(D) - (hit(D) - copy(D)), copy being the measured KV transfer time of
+ * the hit path. Its KV bytes divided by this budget is the bandwidth a cache
+ * path must sustain to match recomputation. */
+kvx_status kvx_max_io(const kvx_curve* cold, const kvx_curve* hit, const kvx_curve* copy,
+                      int64_t doc_tokens, double* out_seconds);
+
 /* Pinned host memory of exactly `bytes` (hipHostMalloc), for host images. */
 kvx_status kvx_pinned_alloc(int64_t bytes, void** out);
 kvx_status kvx_pinned_free(void* p);

@@ -36,6 +36,11 @@ class KvxRingStats(ctypes.Structure):
                 ("wait_fill_ms", ctypes.c_double), ("enqueue_ms", ctypes.c_double)]
 
 
+class KvxCurve(ctypes.Structure):
+    _fields_ = [("tokens", ctypes.POINTER(ctypes.c_double)),
+                ("seconds", ctypes.POINTER(ctypes.c_double)), ("n", c_i32)]
+
+
 # name -> (restype, argtypes); every symbol include/kvx.h declares.
 SIGNATURES = {
     "kvx_bytes_per_token": (c_i64, [c_i32, c_i32, c_i32, c_i32]),
@@ -68,6 +73,17 @@ SIGNATURES = {
     "kvx_ring_destroy": (ctypes.c_int, [c_vp]),
     "kvx_block_hashes": (c_i64, [c_vp, c_i64, c_i32, ctypes.c_uint64, c_vp]),
     "kvx_dedupe_keys": (ctypes.c_int, [c_vp, c_i32, c_vp]),
+    "kvx_curve_eval": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.c_double,
+                                      ctypes.POINTER(ctypes.c_double)]),
+    "kvx_load_beats_recompute": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.POINTER(KvxCurve),
+                                                c_i64, c_i64, ctypes.POINTER(c_i32)]),
+    "kvx_break_even_prefix": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.POINTER(KvxCurve),
+                                             c_i64, c_i32, ctypes.POINTER(c_i64)]),
+    "kvx_break_even_tokens": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.POINTER(KvxCurve),
+                                             c_i64, c_i32, ctypes.POINTER(c_i64)]),
+    "kvx_max_io": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.POINTER(KvxCurve),
+                                  ctypes.POINTER(KvxCurve), c_i64,
+                                  ctypes.POINTER(ctypes.c_double)]),
     "kvx_pinned_alloc": (ctypes.c_int, [c_i64, ctypes.POINTER(c_vp)]),
     "kvx_pinned_free": (ctypes.c_int, [c_vp]),
 }

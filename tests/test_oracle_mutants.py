@@ -54,3 +54,55 @@ def test_pins_reject_mutant(name, tmp_path):
                         os.path.join(ROOT, "tests", "test_oracle_pins.py")],
                        env=env, cwd=ROOT, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"pins did not catch mutant {name}:\n{r.stdout[-2000:]}"
+
+
+# ---- the break-even oracle (Python): text edits of oracle/breakeven.py, loaded
+# as a module and run through the oracle pins of test_breakeven.py in-process.
+
+BE_SRC = os.path.join(ROOT, "oracle", "breakeven.py")
+BE_MUTANTS = {
+    "pays_not_strict": ("return g(P) + f(D - P) < f(D)", "return g(P) + f(D - P) <= f(D)"),
+    "suffix_recompute_dropped": ("return g(P) + f(D - P) < f(D)", "return g(P) < f(D)"),
+    "max_io_copy_sign": ("return f(D) - (g(D) - copy(D))", "return f(D) - g(D) - copy(D)"),
+    "threshold_first_crossing": ("if all(g(y) < f(y) for y in grid if y >= x):",
+                                 "if g(x) < f(x):"),
+    "no_segment_walk": ("    while i < n - 2 and x > tokens[i + 1]:\n        i += 1\n", ""),
+    "extrapolation_clamped": ("    return y0 + slope * (x - x0)",
+                              "    return y0 + slope * (min(max(x, tokens[0]), tokens[-1]) - x0)"),
+    "prefix_grid_starts_at_zero": ("for P in range(granularity, D + 1, granularity):",
+                                   "for P in range(0, D + 1, granularity):"),
+    "gate_declines_empty_loads": ("return [lb == 0 or lb * block_size >= gate_tokens",
+                                  "return [lb * block_size >= gate_tokens"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(BE_MUTANTS))
+def test_breakeven_pins_reject_mutant(name, tmp_path, monkeypatch):
+    import importlib.util
+
+    old, new = BE_MUTANTS[name]
+    text = open(BE_SRC).read()
+    assert text.count(old) >= 1, f"mutation anchor for {name} not found"
+    path = tmp_path / "breakeven_mutant.py"
+    path.write_text(text.replace(old, new, 1))
+    spec = importlib.util.spec_from_file_location("breakeven_mutant", path)
+    mod = importlib.util.module_from_spec(spec)
+    spec.loader.exec_module(mod)
+    sys.path.insert(0, os.path.join(ROOT, "tests"))
+    try:
+        import test_breakeven as tb
+    finally:
+        sys.path.pop(0)
+    monkeypatch.setattr(tb, "ob", mod)
+    caught = False
+    pins = [(tb.test_oracle_curve_interpolates_and_extrapolates, ()),
+            (tb.test_oracle_special_cases, ()), (tb.test_oracle_exact_tie_does_not_pay, ()),
+            (tb.test_oracle_brute_force_frontier_is_minimal, ())]
+    pins += [(tb.test_oracle_linear_closed_forms, case) for case in tb.LINES]
+    for fn, args in pins:
+        try:
+            fn(*args)
+        except Exception:
+            caught = True
+            break
+    assert caught, f"break-even pins did not catch mutant {name}"
