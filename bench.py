@@ -77,6 +77,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-blocks", type=int, default=1250)
     ap.add_argument("--probe-reps", type=int, default=10)
+    ap.add_argument("--offload-reps", type=int, default=3,
+                    help="reps of the staged offload leg (8b-80k), timed after the steps")
     return ap.parse_args()
 
 
@@ -216,6 +218,7 @@ def run_80k(args):
     wall_ms = (time.perf_counter() - t_begin) * 1e3
     kvx.kvx_check()
     log("timed steps done")
+    offload = offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe)
 
     med = {k: statistics.median(v) for k, v in rec.items()}
     mean_g = statistics.mean(rec["gather_ms"])
@@ -251,6 +254,7 @@ def run_80k(args):
         "restore_breakdown_ms": {"fill_thread_sum": round(med["fill_ms"], 2),
                                  "enqueue_wait_for_fill": round(med["wait_fill_ms"], 2),
                                  "device_span": round(med["restore_dev_ms"], 2)},
+        "offload": offload,
         "probes": {k: round(v, 2) for k, v in probe.items()},
         "roofline": {"bound": "hbm",
                      "kernel": "gather (copy_units_kernel<true, false, layout %s>)" % args.layout,
@@ -262,6 +266,47 @@ def run_80k(args):
     print(json.dumps(out), flush=True)
     ring.close()
     image.free()
+
+
+def offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe):
+    """The store direction at the same size: gather of the prefix blocks into
+    ring slots and D2H into host chunks (the pinned restore image is reused as
+    the sink once the timed steps are done), timed separately after them."""
+    import torch
+
+    import paper_2609_11744_amd as kvx
+
+    if args.offload_reps <= 0:
+        return None
+    BS = cache.block_size
+    bpc = ct // BS
+    per_block = image.nbytes // n
+    sinks = [(image.array[b * per_block:min(n, b + bpc) * per_block], b, min(bpc, n - b))
+             for b in range(0, n, bpc)]
+    ring = kvx.StagingRing(dev, args.slots, args.slot_mib << 20)
+    try:
+        ring.bind_offload(cache, 0, L, ct, sinks, drain_threads=args.fill_threads)
+        times, drain, wait = [], [], []
+        kvx.kvx_offload_to_staging(ring, bt_src)  # warm-up
+        for _ in range(args.offload_reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            kvx.kvx_offload_to_staging(ring, bt_src)  # returns once every byte is in the sinks
+            times.append(time.perf_counter() - t0)
+            st = ring.stats()
+            drain.append(st["fill_ms"])
+            wait.append(st["wait_fill_ms"])
+        kvx.kvx_check()
+    finally:
+        ring.close()
+    t = statistics.median(times)
+    gbps = image.nbytes / t / 1e9
+    log("offload leg done")
+    return {"offload_ms": round(t * 1e3, 3), "offload_GBps": round(gbps, 2),
+            "offload_frac_of_d2h": round(gbps / probe["d2h_GBps"], 4),
+            "reps": args.offload_reps,
+            "breakdown_ms": {"drain_thread_sum": round(statistics.median(drain), 2),
+                             "wait_for_drain": round(statistics.median(wait), 2)}}
 
 
 def cpu_baseline(args, L, BS, H, D, E, perm):
