@@ -286,7 +286,7 @@ def offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe):
     ring = kvx.StagingRing(dev, args.slots, args.slot_mib << 20)
     try:
         ring.bind_offload(cache, 0, L, ct, sinks, drain_threads=args.fill_threads)
-        times, drain, wait = [], [], []
+        times, drain, wait, st = [], [], [], {}
         kvx.kvx_offload_to_staging(ring, bt_src)  # warm-up
         for _ in range(args.offload_reps):
             torch.cuda.synchronize()
@@ -305,6 +305,8 @@ def offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe):
     return {"offload_ms": round(t * 1e3, 3), "offload_GBps": round(gbps, 2),
             "offload_frac_of_d2h": round(gbps / probe["d2h_GBps"], 4),
             "reps": args.offload_reps,
+            "d2h_copies": "DMA engine (id bit %d)" % st["dma_engine"] if st.get("dma_d2h")
+                          else "HIP runtime",
             "breakdown_ms": {"drain_thread_sum": round(statistics.median(drain), 2),
                              "wait_for_drain": round(statistics.median(wait), 2)}}
 

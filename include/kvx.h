@@ -298,6 +298,12 @@ typedef struct kvx_ring_stats {
   double fill_ms;         /* summed fill (restore) or drain (offload) thread copy time */
   double wait_fill_ms;    /* time the enqueuing thread waited for fill or drain threads */
   double enqueue_ms;      /* wall time of the last restore or offload call */
+  int32_t dma_d2h;        /* 1: the last offload's device-to-host copies ran on the GPU's DMA
+                             engine (issued directly); 0: restore, or copies through the HIP
+                             runtime (which may run them as a copy kernel on compute units) */
+  int32_t dma_engine;     /* with dma_d2h: the engine's id bit (the fastest of the runtime's
+                             preferred, else available, engines, timed when the ring was
+                             created); 0 = the runtime's own choice */
 } kvx_ring_stats;
 
 kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out);
@@ -309,11 +315,13 @@ kvx_status kvx_ring_abort(kvx_ring* ring);
 /* Fault-injection hooks for testing the slot-reuse protocol from the host.
  * max_delay_us > 0: each fill or drain thread pauses a pseudo-random 0 ..
  * max_delay_us microseconds before every piece (varies the interleavings).
- * poison != 0: a restore's fill threads overwrite their share of a released
+ * flags bit 0: a restore's fill threads overwrite their share of a released
  * host slot with 0xA5 bytes (then pause) before refilling it, so a copy that
- * still read a released slot would deliver the poison. Off by default; call
- * between transfers. */
-kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t poison);
+ * still read a released slot would deliver the poison.
+ * flags bit 1: offload copies go through the HIP runtime on the side stream
+ * even when the DMA engine is set up (exercises that path).
+ * Other bits: KVX_EINVAL. Off by default; call between transfers. */
+kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t flags);
 
 /* Wait for the ring's side stream and last restore, then free everything the
  * ring owns. */

@@ -45,6 +45,6 @@ def build_library(jobs: int = 8) -> str:
         raise RuntimeError(f"compile failed: {bad}")
     tmp = LIB + ".tmp"
     subprocess.run(["hipcc", "--offload-arch=gfx950", "-shared", "-fPIC", "-o", tmp, *objs,
-                    "-lpthread"], check=True, cwd=ROOT)
+                    "-lpthread", "-L/opt/rocm/lib", "-lhsa-runtime64"], check=True, cwd=ROOT)
     os.replace(tmp, LIB)
     return LIB

@@ -1,8 +1,8 @@
 // Bounded pinned staging ring: the staged restore (load) and the staged
 // offload (store) of Sec. 6.4. The pool is one contiguous, aligned, pinned
 // host allocation cut into fixed slots; a transfer larger than the pool moves
-// piece by piece; a slot is reused only after the device event of the copy
-// that last used it has completed. Stores use the reverse pipeline.
+// piece by piece; a slot is reused only after the copy that last used it has
+// completed. Stores use the reverse pipeline.
 //
 // Restore, piece i on slot s = i mod n_slots:
 //   fill    host threads copy the piece's chunk images into host slot s, after
@@ -13,17 +13,26 @@
 //   scatter the caller's stream waits on copy_done[s], runs one fused
 //           chunk-list scatter from device slot s, records dev_done[s].
 // Offload, piece i on slot s:
-//   gather  the caller's stream waits on copy_done[s] (the D2H copy of piece
-//           i - n_slots has read device slot s), runs one fused chunk-list
-//           gather into device slot s, records dev_done[s];
-//   D2H     once the drain threads have emptied host slot s, the side stream
-//           waits on dev_done[s], copies device slot s to host slot s and
-//           records copy_done[s];
-//   drain   host threads wait on copy_done[s] and copy host slot s to the
+//   gather  once the D2H copy of piece i - n_slots has left device slot s,
+//           the caller's stream runs one fused chunk-list gather into it and
+//           records dev_done[s] (a system-scope release);
+//   D2H     when dev_done[s] has completed and the drain threads have emptied
+//           host slot s, device slot s is copied to host slot s by the GPU's
+//           DMA engine, completion on dma_done[s];
+//   drain   host threads wait on dma_done[s] and copy host slot s to the
 //           chunks' destinations.
+// The D2H copies are issued to the DMA engine directly (HSA async copy):
+// enqueued through the HIP runtime, a device-to-host copy may run as a copy
+// kernel instead, which occupies compute units for the whole link-bound
+// transfer and starves the kernels it was meant to overlap (Sec. 5.1 contrasts
+// DMA copies with a copy kernel that consumes GPU compute). If the DMA engine
+// cannot be set up, the offload falls back to the HIP copy on a side stream
+// ordered by copy_done / dev_done events, and the ring's stats say so.
 // The enqueuing thread never waits for the device in a restore; fill and
-// drain threads wait on copy_done events (blocking-sync events: they sleep).
+// drain threads wait on copy_done events or DMA signals (they sleep).
 #include <hip/hip_runtime_api.h>
+#include <hsa/hsa.h>
+#include <hsa/hsa_ext_amd.h>
 
 #include <algorithm>
 #include <atomic>
@@ -54,6 +63,13 @@ struct kvx_ring {
   std::vector<hipEvent_t> copy_done;  // H2D / D2H of the slot's last piece (host waits)
   std::vector<hipEvent_t> dev_done;   // scatter / gather of the slot's last piece
 
+  // offload D2H on the DMA engine
+  bool dma = false;
+  bool hsa_up = false;
+  hsa_agent_t gpu_agent{}, cpu_agent{};
+  uint32_t dma_engine = 0;             // SDMA engine id bit for the copies; 0: the runtime's choice
+  std::vector<hsa_signal_t> dma_done;  // per slot: copies of its last piece still running
+
   // binding
   Dir dir = Dir::kNone;
   std::vector<void*> kptr, vptr;
@@ -79,6 +95,7 @@ struct kvx_ring {
   // test hooks (kvx_ring_set_test_hooks)
   int32_t hook_max_delay_us = 0;
   bool hook_poison = false;
+  bool hook_hip_d2h = false;  // offload D2H through the HIP runtime even with the DMA engine set up
 };
 
 namespace {
@@ -102,7 +119,17 @@ struct DeviceGuard {
 };
 
 // Wait until nothing the ring enqueued can still touch its slots or tables.
+// Whether this ring's offload copies go to the DMA engine.
+bool use_dma(const kvx_ring* r) { return r->dma && !r->hook_hip_d2h; }
+
+// Block until the slot's DMA copies have finished; false if one failed.
+bool wait_dma(kvx_ring* r, int32_t s) {
+  return hsa_signal_wait_scacquire(r->dma_done[(size_t)s], HSA_SIGNAL_CONDITION_LT, 1, UINT64_MAX,
+                                   HSA_WAIT_STATE_BLOCKED) == 0;
+}
+
 void drain_device(kvx_ring* r) {
+  for (size_t s = 0; s < r->dma_done.size(); ++s) (void)wait_dma(r, (int32_t)s);
   if (r->side) (void)hipStreamSynchronize(r->side);
   for (hipEvent_t e : r->dev_done)
     if (e) (void)hipEventSynchronize(e);
@@ -118,6 +145,11 @@ void destroy_resources(kvx_ring* r) {
     if (e) (void)hipEventDestroy(e);
   r->dev_done.clear();
   r->copy_done.clear();
+  for (hsa_signal_t sig : r->dma_done) (void)hsa_signal_destroy(sig);
+  r->dma_done.clear();
+  if (r->hsa_up) (void)hsa_shut_down();
+  r->hsa_up = false;
+  r->dma = false;
   if (r->side) (void)hipStreamDestroy(r->side);
   r->side = nullptr;
   if (r->host) (void)hipHostFree(r->host);
@@ -217,7 +249,7 @@ void drain_worker(kvx_ring* r, int w) {
       r->cv_enqueued.wait(lock, [&] { return r->enqueued > i || r->stop.load(); });
     }
     if (r->stop.load()) break;
-    if (hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
+    if (use_dma(r) ? !wait_dma(r, s) : hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
       r->worker_error.store(1);
       signal_stop(r);
       break;
@@ -236,6 +268,38 @@ kvx_status launch_piece(kvx_ring* r, bool to_packed, const kvx::Piece& p, const 
   return kvx::launch_copy_chunks(to_packed, &r->cache, p.l_begin, p.l_end, bt, r->plan.table_len,
                                  r->d_refs + p.ref_first, p.ref_count, r->chunk_tokens, dslot,
                                  r->slot_bytes, stream);
+}
+
+hsa_status_t dma_copy(kvx_ring* r, void* dst, const void* src, size_t bytes, hsa_signal_t sig) {
+  if (r->dma_engine)
+    return hsa_amd_memory_async_copy_on_engine(dst, r->cpu_agent, src, r->gpu_agent, bytes, 0,
+                                               nullptr, sig,
+                                               (hsa_amd_sdma_engine_id_t)r->dma_engine, true);
+  return hsa_amd_memory_async_copy(dst, r->cpu_agent, src, r->gpu_agent, bytes, 0, nullptr, sig);
+}
+
+// D2H of an offload piece on the DMA engine: device slot s to host slot s, or
+// with no drain threads straight to the piece's destinations. dma_done[s]
+// counts the piece's copies down to 0 (negative on a copy error).
+kvx_status issue_dma(kvx_ring* r, const kvx::Piece& p, int32_t s, uint8_t* dslot, uint8_t* hslot) {
+  hsa_signal_t sig = r->dma_done[(size_t)s];
+  const bool whole = r->threads > 0;
+  const int64_t n = whole ? 1 : (int64_t)p.spans.size();
+  if (n == 0) return KVX_OK;
+  hsa_signal_store_screlease(sig, n);
+  int64_t issued = 0;
+  for (int64_t k = 0; k < n; ++k) {
+    void* dst = whole ? (void*)hslot : (void*)p.spans[(size_t)k].host;
+    const void* src = whole ? (const void*)dslot : (const void*)(dslot + p.spans[(size_t)k].slot_off);
+    const size_t bytes = (size_t)(whole ? p.bytes : p.spans[(size_t)k].bytes);
+    if (dma_copy(r, dst, src, bytes, sig) != HSA_STATUS_SUCCESS) break;
+    ++issued;
+  }
+  if (issued < n) {  // the copies never issued will never count down: do it here
+    hsa_signal_subtract_screlease(sig, n - issued);
+    return KVX_EHIP;
+  }
+  return KVX_OK;
 }
 
 kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
@@ -308,7 +372,41 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
       st = launch_piece(r, false, p, bt, dslot, stream);
       if (st != KVX_OK) break;
       if (hipEventRecord(r->dev_done[s], stream) != hipSuccess) st = KVX_EHIP;
-    } else {
+    } else if (use_dma(r)) {
+      if (r->closed.load()) {
+        st = KVX_ECLOSED;
+        break;
+      }
+      // Device slot s is free once the copy of piece i - S has finished.
+      if (i >= S && !wait_dma(r, s)) {
+        st = KVX_EHIP;
+        break;
+      }
+      st = launch_piece(r, true, p, bt, dslot, stream);
+      if (st != KVX_OK) break;
+      if (hipEventRecord(r->dev_done[s], stream) != hipSuccess) {
+        st = KVX_EHIP;
+        break;
+      }
+      // Host slot s is free once the drains of piece i - S are done; the
+      // gather runs meanwhile.
+      if (T > 0 && i >= S) wait_parts(i - S);
+      if (r->stop.load()) {
+        st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
+        break;
+      }
+      if (hipEventSynchronize(r->dev_done[s]) != hipSuccess) {
+        st = KVX_EHIP;
+        break;
+      }
+      st = issue_dma(r, p, s, dslot, hslot);
+      if (st != KVX_OK) break;
+      {
+        std::lock_guard<std::mutex> lock(r->mu);
+        r->enqueued = i + 1;
+      }
+      r->cv_enqueued.notify_all();
+    } else {  // offload through the HIP runtime
       if (r->closed.load()) {
         st = KVX_ECLOSED;
         break;
@@ -355,11 +453,24 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
     if (T > 0) {
       for (int64_t i = std::max<int64_t>(0, P - S); i < P && !r->stop.load(); ++i) wait_parts(i);
       if (r->stop.load()) st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
+    } else if (use_dma(r)) {
+      for (int32_t s = 0; s < S; ++s)
+        if (!wait_dma(r, s)) st = KVX_EHIP;
     } else if (hipStreamSynchronize(r->side) != hipSuccess) {
       st = KVX_EHIP;
     }
   }
-  if (st != KVX_OK) signal_stop(r);
+  if (st != KVX_OK) {
+    signal_stop(r);
+    if (dir == Dir::kOffload) {
+      // Nothing may still write a destination once the call has returned.
+      if (use_dma(r)) {
+        for (int32_t s = 0; s < S; ++s) (void)wait_dma(r, s);
+      } else {
+        (void)hipStreamSynchronize(r->side);
+      }
+    }
+  }
   for (auto& th : workers) th.join();
   r->stop.store(false);
   r->stats.pieces = st == KVX_OK ? P : 0;
@@ -369,7 +480,109 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
   r->stats.fill_ms = (double)r->busy_ns.load() / 1e6;
   r->stats.wait_fill_ms = wait_ms;
   r->stats.enqueue_ms = ms_since(t_start);
+  r->stats.dma_d2h = dir == Dir::kOffload && use_dma(r) ? 1 : 0;
+  r->stats.dma_engine = r->stats.dma_d2h ? (int32_t)r->dma_engine : 0;
   return st;
+}
+
+struct AgentSearch {
+  uint32_t domain = 0, bus = 0, dev = 0;
+  hsa_agent_t gpu{}, cpu{};
+  bool gpu_found = false, cpu_found = false;
+};
+
+hsa_status_t find_agent(hsa_agent_t a, void* data) {
+  AgentSearch* q = static_cast<AgentSearch*>(data);
+  hsa_device_type_t type;
+  if (hsa_agent_get_info(a, HSA_AGENT_INFO_DEVICE, &type) != HSA_STATUS_SUCCESS)
+    return HSA_STATUS_SUCCESS;
+  if (type == HSA_DEVICE_TYPE_CPU && !q->cpu_found) {
+    q->cpu = a;
+    q->cpu_found = true;
+  } else if (type == HSA_DEVICE_TYPE_GPU && !q->gpu_found) {
+    uint32_t bdf = 0, domain = 0;  // bdf = bus << 8 | device << 3 | function
+    if (hsa_agent_get_info(a, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_BDFID, &bdf) ==
+            HSA_STATUS_SUCCESS &&
+        hsa_agent_get_info(a, (hsa_agent_info_t)HSA_AMD_AGENT_INFO_DOMAIN, &domain) ==
+            HSA_STATUS_SUCCESS &&
+        domain == q->domain && (bdf >> 8) == q->bus && ((bdf >> 3) & 31) == q->dev) {
+      q->gpu = a;
+      q->gpu_found = true;
+    }
+  }
+  return HSA_STATUS_SUCCESS;
+}
+
+// Device-to-host bandwidth differs several-fold between a GPU's DMA engines
+// (only some sit close to the host link), and an engine left to the runtime
+// may be any of them. The candidates are the runtime's preferred engines for
+// this direction, or with no preference every available engine; with more
+// than one, a short copy device slot 0 -> host slot 0 is timed on each and the
+// fastest kept. With no candidates the choice stays with the runtime.
+void pick_engine(kvx_ring* r) {
+  uint32_t cand = 0;
+  if (hsa_amd_memory_get_preferred_copy_engine(r->cpu_agent, r->gpu_agent, &cand) !=
+      HSA_STATUS_SUCCESS)
+    cand = 0;
+  if (cand == 0 &&
+      hsa_amd_memory_copy_engine_status(r->cpu_agent, r->gpu_agent, &cand) != HSA_STATUS_SUCCESS)
+    cand = 0;
+  r->dma_engine = 0;
+  if (cand == 0) return;
+  if ((cand & (cand - 1)) == 0) {
+    r->dma_engine = cand;
+    return;
+  }
+  const size_t bytes = (size_t)std::min<int64_t>(r->slot_bytes, 4 << 20);
+  hsa_signal_t sig = r->dma_done[0];
+  double best = 0;
+  uint32_t best_bit = 0;
+  for (uint32_t bit = 1; bit != 0 && bit <= cand; bit <<= 1) {
+    if (!(cand & bit)) continue;
+    r->dma_engine = bit;
+    hsa_signal_store_screlease(sig, 2);
+    const auto t0 = clk::now();
+    int issued = 0;
+    for (; issued < 2; ++issued)
+      if (dma_copy(r, r->host, r->landing, bytes, sig) != HSA_STATUS_SUCCESS) break;
+    if (issued < 2) hsa_signal_subtract_screlease(sig, 2 - issued);
+    const bool ok = wait_dma(r, 0) && issued == 2;
+    const double rate = (double)bytes * 2 / std::max(1e-9, ms_since(t0));
+    if (!ok) hsa_signal_store_screlease(sig, 0);
+    if (ok && rate > best) {
+      best = rate;
+      best_bit = bit;
+    }
+  }
+  r->dma_engine = best_bit;
+}
+
+// Find the HSA agents of the ring's GPU (by PCI location) and of the host,
+// and make one completion signal per slot. On any failure the ring keeps the
+// HIP copy path.
+void setup_dma(kvx_ring* r) {
+  int bus = -1, dev = -1, domain = -1;
+  if (hipDeviceGetAttribute(&bus, hipDeviceAttributePciBusId, r->device) != hipSuccess ||
+      hipDeviceGetAttribute(&dev, hipDeviceAttributePciDeviceId, r->device) != hipSuccess ||
+      hipDeviceGetAttribute(&domain, hipDeviceAttributePciDomainId, r->device) != hipSuccess)
+    return;
+  if (hsa_init() != HSA_STATUS_SUCCESS) return;
+  r->hsa_up = true;
+  AgentSearch q;
+  q.domain = (uint32_t)domain;
+  q.bus = (uint32_t)bus;
+  q.dev = (uint32_t)dev;
+  if (hsa_iterate_agents(find_agent, &q) != HSA_STATUS_SUCCESS || !q.gpu_found || !q.cpu_found)
+    return;
+  r->gpu_agent = q.gpu;
+  r->cpu_agent = q.cpu;
+  for (int32_t s = 0; s < r->n_slots; ++s) {
+    hsa_signal_t sig{};
+    if (hsa_signal_create(0, 0, nullptr, &sig) != HSA_STATUS_SUCCESS) return;
+    r->dma_done.push_back(sig);
+  }
+  r->dma = true;
+  pick_engine(r);
 }
 
 bool is_pinned(const void* p) {
@@ -496,9 +709,11 @@ kvx_status kvx_ring_create(int device, int32_t n_slots, int64_t slot_bytes, void
     for (int32_t s = 0; st == KVX_OK && s < n_slots; ++s) {
       if (hipEventCreateWithFlags(&r->copy_done[s], hipEventDisableTiming | hipEventBlockingSync) !=
               hipSuccess ||
-          hipEventCreateWithFlags(&r->dev_done[s], hipEventDisableTiming) != hipSuccess)
+          hipEventCreateWithFlags(&r->dev_done[s], hipEventDisableTiming | hipEventBlockingSync |
+                                                       hipEventReleaseToSystem) != hipSuccess)
         st = KVX_EHIP;
     }
+    if (st == KVX_OK) setup_dma(r);
     if (st != KVX_OK) {
       destroy_resources(r);
       delete r;
@@ -578,10 +793,11 @@ kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hi
   }
 }
 
-kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t poison) {
-  if (!ring || max_delay_us < 0 || max_delay_us > 1000000) return KVX_EINVAL;
+kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t flags) {
+  if (!ring || max_delay_us < 0 || max_delay_us > 1000000 || (flags & ~3)) return KVX_EINVAL;
   ring->hook_max_delay_us = max_delay_us;
-  ring->hook_poison = poison != 0;
+  ring->hook_poison = (flags & 1) != 0;
+  ring->hook_hip_d2h = (flags & 2) != 0;
   return KVX_OK;
 }
 

@@ -173,8 +173,11 @@ def test_chunk_list_restore_equals_oracle(case):
         assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
 
 
+@pytest.mark.parametrize("hip_d2h", [False, True], ids=["dma", "hip"])
 @pytest.mark.parametrize("case", RING, ids=[f"ring{i}" for i in range(len(RING))])
-def test_offload_equals_oracle_gather(case):
+def test_offload_equals_oracle_gather(case, hip_d2h):
+    """Both device-to-host paths: the DMA engine driven directly (default) and
+    the HIP runtime copy on the side stream."""
     L, ct, slots, slot_bytes, threads = case
     s = oracle.Shape(L, 300, 16, 2, 64, 2)
     seed = 80 + slots
@@ -197,11 +200,13 @@ def test_offload_equals_oracle_gather(case):
         sinks = [np.full(nb * per_block, 0xEE, np.uint8) for _, nb in sizes]
     ring = kvx.StagingRing(DEV, slots, slot_bytes)
     try:
+        ring.set_test_hooks(hip_d2h=hip_d2h)
         ring.bind_offload(cache, 0, L, ct, [(b, bt0, nb) for b, (bt0, nb) in zip(sinks, sizes)],
                           drain_threads=threads)
         for _ in range(2):
             kvx.kvx_offload_to_staging(ring, _bt(bt))
         _check()
+        assert ring.stats()["dma_d2h"] == (0 if hip_d2h else 1)
     finally:
         ring.close()
     for b, (bt0, nb) in zip(sinks, sizes):

@@ -63,8 +63,9 @@ def test_restore_with_pauses_and_poisoned_slots(case):
         assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
 
 
+@pytest.mark.parametrize("hip_d2h", [False, True], ids=["dma", "hip"])
 @pytest.mark.parametrize("case", STRESS, ids=[f"s{i}" for i in range(len(STRESS))])
-def test_offload_with_pauses(case):
+def test_offload_with_pauses(case, hip_d2h):
     slots, slot_bytes, threads, delay, ct = case
     s = oracle.Shape(4, 400, 16, 2, 64, 2)
     n = 150
@@ -79,10 +80,11 @@ def test_offload_with_pauses(case):
               for b in range(0, n, bpc)]
     ring = kvx.StagingRing(DEV, slots, slot_bytes)
     try:
-        ring.set_test_hooks(max_delay_us=delay)
+        ring.set_test_hooks(max_delay_us=delay, hip_d2h=hip_d2h)
         ring.bind_offload(cache, 0, 4, ct, chunks, drain_threads=threads)
         kvx.kvx_offload_to_staging(ring, _bt(bt))
         kvx.kvx_check()
+        assert ring.stats()["dma_d2h"] == (0 if hip_d2h else 1)
     finally:
         ring.close()
     image = np.concatenate([c[0] for c in chunks])
