@@ -49,9 +49,12 @@ KERNELS_SRC = os.path.join(ROOT, "paper_2609_11744_amd", "csrc", "kvx_kernels.hi
 # only for the kernel source they were taken on (sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "c82c36ebddb94cb8100ac59963a175ff0a802e1f7120e1e1a6541af55195efb5",
-    "fetch_bytes": 10488342792,   # FETCH_SIZE 5,121,313.9 KiB x 1.99998 (copy calibration)
-    "write_bytes": 10489107264,   # WRITE_SIZE 10,243,268.8 KiB x 1.0
+    "kernels_sha256": "0e91204deae29a56714284400a7ca1127492dd1234a606f6bd3c328331dc715e",
+    # cache layout -> (fetched, written) HBM bytes of one gather launch at the
+    # default 80k-token workload: FETCH_SIZE KiB x 1.99999 (copy calibration),
+    # WRITE_SIZE KiB x 1.0
+    "nhd": (10488394334, 10488066048),         # 5,121,315.6 / 10,242,252.0 KiB
+    "paged_attn": (10488509635, 10488453018),  # 5,121,371.9 / 10,242,629.9 KiB
 }
 
 
@@ -230,9 +233,9 @@ def run_80k(args):
     restore_GBps = payload / med["restore_ms"] / 1e6
     cpu = None if args.no_cpu_baseline else cpu_baseline(args, L, BS, H, D, E, perm)
     traffic = None
-    if GATHER_TRAFFIC["kernels_sha256"] == kernels_sha256() and layout == kvx.KVX_LAYOUT_NHD and \
+    if GATHER_TRAFFIC["kernels_sha256"] == kernels_sha256() and args.layout in GATHER_TRAFFIC and \
             (args.num_blocks, args.prefix_blocks, args.chunk_tokens) == (20000, 5000, 256):
-        traffic = GATHER_TRAFFIC["fetch_bytes"] + GATHER_TRAFFIC["write_bytes"]
+        traffic = sum(GATHER_TRAFFIC[args.layout])
 
     out = base_record(
         args, "KV gather/scatter GB/s & % HBM peak; 80k-token prefix restore ms",
