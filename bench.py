@@ -91,7 +91,8 @@ def kernels_sha256() -> str:
 
 
 def probes(dev, reps):
-    """Same-run link and copy probes: 1 GiB pinned H2D / D2H, 4 GiB D2D."""
+    """Same-run link and copy probes: 1 GiB pinned H2D / D2H, 4 GiB D2D, and
+    the HBM read / write / copy rates of a kernel shaped like the slab mover."""
     import torch
 
     def timed_copy(dst, src, n):
@@ -114,6 +115,25 @@ def probes(dev, reps):
     dd = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
     ds = torch.empty(4 << 30, dtype=torch.uint8, device=dev)
     p["d2d_copy_GBps_rw"] = 2 * (4 << 30) / timed_copy(dd, ds, 5) / 1e6
+
+    # The slab mover's own shape on contiguous memory: reading only, writing
+    # only, copying (kvx_probe_stream), 4 GiB each, median of 5.
+    import paper_2609_11744_amd as kvx
+
+    def timed_probe(mode, n):
+        out = []
+        for _ in range(n):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            kvx.kvx_probe_stream(ds if mode != 1 else None, dd if mode != 0 else None, 4 << 30, mode)
+            b.record()
+            b.synchronize()
+            out.append(a.elapsed_time(b))
+        return statistics.median(out)
+
+    p["hbm_read_GBps"] = (4 << 30) / timed_probe(0, 5) / 1e6
+    p["hbm_write_GBps"] = (4 << 30) / timed_probe(1, 5) / 1e6
+    p["hbm_copy_GBps_rw"] = 2 * (4 << 30) / timed_probe(2, 5) / 1e6
     del dd, ds
     torch.cuda.empty_cache()
     log(f"probes: {p}")
@@ -263,7 +283,9 @@ def run_80k(args):
                      "kernel": "gather (copy_units_kernel<true, false, layout %s>)" % args.layout,
                      "achieved": round(gather_GBps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(gather_GBps / HBM_PEAK_GBPS, 4),
-                     "traffic": traffic, "algorithmic_bytes": rw},
+                     "traffic": traffic, "algorithmic_bytes": rw,
+                     "copy_ceiling_GBps": round(probe["hbm_copy_GBps_rw"], 1),
+                     "frac_of_copy_ceiling": round(gather_GBps / probe["hbm_copy_GBps_rw"], 4)},
         "cpu_baseline": cpu,
     })
     print(json.dumps(out), flush=True)

@@ -388,6 +388,18 @@ kvx_status kvx_break_even_tokens(const kvx_curve* cold, const kvx_curve* hit, in
 kvx_status kvx_max_io(const kvx_curve* cold, const kvx_curve* hit, const kvx_curve* copy,
                       int64_t doc_tokens, double* out_seconds);
 
+/* ---- measurement helper --------------------------------------------------------- */
+
+/* HBM probe with the slab mover's shape (one workgroup per 32 KiB of
+ * contiguous memory, 1024 threads x two 16-byte non-temporal vectors,
+ * XCD-contiguous order), enqueued on `stream`. mode 0 reads `bytes` of src,
+ * 1 writes `bytes` of dst, 2 copies src to dst. `bytes` a multiple of 32 KiB,
+ * device pointers 16-byte aligned (src unused for mode 1, dst for mode 0);
+ * else KVX_EINVAL. Mode 1 overwrites dst with a pattern. For roofline context
+ * only: not part of the KV path. */
+kvx_status kvx_probe_stream(const void* src, void* dst, int64_t bytes, int32_t mode,
+                            hipStream_t stream);
+
 /* Pinned host memory of exactly `bytes` (hipHostMalloc), for host images. */
 kvx_status kvx_pinned_alloc(int64_t bytes, void** out);
 kvx_status kvx_pinned_free(void* p);

@@ -434,6 +434,17 @@ def kvx_dedupe_keys(keys):
     return first[:k.size]
 
 
+def kvx_probe_stream(src, dst, nbytes: int, mode: int, stream=None) -> None:
+    """HBM probe (roofline context): mode 0 read src, 1 write dst, 2 copy src -> dst."""
+    for t in (src, dst):
+        if t is not None and (not t.is_cuda or t.numel() * t.element_size() < nbytes):
+            raise ValueError("probe buffers must be device tensors of at least nbytes")
+    st = _native.lib().kvx_probe_stream(src.data_ptr() if src is not None else None,
+                                        dst.data_ptr() if dst is not None else None, nbytes, mode,
+                                        _stream_handle(stream))
+    _ok(st, "kvx_probe_stream")
+
+
 def kvx_offload_to_staging(ring: StagingRing, block_table, stream=None) -> None:
     ptr = _table_ptr(ring._cache, block_table, ring.n_blocks) if ring._cache is not None else None
     st = _native.lib().kvx_offload_to_staging(ring.handle, ptr, _stream_handle(stream))
@@ -446,5 +457,5 @@ __all__ = [
     "kvx_plan_pieces", "kvx_restore_from_staging", "shape_only_cache", "KVX_MAX_LAYERS",
     "kvx_gather_chunks", "kvx_scatter_chunks", "chunk_refs", "kvx_offload_to_staging",
     "kvx_block_hashes", "kvx_dedupe_keys", "KVX_LAYOUT_NHD", "KVX_LAYOUT_HND",
-    "KVX_LAYOUT_PAGED_ATTN", "layer_shapes",
+    "KVX_LAYOUT_PAGED_ATTN", "layer_shapes", "kvx_probe_stream",
 ]

@@ -85,6 +85,7 @@ SIGNATURES = {
     "kvx_max_io": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.POINTER(KvxCurve),
                                   ctypes.POINTER(KvxCurve), c_i64,
                                   ctypes.POINTER(ctypes.c_double)]),
+    "kvx_probe_stream": (ctypes.c_int, [c_vp, c_vp, c_i64, c_i32, c_vp]),
     "kvx_pinned_alloc": (ctypes.c_int, [c_i64, ctypes.POINTER(c_vp)]),
     "kvx_pinned_free": (ctypes.c_int, [c_vp]),
 }

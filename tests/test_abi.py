@@ -178,3 +178,19 @@ def test_layout_validation_on_the_host():
     assert call(kvx.KVX_LAYOUT_HND, BS=32) == kvx.KVX_EINVAL  # 64 KiB slab > 48 KiB LDS image
     assert call(kvx.KVX_LAYOUT_PAGED_ATTN, H=1, D=4, e=2) == kvx.KVX_EINVAL  # 8-byte rows
     assert call(kvx.KVX_LAYOUT_HND, H=1, D=12, e=2) == kvx.KVX_EINVAL       # 24-byte rows
+
+
+def test_probe_rejects_bad_arguments_on_the_host():
+    """kvx_probe_stream validates before it enqueues anything (the fake device
+    addresses below are never dereferenced)."""
+    import paper_2609_11744_amd as kvx
+    from paper_2609_11744_amd import _native
+
+    lib = _native.lib()
+    unit = 32 << 10
+    assert lib.kvx_probe_stream(None, None, unit, 0, None) == kvx.KVX_EINVAL  # read: no src
+    assert lib.kvx_probe_stream(None, None, unit, 1, None) == kvx.KVX_EINVAL  # write: no dst
+    assert lib.kvx_probe_stream(4096, 8192, unit + 16, 2, None) == kvx.KVX_EINVAL  # size
+    assert lib.kvx_probe_stream(4096, 8192, unit, 3, None) == kvx.KVX_EINVAL  # mode
+    assert lib.kvx_probe_stream(4100, 8192, unit, 2, None) == kvx.KVX_EINVAL  # alignment
+    assert lib.kvx_probe_stream(4096, 8192, -unit, 2, None) == kvx.KVX_EINVAL

@@ -310,3 +310,63 @@ def test_ordered_scatter_with_bad_ids_skips_only_those():
     subst[bad_pos] = spare
     oracle.scatter(s, *mirror, 0, 2, subst, 32, img)
     _compare_paged(cache, s, mirror, range(2), good, "bad-id ordered scatter")
+
+
+# ---- calls larger than one dispatch ---------------------------------------------
+
+def test_launch_split_above_2_22_units():
+    """A call of more than 2^22 units is split into several launches (a grid
+    counts its work-items in 32 bits). 16-byte slabs (1 token x 1 head x 8 dims,
+    bf16) over 64 layers and 40,000 blocks make 5,120,000 units per call: the
+    gather, the destination-ordered scatter and the chunk-list gather, each
+    bit-exact against the oracle."""
+    s = oracle.Shape(64, 80004, 1, 1, 8, 2)
+    n, ct, L = 40000, 16, 64
+    assert n * L * 2 > 1 << 22
+    seed = 123
+    bt_src, bt_dst = seeded_ids(seed, s.num_blocks, n, n)
+    fill = SRC(seed, kvsynth.MODE_RAW)
+    cache = device_cache(s, fill, DEV)
+    mirror = host_mirror(s, fill, range(s.num_blocks))
+    expect = oracle.gather(s, *mirror, 0, L, bt_src, ct)
+    dst = _packed(expect.size)
+    kvx.kvx_gather_blocks(cache, 0, L, _bt(bt_src), n, ct, dst)
+    _sync_check()
+    bad = first_mismatch(to_host(dst)[:expect.size], expect)
+    assert bad is None, f"split gather differs at byte {bad}"
+    kvx.kvx_scatter_blocks(cache, 0, L, _bt(bt_dst), n, ct, dst)
+    _sync_check()
+    oracle.scatter(s, *mirror, 0, L, bt_dst, ct, expect)
+    for l in range(L):
+        assert np.array_equal(to_host(cache.k[l]), mirror[0][l]), f"K layer {l}"
+        assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
+    # the same image through the chunk-list kernel: 2,500 chunks of 16 blocks
+    per_block = oracle.packed_bytes(s, 0, L, 1)
+    refs = [(b * per_block, b, min(16, n - b)) for b in range(0, n, 16)]
+    packed = torch.full((expect.size + 4096,), 0x5A, dtype=torch.uint8, device=DEV)
+    kvx.kvx_gather_chunks(cache, 0, L, _bt(bt_src), n, kvx.chunk_refs(refs, DEV), len(refs), ct,
+                          packed)
+    _sync_check()
+    got = to_host(packed)
+    bad = first_mismatch(got[:expect.size], expect)
+    assert bad is None, f"split chunk-list gather differs at byte {bad}"
+    assert (got[expect.size:] == 0x5A).all()
+
+
+def test_probe_stream_copies_exactly():
+    """The roofline probe's copy mode is a plain copy; the write mode writes
+    every 16-byte vector; the read mode leaves its source alone."""
+    n = 64 << 20
+    src = torch.randint(0, 256, (n,), dtype=torch.uint8, device=DEV)
+    keep = src.clone()
+    dst = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    kvx.kvx_probe_stream(src, dst, n, 2)
+    _sync_check()
+    assert torch.equal(dst, src)
+    kvx.kvx_probe_stream(src, None, n, 0)
+    dst.zero_()
+    kvx.kvx_probe_stream(None, dst, n, 1)
+    _sync_check()
+    assert torch.equal(src, keep)
+    words = dst.view(torch.int32).view(-1, 4)
+    assert bool((words[:, 2] == 0x9E3779B9 - 2**32).all()) and bool((words[:, 3] == 0x7F4A7C15).all())
