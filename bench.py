@@ -443,6 +443,34 @@ def run_sweep(args):
             ring.close()
         rows.append(row)
         log(f"chunk {ct}: {row}")
+    extras = {}
+    # Block-id locality: the same 256-token-chunk gather / scatter with the
+    # source and destination ids each sorted ascending instead of random.
+    bs_src = torch.sort(bt_src).values.contiguous()
+    bs_dst = torch.sort(bt_dst).values.contiguous()
+    g = event_ms(lambda: kvx.kvx_gather_blocks(cache, 0, L, bs_src, n, 256, packed), reps)
+    s = event_ms(lambda: kvx.kvx_scatter_blocks(cache, 0, L, bs_dst, n, 256, packed), reps)
+    extras["sorted_ids_chunk256"] = {
+        "gather_GBps_rw": round(2 * payload / statistics.median(g) / 1e6, 1),
+        "scatter_GBps_rw": round(2 * payload / statistics.median(s) / 1e6, 1)}
+    # Transfer granularity: one 16-token chunk (2 MiB) per host-link copy
+    # (4 slots of 2 MiB) against the same chunks packed into 64 MiB slots.
+    for name, slot_bytes in (("one_chunk_per_copy", 2 << 20), ("packed_64MiB_slots", 64 << 20)):
+        ring = kvx.StagingRing(dev, 4, slot_bytes)
+        ring.bind(cache, 0, L, n, 16, image, fill_threads=args.fill_threads)
+        times = []
+        for i in range(reps + 1):
+            t0 = time.perf_counter()
+            kvx.kvx_restore_from_staging(ring, bt_dst)
+            torch.cuda.synchronize()
+            if i:
+                times.append((time.perf_counter() - t0) * 1e3)
+        ms = statistics.median(times)
+        extras[name] = {"chunk_tokens": 16, "slots": 4, "slot_bytes": slot_bytes,
+                        "pieces": ring.stats()["pieces"], "restore_ms": round(ms, 3),
+                        "frac_of_h2d": round(payload / ms / 1e6 / probe["h2d_GBps"], 4)}
+        ring.close()
+    log(f"extras: {extras}")
     kvx.kvx_check()
     wall = (time.perf_counter() - t_begin) * 1e3
     best = max(min(r["gather_GBps_rw"], r["scatter_GBps_rw"]) for r in rows)
@@ -452,7 +480,8 @@ def run_sweep(args):
                                    "a 20000-block pool; chunks 16/64/256/1024; rings 2/4/8 x 64 MiB",
                        "num_blocks": NB, "prefix_tokens": n * BS, "parallelism": "single GPU"})
     out["ms_per_step_note"] = "wall time of the whole sweep"
-    out.update({"sweep": rows, "probes": {k: round(v, 2) for k, v in probe.items()}})
+    out.update({"sweep": rows, "extras": extras,
+                "probes": {k: round(v, 2) for k, v in probe.items()}})
     print(json.dumps(out), flush=True)
     image.free()
 
