@@ -214,6 +214,10 @@ def run_80k(args):
         e[1].record()
         kvx.kvx_scatter_blocks(cache, 0, L, bt_dst, n, ct, packed)
         e[2].record()
+        # The restore is timed as its own phase, from its first fill to its last
+        # scatter: the gather and scatter above finish first, so its pipeline
+        # does not queue behind them.
+        e[2].synchronize()
         t_r = time.perf_counter()
         kvx.kvx_restore_from_staging(ring, bt_rst)
         e[3].record()
