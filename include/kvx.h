@@ -302,8 +302,9 @@ typedef struct kvx_ring_stats {
                              engine (issued directly); 0: restore, or copies through the HIP
                              runtime (which may run them as a copy kernel on compute units) */
   int32_t dma_engine;     /* with dma_d2h: the engine's id bit (the fastest of the runtime's
-                             preferred, else available, engines, timed when the ring was
-                             created); 0 = the runtime's own choice */
+                             preferred, else available, engines, timed by the first ring
+                             created on the device in the process); 0 = the runtime's own
+                             choice */
 } kvx_ring_stats;
 
 kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out);
