@@ -71,7 +71,8 @@ typedef enum kvx_status {
   KVX_EHIP = -3,       /* a HIP runtime call failed */
   KVX_EBADBLOCK = -4,  /* a kernel met a block id outside [0, num_blocks) */
   KVX_ECLOSED = -5,    /* the ring was aborted while a restore was running */
-  KVX_EINTERNAL = -6   /* invariant violated inside the library */
+  KVX_EINTERNAL = -6,  /* invariant violated inside the library */
+  KVX_EIO = -7         /* a storage-tier file could not be opened, read, written or published */
 } kvx_status;
 
 /* Largest layer range a single call may cover. */
@@ -312,6 +313,72 @@ kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out);
 /* Make a running or later restore on this ring return KVX_ECLOSED. Safe to
  * call from another thread. */
 kvx_status kvx_ring_abort(kvx_ring* ring);
+
+/* ---- storage tier (files) ------------------------------------------------------ *
+ *
+ * One file per chunk (storage block, Sec. 6.4) holding the chunk's packed
+ * image. Files are read and written by one reactor thread through io_uring
+ * with at most io_depth transfers in flight (Sec. 6.4: the I/O depth, not a
+ * thread count, sets storage concurrency), with O_DIRECT wherever every
+ * transfer on a file is 4 KiB aligned (Sec. 6.3). A written file is published
+ * by hard-linking a uniquely named temporary file in the same directory to the
+ * final name and removing the temporary name: atomic, and first-writer-wins if
+ * the name already exists (then the existing file is kept and the call still
+ * succeeds), so a reader of a final name sees a whole file or none (Sec. 6.3).
+ * Files are not fsync'ed. Where io_uring is unavailable, or KVX_IO_NO_URING=1
+ * is set in the environment, the same calls run one blocking pread / pwrite at
+ * a time. */
+
+typedef struct {
+  const char* path;   /* the chunk's file (copied at bind) */
+  int32_t bt_offset;  /* first entry of the chunk in the transfer's block table */
+  int32_t n_blocks;   /* 1 .. chunk_tokens / block_size */
+} kvx_file_chunk;
+
+/* Bind the next restores to chunk files: as kvx_ring_bind_chunks, with each
+ * chunk's image read from its file (its whole size: (l1 - l0) * 2 * n_blocks
+ * * slab bytes) into the staging slots by the reactor instead of fill
+ * threads; a slot is read into only after its previous H2D copy completed.
+ * io_depth 1..256. A missing or short file makes the restore return KVX_EIO
+ * (slots already scattered stay scattered). */
+kvx_status kvx_ring_bind_files(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int32_t l1,
+                               int32_t chunk_tokens, const kvx_file_chunk* chunks,
+                               int32_t n_chunks, int32_t io_depth);
+
+/* Bind the next offloads to chunk files: as kvx_ring_bind_offload, with each
+ * chunk's image written from the staging slots to its file and published once
+ * complete (missing directories are created). io_depth 1..256. */
+kvx_status kvx_ring_bind_offload_files(kvx_ring* ring, const kvx_cache* cache, int32_t l0,
+                                       int32_t l1, int32_t chunk_tokens,
+                                       const kvx_file_chunk* chunks, int32_t n_chunks,
+                                       int32_t io_depth);
+
+/* Hash-addressed chunk path (Sec. 6.3: the path follows from the model
+ * configuration and the prefix hash, intermediate directories spread the
+ * entries): "<root>/<tag>/<k0>/<k1>/<key>.kvc" with k0, k1 the top two bytes of
+ * key in hex and key as 16 hex digits; tag names the model configuration and
+ * holds no '/'. Writes the NUL-terminated path to out[cap] and returns its
+ * length, or -1 on a bad argument or a path longer than cap - 1. */
+int32_t kvx_chunk_path(const char* root, const char* tag, uint64_t key, char* out, int32_t cap);
+
+/* One host-side transfer of the storage tier: bytes [offset, offset + bytes)
+ * of the file at path from / into buf (caller-owned host memory). */
+typedef struct {
+  const char* path;
+  void* buf;
+  int64_t offset;
+  int64_t bytes;
+} kvx_file_io;
+
+/* Read every op's byte range of its file into its buffer (ops naming one path
+ * share one open file), io_depth 1..256 in flight; returns when all are done.
+ * KVX_EIO if a file is missing or shorter than an op needs. */
+kvx_status kvx_read_files(const kvx_file_io* ops, int32_t n, int32_t io_depth);
+
+/* Write and publish whole files: the ops naming one path must tile [0, size)
+ * of that file exactly (KVX_EINVAL otherwise); each file is published as
+ * above once all of its bytes are written. */
+kvx_status kvx_write_files(const kvx_file_io* ops, int32_t n, int32_t io_depth);
 
 /* Fault-injection hooks for testing the slot-reuse protocol from the host.
  * max_delay_us > 0: each fill or drain thread pauses a pseudo-random 0 ..

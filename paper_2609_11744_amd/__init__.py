@@ -16,12 +16,13 @@ Operations (sections of the paper they follow):
 from __future__ import annotations
 
 import ctypes
+import os
 
 from . import _native
 from ._native import KvxCache, KvxChunkRef, KvxHostChunk, KvxPiece, KvxRingStats
 
-KVX_OK, KVX_EINVAL, KVX_ENOMEM, KVX_EHIP, KVX_EBADBLOCK, KVX_ECLOSED, KVX_EINTERNAL = (
-    0, -1, -2, -3, -4, -5, -6)
+KVX_OK, KVX_EINVAL, KVX_ENOMEM, KVX_EHIP, KVX_EBADBLOCK, KVX_ECLOSED, KVX_EINTERNAL, KVX_EIO = (
+    0, -1, -2, -3, -4, -5, -6, -7)
 KVX_MAX_LAYERS = 128
 KVX_LAYOUT_NHD, KVX_LAYOUT_HND, KVX_LAYOUT_PAGED_ATTN = 0, 1, 2
 
@@ -377,6 +378,34 @@ class StagingRing:
         self._source, self._cache = keep, cache
         self.n_blocks = max((bt0 + nb for _, bt0, nb in chunks), default=0)
 
+    def _file_chunks(self, chunks):
+        arr = (_native.KvxFileChunk * max(len(chunks), 1))()
+        keep = []
+        for i, (path, bt0, nb) in enumerate(chunks):
+            b = os.fsencode(path)
+            keep.append(b)
+            arr[i] = _native.KvxFileChunk(b, bt0, nb)
+        return arr, keep
+
+    def bind_files(self, cache, l0, l1, chunk_tokens, chunks, io_depth=8):
+        """Restore binding over chunk files [(path, bt_offset, n_blocks)] (storage tier)."""
+        arr, keep = self._file_chunks(chunks)
+        _ok(_native.lib().kvx_ring_bind_files(self.handle, ctypes.byref(cache.c_struct()), l0, l1,
+                                              chunk_tokens, arr, len(chunks), io_depth),
+            "kvx_ring_bind_files")
+        self._source, self._cache = keep, cache
+        self.n_blocks = max((bt0 + nb for _, bt0, nb in chunks), default=0)
+
+    def bind_offload_files(self, cache, l0, l1, chunk_tokens, chunks, io_depth=8):
+        """Offload binding to chunk files [(path, bt_offset, n_blocks)], published on completion."""
+        arr, keep = self._file_chunks(chunks)
+        _ok(_native.lib().kvx_ring_bind_offload_files(self.handle, ctypes.byref(cache.c_struct()),
+                                                      l0, l1, chunk_tokens, arr, len(chunks),
+                                                      io_depth),
+            "kvx_ring_bind_offload_files")
+        self._source, self._cache = keep, cache
+        self.n_blocks = max((bt0 + nb for _, bt0, nb in chunks), default=0)
+
     def stats(self) -> dict:
         s = KvxRingStats()
         _ok(_native.lib().kvx_ring_stats_get(self.handle, ctypes.byref(s)), "kvx_ring_stats_get")
@@ -445,6 +474,49 @@ def kvx_probe_stream(src, dst, nbytes: int, mode: int, stream=None) -> None:
     _ok(st, "kvx_probe_stream")
 
 
+def kvx_chunk_path(root: str, tag: str, key: int) -> str:
+    """Hash-addressed chunk file path: <root>/<tag>/<k0>/<k1>/<key>.kvc."""
+    out = ctypes.create_string_buffer(4096)
+    n = _native.lib().kvx_chunk_path(os.fsencode(root), os.fsencode(tag), key & (2**64 - 1), out,
+                                     len(out))
+    if n < 0:
+        raise KvxError(KVX_EINVAL, "kvx_chunk_path")
+    return os.fsdecode(out.value)
+
+
+def _file_ios(ops):
+    import numpy as np
+
+    arr = (_native.KvxFileIo * max(len(ops), 1))()
+    keep = []
+    for i, (path, buf, offset) in enumerate(ops):
+        if isinstance(buf, PinnedBuffer):
+            ptr, size = buf.ptr, buf.nbytes
+        else:
+            a = np.asarray(buf)
+            if a.dtype != np.uint8 or not a.flags.c_contiguous:
+                raise ValueError("file buffers must be contiguous uint8 arrays")
+            ptr, size = a.ctypes.data, a.nbytes
+            keep.append(a)
+        b = os.fsencode(path)
+        keep.append(b)
+        arr[i] = _native.KvxFileIo(b, ptr, offset, size)
+    return arr, keep
+
+
+def kvx_read_files(ops, io_depth: int = 8) -> None:
+    """Read [(path, buffer, file offset)]: each buffer is filled from its file."""
+    arr, keep = _file_ios(ops)
+    _ok(_native.lib().kvx_read_files(arr, len(ops), io_depth), "kvx_read_files")
+
+
+def kvx_write_files(ops, io_depth: int = 8) -> None:
+    """Write and publish files from [(path, buffer, file offset)]; a file's ops
+    must tile it exactly."""
+    arr, keep = _file_ios(ops)
+    _ok(_native.lib().kvx_write_files(arr, len(ops), io_depth), "kvx_write_files")
+
+
 def kvx_offload_to_staging(ring: StagingRing, block_table, stream=None) -> None:
     ptr = _table_ptr(ring._cache, block_table, ring.n_blocks) if ring._cache is not None else None
     st = _native.lib().kvx_offload_to_staging(ring.handle, ptr, _stream_handle(stream))
@@ -457,5 +529,6 @@ __all__ = [
     "kvx_plan_pieces", "kvx_restore_from_staging", "shape_only_cache", "KVX_MAX_LAYERS",
     "kvx_gather_chunks", "kvx_scatter_chunks", "chunk_refs", "kvx_offload_to_staging",
     "kvx_block_hashes", "kvx_dedupe_keys", "KVX_LAYOUT_NHD", "KVX_LAYOUT_HND",
-    "KVX_LAYOUT_PAGED_ATTN", "layer_shapes", "kvx_probe_stream",
+    "KVX_LAYOUT_PAGED_ATTN", "layer_shapes", "kvx_probe_stream", "kvx_chunk_path",
+    "kvx_read_files", "kvx_write_files", "KVX_EIO",
 ]

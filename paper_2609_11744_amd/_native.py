@@ -37,6 +37,14 @@ class KvxRingStats(ctypes.Structure):
                 ("dma_d2h", c_i32), ("dma_engine", c_i32)]
 
 
+class KvxFileChunk(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_char_p), ("bt_offset", c_i32), ("n_blocks", c_i32)]
+
+
+class KvxFileIo(ctypes.Structure):
+    _fields_ = [("path", ctypes.c_char_p), ("buf", c_vp), ("offset", c_i64), ("bytes", c_i64)]
+
+
 class KvxCurve(ctypes.Structure):
     _fields_ = [("tokens", ctypes.POINTER(ctypes.c_double)),
                 ("seconds", ctypes.POINTER(ctypes.c_double)), ("n", c_i32)]
@@ -86,6 +94,15 @@ SIGNATURES = {
                                   ctypes.POINTER(KvxCurve), c_i64,
                                   ctypes.POINTER(ctypes.c_double)]),
     "kvx_probe_stream": (ctypes.c_int, [c_vp, c_vp, c_i64, c_i32, c_vp]),
+    "kvx_ring_bind_files": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32,
+                                           ctypes.POINTER(KvxFileChunk), c_i32, c_i32]),
+    "kvx_ring_bind_offload_files": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32,
+                                                   c_i32, ctypes.POINTER(KvxFileChunk), c_i32,
+                                                   c_i32]),
+    "kvx_chunk_path": (c_i32, [ctypes.c_char_p, ctypes.c_char_p, ctypes.c_uint64,
+                               ctypes.c_char_p, c_i32]),
+    "kvx_read_files": (ctypes.c_int, [ctypes.POINTER(KvxFileIo), c_i32, c_i32]),
+    "kvx_write_files": (ctypes.c_int, [ctypes.POINTER(KvxFileIo), c_i32, c_i32]),
     "kvx_pinned_alloc": (ctypes.c_int, [c_i64, ctypes.POINTER(c_vp)]),
     "kvx_pinned_free": (ctypes.c_int, [c_vp]),
 }

@@ -202,6 +202,7 @@ const char* kvx_strerror(kvx_status s) {
     case KVX_EBADBLOCK: return "block id out of range";
     case KVX_ECLOSED: return "ring aborted";
     case KVX_EINTERNAL: return "internal error";
+    case KVX_EIO: return "storage-tier file I/O failed";
   }
   return "unknown status";
 }

@@ -48,6 +48,7 @@
 
 #include "kvx.h"
 #include "kvx_internal.h"
+#include "kvx_io.h"
 
 namespace {
 enum class Dir { kNone, kRestore, kOffload };
@@ -85,7 +86,7 @@ struct kvx_ring {
   // ends the current transfer (closed, or an internal failure).
   std::atomic<bool> closed{false};
   std::atomic<bool> stop{false};
-  std::atomic<int> worker_error{0};
+  std::atomic<int> worker_error{0};  // a fill / drain failure's kvx_status (0: none)
   std::mutex mu;
   std::condition_variable cv_host, cv_enqueued;
   int64_t enqueued = 0;               // pieces whose slot copy is enqueued
@@ -97,6 +98,13 @@ struct kvx_ring {
   int32_t hook_max_delay_us = 0;
   bool hook_poison = false;
   bool hook_hip_d2h = false;  // offload D2H through the HIP runtime even with the DMA engine set up
+
+  // storage tier: the bound chunks live in files (kvx_ring_bind_files /
+  // kvx_ring_bind_offload_files); a reactor thread replaces the fill / drain
+  // threads
+  bool files_mode = false;
+  int32_t io_depth = 0;
+  std::vector<kvx::TierFile> files;
 };
 
 namespace {
@@ -160,6 +168,8 @@ void destroy_resources(kvx_ring* r) {
   if (r->d_refs) (void)hipFree(r->d_refs);
   r->d_refs = nullptr;
   r->d_refs_cap = 0;
+  for (auto& f : r->files) kvx::close_tier_file(&f);
+  r->files.clear();
 }
 
 // Copy share w of T of a piece between host slot s and its spans.
@@ -212,7 +222,7 @@ void fill_worker(kvx_ring* r, int w) {
     }
     if (r->stop.load()) break;
     if (hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
-      r->worker_error.store(1);
+      r->worker_error.store(KVX_EHIP);
       signal_stop(r);
       break;
     }
@@ -251,7 +261,7 @@ void drain_worker(kvx_ring* r, int w) {
     }
     if (r->stop.load()) break;
     if (use_dma(r) ? !wait_dma(r, s) : hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
-      r->worker_error.store(1);
+      r->worker_error.store(KVX_EHIP);
       signal_stop(r);
       break;
     }
@@ -262,6 +272,216 @@ void drain_worker(kvx_ring* r, int w) {
     if (++r->parts_done[(size_t)i] == T) r->cv_host.notify_all();
   }
   r->busy_ns.fetch_add(busy);
+}
+
+// ---- storage tier -----------------------------------------------------------
+//
+// A bound chunk file f is planned as if its image sat at the notional host
+// address (f + 1) << kFileShift (never dereferenced), so the planner's spans
+// name (file, byte offset in the file) directly.
+constexpr int kFileShift = 40;
+
+int32_t span_file(const kvx::Span& sp) {
+  return (int32_t)(((uintptr_t)sp.host >> kFileShift) - 1);
+}
+
+int64_t span_offset(const kvx::Span& sp) {
+  return (int64_t)((uintptr_t)sp.host & (((uintptr_t)1 << kFileShift) - 1));
+}
+
+// Status of a transfer stopped early: the worker's failure, else an abort.
+kvx_status worker_status(const kvx_ring* r) {
+  const int e = r->worker_error.load();
+  return e ? (kvx_status)e : KVX_ECLOSED;
+}
+
+void mark_piece_done(kvx_ring* r, int64_t i) {
+  std::lock_guard<std::mutex> lock(r->mu);
+  r->parts_done[(size_t)i] = r->threads;
+  r->cv_host.notify_all();
+}
+
+void fail_worker(kvx_ring* r, kvx_status st) {
+  r->worker_error.store(st);
+  signal_stop(r);
+}
+
+// Restore reactor: read each piece's spans from the chunk files into its host
+// slot, up to io_depth reads in flight, starting a piece only once its slot's
+// previous H2D copy has completed; a piece is handed to the enqueuing thread
+// when all of its reads have landed.
+void file_fill_worker(kvx_ring* r) {
+  const int32_t S = r->n_slots;
+  const int64_t P = (int64_t)r->plan.pieces.size();
+  const auto t0 = clk::now();
+  kvx::IoEngine io;
+  if (io.init(r->io_depth, false) != KVX_OK) {
+    fail_worker(r, KVX_EINTERNAL);
+    return;
+  }
+  std::vector<int32_t> left((size_t)P, 0);
+  std::vector<uint64_t> done;
+  int64_t next = 0;  // next piece to start
+  size_t span = 0;   // next span of that piece
+  int64_t complete = 0;
+  kvx_status st = KVX_OK;
+  while (st == KVX_OK && complete < P && !r->stop.load()) {
+    // Start reads while the depth allows and the next piece's slot is free.
+    bool blocked = false;
+    while (st == KVX_OK && next < P && io.inflight() < io.depth()) {
+      const int32_t s = (int32_t)(next % S);
+      const kvx::Piece& p = r->plan.pieces[(size_t)next];
+      if (span == 0) {
+        if (next >= S) {
+          bool enq;
+          {
+            std::lock_guard<std::mutex> lock(r->mu);
+            enq = r->enqueued > next - S;
+          }
+          if (!enq || hipEventQuery(r->copy_done[s]) != hipSuccess) {
+            blocked = true;
+            break;
+          }
+        }
+        left[(size_t)next] = (int32_t)p.spans.size();
+      }
+      const kvx::Span& sp = p.spans[span];
+      kvx::TierFile& f = r->files[(size_t)span_file(sp)];
+      st = kvx::open_tier_file(&f, false);
+      if (st == KVX_OK)
+        st = io.start(&f, r->host + (int64_t)s * r->slot_bytes + sp.slot_off, span_offset(sp),
+                      sp.bytes, (uint64_t)next);
+      if (++span == p.spans.size()) {
+        span = 0;
+        ++next;
+      }
+      if (!io.uring()) break;  // synchronous: report each read as it finishes
+    }
+    if (st != KVX_OK) break;
+    if (io.pending() == 0 && blocked) {
+      // Nothing in flight: wait for the slot of piece `next` to be released.
+      const int32_t s = (int32_t)(next % S);
+      {
+        std::unique_lock<std::mutex> lock(r->mu);
+        r->cv_enqueued.wait(lock, [&] { return r->enqueued > next - S || r->stop.load(); });
+      }
+      if (r->stop.load()) break;
+      if (hipEventSynchronize(r->copy_done[s]) != hipSuccess) st = KVX_EHIP;
+      continue;
+    }
+    done.clear();
+    st = io.wait(&done);
+    for (uint64_t t : done)
+      if (--left[(size_t)t] == 0) {
+        mark_piece_done(r, (int64_t)t);
+        ++complete;
+      }
+  }
+  while (io.inflight() > 0) {  // reads still landing in the slots
+    const int32_t before = io.inflight();
+    done.clear();
+    if (io.wait(&done) != KVX_OK && io.inflight() == before) break;
+  }
+  for (auto& f : r->files) kvx::close_tier_file(&f);
+  r->busy_ns.fetch_add(std::chrono::duration_cast<std::chrono::nanoseconds>(clk::now() - t0).count());
+  if (st != KVX_OK) fail_worker(r, st);
+}
+
+// Offload reactor: as each piece's D2H copy completes, write its spans from
+// the host slot into the chunk files (up to io_depth writes in flight),
+// publishing each file once all of its bytes landed; a piece's slot is
+// released when all of its writes have landed.
+void file_drain_worker(kvx_ring* r) {
+  const int32_t S = r->n_slots;
+  const int64_t P = (int64_t)r->plan.pieces.size();
+  const auto t0 = clk::now();
+  kvx::IoEngine io;
+  if (io.init(r->io_depth, true) != KVX_OK) {
+    fail_worker(r, KVX_EINTERNAL);
+    return;
+  }
+  std::vector<int32_t> left((size_t)P, 0);
+  std::vector<uint64_t> done;
+  std::vector<int32_t> to_sync;  // buffered files fully written, to flush before publishing
+  kvx_status st = KVX_OK;
+  // Finish what has landed: release pieces whose writes are all done, publish
+  // direct files at once and queue buffered ones for their flush; then start
+  // queued flushes while the depth allows.
+  auto reap = [&]() {
+    done.clear();
+    kvx_status w = io.wait(&done);
+    for (uint64_t t : done) {
+      if (t & kvx::kSyncTag) {
+        if (w == KVX_OK) w = kvx::publish_tier_file(&r->files[(size_t)(t & ~kvx::kSyncTag)]);
+        continue;
+      }
+      const kvx::Piece& p = r->plan.pieces[(size_t)(t >> 20)];
+      const kvx::Span& sp = p.spans[(size_t)(t & 0xFFFFF)];
+      kvx::TierFile& f = r->files[(size_t)span_file(sp)];
+      // (several of a file's transfers can finish in one wait: act once)
+      if (w == KVX_OK && f.written == f.size && !f.published && !f.flushing) {
+        if (f.direct) {
+          w = kvx::publish_tier_file(&f);
+        } else {
+          f.flushing = true;
+          to_sync.push_back(span_file(sp));
+        }
+      }
+      if (--left[(size_t)(t >> 20)] == 0) mark_piece_done(r, (int64_t)(t >> 20));
+    }
+    while (w == KVX_OK && !to_sync.empty() && io.inflight() < io.depth()) {
+      const int32_t fi = to_sync.back();
+      to_sync.pop_back();
+      w = io.start_datasync(&r->files[(size_t)fi], kvx::kSyncTag | (uint64_t)fi);
+    }
+    return w;
+  };
+  for (int64_t i = 0; st == KVX_OK && i < P && !r->stop.load(); ++i) {
+    const int32_t s = (int32_t)(i % S);
+    const kvx::Piece& p = r->plan.pieces[(size_t)i];
+    // Wait for piece i's D2H copy to be enqueued. The enqueuing thread may be
+    // waiting for an earlier piece's slot, which only reaping its writes
+    // releases: sleep only with nothing in flight, else reap meanwhile.
+    for (;;) {
+      {
+        std::lock_guard<std::mutex> lock(r->mu);
+        if (r->enqueued > i || r->stop.load()) break;
+      }
+      if (io.pending() > 0) {
+        st = reap();
+        if (st != KVX_OK) break;
+        continue;
+      }
+      std::unique_lock<std::mutex> lock(r->mu);
+      r->cv_enqueued.wait(lock, [&] { return r->enqueued > i || r->stop.load(); });
+      break;
+    }
+    if (st != KVX_OK || r->stop.load()) break;
+    if (use_dma(r) ? !wait_dma(r, s) : hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
+      st = KVX_EHIP;
+      break;
+    }
+    left[(size_t)i] = (int32_t)p.spans.size();
+    for (size_t k = 0; st == KVX_OK && k < p.spans.size(); ++k) {
+      while (st == KVX_OK && io.inflight() >= io.depth()) st = reap();
+      if (st != KVX_OK) break;
+      const kvx::Span& sp = p.spans[k];
+      kvx::TierFile& f = r->files[(size_t)span_file(sp)];
+      st = kvx::open_tier_file(&f, true);
+      if (st == KVX_OK)
+        st = io.start(&f, r->host + (int64_t)s * r->slot_bytes + sp.slot_off, span_offset(sp),
+                      sp.bytes, ((uint64_t)i << 20) | (uint64_t)k);
+    }
+  }
+  while (st == KVX_OK && (io.pending() > 0 || !to_sync.empty())) st = reap();
+  while (io.inflight() > 0) {  // after an error: let what is in flight land
+    const int32_t before = io.inflight();
+    done.clear();
+    if (io.wait(&done) != KVX_OK && io.inflight() == before) break;
+  }
+  for (auto& f : r->files) kvx::close_tier_file(&f);  // unpublished temporaries are removed
+  r->busy_ns.fetch_add(std::chrono::duration_cast<std::chrono::nanoseconds>(clk::now() - t0).count());
+  if (st != KVX_OK) fail_worker(r, st);
 }
 
 kvx_status launch_piece(kvx_ring* r, bool to_packed, const kvx::Piece& p, const int32_t* bt,
@@ -325,8 +545,11 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
   kvx_status st = KVX_OK;
   double wait_ms = 0;
   try {
-    for (int w = 0; w < T; ++w)
-      workers.emplace_back(dir == Dir::kRestore ? fill_worker : drain_worker, r, w);
+    if (r->files_mode)
+      workers.emplace_back(dir == Dir::kRestore ? file_fill_worker : file_drain_worker, r);
+    else
+      for (int w = 0; w < T; ++w)
+        workers.emplace_back(dir == Dir::kRestore ? fill_worker : drain_worker, r, w);
   } catch (...) {
     st = KVX_ENOMEM;
   }
@@ -344,7 +567,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
     if (dir == Dir::kRestore) {
       if (T > 0) wait_parts(i);
       if (r->stop.load() || r->closed.load()) {
-        st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
+        st = worker_status(r);
         break;
       }
       bool ok = hipStreamWaitEvent(r->side, r->dev_done[s], 0) == hipSuccess;
@@ -393,7 +616,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
       // gather runs meanwhile.
       if (T > 0 && i >= S) wait_parts(i - S);
       if (r->stop.load()) {
-        st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
+        st = worker_status(r);
         break;
       }
       if (hipEventSynchronize(r->dev_done[s]) != hipSuccess) {
@@ -424,7 +647,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
       }
       if (T > 0 && i >= S) wait_parts(i - S);  // host slot s emptied by the drains
       if (r->stop.load()) {
-        st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
+        st = worker_status(r);
         break;
       }
       bool ok = hipStreamWaitEvent(r->side, r->dev_done[s], 0) == hipSuccess;
@@ -453,7 +676,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
     // threads, the last device-to-host copies) have finished.
     if (T > 0) {
       for (int64_t i = std::max<int64_t>(0, P - S); i < P && !r->stop.load(); ++i) wait_parts(i);
-      if (r->stop.load()) st = r->worker_error.load() ? KVX_EHIP : KVX_ECLOSED;
+      if (r->stop.load()) st = worker_status(r);
     } else if (use_dma(r)) {
       for (int32_t s = 0; s < S; ++s)
         if (!wait_dma(r, s)) st = KVX_EHIP;
@@ -675,6 +898,43 @@ kvx_status bind(kvx_ring* r, Dir dir, const kvx_cache* cache, int32_t l0, int32_
   r->plan.refs.swap(plan.refs);
   r->plan.table_len = plan.table_len;
   r->dir = dir;
+  for (auto& f : r->files) kvx::close_tier_file(&f);
+  r->files.clear();
+  r->files_mode = false;
+  r->io_depth = 0;
+  return KVX_OK;
+}
+
+// Bind to chunk files: plan the chunks at their notional addresses.
+kvx_status bind_files(kvx_ring* r, Dir dir, const kvx_cache* cache, int32_t l0, int32_t l1,
+                      int32_t chunk_tokens, const kvx_file_chunk* chunks, int32_t n_chunks,
+                      int32_t io_depth) {
+  if (n_chunks < 0 || (n_chunks > 0 && !chunks) || n_chunks >= (1 << 22) || io_depth < 1 ||
+      io_depth > 256)
+    return KVX_EINVAL;
+  kvx::Geometry g;
+  kvx_status st = kvx::validate(cache, l0, l1, 0, chunk_tokens, false, &g);
+  if (st != KVX_OK) return st;
+  std::vector<kvx::TierFile> files((size_t)n_chunks);
+  std::vector<kvx::HostChunk> hc((size_t)n_chunks);
+  for (int32_t f = 0; f < n_chunks; ++f) {
+    const kvx_file_chunk& c = chunks[f];
+    if (!c.path || !c.path[0] || c.n_blocks < 1) return KVX_EINVAL;
+    files[(size_t)f].path = c.path;
+    files[(size_t)f].size = (int64_t)(l1 - l0) * 2 * c.n_blocks * g.slab;
+    if (files[(size_t)f].size >= ((int64_t)1 << kFileShift)) return KVX_EINVAL;
+    hc[(size_t)f] = kvx::HostChunk{reinterpret_cast<uint8_t*>((uintptr_t)(f + 1) << kFileShift),
+                                   c.bt_offset, c.n_blocks};
+  }
+  st = bind(r, dir, cache, l0, l1, chunk_tokens, std::move(hc), 1);
+  if (st != KVX_OK) return st;
+  // The staging slots are pinned host memory, which cannot be the target of a
+  // direct transfer here (EFAULT): the ring's files use buffered I/O, flushed
+  // before publication and dropped from the page cache after use.
+  for (auto& f : files) f.direct = false;
+  r->files = std::move(files);
+  r->files_mode = true;
+  r->io_depth = io_depth;
   return KVX_OK;
 }
 
@@ -793,6 +1053,29 @@ kvx_status kvx_ring_bind_offload(kvx_ring* r, const kvx_cache* cache, int32_t l0
     kvx_status st = host_chunks(chunks, n_chunks, &v);
     if (st != KVX_OK) return st;
     return bind(r, Dir::kOffload, cache, l0, l1, chunk_tokens, std::move(v), drain_threads);
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}
+
+kvx_status kvx_ring_bind_files(kvx_ring* r, const kvx_cache* cache, int32_t l0, int32_t l1,
+                               int32_t chunk_tokens, const kvx_file_chunk* chunks,
+                               int32_t n_chunks, int32_t io_depth) {
+  if (!r || !cache) return KVX_EINVAL;
+  try {
+    return bind_files(r, Dir::kRestore, cache, l0, l1, chunk_tokens, chunks, n_chunks, io_depth);
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}
+
+kvx_status kvx_ring_bind_offload_files(kvx_ring* r, const kvx_cache* cache, int32_t l0,
+                                       int32_t l1, int32_t chunk_tokens,
+                                       const kvx_file_chunk* chunks, int32_t n_chunks,
+                                       int32_t io_depth) {
+  if (!r || !cache) return KVX_EINVAL;
+  try {
+    return bind_files(r, Dir::kOffload, cache, l0, l1, chunk_tokens, chunks, n_chunks, io_depth);
   } catch (...) {
     return KVX_EINTERNAL;
   }
