@@ -194,3 +194,14 @@ def test_probe_rejects_bad_arguments_on_the_host():
     assert lib.kvx_probe_stream(4096, 8192, unit, 3, None) == kvx.KVX_EINVAL  # mode
     assert lib.kvx_probe_stream(4100, 8192, unit, 2, None) == kvx.KVX_EINVAL  # alignment
     assert lib.kvx_probe_stream(4096, 8192, -unit, 2, None) == kvx.KVX_EINVAL
+
+
+def test_layer_range_limit_on_the_host():
+    """A call covers at most KVX_MAX_LAYERS (128) layers."""
+    import paper_2609_11744_amd as kvx
+
+    c = kvx.shape_only_cache(130, 100, 16, 8, 128, 2)
+    assert kvx.KVX_MAX_LAYERS == 128
+    assert kvx.kvx_packed_bytes(c, 1, 129, 10) == 128 * 2 * 10 * 16 * 8 * 128 * 2
+    assert kvx.kvx_packed_bytes(c, 0, 129, 10) == -1
+    assert kvx.kvx_packed_bytes(c, 0, 131, 10) == -1

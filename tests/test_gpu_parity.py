@@ -138,6 +138,7 @@ EDGE = [
     (2, 30, 8, 2, 32, 4, 0, 2, 11, 16),       # 4-byte elements
     (2, 30, 8, 1, 32, 8, 0, 2, 6, 24),        # 8-byte elements
     (5, 25, 2, 1, 8, 2, 2, 5, 1, 2),          # a single block
+    (130, 12, 2, 1, 8, 2, 1, 129, 5, 4),      # the largest layer range a call takes (128)
 ]
 
 
