@@ -94,6 +94,13 @@ def kernels_sha256() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
+def copies_desc(stats):
+    """How a ring's last transfer moved its host-link copies."""
+    if stats.get("dma"):
+        return "DMA engine (id bit %d)" % stats["dma_engine"]
+    return "HIP runtime"
+
+
 def probes(dev, reps):
     """Same-run link and copy probes: 1 GiB pinned H2D / D2H, 4 GiB D2D, and
     the HBM read / write / copy rates of a kernel shaped like the slab mover."""
@@ -282,6 +289,7 @@ def run_80k(args):
         "restore_ms": round(med["restore_ms"], 3),
         "restore_GBps": round(restore_GBps, 2),
         "restore_frac_of_h2d": round(restore_GBps / probe["h2d_GBps"], 4),
+        "h2d_copies": copies_desc(ring.stats()),
         "restore_breakdown_ms": {"fill_thread_sum": round(med["fill_ms"], 2),
                                  "enqueue_wait_for_fill": round(med["wait_fill_ms"], 2),
                                  "device_span": round(med["restore_dev_ms"], 2)},
@@ -338,8 +346,7 @@ def offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe):
     return {"offload_ms": round(t * 1e3, 3), "offload_GBps": round(gbps, 2),
             "offload_frac_of_d2h": round(gbps / probe["d2h_GBps"], 4),
             "reps": args.offload_reps,
-            "d2h_copies": "DMA engine (id bit %d)" % st["dma_engine"] if st.get("dma_d2h")
-                          else "HIP runtime",
+            "d2h_copies": copies_desc(st),
             "breakdown_ms": {"drain_thread_sum": round(statistics.median(drain), 2),
                              "wait_for_drain": round(statistics.median(wait), 2)}}
 
@@ -579,6 +586,7 @@ def run_batch(args):
         alone["offload"].append(time.perf_counter() - t0)
     alone = {k: min(v) for k, v in alone.items()}
     o_stats = o_ring.stats()
+    r_stats = r_ring.stats()
     out = base_record(args, "KV staged restore GB/s (70B batched step, offload concurrent)", "GB/s",
                       round(rb / med["restore"] / 1e9, 2), round(med["step"] * 1e3, 2),
                       {"workload": "70b-shaped paged KV, 64 requests on a seeded prefix tree "
@@ -594,6 +602,8 @@ def run_batch(args):
                 "offload_frac_of_d2h": round(ob / med["offload"] / 1e9 / probe["d2h_GBps"], 4),
                 "restore_ms": round(med["restore"] * 1e3, 2),
                 "offload_ms": round(med["offload"] * 1e3, 2),
+                "link_GBps_both_ways": round((rb + ob) / med["step"] / 1e9, 2),
+                "h2d_copies": copies_desc(r_stats), "d2h_copies": copies_desc(o_stats),
                 "alone": {"restore_GBps": round(rb / alone["restore"] / 1e9, 2),
                           "offload_GBps": round(ob / alone["offload"] / 1e9, 2),
                           "offload_drain_thread_ms": round(o_stats["fill_ms"], 2),

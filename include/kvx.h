@@ -219,9 +219,12 @@ typedef struct kvx_ring kvx_ring;
 /* Create a ring on `device` with n_slots (>= 1) slots of slot_bytes (a
  * positive multiple of 4096): one hipHostMalloc allocation of
  * n_slots * slot_bytes pinned bytes, one non-blocking side stream at default
- * priority, and per-slot events. device_landing is the device buffer that
- * H2D copies land in (n_slots * slot_bytes bytes, 16-byte aligned, owned by
- * the caller); NULL makes the ring allocate its own. */
+ * priority, per-slot events and, where the HSA runtime exposes the GPU's DMA
+ * engines, per-slot completion signals. The first ring created on a device in
+ * the process also times the engines (a few milliseconds, on 8 MiB device and
+ * 8 MiB pinned buffers of its own, freed afterwards). device_landing is the
+ * device buffer that H2D copies land in (n_slots * slot_bytes bytes, 16-byte
+ * aligned, owned by the caller); NULL makes the ring allocate its own. */
 kvx_status kvx_ring_create(int device, int32_t n_slots, int64_t slot_bytes, void* device_landing,
                            kvx_ring** out);
 
@@ -240,14 +243,18 @@ kvx_status kvx_ring_bind(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int
 /* Restore the bound image into the blocks named by block_table (device
  * int32[n_blocks], distinct destination ids). For piece i on slot s = i mod
  * n_slots: fill threads copy the piece into host slot s once the H2D copy of
- * piece i - n_slots has completed; the side stream waits until the scatter of
- * piece i - n_slots has finished reading device slot s, copies host slot s
- * to device slot s and records an event; `stream` waits on that event and
- * runs the scatter of the piece. Returns once every piece is enqueued (the
- * host thread waits for fill threads, never for the device); all scatters
- * are ordered on `stream`. The cache equals the scatter of the whole image
- * once `stream` completes. KVX_ECLOSED if kvx_ring_abort was called; pieces
- * already enqueued still complete. */
+ * piece i - n_slots has completed; once the scatter of piece i - n_slots has
+ * finished reading device slot s, host slot s is copied to device slot s by a
+ * DMA engine; once the host has seen that copy complete, `stream` runs the
+ * scatter of the piece (the copy of piece i + 1 is issued before that wait,
+ * so the engine never idles). Returns once every piece's scatter is enqueued
+ * (the host thread waits for fill threads and for the copies, not for the
+ * scatters); all scatters are ordered on `stream`. Without DMA engines (see
+ * kvx_ring_stats.dma) the copies go through the HIP runtime on the side
+ * stream, ordered by events, and the call returns once every piece is
+ * enqueued without waiting for the device. The cache equals the scatter of
+ * the whole image once `stream` completes. KVX_ECLOSED if kvx_ring_abort was
+ * called; scatters already enqueued still complete. */
 kvx_status kvx_restore_from_staging(kvx_ring* ring, const int32_t* block_table,
                                     hipStream_t stream);
 
@@ -284,13 +291,14 @@ kvx_status kvx_ring_bind_offload(kvx_ring* ring, const kvx_cache* cache, int32_t
                                  int32_t n_chunks, int32_t drain_threads);
 
 /* Offload the bound chunks, reading the blocks named by block_table (device).
- * For piece i on slot s = i mod n_slots: `stream` waits until device slot s is
- * no longer read by the copy of piece i - n_slots, gathers the piece into it
- * (one fused launch) and records an event; the side stream waits on it and
- * copies device slot s to host slot s once the drain threads have emptied
- * host slot s; drain threads copy host slot s to the chunks' destinations once
- * that copy has completed. Returns when every destination holds its image (it
- * waits for the device). KVX_ECLOSED after kvx_ring_abort. */
+ * For piece i on slot s = i mod n_slots: once the copy of piece i - n_slots
+ * has left device slot s, `stream` gathers the piece into it (one fused
+ * launch) and records an event; once that event has completed and the drain
+ * threads have emptied host slot s, device slot s is copied to host slot s by
+ * a DMA engine (without DMA engines: by the HIP runtime on the side stream);
+ * drain threads copy host slot s to the chunks' destinations once that copy
+ * has completed. Returns when every destination holds its image (it waits for
+ * the device). KVX_ECLOSED after kvx_ring_abort. */
 kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hipStream_t stream);
 
 typedef struct kvx_ring_stats {
@@ -299,13 +307,16 @@ typedef struct kvx_ring_stats {
   double fill_ms;         /* summed fill (restore) or drain (offload) thread copy time */
   double wait_fill_ms;    /* time the enqueuing thread waited for fill or drain threads */
   double enqueue_ms;      /* wall time of the last restore or offload call */
-  int32_t dma_d2h;        /* 1: the last offload's device-to-host copies ran on the GPU's DMA
-                             engine (issued directly); 0: restore, or copies through the HIP
-                             runtime (which may run them as a copy kernel on compute units) */
-  int32_t dma_engine;     /* with dma_d2h: the engine's id bit (the fastest of the runtime's
-                             preferred, else available, engines, timed by the first ring
-                             created on the device in the process); 0 = the runtime's own
-                             choice */
+  int32_t dma;            /* 1: the last transfer's host-link copies were issued to the GPU's
+                             DMA engines directly; 0: through the HIP runtime on the side
+                             stream (which may run a device-to-host copy as a copy kernel on
+                             compute units) */
+  int32_t dma_engine;     /* with dma: the engine id bit of that direction (restore: H2D,
+                             offload: D2H). The device's pair is timed by the first ring
+                             created on it in the process: of the runtime's preferred (else
+                             available) engines, those fast alone in each direction, and of
+                             those the D2H / H2D pair fastest running at once. 0 = the
+                             runtime's own choice */
 } kvx_ring_stats;
 
 kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out);
@@ -386,8 +397,9 @@ kvx_status kvx_write_files(const kvx_file_io* ops, int32_t n, int32_t io_depth);
  * flags bit 0: a restore's fill threads overwrite their share of a released
  * host slot with 0xA5 bytes (then pause) before refilling it, so a copy that
  * still read a released slot would deliver the poison.
- * flags bit 1: offload copies go through the HIP runtime on the side stream
- * even when the DMA engine is set up (exercises that path).
+ * flags bit 1: the host-link copies (both directions) go through the HIP
+ * runtime on the side stream even when the DMA engines are set up (exercises
+ * that path); changing it first waits for the ring's copies in flight.
  * Other bits: KVX_EINVAL. Off by default; call between transfers. */
 kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t flags);
 

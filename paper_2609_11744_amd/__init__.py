@@ -414,10 +414,11 @@ class StagingRing:
     def abort(self):
         _ok(_native.lib().kvx_ring_abort(self.handle), "kvx_ring_abort")
 
-    def set_test_hooks(self, max_delay_us=0, poison=False, hip_d2h=False):
+    def set_test_hooks(self, max_delay_us=0, poison=False, hip_copies=False):
         """Fault injection: random fill/drain pauses, poisoning of released slots;
-        hip_d2h routes offload copies through the HIP runtime instead of the DMA engine."""
-        flags = (1 if poison else 0) | (2 if hip_d2h else 0)
+        hip_copies routes the host-link copies (both directions) through the HIP
+        runtime instead of the DMA engines."""
+        flags = (1 if poison else 0) | (2 if hip_copies else 0)
         _ok(_native.lib().kvx_ring_set_test_hooks(self.handle, max_delay_us, flags),
             "kvx_ring_set_test_hooks")
 

@@ -34,7 +34,7 @@ class KvxHostChunk(ctypes.Structure):
 class KvxRingStats(ctypes.Structure):
     _fields_ = [("pieces", c_i64), ("bytes", c_i64), ("fill_ms", ctypes.c_double),
                 ("wait_fill_ms", ctypes.c_double), ("enqueue_ms", ctypes.c_double),
-                ("dma_d2h", c_i32), ("dma_engine", c_i32)]
+                ("dma", c_i32), ("dma_engine", c_i32)]
 
 
 class KvxFileChunk(ctypes.Structure):

@@ -7,29 +7,37 @@
 // Restore, piece i on slot s = i mod n_slots:
 //   fill    host threads copy the piece's chunk images into host slot s, after
 //           the H2D copy of piece i - n_slots (which read host slot s) is done;
-//   H2D     the side stream waits until device slot s is free (the scatter of
-//           piece i - n_slots has read it), copies host slot s to device slot
-//           s and records copy_done[s];
-//   scatter the caller's stream waits on copy_done[s], runs one fused
-//           chunk-list scatter from device slot s, records dev_done[s].
+//   H2D     once the scatter of piece i - n_slots has finished reading device
+//           slot s (the host waits on dev_done[s]), host slot s is copied to
+//           device slot s by a DMA engine, completion on dma_done[s];
+//   scatter once the host has seen that copy complete, the caller's stream
+//           runs one fused chunk-list scatter from device slot s and records
+//           dev_done[s]. The copy of piece i + 1 is issued before the host
+//           waits for the copy of piece i, so the engine always holds the
+//           next copy and the link does not idle while a scatter is launched.
 // Offload, piece i on slot s:
 //   gather  once the D2H copy of piece i - n_slots has left device slot s,
 //           the caller's stream runs one fused chunk-list gather into it and
 //           records dev_done[s] (a system-scope release);
 //   D2H     when dev_done[s] has completed and the drain threads have emptied
-//           host slot s, device slot s is copied to host slot s by the GPU's
-//           DMA engine, completion on dma_done[s];
+//           host slot s, device slot s is copied to host slot s by a DMA
+//           engine, completion on dma_done[s];
 //   drain   host threads wait on dma_done[s] and copy host slot s to the
 //           chunks' destinations.
-// The D2H copies are issued to the DMA engine directly (HSA async copy):
-// enqueued through the HIP runtime, a device-to-host copy may run as a copy
+// The copies are issued to the GPU's DMA engines directly (HSA async copy).
+// Enqueued through the HIP runtime, a device-to-host copy may run as a copy
 // kernel instead, which occupies compute units for the whole link-bound
 // transfer and starves the kernels it was meant to overlap (Sec. 5.1 contrasts
-// DMA copies with a copy kernel that consumes GPU compute). If the DMA engine
-// cannot be set up, the offload falls back to the HIP copy on a side stream
-// ordered by copy_done / dev_done events, and the ring's stats say so.
-// The enqueuing thread never waits for the device in a restore; fill and
-// drain threads wait on copy_done events or DMA signals (they sleep).
+// DMA copies with a copy kernel that consumes GPU compute); and choosing the
+// engines makes a restore and an offload running at once use the link in
+// both directions (an H2D and a D2H engine that share a link path split it
+// instead). The engines are chosen once per device by timing (pick_engines).
+// A kernel launched after the host has observed a DMA completion reads the
+// copied bytes: the launch acquires device memory at system scope. If the DMA
+// engines cannot be set up, both directions fall back to HIP copies on a side
+// stream ordered by copy_done / dev_done events (the restore's enqueuing
+// thread then never waits for the device), and the ring's stats say so.
+// Fill and drain threads wait on copy_done events or DMA signals (they sleep).
 #include <hip/hip_runtime_api.h>
 #include <hsa/hsa.h>
 #include <hsa/hsa_ext_amd.h>
@@ -65,12 +73,12 @@ struct kvx_ring {
   std::vector<hipEvent_t> copy_done;  // H2D / D2H of the slot's last piece (host waits)
   std::vector<hipEvent_t> dev_done;   // scatter / gather of the slot's last piece
 
-  // offload D2H on the DMA engine
+  // host-link copies on the DMA engines
   bool dma = false;
   bool hsa_up = false;
   hsa_agent_t gpu_agent{}, cpu_agent{};
-  uint32_t dma_engine = 0;             // SDMA engine id bit for the copies; 0: the runtime's choice
-  std::vector<hsa_signal_t> dma_done;  // per slot: copies of its last piece still running
+  uint32_t d2h_engine = 0, h2d_engine = 0;  // SDMA engine id bits; 0: the runtime's choice
+  std::vector<hsa_signal_t> dma_done;       // per slot: copies of its last piece still running
 
   // binding
   Dir dir = Dir::kNone;
@@ -97,7 +105,7 @@ struct kvx_ring {
   // test hooks (kvx_ring_set_test_hooks)
   int32_t hook_max_delay_us = 0;
   bool hook_poison = false;
-  bool hook_hip_d2h = false;  // offload D2H through the HIP runtime even with the DMA engine set up
+  bool hook_hip_copies = false;  // copies through the HIP runtime even with the DMA engines set up
 
   // storage tier: the bound chunks live in files (kvx_ring_bind_files /
   // kvx_ring_bind_offload_files); a reactor thread replaces the fill / drain
@@ -127,9 +135,8 @@ struct DeviceGuard {
   }
 };
 
-// Wait until nothing the ring enqueued can still touch its slots or tables.
-// Whether this ring's offload copies go to the DMA engine.
-bool use_dma(const kvx_ring* r) { return r->dma && !r->hook_hip_d2h; }
+// Whether this ring's copies go to the DMA engines.
+bool use_dma(const kvx_ring* r) { return r->dma && !r->hook_hip_copies; }
 
 // Block until the slot's DMA copies have finished; false if one failed.
 bool wait_dma(kvx_ring* r, int32_t s) {
@@ -137,6 +144,19 @@ bool wait_dma(kvx_ring* r, int32_t s) {
                                    HSA_WAIT_STATE_BLOCKED) == 0;
 }
 
+// Block until the host-link copy of the slot's last piece has finished.
+bool wait_copy(kvx_ring* r, int32_t s) {
+  return use_dma(r) ? wait_dma(r, s) : hipEventSynchronize(r->copy_done[(size_t)s]) == hipSuccess;
+}
+
+// Whether that copy has finished successfully (a failed one never counts as
+// finished: wait_copy reports it).
+bool copy_finished(kvx_ring* r, int32_t s) {
+  if (use_dma(r)) return hsa_signal_load_scacquire(r->dma_done[(size_t)s]) == 0;
+  return hipEventQuery(r->copy_done[(size_t)s]) == hipSuccess;
+}
+
+// Wait until nothing the ring enqueued can still touch its slots or tables.
 void drain_device(kvx_ring* r) {
   for (size_t s = 0; s < r->dma_done.size(); ++s) (void)wait_dma(r, (int32_t)s);
   if (r->side) (void)hipStreamSynchronize(r->side);
@@ -216,12 +236,12 @@ void fill_worker(kvx_ring* r, int w) {
     hook_pause(r, &rng);
     const int32_t s = (int32_t)(i % S);
     if (i >= S) {
-      // copy_done[s] must hold the record of piece i - S before we wait on it.
+      // The copy of piece i - S must have been issued before we wait for it.
       std::unique_lock<std::mutex> lock(r->mu);
       r->cv_enqueued.wait(lock, [&] { return r->enqueued > i - S || r->stop.load(); });
     }
     if (r->stop.load()) break;
-    if (hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
+    if (!wait_copy(r, s)) {
       r->worker_error.store(KVX_EHIP);
       signal_stop(r);
       break;
@@ -260,7 +280,7 @@ void drain_worker(kvx_ring* r, int w) {
       r->cv_enqueued.wait(lock, [&] { return r->enqueued > i || r->stop.load(); });
     }
     if (r->stop.load()) break;
-    if (use_dma(r) ? !wait_dma(r, s) : hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
+    if (!wait_copy(r, s)) {
       r->worker_error.store(KVX_EHIP);
       signal_stop(r);
       break;
@@ -338,7 +358,7 @@ void file_fill_worker(kvx_ring* r) {
             std::lock_guard<std::mutex> lock(r->mu);
             enq = r->enqueued > next - S;
           }
-          if (!enq || hipEventQuery(r->copy_done[s]) != hipSuccess) {
+          if (!enq || !copy_finished(r, s)) {
             blocked = true;
             break;
           }
@@ -366,7 +386,7 @@ void file_fill_worker(kvx_ring* r) {
         r->cv_enqueued.wait(lock, [&] { return r->enqueued > next - S || r->stop.load(); });
       }
       if (r->stop.load()) break;
-      if (hipEventSynchronize(r->copy_done[s]) != hipSuccess) st = KVX_EHIP;
+      if (!wait_copy(r, s)) st = KVX_EHIP;
       continue;
     }
     done.clear();
@@ -457,7 +477,7 @@ void file_drain_worker(kvx_ring* r) {
       break;
     }
     if (st != KVX_OK || r->stop.load()) break;
-    if (use_dma(r) ? !wait_dma(r, s) : hipEventSynchronize(r->copy_done[s]) != hipSuccess) {
+    if (!wait_copy(r, s)) {
       st = KVX_EHIP;
       break;
     }
@@ -491,18 +511,22 @@ kvx_status launch_piece(kvx_ring* r, bool to_packed, const kvx::Piece& p, const 
                                  r->slot_bytes, stream);
 }
 
-hsa_status_t dma_copy(kvx_ring* r, void* dst, const void* src, size_t bytes, hsa_signal_t sig) {
-  if (r->dma_engine)
-    return hsa_amd_memory_async_copy_on_engine(dst, r->cpu_agent, src, r->gpu_agent, bytes, 0,
-                                               nullptr, sig,
-                                               (hsa_amd_sdma_engine_id_t)r->dma_engine, true);
-  return hsa_amd_memory_async_copy(dst, r->cpu_agent, src, r->gpu_agent, bytes, 0, nullptr, sig);
+// One async copy on a DMA engine (engine 0: the runtime's choice); the copy
+// decrements sig when it has finished.
+hsa_status_t engine_copy(void* dst, hsa_agent_t dst_agent, const void* src, hsa_agent_t src_agent,
+                         size_t bytes, uint32_t engine, hsa_signal_t sig) {
+  if (engine)
+    return hsa_amd_memory_async_copy_on_engine(dst, dst_agent, src, src_agent, bytes, 0, nullptr,
+                                               sig, (hsa_amd_sdma_engine_id_t)engine, true);
+  return hsa_amd_memory_async_copy(dst, dst_agent, src, src_agent, bytes, 0, nullptr, sig);
 }
 
-// D2H of an offload piece on the DMA engine: device slot s to host slot s, or
-// with no drain threads straight to the piece's destinations. dma_done[s]
-// counts the piece's copies down to 0 (negative on a copy error).
-kvx_status issue_dma(kvx_ring* r, const kvx::Piece& p, int32_t s, uint8_t* dslot, uint8_t* hslot) {
+// The host-link copies of piece p on slot s: H2D (restore) host slot s to
+// device slot s, or D2H (offload) device slot s to host slot s; without fill
+// or drain threads, one copy per span between its host address and its place
+// in the device slot. dma_done[s] counts the piece's copies down to 0.
+kvx_status issue_dma(kvx_ring* r, const kvx::Piece& p, int32_t s, uint8_t* dslot, uint8_t* hslot,
+                     bool h2d) {
   hsa_signal_t sig = r->dma_done[(size_t)s];
   const bool whole = r->threads > 0;
   const int64_t n = whole ? 1 : (int64_t)p.spans.size();
@@ -510,10 +534,13 @@ kvx_status issue_dma(kvx_ring* r, const kvx::Piece& p, int32_t s, uint8_t* dslot
   hsa_signal_store_screlease(sig, n);
   int64_t issued = 0;
   for (int64_t k = 0; k < n; ++k) {
-    void* dst = whole ? (void*)hslot : (void*)p.spans[(size_t)k].host;
-    const void* src = whole ? (const void*)dslot : (const void*)(dslot + p.spans[(size_t)k].slot_off);
+    uint8_t* host = whole ? hslot : p.spans[(size_t)k].host;
+    uint8_t* dev = whole ? dslot : dslot + p.spans[(size_t)k].slot_off;
     const size_t bytes = (size_t)(whole ? p.bytes : p.spans[(size_t)k].bytes);
-    if (dma_copy(r, dst, src, bytes, sig) != HSA_STATUS_SUCCESS) break;
+    const hsa_status_t hs =
+        h2d ? engine_copy(dev, r->gpu_agent, host, r->cpu_agent, bytes, r->h2d_engine, sig)
+            : engine_copy(host, r->cpu_agent, dev, r->gpu_agent, bytes, r->d2h_engine, sig);
+    if (hs != HSA_STATUS_SUCCESS) break;
     ++issued;
   }
   if (issued < n) {  // the copies never issued will never count down: do it here
@@ -521,6 +548,17 @@ kvx_status issue_dma(kvx_ring* r, const kvx::Piece& p, int32_t s, uint8_t* dslot
     return KVX_EHIP;
   }
   return KVX_OK;
+}
+
+// Restore on the DMA engines: scatter piece j once the host has seen its copy
+// complete (the launch then reads the copied bytes of device slot j mod S).
+kvx_status scatter_copied(kvx_ring* r, int64_t j, const int32_t* bt, hipStream_t stream) {
+  const int32_t s = (int32_t)(j % r->n_slots);
+  if (!wait_dma(r, s)) return KVX_EHIP;
+  kvx_status st = launch_piece(r, false, r->plan.pieces[(size_t)j], bt,
+                               r->landing + (int64_t)s * r->slot_bytes, stream);
+  if (st != KVX_OK) return st;
+  return hipEventRecord(r->dev_done[(size_t)s], stream) == hipSuccess ? KVX_OK : KVX_EHIP;
 }
 
 kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
@@ -559,12 +597,42 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
     r->cv_host.wait(lock, [&] { return r->parts_done[(size_t)i] == T || r->stop.load(); });
     wait_ms += ms_since(t0);
   };
+  int64_t copied = -1;  // restore on the DMA engines: the piece copied but not yet scattered
   for (int64_t i = 0; st == KVX_OK && i < P; ++i) {
     const int32_t s = (int32_t)(i % S);
     const kvx::Piece& p = r->plan.pieces[(size_t)i];
     uint8_t* dslot = r->landing + (int64_t)s * r->slot_bytes;
     uint8_t* hslot = r->host + (int64_t)s * r->slot_bytes;
-    if (dir == Dir::kRestore) {
+    if (dir == Dir::kRestore && use_dma(r)) {
+      if (T > 0) wait_parts(i);
+      if (r->stop.load() || r->closed.load()) {
+        st = worker_status(r);
+        break;
+      }
+      // With one slot, the pending piece must be scattered out of it first.
+      if (copied >= 0 && copied % S == s) {
+        st = scatter_copied(r, copied, bt, stream);
+        copied = -1;
+        if (st != KVX_OK) break;
+      }
+      // Device slot s is free once the scatter that last read it (piece
+      // i - S, or the previous transfer's) has finished.
+      if (hipEventSynchronize(r->dev_done[s]) != hipSuccess) {
+        st = KVX_EHIP;
+        break;
+      }
+      st = issue_dma(r, p, s, dslot, hslot, true);
+      if (st != KVX_OK) break;
+      {
+        std::lock_guard<std::mutex> lock(r->mu);
+        r->enqueued = i + 1;
+      }
+      r->cv_enqueued.notify_all();
+      // The copy of piece i is queued behind that of the pending piece: wait
+      // for the pending one and scatter it meanwhile.
+      if (copied >= 0) st = scatter_copied(r, copied, bt, stream);
+      copied = i;
+    } else if (dir == Dir::kRestore) {
       if (T > 0) wait_parts(i);
       if (r->stop.load() || r->closed.load()) {
         st = worker_status(r);
@@ -623,7 +691,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
         st = KVX_EHIP;
         break;
       }
-      st = issue_dma(r, p, s, dslot, hslot);
+      st = issue_dma(r, p, s, dslot, hslot, false);
       if (st != KVX_OK) break;
       {
         std::lock_guard<std::mutex> lock(r->mu);
@@ -671,6 +739,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
       r->cv_enqueued.notify_all();
     }
   }
+  if (st == KVX_OK && copied >= 0) st = scatter_copied(r, copied, bt, stream);
   if (st == KVX_OK && dir == Dir::kOffload) {
     // The destinations are complete once the last drains (or, without drain
     // threads, the last device-to-host copies) have finished.
@@ -686,8 +755,9 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
   }
   if (st != KVX_OK) {
     signal_stop(r);
-    if (dir == Dir::kOffload) {
-      // Nothing may still write a destination once the call has returned.
+    if (dir == Dir::kOffload || use_dma(r)) {
+      // Nothing may still write a destination or a device slot once the call
+      // has returned (a restore's HIP copies are ordered by events instead).
       if (use_dma(r)) {
         for (int32_t s = 0; s < S; ++s) (void)wait_dma(r, s);
       } else {
@@ -704,8 +774,9 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
   r->stats.fill_ms = (double)r->busy_ns.load() / 1e6;
   r->stats.wait_fill_ms = wait_ms;
   r->stats.enqueue_ms = ms_since(t_start);
-  r->stats.dma_d2h = dir == Dir::kOffload && use_dma(r) ? 1 : 0;
-  r->stats.dma_engine = r->stats.dma_d2h ? (int32_t)r->dma_engine : 0;
+  r->stats.dma = use_dma(r) ? 1 : 0;
+  r->stats.dma_engine =
+      use_dma(r) ? (int32_t)(dir == Dir::kRestore ? r->h2d_engine : r->d2h_engine) : 0;
   return st;
 }
 
@@ -737,60 +808,155 @@ hsa_status_t find_agent(hsa_agent_t a, void* data) {
   return HSA_STATUS_SUCCESS;
 }
 
-// Device-to-host bandwidth differs several-fold between a GPU's DMA engines
-// (only some sit close to the host link), and an engine left to the runtime
-// may be any of them (measured through the runtime a torch process loads: one
-// of the four fast engines moved 17.5 GB/s where the other three moved 51).
-// The candidates are the runtime's preferred engines for this direction, or
-// with no preference every available engine; with more than one, a short copy
-// device slot 0 -> host slot 0 is timed on each (after an untimed one) and the
-// fastest kept. With no candidates the choice stays with the runtime.
-void pick_engine(kvx_ring* r) {
-  uint32_t cand = 0;
-  if (hsa_amd_memory_get_preferred_copy_engine(r->cpu_agent, r->gpu_agent, &cand) !=
-      HSA_STATUS_SUCCESS)
-    cand = 0;
-  if (cand == 0 &&
-      hsa_amd_memory_copy_engine_status(r->cpu_agent, r->gpu_agent, &cand) != HSA_STATUS_SUCCESS)
-    cand = 0;
-  r->dma_engine = 0;
-  if (cand == 0) return;
-  if ((cand & (cand - 1)) == 0) {
-    r->dma_engine = cand;
-    return;
+// Copies between the device and pinned host memory on chosen engines, timed
+// from the host. Each direction has its own half of both buffers, so the two
+// directions can run at once.
+struct EngineProbe {
+  static constexpr size_t kHalf = 4 << 20;
+  hsa_agent_t gpu{}, cpu{};
+  uint8_t* dev = nullptr;   // 2 * kHalf device bytes
+  uint8_t* host = nullptr;  // 2 * kHalf pinned bytes
+  hsa_signal_t sig[2]{};    // D2H, H2D
+  bool ready = false;
+
+  bool init(const kvx_ring* r) {
+    gpu = r->gpu_agent;
+    cpu = r->cpu_agent;
+    void* d = nullptr;
+    void* h = nullptr;
+    if (hipMalloc(&d, 2 * kHalf) != hipSuccess) return false;
+    dev = (uint8_t*)d;
+    if (hipHostMalloc(&h, 2 * kHalf, hipHostMallocDefault) != hipSuccess) return false;
+    host = (uint8_t*)h;
+    if (hsa_signal_create(0, 0, nullptr, &sig[0]) != HSA_STATUS_SUCCESS) return false;
+    if (hsa_signal_create(0, 0, nullptr, &sig[1]) != HSA_STATUS_SUCCESS) {
+      (void)hsa_signal_destroy(sig[0]);
+      sig[0].handle = 0;
+      return false;
+    }
+    ready = true;
+    return true;
   }
-  const size_t bytes = (size_t)std::min<int64_t>(r->slot_bytes, 4 << 20);
-  hsa_signal_t sig = r->dma_done[0];
-  // An engine's first copy in a process pays a one-time setup that is many
-  // times a 4 MiB copy: give every candidate an untimed small copy first.
-  for (uint32_t bit = 1; bit != 0 && bit <= cand; bit <<= 1) {
-    if (!(cand & bit)) continue;
-    r->dma_engine = bit;
-    hsa_signal_store_screlease(sig, 1);
-    if (dma_copy(r, r->host, r->landing, 64 << 10, sig) != HSA_STATUS_SUCCESS)
-      hsa_signal_store_screlease(sig, 0);
-    if (!wait_dma(r, 0)) hsa_signal_store_screlease(sig, 0);
+
+  ~EngineProbe() {
+    for (hsa_signal_t s : sig)
+      if (s.handle) (void)hsa_signal_destroy(s);
+    if (host) (void)hipHostFree(host);
+    if (dev) (void)hipFree(dev);
   }
-  double best = 0;
-  uint32_t best_bit = 0;
-  for (uint32_t bit = 1; bit != 0 && bit <= cand; bit <<= 1) {
-    if (!(cand & bit)) continue;
-    r->dma_engine = bit;
-    hsa_signal_store_screlease(sig, 2);
+
+  // Issue `reps` copies of `bytes` in each direction (engine id bits, 0: the
+  // runtime's choice), both directions interleaved so they start together;
+  // wait for all and return the combined rate in bytes per second, 0 if a
+  // copy failed.
+  double run(uint32_t d2h, int d2h_reps, uint32_t h2d, int h2d_reps, size_t bytes) {
+    const int reps[2] = {d2h_reps, h2d_reps};
+    int issued[2] = {0, 0};
+    hsa_signal_store_screlease(sig[0], reps[0]);
+    hsa_signal_store_screlease(sig[1], reps[1]);
     const auto t0 = clk::now();
-    int issued = 0;
-    for (; issued < 2; ++issued)
-      if (dma_copy(r, r->host, r->landing, bytes, sig) != HSA_STATUS_SUCCESS) break;
-    if (issued < 2) hsa_signal_subtract_screlease(sig, 2 - issued);
-    const bool ok = wait_dma(r, 0) && issued == 2;
-    const double rate = (double)bytes * 2 / std::max(1e-9, ms_since(t0));
-    if (!ok) hsa_signal_store_screlease(sig, 0);
-    if (ok && rate > best) {
-      best = rate;
-      best_bit = bit;
+    for (int k = 0; k < std::max(reps[0], reps[1]); ++k) {
+      if (k < reps[0] && issued[0] == k &&
+          engine_copy(host, cpu, dev, gpu, bytes, d2h, sig[0]) == HSA_STATUS_SUCCESS)
+        ++issued[0];
+      if (k < reps[1] && issued[1] == k &&
+          engine_copy(dev + kHalf, gpu, host + kHalf, cpu, bytes, h2d, sig[1]) ==
+              HSA_STATUS_SUCCESS)
+        ++issued[1];
+    }
+    bool ok = true;
+    for (int d = 0; d < 2; ++d) {
+      if (issued[d] < reps[d]) {
+        hsa_signal_subtract_screlease(sig[d], reps[d] - issued[d]);
+        ok = false;
+      }
+      ok = hsa_signal_wait_scacquire(sig[d], HSA_SIGNAL_CONDITION_LT, 1, UINT64_MAX,
+                                     HSA_WAIT_STATE_ACTIVE) == 0 &&
+           ok;
+    }
+    const double sec = std::chrono::duration<double>(clk::now() - t0).count();
+    return ok ? (double)bytes * (reps[0] + reps[1]) / std::max(1e-9, sec) : 0;
+  }
+};
+
+// The runtime's preferred engines for copies from src to dst, else every
+// available one (id bits; 0: none named).
+uint32_t engine_candidates(hsa_agent_t dst, hsa_agent_t src) {
+  uint32_t c = 0;
+  if (hsa_amd_memory_get_preferred_copy_engine(dst, src, &c) != HSA_STATUS_SUCCESS) c = 0;
+  if (c == 0 && hsa_amd_memory_copy_engine_status(dst, src, &c) != HSA_STATUS_SUCCESS) c = 0;
+  return c;
+}
+
+// The candidates whose rate alone, in one direction, is within 15 % of the
+// best candidate's.
+uint32_t fast_engines(EngineProbe* pr, uint32_t cand, bool h2d) {
+  if ((cand & (cand - 1)) == 0) return cand;  // none or one
+  double rate[32] = {};
+  double best = 0;
+  for (int b = 0; b < 32; ++b)
+    if (cand >> b & 1) {
+      const uint32_t e = 1u << b;
+      rate[b] = h2d ? pr->run(0, 0, e, 2, EngineProbe::kHalf) : pr->run(e, 2, 0, 0, EngineProbe::kHalf);
+      best = std::max(best, rate[b]);
+    }
+  uint32_t fast = 0;
+  for (int b = 0; b < 32; ++b)
+    if ((cand >> b & 1) && rate[b] > 0 && rate[b] >= 0.85 * best) fast |= 1u << b;
+  return fast;
+}
+
+struct Engines {
+  uint32_t d2h = 0, h2d = 0;
+};
+
+// Choose the D2H and H2D engines of a device. Engines differ several-fold in
+// host-link bandwidth (only some sit close to the link), an engine left to
+// the runtime may be any of them, and one of the fast ids can be slow in a
+// given process; an H2D and a D2H engine running at once reach the link's
+// full duplex rate only on some pairs (others share a path and split it).
+// So: every candidate gets an untimed small copy first (an engine's first
+// copy in a process pays a one-time setup many times a 4 MiB copy), then each
+// direction keeps the candidates that are fast alone (2 x 4 MiB each), and of
+// those the (D2H, H2D) pair with the highest combined rate running at once
+// (4 x 4 MiB each way) is chosen. A direction with no candidate stays with
+// the runtime's choice.
+Engines pick_engines(const kvx_ring* r) {
+  Engines e;
+  const uint32_t cd = engine_candidates(r->cpu_agent, r->gpu_agent);
+  const uint32_t ch = engine_candidates(r->gpu_agent, r->cpu_agent);
+  EngineProbe pr;
+  if (!pr.init(r)) {  // untimed: a lone candidate, else the runtime's choice
+    e.d2h = (cd & (cd - 1)) == 0 ? cd : 0;
+    e.h2d = (ch & (ch - 1)) == 0 ? ch : 0;
+    return e;
+  }
+  for (int b = 0; b < 32; ++b) {
+    if (cd >> b & 1) (void)pr.run(1u << b, 1, 0, 0, 64 << 10);
+    if (ch >> b & 1) (void)pr.run(0, 0, 1u << b, 1, 64 << 10);
+  }
+  const uint32_t fd = fast_engines(&pr, cd, false);
+  const uint32_t fh = fast_engines(&pr, ch, true);
+  e.d2h = fd & (~fd + 1);  // lowest fast id until a pair is timed
+  e.h2d = fh & (~fh + 1);
+  if ((fd & (fd - 1)) == 0 && (fh & (fh - 1)) == 0) return e;
+  double best = 0;
+  for (int bd = 0; bd < 32; ++bd) {
+    const uint32_t d = 1u << bd;
+    if (fd ? !(fd & d) : bd > 0) continue;  // no fast D2H engine: the runtime's (0) only
+    for (int bh = 0; bh < 32; ++bh) {
+      const uint32_t h = 1u << bh;
+      if (fh ? !(fh & h) : bh > 0) continue;
+      const double rate =
+          pr.run(fd ? d : 0, 4, fh ? h : 0, 4, EngineProbe::kHalf);
+      if (rate > best) {
+        best = rate;
+        e.d2h = fd ? d : 0;
+        e.h2d = fh ? h : 0;
+      }
     }
   }
-  r->dma_engine = best_bit;
+  return e;
 }
 
 // Find the HSA agents of the ring's GPU (by PCI location) and of the host,
@@ -821,15 +987,21 @@ void setup_dma(kvx_ring* r) {
   // The choice is a property of the device: timed by the first ring created on
   // it in this process, reused by the others.
   static std::mutex mu;
-  static std::vector<std::pair<int, uint32_t>> picked;  // (device, engine bit)
+  static std::vector<std::pair<int, Engines>> picked;
   std::lock_guard<std::mutex> lock(mu);
+  Engines e;
+  bool found = false;
   for (const auto& d : picked)
     if (d.first == r->device) {
-      r->dma_engine = d.second;
-      return;
+      e = d.second;
+      found = true;
     }
-  pick_engine(r);
-  picked.emplace_back(r->device, r->dma_engine);
+  if (!found) {
+    e = pick_engines(r);
+    picked.emplace_back(r->device, e);
+  }
+  r->d2h_engine = e.d2h;
+  r->h2d_engine = e.h2d;
 }
 
 bool is_pinned(const void* p) {
@@ -1102,9 +1274,21 @@ kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hi
 
 kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t flags) {
   if (!ring || max_delay_us < 0 || max_delay_us > 1000000 || (flags & ~3)) return KVX_EINVAL;
+  const bool hip_copies = (flags & 2) != 0;
+  if (hip_copies != ring->hook_hip_copies) {
+    // A restore through the HIP runtime returns with copies still in flight;
+    // the other path's waits do not see them: let them finish first.
+    try {
+      DeviceGuard dg(ring->device);
+      if (!dg.ok) return KVX_EHIP;
+      drain_device(ring);
+    } catch (...) {
+      return KVX_EINTERNAL;
+    }
+  }
   ring->hook_max_delay_us = max_delay_us;
   ring->hook_poison = (flags & 1) != 0;
-  ring->hook_hip_d2h = (flags & 2) != 0;
+  ring->hook_hip_copies = hip_copies;
   return KVX_OK;
 }
 

@@ -142,8 +142,11 @@ def _arr(b):
     return b.array if isinstance(b, kvx.PinnedBuffer) else b
 
 
+@pytest.mark.parametrize("hip_copies", [False, True], ids=["dma", "hip"])
 @pytest.mark.parametrize("case", RING, ids=[f"ring{i}" for i in range(len(RING))])
-def test_chunk_list_restore_equals_oracle(case):
+def test_chunk_list_restore_equals_oracle(case, hip_copies):
+    """Both host-to-device paths: the DMA engine driven directly (default) and
+    the HIP runtime copy on the side stream."""
     L, ct, slots, slot_bytes, threads = case
     s = oracle.Shape(L, 300, 16, 2, 64, 2)
     seed = 70 + slots
@@ -159,11 +162,13 @@ def test_chunk_list_restore_equals_oracle(case):
     mirror = host_mirror(s, Filled(seed, kvsynth.ROLE_DST), range(s.num_blocks))
     ring = kvx.StagingRing(DEV, slots, slot_bytes)
     try:
+        ring.set_test_hooks(hip_copies=hip_copies)
         ring.bind_chunks(cache, 0, L, ct, [(b, bt0, nb) for b, (bt0, nb) in zip(bufs, sizes)],
                          fill_threads=threads)
         for _ in range(2):
             kvx.kvx_restore_from_staging(ring, _bt(bt))
             _check()
+        assert ring.stats()["dma"] == (0 if hip_copies else 1)
     finally:
         ring.close()
     for b, (bt0, nb) in zip(bufs, sizes):
@@ -173,9 +178,9 @@ def test_chunk_list_restore_equals_oracle(case):
         assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
 
 
-@pytest.mark.parametrize("hip_d2h", [False, True], ids=["dma", "hip"])
+@pytest.mark.parametrize("hip_copies", [False, True], ids=["dma", "hip"])
 @pytest.mark.parametrize("case", RING, ids=[f"ring{i}" for i in range(len(RING))])
-def test_offload_equals_oracle_gather(case, hip_d2h):
+def test_offload_equals_oracle_gather(case, hip_copies):
     """Both device-to-host paths: the DMA engine driven directly (default) and
     the HIP runtime copy on the side stream."""
     L, ct, slots, slot_bytes, threads = case
@@ -200,13 +205,13 @@ def test_offload_equals_oracle_gather(case, hip_d2h):
         sinks = [np.full(nb * per_block, 0xEE, np.uint8) for _, nb in sizes]
     ring = kvx.StagingRing(DEV, slots, slot_bytes)
     try:
-        ring.set_test_hooks(hip_d2h=hip_d2h)
+        ring.set_test_hooks(hip_copies=hip_copies)
         ring.bind_offload(cache, 0, L, ct, [(b, bt0, nb) for b, (bt0, nb) in zip(sinks, sizes)],
                           drain_threads=threads)
         for _ in range(2):
             kvx.kvx_offload_to_staging(ring, _bt(bt))
         _check()
-        assert ring.stats()["dma_d2h"] == (0 if hip_d2h else 1)
+        assert ring.stats()["dma"] == (0 if hip_copies else 1)
     finally:
         ring.close()
     for b, (bt0, nb) in zip(sinks, sizes):

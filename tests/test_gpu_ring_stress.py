@@ -32,11 +32,13 @@ STRESS = [
     (2, 64 << 10, 3, 300, 32),
     (2, 32 << 10, 1, 200, 64),     # chunks larger than a slot: layer pieces
     (3, 128 << 10, 4, 500, 16),
+    (1, 64 << 10, 2, 300, 32),     # one slot: each piece's scatter must drain it first
 ]
 
 
+@pytest.mark.parametrize("hip_copies", [False, True], ids=["dma", "hip"])
 @pytest.mark.parametrize("case", STRESS, ids=[f"s{i}" for i in range(len(STRESS))])
-def test_restore_with_pauses_and_poisoned_slots(case):
+def test_restore_with_pauses_and_poisoned_slots(case, hip_copies):
     slots, slot_bytes, threads, delay, ct = case
     s = oracle.Shape(4, 400, 16, 2, 64, 2)
     n = 150
@@ -48,13 +50,14 @@ def test_restore_with_pauses_and_poisoned_slots(case):
                                mode=kvsynth.MODE_RAW)
     ring = kvx.StagingRing(DEV, slots, slot_bytes)
     try:
-        ring.set_test_hooks(max_delay_us=delay, poison=True)
+        ring.set_test_hooks(max_delay_us=delay, poison=True, hip_copies=hip_copies)
         ring.bind(cache, 0, 4, n, ct, image, fill_threads=threads)
         for _ in range(2):
             kvx.kvx_restore_from_staging(ring, _bt(bt))
         torch.cuda.synchronize()
         kvx.kvx_check()
         assert ring.stats()["pieces"] > 3 * slots  # every slot reused several times
+        assert ring.stats()["dma"] == (0 if hip_copies else 1)
     finally:
         ring.close()
     oracle.restore(s, *mirror, 0, 4, bt, ct, image)
@@ -63,9 +66,9 @@ def test_restore_with_pauses_and_poisoned_slots(case):
         assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
 
 
-@pytest.mark.parametrize("hip_d2h", [False, True], ids=["dma", "hip"])
+@pytest.mark.parametrize("hip_copies", [False, True], ids=["dma", "hip"])
 @pytest.mark.parametrize("case", STRESS, ids=[f"s{i}" for i in range(len(STRESS))])
-def test_offload_with_pauses(case, hip_d2h):
+def test_offload_with_pauses(case, hip_copies):
     slots, slot_bytes, threads, delay, ct = case
     s = oracle.Shape(4, 400, 16, 2, 64, 2)
     n = 150
@@ -80,11 +83,11 @@ def test_offload_with_pauses(case, hip_d2h):
               for b in range(0, n, bpc)]
     ring = kvx.StagingRing(DEV, slots, slot_bytes)
     try:
-        ring.set_test_hooks(max_delay_us=delay, hip_d2h=hip_d2h)
+        ring.set_test_hooks(max_delay_us=delay, hip_copies=hip_copies)
         ring.bind_offload(cache, 0, 4, ct, chunks, drain_threads=threads)
         kvx.kvx_offload_to_staging(ring, _bt(bt))
         kvx.kvx_check()
-        assert ring.stats()["dma_d2h"] == (0 if hip_d2h else 1)
+        assert ring.stats()["dma"] == (0 if hip_copies else 1)
     finally:
         ring.close()
     image = np.concatenate([c[0] for c in chunks])

@@ -34,17 +34,17 @@ def _chunks(root, n, bpc, tag="m"):
 
 
 CASES = [
-    # (shape args, n, chunk_tokens, slots, slot_bytes, io_depth, hip_d2h)
+    # (shape args, n, chunk_tokens, slots, slot_bytes, io_depth, hip_copies)
     ((4, 400, 16, 2, 64, 2), 150, 64, 2, 256 << 10, 4, False),   # several chunks per slot
     ((4, 400, 16, 2, 64, 2), 150, 64, 3, 48 << 10, 2, False),    # chunks split by layers
-    ((4, 400, 16, 2, 64, 2), 150, 64, 2, 256 << 10, 1, True),    # D2H through the runtime
+    ((4, 400, 16, 2, 64, 2), 150, 64, 2, 256 << 10, 1, True),    # copies through the runtime
     ((3, 300, 5, 2, 16, 2), 70, 15, 2, 64 << 10, 8, False),      # 320-byte slabs: buffered I/O
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[f"c{i}" for i in range(len(CASES))])
 def test_offload_to_files_then_restore_from_files(tmp_path, case):
-    shape_args, n, ct, slots, slot_bytes, depth, hip_d2h = case
+    shape_args, n, ct, slots, slot_bytes, depth, hip_copies = case
     s = oracle.Shape(*shape_args)
     L, BS = s.num_layers, s.block_size
     seed = 300 + n + depth
@@ -55,7 +55,7 @@ def test_offload_to_files_then_restore_from_files(tmp_path, case):
     chunks = _chunks(tmp_path, n, ct // BS)
     ring = kvx.StagingRing(DEV, slots, slot_bytes)
     try:
-        ring.set_test_hooks(hip_d2h=hip_d2h)
+        ring.set_test_hooks(hip_copies=hip_copies)
         ring.bind_offload_files(cache, 0, L, ct, chunks, io_depth=depth)
         kvx.kvx_offload_to_staging(ring, _bt(bt_src))
         kvx.kvx_check()
