@@ -2,7 +2,7 @@
 
 Thin Python binding over the C ABI of ``libkvx.so`` (include/kvx.h): the
 functions below marshal arguments and call the library; every byte of the
-path is moved by the library's HIP kernels and HIP copies. PyTorch provides
+path is moved by the library's HIP kernels, DMA-engine copies and file I/O. PyTorch provides
 device memory and streams only. There is no CPU fallback: importing works
 without a GPU, but any call that moves data needs the built library and a GPU.
 
@@ -11,7 +11,8 @@ Operations (sections of the paper they follow):
     (offload side of the batched block copy, Secs. 6.2 and 6.4);
   * kvx_scatter_blocks -- unpack chunks into paged blocks (load side);
   * kvx_restore_from_staging -- feed scatters through a bounded pinned
-    staging ring with H2D copies on a side stream (Sec. 6.4).
+    staging ring, the host-to-device copies on a DMA engine (Sec. 6.4);
+  * kvx_offload_to_staging -- the reverse pipeline for stores.
 """
 from __future__ import annotations
 
