@@ -49,12 +49,12 @@ KERNELS_SRC = os.path.join(ROOT, "paper_2609_11744_amd", "csrc", "kvx_kernels.hi
 # only for the kernel source they were taken on (sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "0e91204deae29a56714284400a7ca1127492dd1234a606f6bd3c328331dc715e",
+    "kernels_sha256": "2f1eaf1458efb5dd3314d2a373d173672772b32a5a84d0c4eded416299996a3c",
     # cache layout -> (fetched, written) HBM bytes of one gather launch at the
     # default 80k-token workload: FETCH_SIZE KiB x 1.99999 (copy calibration),
     # WRITE_SIZE KiB x 1.0
-    "nhd": (10488394334, 10488066048),         # 5,121,315.6 / 10,242,252.0 KiB
-    "paged_attn": (10488509635, 10488453018),  # 5,121,371.9 / 10,242,629.9 KiB
+    "nhd": (10488880145, 10485761408),         # 5,121,554.2 / 10,240,001.4 KiB
+    "paged_attn": (10488507212, 10488819200),  # 5,121,371.9 / 10,242,987.5 KiB
 }
 
 

@@ -1,5 +1,5 @@
 // Measurement helper: the HBM rate that a kernel shaped like the slab mover
-// (one workgroup per 32 KiB, 1024 threads x two 16-byte non-temporal vectors,
+// (one workgroup per 4 KiB, 256 threads x one 16-byte non-temporal vector,
 // XCD-contiguous workgroup order) reaches on contiguous memory when it only
 // reads, only writes, or copies. The bench reports these beside the spec peak,
 // so the gap between a gather and 8 TB/s can be split into what any copy of
@@ -13,9 +13,9 @@ namespace {
 
 typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 
-constexpr int kThreads = 1024;
-constexpr int kVec = 2;
-constexpr int64_t kUnit = (int64_t)kThreads * kVec * 16;  // 32 KiB per workgroup
+constexpr int kThreads = 256;
+constexpr int kVec = 1;
+constexpr int64_t kUnit = (int64_t)kThreads * kVec * 16;  // 4 KiB per workgroup
 constexpr uint32_t kXcds = 8;
 constexpr uint32_t kMaxUnitsPerLaunch = 1u << 22;
 
@@ -60,6 +60,7 @@ extern "C" kvx_status kvx_probe_stream(const void* src, void* dst, int64_t bytes
   if ((mode != 1 && !src) || (mode != 0 && !dst)) return KVX_EINVAL;
   if (((uintptr_t)src & 15) || ((uintptr_t)dst & 15)) return KVX_EINVAL;
   const int64_t units = bytes / kUnit;
+  if (units > 0x7FFFFFFF) return KVX_EINVAL;  // unit indexes are 32-bit
   for (int64_t base = 0; base < units; base += kMaxUnitsPerLaunch) {
     const uint32_t cnt = (uint32_t)(units - base < kMaxUnitsPerLaunch ? units - base
                                                                       : kMaxUnitsPerLaunch);

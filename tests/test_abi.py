@@ -187,7 +187,7 @@ def test_probe_rejects_bad_arguments_on_the_host():
     from paper_2609_11744_amd import _native
 
     lib = _native.lib()
-    unit = 32 << 10
+    unit = 4 << 10
     assert lib.kvx_probe_stream(None, None, unit, 0, None) == kvx.KVX_EINVAL  # read: no src
     assert lib.kvx_probe_stream(None, None, unit, 1, None) == kvx.KVX_EINVAL  # write: no dst
     assert lib.kvx_probe_stream(4096, 8192, unit + 16, 2, None) == kvx.KVX_EINVAL  # size
