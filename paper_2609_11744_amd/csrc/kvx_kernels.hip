@@ -4,7 +4,7 @@
 // The work is pure data movement, bound by HBM bandwidth, so the kernels use
 // no MFMA. With the default cache layout every slab is contiguous and in the
 // same order on both sides, so nothing is transposed and no LDS is used; the
-// other cache layouts stage each slab through LDS (see move_slab_transposed).
+// other cache layouts move a slab head by head (see move_head).
 // A unit is a slab (layer, K|V, block) of `slab` bytes. With the default
 // layout one workgroup moves one part of a unit: 256 threads, one 16-byte
 // vector each, so a part is 4 KiB (a 32 KiB slab is 8 parts; the last part of
@@ -60,8 +60,9 @@ struct LayerPtrs {
 // m = ceil(2^32 / d) and n / d = umulhi(n, m) whenever n * d < 2^32 (the
 // rounding error of m, below d, then moves n * m / 2^32 by less than 1/d);
 // m = 0 stands for d = 1. Every numerator here is an element or vector index
-// inside one slab and every divisor a slab dimension; a transposed slab is at
-// most kMaxTransposedSlab (48 KiB) bytes, so both are below 2^16.
+// inside one head's part of a slab and every divisor a slab dimension; a
+// transposed slab is at most kMaxTransposedSlab (48 KiB) bytes, so both are
+// below 2^16.
 struct FastDiv {
   uint32_t d;
   uint32_t m;
@@ -71,16 +72,15 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, FastDiv f) {
   return f.m ? __umulhi(n, f.m) : n;
 }
 
-// Shape of one slab, for the transposing layouts.
+// Shape of one head's part of a slab, for the reordering layouts.
 struct SlabGeom {
   FastDiv bs;      // tokens per block
-  FastDiv h;       // KV heads
   FastDiv d;       // head dim (elements)
   FastDiv v16;     // 16-byte vectors per (token, head) row: d * elem_bytes / 16
-  FastDiv pad[2];  // LDS pad period of K and V slabs (see lds_slot)
+  FastDiv pad[2];  // LDS pad period of K and V parts (see lds_slot)
   uint32_t x;      // elements per 16-byte vector: 16 / elem_bytes
-  uint32_t ntv;    // V tile path: vectors per (head, dim) row, bs / x; 0 if bs % x != 0
-  uint32_t tiles;  // V tile path: x-by-x tiles per slab, n16 / x
+  uint32_t nh;     // vectors of one head: bs * v16
+  uint32_t prow;   // packed row stride in vectors: heads * v16
   uint32_t pad_;
 };
 
@@ -131,22 +131,26 @@ __device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __rest
 //   KVX_LAYOUT_PAGED_ATTN  K [head][dim / x][token][x] (x = 16 / elem_bytes: the
 //                          16-byte vectors of a row are re-strided), V
 //                          [head][dim][token] (an element transpose).
-// Such a slab is staged through LDS so that both global sides stay coalesced
-// (consecutive lanes on consecutive 16-byte vectors) and only LDS sees the
-// reordering:
-//   * vector permutations (HND, paged-attention K): load the slab in source
-//     order into LDS, then write it in destination order, each lane fetching
-//     the source vector its output vector is;
-//   * the V element transpose works on x-by-x tiles (x dims by x tokens of one
-//     head: x vectors on each side) transposed in registers. A gather reads a
-//     tile's x cache rows from LDS and writes its x packed vectors to global
-//     memory; a scatter reads a tile's x packed vectors from global memory and
-//     writes its x cache rows into LDS, which is then stored in cache order.
-//     If bs is not a multiple of x the tiles do not exist and each output
-//     vector is assembled element by element from LDS instead.
-// Each thread issues all of its global loads before it waits for any of them,
-// so the whole slab is in flight at once (a transposed slab is at most
-// kMaxSlabVectors vectors, kVecPerThread per thread).
+// In every one of them a head's data is contiguous on the cache side (nh =
+// bs * v16 vectors), and on the packed side it is one v16-vector row per token
+// at stride prow = heads * v16. So a workgroup moves one head (the slab's
+// parts are its heads), one vector per thread for the usual shapes; inside a
+// head, local packed vector w = t * v16 + dv sits at packed_at(w).
+//   * HND: the head's cache rows are its packed rows in the same order, so
+//     vectors move directly (no LDS); the packed side is 16 * v16-byte runs.
+//   * paged-attention K: a vector permutation. The head is loaded in source
+//     order into LDS, then written in destination order, each lane fetching
+//     the source vector its output vector is.
+//   * paged-attention V: an element transpose. The head is loaded in source
+//     order into LDS, then each output vector is assembled element by element
+//     from it.
+// Both global sides stay coalesced (consecutive lanes on consecutive 16-byte
+// vectors, or whole packed rows) and only LDS sees the reordering; the LDS
+// image is padded so that a wave's strided reads land on distinct banks. A
+// thread holds V vectors of the head, all of its loads issued before it waits
+// for any of them: V = 1 when a head fits one vector per thread (the usual
+// shapes: few registers, full occupancy), else kVecPerThread, enough for the
+// largest head (kMaxSlabVectors).
 
 constexpr int kTransposeThreads = 256;
 constexpr uint32_t kMaxSlabVectors = 48 * 1024 / 16;
@@ -155,9 +159,8 @@ constexpr int kVecPerThread = (int)(kMaxSlabVectors / kTransposeThreads);  // 12
 extern __shared__ __attribute__((aligned(16))) unsigned char kvx_lds[];
 
 // LDS slot of vector v: one pad vector after every `pad` vectors. The pad
-// period is the stride at which the slab's strided LDS accesses walk (chosen
-// per layout and direction on the host), so a wave's 16-byte accesses at that
-// stride land on distinct banks.
+// period is the stride at which the head's strided LDS accesses walk (chosen
+// per layout and direction on the host).
 __device__ __forceinline__ uint32_t lds_slot(uint32_t v, FastDiv pad) { return v + fdiv(v, pad); }
 
 // Quotient and remainder.
@@ -167,226 +170,165 @@ __device__ __forceinline__ uint32_t divmod(uint32_t n, FastDiv f, uint32_t& rem)
   return q;
 }
 
-// Source vector index of destination vector w for a vector permutation
-// (HND K/V, paged-attention K). Gather: destination = packed, source = cache.
-template <bool kToPacked, int kLayout>
-__device__ __forceinline__ uint32_t src_vector(uint32_t w, const SlabGeom& g) {
-  uint32_t t, h, dv;
-  if (kToPacked) {  // w = (t * h + hh) * v16 + dv in packed order
-    t = divmod(divmod(w, g.v16, dv), g.h, h);
-    return kLayout == KVX_LAYOUT_HND ? (h * g.bs.d + t) * g.v16.d + dv
-                                     : (h * g.v16.d + dv) * g.bs.d + t;
-  }
-  if (kLayout == KVX_LAYOUT_HND)  // w = (h * bs + t) * v16 + dv in cache order
-    h = divmod(divmod(w, g.v16, dv), g.bs, t);
-  else                            // w = (h * v16 + dv) * bs + t in cache order
-    h = divmod(divmod(w, g.bs, t), g.v16, dv);
-  return (t * g.h.d + h) * g.v16.d + dv;
+// Packed-side offset (in vectors, from the head's first row) of local packed
+// vector w = t * v16 + dv.
+__device__ __forceinline__ uint32_t packed_at(uint32_t w, const SlabGeom& g) {
+  uint32_t dv;
+  const uint32_t t = divmod(w, g.v16, dv);
+  return t * g.prow + dv;
 }
 
-// Load n16 source vectors in order into the padded LDS image.
-template <int T>
-__device__ __forceinline__ void stage_in(const v4u* __restrict__ src, uint32_t n16, FastDiv pad) {
+// HND: local vector w is cache vector w and local packed vector w.
+template <bool kToPacked, int T, int V>
+__device__ __forceinline__ void move_head_rows(const v4u* __restrict__ src, v4u* __restrict__ dst,
+                                               const SlabGeom& g) {
+  v4u r[V];
+#pragma unroll
+  for (int q = 0; q < V; ++q) {
+    const uint32_t w = threadIdx.x + q * T;
+    if (w < g.nh) r[q] = __builtin_nontemporal_load(src + (kToPacked ? w : packed_at(w, g)));
+  }
+#pragma unroll
+  for (int q = 0; q < V; ++q) {
+    const uint32_t w = threadIdx.x + q * T;
+    if (w < g.nh) __builtin_nontemporal_store(r[q], dst + (kToPacked ? packed_at(w, g) : w));
+  }
+}
+
+// Load the head's nh source vectors, in source order, into the padded LDS
+// image. A gather reads the cache (contiguous), a scatter the packed rows.
+template <bool kToPacked, int T, int V>
+__device__ __forceinline__ void stage_in(const v4u* __restrict__ src, const SlabGeom& g,
+                                         FastDiv pad) {
   v4u* lds = reinterpret_cast<v4u*>(kvx_lds);
-  v4u r[kVecPerThread];
+  v4u r[V];
 #pragma unroll
-  for (int q = 0; q < kVecPerThread; ++q) {
+  for (int q = 0; q < V; ++q) {
     const uint32_t v = threadIdx.x + q * T;
-    if (v < n16) r[q] = __builtin_nontemporal_load(src + v);
+    if (v < g.nh) r[q] = __builtin_nontemporal_load(src + (kToPacked ? v : packed_at(v, g)));
   }
 #pragma unroll
-  for (int q = 0; q < kVecPerThread; ++q) {
+  for (int q = 0; q < V; ++q) {
     const uint32_t v = threadIdx.x + q * T;
-    if (v < n16) lds[lds_slot(v, pad)] = r[q];
+    if (v < g.nh) lds[lds_slot(v, pad)] = r[q];
   }
 }
 
-// x-by-x transpose of elements E held as x 16-byte vectors: b[j] element i =
-// a[i] element j.
+// Write the head's nh destination vectors, in destination order, each
+// produced by f(w). A gather writes the packed rows, a scatter the cache.
+template <bool kToPacked, int T, int V, typename F>
+__device__ __forceinline__ void stage_out(v4u* __restrict__ dst, const SlabGeom& g, F f) {
+  v4u r[V];
+#pragma unroll
+  for (int q = 0; q < V; ++q) {
+    const uint32_t w = threadIdx.x + q * T;
+    if (w < g.nh) r[q] = f(w);
+  }
+#pragma unroll
+  for (int q = 0; q < V; ++q) {
+    const uint32_t w = threadIdx.x + q * T;
+    if (w < g.nh) __builtin_nontemporal_store(r[q], dst + (kToPacked ? packed_at(w, g) : w));
+  }
+}
+
+// Paged-attention K: source vector (in the LDS image) of destination vector w.
+// Cache order inside a head is w = dv * bs + t, packed order w = t * v16 + dv.
+template <bool kToPacked>
+__device__ __forceinline__ uint32_t k_source(uint32_t w, const SlabGeom& g) {
+  uint32_t lo;
+  if (kToPacked) {
+    const uint32_t t = divmod(w, g.v16, lo);  // lo = dv
+    return lo * g.bs.d + t;
+  }
+  const uint32_t dv = divmod(w, g.bs, lo);    // lo = t
+  return lo * g.v16.d + dv;
+}
+
 template <typename E>
 struct ElemRow {
   E e[16 / sizeof(E)];
 };
 
-template <typename E>
-__device__ __forceinline__ void transpose_tile(const v4u* a, v4u* b) {
-  constexpr int X = 16 / sizeof(E);
-  ElemRow<E> in[X];
-#pragma unroll
-  for (int i = 0; i < X; ++i) in[i] = __builtin_bit_cast(ElemRow<E>, a[i]);
-#pragma unroll
-  for (int j = 0; j < X; ++j) {
-    ElemRow<E> o;
-#pragma unroll
-    for (int i = 0; i < X; ++i) o.e[i] = in[i].e[j];
-    b[j] = __builtin_bit_cast(v4u, o);
-  }
-}
-
-// Tile k of a V slab -> (head, dim vector dv, token vector tv). Tiles are
-// numbered dv fastest, then head, then tv, so for each of a tile's x packed
-// vectors consecutive lanes address consecutive packed vectors.
-struct Tile {
-  uint32_t cache0;   // cache vector of (head, dim dv * x, token vector tv)
-  uint32_t packed0;  // packed vector of (token tv * x, head, dim vector dv)
-};
-
-__device__ __forceinline__ Tile tile_of(uint32_t k, const SlabGeom& g) {
-  uint32_t dv, h;
-  const uint32_t tv = divmod(divmod(k, g.v16, dv), g.h, h);
-  Tile t;
-  t.cache0 = (h * g.v16.d + dv) * g.x * g.ntv + tv;
-  t.packed0 = (tv * g.x * g.h.d + h) * g.v16.d + dv;
-  return t;
-}
-
-// Paged-attention V gather through x-by-x tiles (the cache image is in LDS).
-// Cache row i of a tile is at stride ntv, packed vector j at stride h * v16.
-template <typename E, int T>
-__device__ __forceinline__ void tiles_to_packed(v4u* __restrict__ dst, const SlabGeom& g,
-                                                FastDiv pad) {
-  constexpr int X = 16 / sizeof(E);
-  const v4u* lds = reinterpret_cast<const v4u*>(kvx_lds);
-  const uint32_t prow = g.h.d * g.v16.d;
-  for (uint32_t k = threadIdx.x; k < g.tiles; k += T) {
-    const Tile t = tile_of(k, g);
-    v4u a[X], b[X];
-#pragma unroll
-    for (int i = 0; i < X; ++i) a[i] = lds[lds_slot(t.cache0 + i * g.ntv, pad)];
-    transpose_tile<E>(a, b);
-#pragma unroll
-    for (int j = 0; j < X; ++j) __builtin_nontemporal_store(b[j], dst + t.packed0 + j * prow);
-  }
-}
-
-// Paged-attention V scatter through x-by-x tiles: read each tile's packed
-// vectors from global memory (all of a thread's tiles in flight at once),
-// transpose, and place the cache rows in LDS.
-template <typename E, int T>
-__device__ __forceinline__ void tiles_from_packed(const v4u* __restrict__ src, const SlabGeom& g,
-                                                  FastDiv pad) {
-  constexpr int X = 16 / sizeof(E);
-  constexpr int kTiles = (kVecPerThread + X - 1) / X;  // tiles per thread at most
-  v4u* lds = reinterpret_cast<v4u*>(kvx_lds);
-  const uint32_t prow = g.h.d * g.v16.d;
-  v4u a[kTiles][X];
-#pragma unroll
-  for (int m = 0; m < kTiles; ++m) {
-    const uint32_t k = threadIdx.x + m * T;
-    if (k < g.tiles) {
-      const Tile t = tile_of(k, g);
-#pragma unroll
-      for (int j = 0; j < X; ++j) a[m][j] = __builtin_nontemporal_load(src + t.packed0 + j * prow);
-    }
-  }
-#pragma unroll
-  for (int m = 0; m < kTiles; ++m) {
-    const uint32_t k = threadIdx.x + m * T;
-    if (k < g.tiles) {
-      const Tile t = tile_of(k, g);
-      v4u b[X];
-      transpose_tile<E>(a[m], b);
-#pragma unroll
-      for (int i = 0; i < X; ++i) lds[lds_slot(t.cache0 + i * g.ntv, pad)] = b[i];
-    }
-  }
-}
-
-// Paged-attention V when bs is not a multiple of x: destination vector w
-// assembled element by element from the LDS image of the source.
+// Paged-attention V: destination vector w assembled element by element from
+// the LDS image of the source. Cache elements inside a head are (dim, t) at
+// dim * bs + t; packed elements (t, dim) at t * d + dim.
 template <bool kToPacked, typename E>
-__device__ __forceinline__ v4u gather_elements(uint32_t w, const SlabGeom& g, FastDiv pad) {
+__device__ __forceinline__ v4u v_elements(uint32_t w, const SlabGeom& g, FastDiv pad) {
   constexpr uint32_t kX = 16 / sizeof(E);
   ElemRow<E> out;
-  uint32_t se, step;  // source element of output element 0, and per-element stride
-  uint32_t t, d, h;
-  if (kToPacked) {  // packed (t, h, d0 + i) <- cache element (h, d0 + i, t): stride bs
+  if (kToPacked) {  // packed (t, dv * x + i) <- cache element (dv * x + i, t): stride bs
     uint32_t dv;
-    t = divmod(divmod(w, g.v16, dv), g.h, h);
-    se = (h * g.d.d + dv * kX) * g.bs.d + t;
-    step = g.bs.d;
+    const uint32_t t = divmod(w, g.v16, dv);
+    const uint32_t e0 = dv * kX * g.bs.d + t;
 #pragma unroll
     for (uint32_t i = 0; i < kX; ++i) {
-      const uint32_t e = se + i * step;
+      const uint32_t e = e0 + i * g.bs.d;
       out.e[i] = reinterpret_cast<const E*>(kvx_lds + 16u * lds_slot(e / kX, pad))[e % kX];
     }
-  } else {          // cache element (h, d, t) <- packed element (t, h, d); t runs fastest
-    h = divmod(divmod(w * kX, g.bs, t), g.d, d);
+  } else {  // cache (dim, t .. t + x - 1) <- packed elements (t + i, dim); t wraps to dim + 1
+    uint32_t t;
+    uint32_t dim = divmod(w * kX, g.bs, t);
 #pragma unroll
     for (uint32_t i = 0; i < kX; ++i) {
-      const uint32_t e = (t * g.h.d + h) * g.d.d + d;
+      const uint32_t e = t * g.d.d + dim;
       out.e[i] = reinterpret_cast<const E*>(kvx_lds + 16u * lds_slot(e / kX, pad))[e % kX];
       if (++t == g.bs.d) {
         t = 0;
-        if (++d == g.d.d) { d = 0; ++h; }
+        ++dim;
       }
     }
   }
   return __builtin_bit_cast(v4u, out);
 }
 
-// Write n16 destination vectors in order, each produced by f(w).
-template <int T, typename F>
-__device__ __forceinline__ void stage_out(v4u* __restrict__ dst, uint32_t n16, F f) {
-  v4u r[kVecPerThread];
-#pragma unroll
-  for (int q = 0; q < kVecPerThread; ++q) {
-    const uint32_t w = threadIdx.x + q * T;
-    if (w < n16) r[q] = f(w);
-  }
-#pragma unroll
-  for (int q = 0; q < kVecPerThread; ++q) {
-    const uint32_t w = threadIdx.x + q * T;
-    if (w < n16) __builtin_nontemporal_store(r[q], dst + w);
-  }
-}
-
-template <bool kToPacked, int kLayout, int kElem, int T>
-__device__ __forceinline__ void move_slab_transposed(const v4u* __restrict__ src,
-                                                     v4u* __restrict__ dst, uint32_t n16,
-                                                     const SlabGeom& g, uint32_t kv) {
+// One head of a slab in a reordering layout (src / dst: the head's cache
+// vectors and its first packed row, in the kernel's direction).
+template <bool kToPacked, int kLayout, int kElem, int T, int V>
+__device__ __forceinline__ void move_head(const v4u* __restrict__ src, v4u* __restrict__ dst,
+                                          const SlabGeom& g, uint32_t kv) {
   typedef typename std::conditional<
       kElem == 1, uint8_t,
       typename std::conditional<kElem == 2, uint16_t,
                                 typename std::conditional<kElem == 4, uint32_t,
                                                           uint64_t>::type>::type>::type E;
-  const FastDiv pad = g.pad[kv];
-  const v4u* lds = reinterpret_cast<const v4u*>(kvx_lds);
-  if (kLayout == KVX_LAYOUT_PAGED_ATTN && kv == 1 && g.tiles != 0) {
-    if (kToPacked) {
-      stage_in<T>(src, n16, pad);
-      __syncthreads();
-      tiles_to_packed<E, T>(dst, g, pad);
-    } else {
-      tiles_from_packed<E, T>(src, g, pad);
-      __syncthreads();
-      stage_out<T>(dst, n16, [&](uint32_t w) { return lds[lds_slot(w, pad)]; });
-    }
+  if (kLayout == KVX_LAYOUT_HND) {
+    move_head_rows<kToPacked, T, V>(src, dst, g);
     return;
   }
-  stage_in<T>(src, n16, pad);
+  const FastDiv pad = g.pad[kv];
+  stage_in<kToPacked, T, V>(src, g, pad);
   __syncthreads();
-  if (kLayout == KVX_LAYOUT_PAGED_ATTN && kv == 1)
-    stage_out<T>(dst, n16, [&](uint32_t w) { return gather_elements<kToPacked, E>(w, g, pad); });
+  const v4u* lds = reinterpret_cast<const v4u*>(kvx_lds);
+  if (kv == 0)
+    stage_out<kToPacked, T, V>(
+        dst, g, [&](uint32_t w) { return lds[lds_slot(k_source<kToPacked>(w, g), pad)]; });
   else
-    stage_out<T>(dst, n16, [&](uint32_t w) {
-      return lds[lds_slot(src_vector<kToPacked, kLayout>(w, g), pad)];
-    });
+    stage_out<kToPacked, T, V>(dst, g,
+                               [&](uint32_t w) { return v_elements<kToPacked, E>(w, g, pad); });
 }
 
-// Move part `part` of one slab (the whole slab for the transposing layouts,
-// whose part is always 0) in the direction and layout of the kernel.
+// Move part `part` of one slab in the direction and layout of the kernel: a
+// 4 KiB piece with the default layout, one head with the reordering ones.
 template <bool kToPacked, int kLayout, int kElem, int T, int V>
 __device__ __forceinline__ void move_unit(char* paged, char* pk, uint32_t n16, const SlabGeom& g,
                                           uint32_t kv, uint32_t part) {
-  const v4u* s = reinterpret_cast<const v4u*>(kToPacked ? paged : pk);
-  v4u* d = reinterpret_cast<v4u*>(kToPacked ? pk : paged);
+  v4u* pv = reinterpret_cast<v4u*>(paged);
+  v4u* kv4 = reinterpret_cast<v4u*>(pk);
   if (kLayout == KVX_LAYOUT_NHD) {
     const uint32_t off = part * (uint32_t)(T * V);  // < n16: part < ceil(n16 / (T * V))
     const uint32_t left = n16 - off;
-    move_slab<T, V>(s + off, d + off, left < (uint32_t)(T * V) ? left : (uint32_t)(T * V));
+    const uint32_t n = left < (uint32_t)(T * V) ? left : (uint32_t)(T * V);
+    if (kToPacked)
+      move_slab<T, V>(pv + off, kv4 + off, n);
+    else
+      move_slab<T, V>(kv4 + off, pv + off, n);
   } else {
-    move_slab_transposed<kToPacked, kLayout, kElem, T>(s, d, n16, g, kv);
+    v4u* cache_head = pv + part * g.nh;       // head `part`: nh contiguous cache vectors
+    v4u* packed_head = kv4 + part * g.v16.d;  // its first packed row
+    if (kToPacked)
+      move_head<true, kLayout, kElem, T, V>(cache_head, packed_head, g, kv);
+    else
+      move_head<false, kLayout, kElem, T, V>(packed_head, cache_head, g, kv);
   }
 }
 
@@ -566,50 +508,60 @@ constexpr uint32_t kPartThreads = 256;
 // Scatters of at least this many blocks run in destination order.
 constexpr int32_t kOrderedScatterMinBlocks = 1024;
 
-// Dynamic LDS bytes for a transposing layout: the padded slab image.
-inline size_t lds_bytes(uint32_t n16, const SlabGeom& sg) {
+// Dynamic LDS bytes for a reordering layout: the padded image of one head
+// (none for HND, which moves rows directly).
+inline size_t lds_bytes(int layout, const SlabGeom& sg) {
+  if (layout != KVX_LAYOUT_PAGED_ATTN) return 0;
   const uint32_t pad = sg.pad[0].d < sg.pad[1].d ? sg.pad[0].d : sg.pad[1].d;
-  return 16u * (size_t)(n16 + n16 / pad + 1);
+  return 16u * (size_t)(sg.nh + sg.nh / pad + 1);
 }
 
 // Launch `cnt` workgroups of kernel K<..., layout, elem, T, V>: the default
-// layout moves 4 KiB parts (kPartThreads threads x 1 vector); the others use
-// 256 threads and the LDS-staged mover, one slab per workgroup.
-#define KVX_DISPATCH(KERNEL, PREFIX, ...)                                                      \
-  do {                                                                                     \
-    if (layout == KVX_LAYOUT_NHD) {                                                        \
-      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_NHD, 0, kPartThreads, 1>), grid,          \
-                         dim3(kPartThreads), 0, stream, __VA_ARGS__);                      \
-    } else if (layout == KVX_LAYOUT_HND) {                                                 \
-      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_HND, 0, 256, 1>), grid, dim3(256),        \
-                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
-    } else if (elem == 1) {                                                                \
-      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 1, 256, 1>), grid, dim3(256), \
-                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
-    } else if (elem == 2) {                                                                \
-      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 2, 256, 1>), grid, dim3(256), \
-                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
-    } else if (elem == 4) {                                                                \
-      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 4, 256, 1>), grid, dim3(256), \
-                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
-    } else {                                                                               \
-      hipLaunchKernelGGL((KERNEL<PREFIX, KVX_LAYOUT_PAGED_ATTN, 8, 256, 1>), grid, dim3(256), \
-                         lds_bytes(n16, sg), stream, __VA_ARGS__);                             \
-    }                                                                                      \
+// layout moves 4 KiB parts (kPartThreads threads x 1 vector); the others move
+// one head per workgroup of 256 threads (paged attention through LDS).
+#define KVX_UNPAREN(...) __VA_ARGS__
+
+// One head per workgroup of kTransposeThreads: one vector per thread when the
+// head fits, else kVecPerThread. PREFIX is the kernel's parenthesized leading
+// template arguments.
+#define KVX_LAUNCH_HEADS(KERNEL, PREFIX, LAYOUT, ELEM, ...)                                 \
+  do {                                                                                 \
+    const dim3 tb(kTransposeThreads);                                                  \
+    if (sg.nh <= (uint32_t)kTransposeThreads)                                          \
+      hipLaunchKernelGGL((KERNEL<KVX_UNPAREN PREFIX, LAYOUT, ELEM, kTransposeThreads, 1>), \
+                         grid, tb, lds_bytes(layout, sg), stream, __VA_ARGS__);        \
+    else                                                                               \
+      hipLaunchKernelGGL(                                                              \
+          (KERNEL<KVX_UNPAREN PREFIX, LAYOUT, ELEM, kTransposeThreads, kVecPerThread>), \
+          grid, tb, lds_bytes(layout, sg), stream, __VA_ARGS__);                       \
   } while (0)
 
-#define KVX_DIR_ORDER(D, O) D, O
+#define KVX_DISPATCH(KERNEL, PREFIX, ...)                                                   \
+  do {                                                                                 \
+    if (layout == KVX_LAYOUT_NHD)                                                      \
+      hipLaunchKernelGGL((KERNEL<KVX_UNPAREN PREFIX, KVX_LAYOUT_NHD, 0, kPartThreads, 1>), \
+                         grid, dim3(kPartThreads), 0, stream, __VA_ARGS__);            \
+    else if (layout == KVX_LAYOUT_HND)                                                 \
+      KVX_LAUNCH_HEADS(KERNEL, PREFIX, KVX_LAYOUT_HND, 0, __VA_ARGS__);                 \
+    else if (elem == 1)                                                                \
+      KVX_LAUNCH_HEADS(KERNEL, PREFIX, KVX_LAYOUT_PAGED_ATTN, 1, __VA_ARGS__);          \
+    else if (elem == 2)                                                                \
+      KVX_LAUNCH_HEADS(KERNEL, PREFIX, KVX_LAYOUT_PAGED_ATTN, 2, __VA_ARGS__);          \
+    else if (elem == 4)                                                                \
+      KVX_LAUNCH_HEADS(KERNEL, PREFIX, KVX_LAYOUT_PAGED_ATTN, 4, __VA_ARGS__);          \
+    else                                                                               \
+      KVX_LAUNCH_HEADS(KERNEL, PREFIX, KVX_LAYOUT_PAGED_ATTN, 8, __VA_ARGS__);          \
+  } while (0)
 
 template <bool kToPacked, bool kOrdered>
 hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, uint32_t n_work,
                   const uint32_t* order, char* packed, int* err, int layout, int elem,
                   hipStream_t stream) {
-  const uint32_t n16 = ug.n16;
   const SlabGeom& sg = ug.sg;
   for (uint32_t base = 0; base < n_work; base += kMaxWorkPerLaunch) {
     const uint32_t cnt = n_work - base < kMaxWorkPerLaunch ? n_work - base : kMaxWorkPerLaunch;
     const dim3 grid(cnt);
-    KVX_DISPATCH(copy_units_kernel, KVX_DIR_ORDER(kToPacked, kOrdered), lp, bt, ug, base, cnt,
+    KVX_DISPATCH(copy_units_kernel, (kToPacked, kOrdered), lp, bt, ug, base, cnt,
                  order, packed, err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
@@ -621,22 +573,22 @@ template <bool kToPacked>
 hipError_t launch_chunks(const LayerPtrs& lp, const int32_t* bt, const kvx_chunk_ref* refs,
                          const ChunkGeom& cg, uint32_t n_work, char* packed, int* err,
                          int layout, int elem, hipStream_t stream) {
-  const uint32_t n16 = cg.n16;
   const SlabGeom& sg = cg.sg;
   for (uint32_t base = 0; base < n_work; base += kMaxWorkPerLaunch) {
     const uint32_t cnt = n_work - base < kMaxWorkPerLaunch ? n_work - base : kMaxWorkPerLaunch;
     const dim3 grid(cnt);
-    KVX_DISPATCH(copy_chunks_kernel, kToPacked, lp, bt, refs, cg, base, cnt, packed, err);
+    KVX_DISPATCH(copy_chunks_kernel, (kToPacked), lp, bt, refs, cg, base, cnt, packed, err);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
 }
 
-// Workgroups per slab for the layout, and log2 of that count when it is a
-// power of two (else 32: the kernels divide).
-void slab_parts(int layout, uint32_t n16, uint32_t* parts, uint32_t* shift) {
-  *parts = layout == KVX_LAYOUT_NHD ? (n16 + kPartThreads - 1) / kPartThreads : 1;
+// Workgroups per slab for the layout (4 KiB pieces with the default layout,
+// heads with the reordering ones), and log2 of that count when it is a power
+// of two (else 32: the kernels divide).
+void slab_parts(int layout, uint32_t n16, uint32_t heads, uint32_t* parts, uint32_t* shift) {
+  *parts = layout == KVX_LAYOUT_NHD ? (n16 + kPartThreads - 1) / kPartThreads : heads;
   *shift = (*parts & (*parts - 1)) == 0 ? (uint32_t)__builtin_ctz(*parts) : 32u;
 }
 
@@ -647,35 +599,26 @@ FastDiv fast_div(uint32_t d) {
   return f;
 }
 
-// Slab shape and LDS pad periods for a transposing layout. The pad period of
-// a slab kind is the stride (in vectors) of its strided LDS accesses:
-//   gather (cache image in LDS): HND reads head rows, stride bs * v16;
-//     paged-attention K and V read token / dim rows, stride bs;
-//   scatter (packed image in LDS): HND and paged-attention K read token rows,
-//     stride h * v16; paged-attention V tiles write dim rows, stride bs, and
-//     the element fallback reads token rows of elements, stride h * d.
+// Head shape and LDS pad periods for a reordering layout. The pad period is
+// the stride (in vectors) of the head's strided LDS reads: a gather (cache
+// image in LDS) reads paged-attention K vectors and V elements of consecutive
+// dims at stride bs; a scatter (packed image in LDS) reads them at stride v16
+// (K: consecutive tokens; V: the x tokens of one output vector). HND uses no
+// LDS.
 SlabGeom slab_geom(const kvx_cache* c, bool to_packed) {
   const uint32_t bs = (uint32_t)c->block_size, h = (uint32_t)c->num_kv_heads,
                  d = (uint32_t)c->head_dim, x = (uint32_t)(16 / c->elem_bytes),
                  v16 = (uint32_t)((int64_t)c->head_dim * c->elem_bytes / 16);
   SlabGeom sg;
   sg.bs = fast_div(bs);
-  sg.h = fast_div(h);
   sg.d = fast_div(d);
   sg.v16 = fast_div(v16 ? v16 : 1);
   sg.x = x;
-  sg.ntv = bs % x == 0 ? bs / x : 0;
-  sg.tiles = sg.ntv * h * v16;  // n16 / x (0 without tiles)
+  sg.nh = bs * v16;
+  sg.prow = h * v16;
   sg.pad_ = 0;
-  uint32_t pk, pv;
-  if (c->layout == KVX_LAYOUT_HND) {
-    pk = pv = to_packed ? bs * v16 : h * v16;
-  } else {
-    pk = to_packed ? bs : h * v16;
-    pv = (to_packed || sg.ntv) ? bs : h * d;
-  }
-  sg.pad[0] = fast_div(pk < 8 ? 8 : pk);
-  sg.pad[1] = fast_div(pv < 8 ? 8 : pv);
+  const uint32_t p = to_packed ? bs : v16;
+  sg.pad[0] = sg.pad[1] = fast_div(p < 8 ? 8 : p);
   return sg;
 }
 
@@ -713,7 +656,7 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.num_blocks = (uint32_t)g.num_blocks;
   ug.n16 = (uint32_t)(g.slab / 16);
   const int layout = cache->layout, elem = cache->elem_bytes;
-  slab_parts(layout, ug.n16, &ug.parts, &ug.parts_shift);
+  slab_parts(layout, ug.n16, (uint32_t)cache->num_kv_heads, &ug.parts, &ug.parts_shift);
   ug.slab = (uint64_t)g.slab;
   ug.sg = slab_geom(cache, to_packed);
   if ((uint64_t)g.n_units * ug.parts > 0x7FFFFFFF) return KVX_EINTERNAL;
@@ -773,7 +716,7 @@ kvx_status launch_copy_chunks(bool to_packed, const kvx_cache* cache, int32_t l0
   cg.num_blocks = (uint32_t)cache->num_blocks;
   cg.n16 = (uint32_t)(slab / 16);
   const int layout = cache->layout, elem = cache->elem_bytes;
-  slab_parts(layout, cg.n16, &cg.parts, &cg.parts_shift);
+  slab_parts(layout, cg.n16, (uint32_t)cache->num_kv_heads, &cg.parts, &cg.parts_shift);
   cg.table_len = table_len;
   cg.slab = (uint64_t)slab;
   cg.packed_bytes = packed_bytes;

@@ -1,7 +1,10 @@
-"""GPU parity for the cache layouts that reorder a slab (staged through LDS):
-KVX_LAYOUT_HND ([head][token][dim]) and KVX_LAYOUT_PAGED_ATTN (keys in 16-byte
-groups [head][dim/x][token][x], values [head][dim][token]), against the
-oracle, which moves elements through the layout's index function."""
+"""GPU parity for the cache layouts that reorder a slab (moved head by head:
+HND rows directly, paged attention through LDS): KVX_LAYOUT_HND
+([head][token][dim]) and KVX_LAYOUT_PAGED_ATTN (keys in 16-byte groups
+[head][dim/x][token][x], values [head][dim][token]), against the oracle, which
+moves elements through the layout's index function. Heads of up to 256
+vectors take the one-vector-per-thread kernels, larger ones the
+twelve-vector kernels."""
 import numpy as np
 import pytest
 
@@ -44,6 +47,9 @@ CASES = [
     (PA, 2, 16, 16, 96, 1, 0, 2, 5, 32),      # 1-byte elements, 24 KiB slabs
     (PA, 2, 1, 8, 64, 2, 0, 2, 9, 3),         # one token per block
     (PA, 2, 3, 5, 40, 2, 0, 2, 7, 9),         # odd block size and head count
+    (HND, 2, 32, 2, 256, 2, 0, 2, 6, 64),     # heads of 1,024 vectors (several per thread)
+    (PA, 2, 16, 1, 1536, 2, 0, 2, 5, 32),     # one 48 KiB head: 12 vectors per thread
+    (HND, 2, 96, 1, 256, 2, 0, 2, 4, 96),     # one 48 KiB head, HND
 ]
 
 
