@@ -85,8 +85,9 @@ typedef enum kvx_status {
  *   KVX_LAYOUT_PAGED_ATTN  K [num_blocks][num_kv_heads][head_dim / x][block_size][x]
  *                          with x = 16 / elem_bytes, V [num_blocks][num_kv_heads]
  *                          [head_dim][block_size] (the paged-attention kernel layout)
- * The two transposing layouts stage each slab through LDS and need
- * head_dim * elem_bytes to be a multiple of 16 and a slab of at most 48 KiB. */
+ * The two reordering layouts move a slab head by head (paged attention through
+ * LDS) and need head_dim * elem_bytes to be a multiple of 16 and a slab of at
+ * most 48 KiB. */
 #define KVX_LAYOUT_NHD 0
 #define KVX_LAYOUT_HND 1
 #define KVX_LAYOUT_PAGED_ATTN 2
