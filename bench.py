@@ -68,7 +68,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="8b-80k",
-                    choices=["8b-80k", "8b-32k-sweep", "70b-batch", "8b-files"])
+                    choices=["8b-80k", "8b-32k-sweep", "70b-batch", "8b-files", "8b-preload"])
     ap.add_argument("--num-blocks", type=int, default=20000)
     ap.add_argument("--prefix-blocks", type=int, default=5000)
     ap.add_argument("--chunk-tokens", type=int, default=256)
@@ -713,6 +713,126 @@ def run_files(args):
     print(json.dumps(out), flush=True)
 
 
+def run_preload(args):
+    """Preloading (Sec. 6.5) on the 8B-shaped 32k-token prefix stored as 128 chunk
+    files of 32 MiB (4 GiB): the request path of a restore (from the call until
+    the cache holds the prefix) when the files are read only on demand (the
+    ring restoring straight from the files), when a preloader read them while
+    the request waited (the path is then the host-to-device copy out of the
+    preloader's pinned pool), and when the request starts halfway through the
+    preload (waiting time half the demand restore)."""
+    import shutil
+
+    import numpy as np
+    import torch
+
+    import kvsynth
+    import paper_2609_11744_amd as kvx
+
+    dev = torch.device("cuda:0")
+    L, BS, H, D, E = 32, 16, 8, 128, 2
+    NB, n, ct = args.num_blocks, 2048, 256
+    bpc = ct // BS
+    per_block = 2 * L * BS * H * D * E
+    payload = n * per_block
+    chunk_bytes = bpc * per_block
+    root = os.path.abspath(args.tier_dir)
+    shutil.rmtree(root, ignore_errors=True)
+    cache = kvx.PagedKVCache.allocate(L, NB, BS, H, D, torch.bfloat16, dev)
+    fill_cache(cache, args.seed, kvsynth.ROLE_SRC)
+    perm = np.random.default_rng(args.seed).permutation(NB).astype(np.int32)
+    bt_src = torch.from_numpy(perm[:n].copy()).to(dev)
+    bt_dst = torch.from_numpy(perm[n:2 * n].copy()).to(dev)
+    chunks = [(kvx.kvx_chunk_path(root, "llama-3-8b-bf16", 0x5A5A5A5A5A5A5A5A ^ (c * 0x9E3779B97F4A7C15)),
+               c * bpc, bpc) for c in range(n // bpc)]
+    paths = [c[0] for c in chunks]
+    reps = max(3, args.steps)
+    probe = probes(dev, 5)
+    reserve = args.io_depth
+    res = {"demand": [], "preloaded": [], "half": []}
+    read_s, half_stats, pre_stats = [], None, None
+    try:
+        ring = kvx.StagingRing(dev, args.slots, args.slot_mib << 20)
+        try:
+            ring.bind_offload_files(cache, 0, L, ct, chunks, io_depth=args.io_depth)
+            kvx.kvx_offload_to_staging(ring, bt_src)
+            # demand only: the ring reads the files as it restores
+            ring.bind_files(cache, 0, L, ct, chunks, io_depth=args.io_depth)
+            for _ in range(reps):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                kvx.kvx_restore_from_staging(ring, bt_dst)
+                torch.cuda.synchronize()
+                res["demand"].append(time.perf_counter() - t0)
+            kvx.kvx_check()
+            log("demand restores done")
+
+            def request(pre):
+                """The request path with a preloader: claim the images, restore
+                them straight from the pool, drop the holds."""
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                imgs = pre.fetch(paths)
+                ring.bind_chunks(cache, 0, L, ct, [(img, c[1], c[2]) for img, c in zip(imgs, chunks)],
+                                 fill_threads=0)
+                kvx.kvx_restore_from_staging(ring, bt_dst)
+                torch.cuda.synchronize()
+                dt = time.perf_counter() - t0
+                pre.release(paths)
+                return dt
+
+            half = statistics.median(res["demand"]) / 2
+            for _ in range(reps):
+                for mode in ("preloaded", "half"):
+                    pre = kvx.Preloader(len(paths) + reserve, chunk_bytes, io_depth=args.io_depth,
+                                        reserve=reserve, pinned=True)
+                    try:
+                        t0 = time.perf_counter()
+                        pre.hint(paths)  # the request is still waiting
+                        if mode == "preloaded":
+                            pre.wait_idle()
+                            read_s.append(time.perf_counter() - t0)
+                        else:
+                            time.sleep(half)
+                        res[mode].append(request(pre))
+                        if mode == "preloaded":
+                            pre_stats = pre.stats()
+                        else:
+                            half_stats = pre.stats()
+                    finally:
+                        pre.close()
+            kvx.kvx_check()
+        finally:
+            ring.close()
+        log("preload restores done")
+    finally:
+        shutil.rmtree(root, ignore_errors=True)
+    med = {k: statistics.median(v) for k, v in res.items()}
+    out = base_record(
+        args, "KV restore request path ms with preloading (32k-token prefix, storage tier)", "ms",
+        round(med["preloaded"] * 1e3, 2), round(med["preloaded"] * 1e3, 2),
+        {"workload": "llama-3-8b-shaped paged KV, 32k-token prefix (2048 blocks, 4 GiB) as 128 "
+                     "chunk files of 256 tokens; 4 x 64 MiB ring; preloader pool of 128 + "
+                     "io_depth slots of 32 MiB",
+         "num_blocks": NB, "prefix_tokens": n * BS, "chunk_tokens": ct, "io_depth": args.io_depth,
+         "parallelism": "single GPU"}, higher=False)
+    out.update({
+        "request_path_ms": {k: round(v * 1e3, 2) for k, v in med.items()},
+        "speedup_preloaded_vs_demand": round(med["demand"] / med["preloaded"], 2),
+        "speedup_half_vs_demand": round(med["demand"] / med["half"], 2),
+        "preloaded_restore_GBps": round(payload / med["preloaded"] / 1e9, 2),
+        "preloaded_frac_of_h2d": round(payload / med["preloaded"] / 1e9 / probe["h2d_GBps"], 4),
+        "demand_restore_GBps": round(payload / med["demand"] / 1e9, 2),
+        "preload_read_GBps": round(payload / statistics.median(read_s) / 1e9, 2),
+        "stats_preloaded": pre_stats, "stats_half": half_stats,
+        "probes": {"h2d_GBps": round(probe["h2d_GBps"], 2)}, "reps": reps,
+        "note": "each request path starts from files whose pages were dropped from the page "
+                "cache; 'half' starts the request after half the demand restore time of "
+                "preloading, so its fetch claims what is staged, joins what is being read and "
+                "reads the rest on demand before the restore"})
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -723,7 +843,7 @@ def main():
 
     torch.cuda.set_device(torch.device("cuda:0"))
     {"8b-80k": run_80k, "8b-32k-sweep": run_sweep, "70b-batch": run_batch,
-     "8b-files": run_files}[args.workload](args)
+     "8b-files": run_files, "8b-preload": run_preload}[args.workload](args)
 
 
 if __name__ == "__main__":

@@ -393,6 +393,82 @@ kvx_status kvx_read_files(const kvx_file_io* ops, int32_t n, int32_t io_depth);
  * above once all of its bytes are written. */
 kvx_status kvx_write_files(const kvx_file_io* ops, int32_t n, int32_t io_depth);
 
+/* ---- preloading (Sec. 6.5) ------------------------------------------------------ *
+ *
+ * Chunk files of requests that are still waiting are read ahead of time into a
+ * bounded pool of host slots (one chunk file per slot), so that when such a
+ * request runs only the host-to-device copy is left on its path: its demand
+ * fetch claims the staged images, which a ring restores straight from the pool
+ * (kvx_ring_bind_chunks with fill_threads 0). One reactor thread reads files
+ * in 16 MiB pieces through io_uring, at most io_depth in flight, and always
+ * serves demand before speculation: speculative pieces are issued only while
+ * no demand file has pieces left to issue; one preload runs at a time (the
+ * files of one kvx_preload_hint call, read concurrently; the next call's
+ * files start when none of them is left), and speculative reads take only
+ * slots beyond the `reserve` free ones. A file is
+ * read at most once while staged: hints for a known file are dropped, and a
+ * fetch claims its image or joins its read. Released images stay staged, so
+ * the pool also caches chunk images: a speculative read may take the slot of
+ * a cached image nobody holds (least recently used first) but never that of a
+ * preloaded image not yet fetched; a demand fetch may take either, cached
+ * images first. Files are read
+ * buffered into a pinned pool (pinned memory cannot take direct transfers on
+ * this platform) and their pages dropped from the page cache after reading.
+ * The calls are thread-safe; kvx_preloader_destroy must not run concurrently
+ * with another call on the same preloader. */
+typedef struct kvx_preloader kvx_preloader;
+
+typedef struct kvx_preload_stats {
+  int64_t hints;           /* files queued by kvx_preload_hint */
+  int64_t spec_deduped;    /* hints for a file already staged, being read or queued */
+  int64_t spec_dropped;    /* hints refused: n_slots files already queued */
+  int64_t spec_reads;      /* files read speculatively to completion */
+  int64_t demand_fetches;  /* distinct files requested by kvx_preload_fetch */
+  int64_t hits_ready;      /* of those, already staged */
+  int64_t hits_inflight;   /* of those, joined a speculative read in progress */
+  int64_t demand_reads;    /* files whose read completed as demand work */
+  int64_t evictions;       /* staged files whose slot was taken for another file */
+  int64_t bytes_read;      /* file bytes read into the pool */
+  int64_t staged;          /* files staged now */
+  int64_t held;            /* files held by fetches now */
+} kvx_preload_stats;
+
+/* n_slots slots of slot_bytes (a positive multiple of 4096; a chunk file must
+ * fit one slot), io_depth 1..256 pieces in flight, reserve 0..n_slots-1 slots
+ * kept free of speculative reads; pinned 1 allocates the pool with
+ * hipHostMalloc (needed to restore from it), 0 with plain aligned memory
+ * (host-only use). Touches every page of the pool (pages are otherwise
+ * mapped on first use, on the request path) and starts the reactor thread. */
+kvx_status kvx_preloader_create(int32_t n_slots, int64_t slot_bytes, int32_t io_depth,
+                                int32_t reserve, int32_t pinned, kvx_preloader** out);
+
+/* Queue the chunk files (paths copied) of one waiting request for
+ * speculative reading: one preload, started after the preloads queued
+ * before it. Returns at once. */
+kvx_status kvx_preload_hint(kvx_preloader* p, const char* const* paths, int32_t n);
+
+/* Demand: make every named file staged (claiming staged images, joining reads
+ * in progress, reading the rest before any speculative work) and hold it:
+ * images[i] / sizes[i] receive the host address and byte size of paths[i]'s
+ * image, valid until kvx_preload_release. Blocks until all are staged.
+ * KVX_ENOMEM if the files held after the call would exceed n_slots (nothing is
+ * held then); KVX_EIO if a file is missing, empty, larger than a slot or
+ * unreadable (nothing is held then). */
+kvx_status kvx_preload_fetch(kvx_preloader* p, const char* const* paths, int32_t n, void** images,
+                             int64_t* sizes);
+
+/* Drop one hold of each named file (KVX_EINVAL, changing nothing, if one is
+ * not held). Released images stay staged until their slot is needed. */
+kvx_status kvx_preload_release(kvx_preloader* p, const char* const* paths, int32_t n);
+
+/* Block until no read is in progress and no queued hint can start. */
+kvx_status kvx_preload_wait_idle(kvx_preloader* p);
+
+kvx_status kvx_preload_stats_get(kvx_preloader* p, kvx_preload_stats* out);
+
+/* Stop the reactor (reads in flight complete first) and free the pool. */
+kvx_status kvx_preloader_destroy(kvx_preloader* p);
+
 /* Fault-injection hooks for testing the slot-reuse protocol from the host.
  * max_delay_us > 0: each fill or drain thread pauses a pseudo-random 0 ..
  * max_delay_us microseconds before every piece (varies the interleavings).

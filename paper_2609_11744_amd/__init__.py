@@ -519,6 +519,69 @@ def kvx_write_files(ops, io_depth: int = 8) -> None:
     _ok(_native.lib().kvx_write_files(arr, len(ops), io_depth), "kvx_write_files")
 
 
+def _paths(paths):
+    enc = [os.fsencode(p) for p in paths]
+    arr = (ctypes.c_char_p * max(len(enc), 1))(*enc)
+    return arr, enc
+
+
+class Preloader:
+    """Bounded pool of host slots that chunk files are read into ahead of their
+    requests (kvx_preloader_*): hint() queues speculative reads, fetch() claims
+    staged images (reading the rest first, before any speculative work) and
+    returns numpy views of them, release() drops the holds."""
+
+    def __init__(self, n_slots: int, slot_bytes: int, io_depth: int = 8, reserve: int = 0,
+                 pinned: bool = True):
+        h = ctypes.c_void_p()
+        _ok(_native.lib().kvx_preloader_create(n_slots, slot_bytes, io_depth, reserve,
+                                               1 if pinned else 0, ctypes.byref(h)),
+            "kvx_preloader_create")
+        self.handle = h.value
+
+    def hint(self, paths) -> None:
+        arr, keep = _paths(paths)
+        _ok(_native.lib().kvx_preload_hint(self.handle, arr, len(paths)), "kvx_preload_hint")
+
+    def fetch(self, paths):
+        """Hold the named files' images; returns one uint8 array view per path
+        (valid until release)."""
+        import numpy as np
+
+        arr, keep = _paths(paths)
+        n = len(paths)
+        imgs = (ctypes.c_void_p * max(n, 1))()
+        sizes = (ctypes.c_int64 * max(n, 1))()
+        _ok(_native.lib().kvx_preload_fetch(self.handle, arr, n, imgs, sizes), "kvx_preload_fetch")
+        return [np.ctypeslib.as_array((ctypes.c_uint8 * sizes[i]).from_address(imgs[i]))
+                for i in range(n)]
+
+    def release(self, paths) -> None:
+        arr, keep = _paths(paths)
+        _ok(_native.lib().kvx_preload_release(self.handle, arr, len(paths)),
+            "kvx_preload_release")
+
+    def wait_idle(self) -> None:
+        _ok(_native.lib().kvx_preload_wait_idle(self.handle), "kvx_preload_wait_idle")
+
+    def stats(self) -> dict:
+        s = _native.KvxPreloadStats()
+        _ok(_native.lib().kvx_preload_stats_get(self.handle, ctypes.byref(s)),
+            "kvx_preload_stats_get")
+        return {f: getattr(s, f) for f, _ in _native.KvxPreloadStats._fields_}
+
+    def close(self) -> None:
+        if self.handle:
+            _native.lib().kvx_preloader_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
 def kvx_offload_to_staging(ring: StagingRing, block_table, stream=None) -> None:
     ptr = _table_ptr(ring._cache, block_table, ring.n_blocks) if ring._cache is not None else None
     st = _native.lib().kvx_offload_to_staging(ring.handle, ptr, _stream_handle(stream))
@@ -531,6 +594,6 @@ __all__ = [
     "kvx_plan_pieces", "kvx_restore_from_staging", "shape_only_cache", "KVX_MAX_LAYERS",
     "kvx_gather_chunks", "kvx_scatter_chunks", "chunk_refs", "kvx_offload_to_staging",
     "kvx_block_hashes", "kvx_dedupe_keys", "KVX_LAYOUT_NHD", "KVX_LAYOUT_HND",
-    "KVX_LAYOUT_PAGED_ATTN", "layer_shapes", "kvx_probe_stream", "kvx_chunk_path",
+    "KVX_LAYOUT_PAGED_ATTN", "layer_shapes", "kvx_probe_stream", "kvx_chunk_path", "Preloader",
     "kvx_read_files", "kvx_write_files", "KVX_EIO",
 ]

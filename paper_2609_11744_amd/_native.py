@@ -45,6 +45,12 @@ class KvxFileIo(ctypes.Structure):
     _fields_ = [("path", ctypes.c_char_p), ("buf", c_vp), ("offset", c_i64), ("bytes", c_i64)]
 
 
+class KvxPreloadStats(ctypes.Structure):
+    _fields_ = [(n, c_i64) for n in ("hints", "spec_deduped", "spec_dropped", "spec_reads",
+                                     "demand_fetches", "hits_ready", "hits_inflight",
+                                     "demand_reads", "evictions", "bytes_read", "staged", "held")]
+
+
 class KvxCurve(ctypes.Structure):
     _fields_ = [("tokens", ctypes.POINTER(ctypes.c_double)),
                 ("seconds", ctypes.POINTER(ctypes.c_double)), ("n", c_i32)]
@@ -103,6 +109,15 @@ SIGNATURES = {
                                ctypes.c_char_p, c_i32]),
     "kvx_read_files": (ctypes.c_int, [ctypes.POINTER(KvxFileIo), c_i32, c_i32]),
     "kvx_write_files": (ctypes.c_int, [ctypes.POINTER(KvxFileIo), c_i32, c_i32]),
+    "kvx_preloader_create": (ctypes.c_int, [c_i32, c_i64, c_i32, c_i32, c_i32,
+                                            ctypes.POINTER(c_vp)]),
+    "kvx_preload_hint": (ctypes.c_int, [c_vp, ctypes.POINTER(ctypes.c_char_p), c_i32]),
+    "kvx_preload_fetch": (ctypes.c_int, [c_vp, ctypes.POINTER(ctypes.c_char_p), c_i32,
+                                         ctypes.POINTER(c_vp), ctypes.POINTER(c_i64)]),
+    "kvx_preload_release": (ctypes.c_int, [c_vp, ctypes.POINTER(ctypes.c_char_p), c_i32]),
+    "kvx_preload_wait_idle": (ctypes.c_int, [c_vp]),
+    "kvx_preload_stats_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxPreloadStats)]),
+    "kvx_preloader_destroy": (ctypes.c_int, [c_vp]),
     "kvx_pinned_alloc": (ctypes.c_int, [c_i64, ctypes.POINTER(c_vp)]),
     "kvx_pinned_free": (ctypes.c_int, [c_vp]),
 }

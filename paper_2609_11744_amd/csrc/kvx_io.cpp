@@ -71,9 +71,12 @@ kvx_status open_tier_file(TierFile* f, bool write) {
 }
 
 // Reopen a file without O_DIRECT (its direct transfers failed) at the same
-// name: the final name for reads, the temporary one for writes.
+// name: the final name for reads, the temporary one for writes. The old
+// descriptor is kept open until the file is closed: other transfers of the
+// file may still be in flight on it (they fail the same way and are repeated
+// on the new one).
 bool reopen_buffered(TierFile* f, bool write) {
-  if (f->fd >= 0) close(f->fd);
+  if (f->fd >= 0) f->retired.push_back(f->fd);
   f->direct = false;
   f->fd = write ? open(f->temp.c_str(), O_WRONLY | O_CLOEXEC)
                 : open(f->path.c_str(), O_RDONLY | O_CLOEXEC);
@@ -87,6 +90,8 @@ kvx_status publish_tier_file(TierFile* f) {
     close(f->fd);
   }
   f->fd = -1;
+  for (int fd : f->retired) close(fd);
+  f->retired.clear();
   const bool linked = link(f->temp.c_str(), f->path.c_str()) == 0 || errno == EEXIST;
   unlink(f->temp.c_str());
   f->temp.clear();
@@ -100,6 +105,8 @@ void close_tier_file(TierFile* f) {
     close(f->fd);
   }
   f->fd = -1;
+  for (int fd : f->retired) close(fd);
+  f->retired.clear();
   if (!f->temp.empty() && !f->published) unlink(f->temp.c_str());
   f->temp.clear();
 }
@@ -117,7 +124,7 @@ kvx_status IoEngine::init(int32_t depth, bool write) {
   if (depth < 1 || depth > 256 || ring_fd_ >= 0 || depth_ > 0) return KVX_EINVAL;
   write_ = write;
   depth_ = depth;
-  ops_.assign((size_t)depth, Op{nullptr, nullptr, 0, 0, 0, false});
+  ops_.assign((size_t)depth, Op{nullptr, nullptr, 0, 0, 0, false, -1});
   const char* off = getenv("KVX_IO_NO_URING");
   if (off && off[0] == '1') return KVX_OK;  // blocking fallback, by request
   io_uring_params p;
@@ -175,7 +182,8 @@ kvx_status IoEngine::submit(int32_t slot) {
   const unsigned idx = tail & *sq_mask_;
   io_uring_sqe* sqe = static_cast<io_uring_sqe*>(sqes_) + idx;
   std::memset(sqe, 0, sizeof *sqe);
-  sqe->fd = op.f->fd;
+  op.fd = op.f->fd;
+  sqe->fd = op.fd;
   sqe->user_data = (uint64_t)slot;
   if (op.left < 0) {
     sqe->opcode = IORING_OP_FSYNC;
@@ -223,7 +231,7 @@ kvx_status IoEngine::start(TierFile* f, uint8_t* buf, int64_t offset, int64_t by
     return KVX_OK;
   }
   const int32_t slot = take_slot();
-  ops_[(size_t)slot] = Op{f, buf, offset, bytes, tag, true};
+  ops_[(size_t)slot] = Op{f, buf, offset, bytes, tag, true, -1};
   return submit(slot);
 }
 
@@ -235,15 +243,16 @@ kvx_status IoEngine::start_datasync(TierFile* f, uint64_t tag) {
     return KVX_OK;
   }
   const int32_t slot = take_slot();
-  ops_[(size_t)slot] = Op{f, nullptr, 0, -1, tag, true};
+  ops_[(size_t)slot] = Op{f, nullptr, 0, -1, tag, true, -1};
   return submit(slot);
 }
 
-kvx_status IoEngine::wait(std::vector<uint64_t>* done) {
-  const size_t before = done->size();
+kvx_status IoEngine::wait(std::vector<uint64_t>* done, std::vector<uint64_t>* failed) {
+  const size_t before = done->size() + (failed ? failed->size() : 0);
+  auto reported = [&]() { return done->size() + (failed ? failed->size() : 0) > before; };
   done->insert(done->end(), finished_.begin(), finished_.end());
   finished_.clear();
-  if (ring_fd_ < 0 || done->size() > before || inflight_ == 0) return KVX_OK;
+  if (ring_fd_ < 0 || reported() || inflight_ == 0) return KVX_OK;
   for (;;) {
     unsigned head = *cq_head_;
     const unsigned tail = __atomic_load_n(cq_tail_, __ATOMIC_ACQUIRE);
@@ -261,19 +270,23 @@ kvx_status IoEngine::wait(std::vector<uint64_t>* done) {
       if (op.left < 0) {  // an fdatasync
         op.live = false;
         --inflight_;
-        if (res < 0) st = KVX_EIO;
-        else done->push_back(op.tag);
+        if (res >= 0) done->push_back(op.tag);
+        else if (failed) failed->push_back(op.tag);
+        else st = KVX_EIO;
         continue;
       }
-      if (res == -EFAULT && op.f->direct) {  // pinned memory: repeat it buffered
+      if (res == -EFAULT && (op.f->direct || op.fd != op.f->fd)) {
+        // pinned memory: repeat it buffered (the file may have been reopened
+        // for another of its transfers already)
         __atomic_store_n(cq_head_, head, __ATOMIC_RELEASE);
-        if (!reopen_buffered(op.f, write_) || submit(slot) != KVX_OK) st = KVX_EIO;
+        if ((op.f->direct && !reopen_buffered(op.f, write_)) || submit(slot) != KVX_OK) st = KVX_EIO;
         continue;
       }
       if (res <= 0) {  // an error, or end of file before the op's last byte
         op.live = false;
         --inflight_;
-        st = KVX_EIO;
+        if (failed) failed->push_back(op.tag);
+        else st = KVX_EIO;
         continue;
       }
       if (write_) op.f->written += res;
@@ -292,7 +305,7 @@ kvx_status IoEngine::wait(std::vector<uint64_t>* done) {
     }
     __atomic_store_n(cq_head_, head, __ATOMIC_RELEASE);
     if (st != KVX_OK) return st;
-    if (done->size() > before || inflight_ == 0) return KVX_OK;
+    if (reported() || inflight_ == 0) return KVX_OK;
     if (!enter(1)) return KVX_EIO;
   }
 }

@@ -37,6 +37,7 @@ struct TierFile {
   int64_t written = 0;    // writes: bytes landed so far
   bool flushing = false;  // writes: complete, its fdatasync queued or running
   bool published = false;
+  std::vector<int> retired;  // descriptors replaced while transfers on them may be in flight
 };
 
 inline bool io_aligned(const void* buf, int64_t offset, int64_t bytes) {
@@ -87,8 +88,11 @@ class IoEngine {
   kvx_status start_datasync(TierFile* f, uint64_t tag);
 
   // Block until at least one started transfer has finished (returns at once
-  // if some already have), then append the finished tags to *done.
-  kvx_status wait(std::vector<uint64_t>* done);
+  // if some already have), then append the finished tags to *done. A failed
+  // transfer (an I/O error, or end of file before its last byte) makes the
+  // call return KVX_EIO, or, with `failed` given, appends its tag there and
+  // counts as finished.
+  kvx_status wait(std::vector<uint64_t>* done, std::vector<uint64_t>* failed = nullptr);
 
  private:
   struct Op {
@@ -98,6 +102,7 @@ class IoEngine {
     int64_t left;     // bytes still to transfer; -1 for an fdatasync
     uint64_t tag;
     bool live;
+    int fd;           // the descriptor its last submission used
   };
   int32_t take_slot();
   kvx_status submit(int32_t slot);

@@ -138,3 +138,26 @@ def test_abort_during_file_offload(tmp_path):
         if os.path.exists(path):
             assert os.path.getsize(path) == per_chunk
     assert not [f for d, _, fs in os.walk(tmp_path) for f in fs if ".tmp." in f]
+
+
+def test_read_files_into_pinned_memory_with_several_transfers_per_file(tmp_path):
+    """Direct reads into pinned memory fail (EFAULT) and are repeated on a
+    buffered descriptor; with several transfers of one file in flight, the
+    others (still on the old descriptor) must be repeated too, not fail."""
+    rng = np.random.default_rng(77)
+    files = []
+    for i in range(6):
+        data = rng.integers(0, 256, 4 << 20, dtype=np.uint8)
+        p = tmp_path / f"r{i}.kvc"
+        data.tofile(p)
+        files.append((str(p), data))
+    dst = kvx.PinnedBuffer(len(files) * (4 << 20))
+    ops = []
+    for i, (p, _) in enumerate(files):
+        for q in range(4):  # four 1 MiB transfers per file, all in flight together
+            off = q << 20
+            ops.append((p, dst.array[i * (4 << 20) + off:i * (4 << 20) + off + (1 << 20)], off))
+    kvx.kvx_read_files(ops, io_depth=16)
+    for i, (_, data) in enumerate(files):
+        assert np.array_equal(dst.array[i * (4 << 20):(i + 1) * (4 << 20)], data), f"file {i}"
+    dst.free()
