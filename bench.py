@@ -344,6 +344,7 @@ def offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe):
             drain.append(st["fill_ms"])
             wait.append(st["wait_fill_ms"])
         kvx.kvx_check()
+        deferred = deferred_store(ring, bt_src, dev, statistics.median(times))
     finally:
         ring.close()
     t = statistics.median(times)
@@ -354,7 +355,63 @@ def offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe):
             "reps": args.offload_reps,
             "d2h_copies": copies_desc(st),
             "breakdown_ms": {"drain_thread_sum": round(statistics.median(drain), 2),
-                             "wait_for_drain": round(statistics.median(wait), 2)}}
+                             "wait_for_drain": round(statistics.median(wait), 2)},
+            "deferred_store": deferred}
+
+
+def deferred_store(ring, bt_src, dev, offload_s):
+    """The store deferred to the next iteration (kvx_offload_begin, gathers on a
+    side stream) beside a compute-bound stand-in for that iteration's forward
+    pass (bf16 8192^3 GEMMs on another stream, as many as take about as long as
+    the offload alone). overlap = time hidden / the shorter of the two alone
+    (1: the shorter one is fully hidden)."""
+    import torch
+
+    import paper_2609_11744_amd as kvx
+
+    side, comp = torch.cuda.Stream(), torch.cuda.Stream()
+    a = torch.randn(8192, 8192, device=dev, dtype=torch.bfloat16)
+    b = torch.randn(8192, 8192, device=dev, dtype=torch.bfloat16)
+    c = torch.empty(8192, 8192, device=dev, dtype=torch.bfloat16)
+
+    def gemms(k):
+        with torch.cuda.stream(comp):
+            for _ in range(k):
+                torch.matmul(a, b, out=c)
+
+    gemms(5)
+    comp.synchronize()
+    t0 = time.perf_counter()
+    gemms(20)
+    comp.synchronize()
+    per = (time.perf_counter() - t0) / 20
+    k = max(1, int(offload_s / per))
+    alone = []
+    for _ in range(3):
+        t0 = time.perf_counter()
+        gemms(k)
+        comp.synchronize()
+        alone.append(time.perf_counter() - t0)
+    both, during = [], []
+    for _ in range(3):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        kvx.kvx_offload_begin(ring, bt_src, stream=side)
+        t1 = time.perf_counter()
+        gemms(k)
+        comp.synchronize()
+        during.append(time.perf_counter() - t1)
+        kvx.kvx_offload_wait(ring)
+        both.append(time.perf_counter() - t0)
+    kvx.kvx_check()
+    t_c, t_b = statistics.median(alone), statistics.median(both)
+    flops = 2.0 * 8192 ** 3 * k
+    return {"gemms": k, "compute_alone_ms": round(t_c * 1e3, 2),
+            "offload_alone_ms": round(offload_s * 1e3, 2),
+            "both_ms": round(t_b * 1e3, 2),
+            "compute_during_store_ms": round(statistics.median(during) * 1e3, 2),
+            "compute_TFLOPs_alone": round(flops / t_c / 1e12, 1),
+            "overlap": round((t_c + offload_s - t_b) / min(t_c, offload_s), 3)}
 
 
 def cpu_baseline(args, L, BS, H, D, E, perm):

@@ -72,7 +72,8 @@ typedef enum kvx_status {
   KVX_EBADBLOCK = -4,  /* a kernel met a block id outside [0, num_blocks) */
   KVX_ECLOSED = -5,    /* the ring was aborted while a restore was running */
   KVX_EINTERNAL = -6,  /* invariant violated inside the library */
-  KVX_EIO = -7         /* a storage-tier file could not be opened, read, written or published */
+  KVX_EIO = -7,        /* a storage-tier file could not be opened, read, written or published */
+  KVX_EBUSY = -8       /* the ring is running an offload started by kvx_offload_begin */
 } kvx_status;
 
 /* Largest layer range a single call may cover. */
@@ -303,6 +304,29 @@ kvx_status kvx_ring_bind_offload(kvx_ring* ring, const kvx_cache* cache, int32_t
  * the device). KVX_ECLOSED after kvx_ring_abort. */
 kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hipStream_t stream);
 
+/* Deferred store (Secs. 2.3, 5.1: the offload API defers the store work of
+ * engine iteration N to iteration N + 1, so the copies to the host overlap
+ * the next forward pass): start the offload of the bound chunks on a thread
+ * the ring owns and return at once. The gathers run after the work already
+ * enqueued on `stream`, on a stream the ring owns with a hardware queue of
+ * its own (created with a compute-unit mask covering every compute unit: the
+ * runtime shares a few hardware queues round-robin among streams, and a store
+ * whose stream shared the forward pass's queue waited behind all of it).
+ * Like any stream created without the non-blocking flag it is ordered
+ * against the legacy default stream, so the forward pass it should overlap
+ * must run on another stream. The copies to the host run on the DMA engine
+ * and the drains on the drain threads, as in kvx_offload_to_staging. Until
+ * kvx_offload_wait has returned, every other call on the ring except
+ * kvx_ring_abort and kvx_ring_destroy returns KVX_EBUSY, and block_table and
+ * the destinations must stay valid. Argument errors found before the start
+ * are returned here; errors of the transfer by kvx_offload_wait. */
+kvx_status kvx_offload_begin(kvx_ring* ring, const int32_t* block_table, hipStream_t stream);
+
+/* Wait for the offload started by kvx_offload_begin and return its status
+ * (KVX_OK at once if none was started). On return every destination holds
+ * its image, as after kvx_offload_to_staging. */
+kvx_status kvx_offload_wait(kvx_ring* ring);
+
 typedef struct kvx_ring_stats {
   int64_t pieces;         /* pieces moved by the last restore or offload */
   int64_t bytes;          /* image bytes moved by it */
@@ -481,8 +505,9 @@ kvx_status kvx_preloader_destroy(kvx_preloader* p);
  * Other bits: KVX_EINVAL. Off by default; call between transfers. */
 kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t flags);
 
-/* Wait for the ring's side stream and last restore, then free everything the
- * ring owns. */
+/* Wait for an offload started by kvx_offload_begin (after kvx_ring_abort it
+ * stops early), the ring's side stream and last restore, then free everything
+ * the ring owns. */
 kvx_status kvx_ring_destroy(kvx_ring* ring);
 
 /* ---- step planning (host) ---------------------------------------------------- */

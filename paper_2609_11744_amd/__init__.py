@@ -24,6 +24,7 @@ from ._native import KvxCache, KvxChunkRef, KvxHostChunk, KvxPiece, KvxRingStats
 
 KVX_OK, KVX_EINVAL, KVX_ENOMEM, KVX_EHIP, KVX_EBADBLOCK, KVX_ECLOSED, KVX_EINTERNAL, KVX_EIO = (
     0, -1, -2, -3, -4, -5, -6, -7)
+KVX_EBUSY = -8
 KVX_MAX_LAYERS = 128
 KVX_LAYOUT_NHD, KVX_LAYOUT_HND, KVX_LAYOUT_PAGED_ATTN = 0, 1, 2
 
@@ -588,6 +589,21 @@ def kvx_offload_to_staging(ring: StagingRing, block_table, stream=None) -> None:
     _ok(st, "kvx_offload_to_staging")
 
 
+def kvx_offload_begin(ring: StagingRing, block_table, stream=None) -> None:
+    """Start the bound offload in the background (the deferred store); finish
+    it with kvx_offload_wait. The block table is kept alive until then."""
+    ptr = _table_ptr(ring._cache, block_table, ring.n_blocks) if ring._cache is not None else None
+    st = _native.lib().kvx_offload_begin(ring.handle, ptr, _stream_handle(stream))
+    _ok(st, "kvx_offload_begin")
+    ring._pending = block_table
+
+
+def kvx_offload_wait(ring: StagingRing) -> None:
+    st = _native.lib().kvx_offload_wait(ring.handle)
+    ring._pending = None
+    _ok(st, "kvx_offload_wait")
+
+
 __all__ = [
     "KvxError", "PagedKVCache", "PinnedBuffer", "StagingRing", "kvx_bytes_per_token",
     "kvx_packed_bytes", "kvx_gather_blocks", "kvx_scatter_blocks", "kvx_check",
@@ -595,5 +611,6 @@ __all__ = [
     "kvx_gather_chunks", "kvx_scatter_chunks", "chunk_refs", "kvx_offload_to_staging",
     "kvx_block_hashes", "kvx_dedupe_keys", "KVX_LAYOUT_NHD", "KVX_LAYOUT_HND",
     "KVX_LAYOUT_PAGED_ATTN", "layer_shapes", "kvx_probe_stream", "kvx_chunk_path", "Preloader",
-    "kvx_read_files", "kvx_write_files", "KVX_EIO",
+    "kvx_read_files", "kvx_write_files", "KVX_EIO", "KVX_EBUSY", "kvx_offload_begin",
+    "kvx_offload_wait",
 ]

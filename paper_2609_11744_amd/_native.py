@@ -82,6 +82,8 @@ SIGNATURES = {
     "kvx_ring_bind_offload": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32,
                                              ctypes.POINTER(KvxHostChunk), c_i32, c_i32]),
     "kvx_offload_to_staging": (ctypes.c_int, [c_vp, c_vp, c_vp]),
+    "kvx_offload_begin": (ctypes.c_int, [c_vp, c_vp, c_vp]),
+    "kvx_offload_wait": (ctypes.c_int, [c_vp]),
     "kvx_ring_stats_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxRingStats)]),
     "kvx_ring_abort": (ctypes.c_int, [c_vp]),
     "kvx_ring_set_test_hooks": (ctypes.c_int, [c_vp, c_i32, c_i32]),

@@ -107,6 +107,14 @@ struct kvx_ring {
   bool hook_poison = false;
   bool hook_hip_copies = false;  // copies through the HIP runtime even with the DMA engines set up
 
+  // deferred store (kvx_offload_begin / kvx_offload_wait): its gathers run on
+  // store_stream after store_begin (recorded on the caller's stream)
+  hipStream_t store_stream = nullptr;
+  hipEvent_t store_begin = nullptr;
+  std::thread async_th;
+  std::atomic<bool> async_busy{false};
+  kvx_status async_status = KVX_OK;
+
   // storage tier: the bound chunks live in files (kvx_ring_bind_files /
   // kvx_ring_bind_offload_files); a reactor thread replaces the fill / drain
   // threads
@@ -160,6 +168,7 @@ bool copy_finished(kvx_ring* r, int32_t s) {
 void drain_device(kvx_ring* r) {
   for (size_t s = 0; s < r->dma_done.size(); ++s) (void)wait_dma(r, (int32_t)s);
   if (r->side) (void)hipStreamSynchronize(r->side);
+  if (r->store_stream) (void)hipStreamSynchronize(r->store_stream);
   for (hipEvent_t e : r->dev_done)
     if (e) (void)hipEventSynchronize(e);
   for (hipEvent_t e : r->copy_done)
@@ -181,6 +190,13 @@ void destroy_resources(kvx_ring* r) {
   r->dma = false;
   if (r->side) (void)hipStreamDestroy(r->side);
   r->side = nullptr;
+  if (r->store_stream) {
+    (void)hipStreamSynchronize(r->store_stream);
+    (void)hipStreamDestroy(r->store_stream);
+  }
+  r->store_stream = nullptr;
+  if (r->store_begin) (void)hipEventDestroy(r->store_begin);
+  r->store_begin = nullptr;
   if (r->host) (void)hipHostFree(r->host);
   r->host = nullptr;
   if (r->owns_landing && r->landing) (void)hipFree(r->landing);
@@ -1122,6 +1138,36 @@ kvx_status host_chunks(const kvx_host_chunk* chunks, int32_t n,
   return KVX_OK;
 }
 
+// The deferred store's own stream. The runtime shares a few hardware queues
+// round-robin among a process's streams, and a store whose stream shared the
+// forward pass's queue waited behind all of it; a stream created with a
+// compute-unit mask gets a queue of its own, and a mask of every compute unit
+// restricts nothing. Without CU masking, a non-blocking stream.
+bool make_store_stream(kvx_ring* r) {
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, r->device) != hipSuccess ||
+      cus <= 0)
+    return false;
+  std::vector<uint32_t> mask((size_t)(cus + 31) / 32, 0u);
+  for (int c = 0; c < cus; ++c) mask[(size_t)c / 32] |= 1u << (c % 32);
+  if (hipExtStreamCreateWithCUMask(&r->store_stream, (uint32_t)mask.size(), mask.data()) !=
+      hipSuccess) {
+    (void)hipGetLastError();
+    r->store_stream = nullptr;
+    if (hipStreamCreateWithFlags(&r->store_stream, hipStreamNonBlocking) != hipSuccess) {
+      r->store_stream = nullptr;
+      return false;
+    }
+  }
+  if (hipEventCreateWithFlags(&r->store_begin, hipEventDisableTiming) != hipSuccess) {
+    (void)hipStreamDestroy(r->store_stream);
+    r->store_stream = nullptr;
+    r->store_begin = nullptr;
+    return false;
+  }
+  return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -1190,6 +1236,7 @@ kvx_status kvx_ring_bind(kvx_ring* r, const kvx_cache* cache, int32_t l0, int32_
                          int32_t n_blocks, int32_t chunk_tokens, const void* host_source,
                          int32_t fill_threads) {
   if (!r || !cache) return KVX_EINVAL;
+  if (r->async_busy.load()) return KVX_EBUSY;
   try {
     kvx::Geometry g;
     kvx_status st = kvx::validate(cache, l0, l1, n_blocks, chunk_tokens, false, &g);
@@ -1208,6 +1255,7 @@ kvx_status kvx_ring_bind_chunks(kvx_ring* r, const kvx_cache* cache, int32_t l0,
                                 int32_t chunk_tokens, const kvx_host_chunk* chunks,
                                 int32_t n_chunks, int32_t fill_threads) {
   if (!r || !cache) return KVX_EINVAL;
+  if (r->async_busy.load()) return KVX_EBUSY;
   try {
     std::vector<kvx::HostChunk> v;
     kvx_status st = host_chunks(chunks, n_chunks, &v);
@@ -1222,6 +1270,7 @@ kvx_status kvx_ring_bind_offload(kvx_ring* r, const kvx_cache* cache, int32_t l0
                                  int32_t chunk_tokens, const kvx_host_chunk* chunks,
                                  int32_t n_chunks, int32_t drain_threads) {
   if (!r || !cache) return KVX_EINVAL;
+  if (r->async_busy.load()) return KVX_EBUSY;
   try {
     std::vector<kvx::HostChunk> v;
     kvx_status st = host_chunks(chunks, n_chunks, &v);
@@ -1236,6 +1285,7 @@ kvx_status kvx_ring_bind_files(kvx_ring* r, const kvx_cache* cache, int32_t l0, 
                                int32_t chunk_tokens, const kvx_file_chunk* chunks,
                                int32_t n_chunks, int32_t io_depth) {
   if (!r || !cache) return KVX_EINVAL;
+  if (r->async_busy.load()) return KVX_EBUSY;
   try {
     return bind_files(r, Dir::kRestore, cache, l0, l1, chunk_tokens, chunks, n_chunks, io_depth);
   } catch (...) {
@@ -1248,6 +1298,7 @@ kvx_status kvx_ring_bind_offload_files(kvx_ring* r, const kvx_cache* cache, int3
                                        const kvx_file_chunk* chunks, int32_t n_chunks,
                                        int32_t io_depth) {
   if (!r || !cache) return KVX_EINVAL;
+  if (r->async_busy.load()) return KVX_EBUSY;
   try {
     return bind_files(r, Dir::kOffload, cache, l0, l1, chunk_tokens, chunks, n_chunks, io_depth);
   } catch (...) {
@@ -1258,6 +1309,7 @@ kvx_status kvx_ring_bind_offload_files(kvx_ring* r, const kvx_cache* cache, int3
 kvx_status kvx_restore_from_staging(kvx_ring* ring, const int32_t* block_table,
                                     hipStream_t stream) {
   if (!ring) return KVX_EINVAL;
+  if (ring->async_busy.load()) return KVX_EBUSY;
   try {
     return run(ring, Dir::kRestore, block_table, stream);
   } catch (...) {
@@ -1267,6 +1319,7 @@ kvx_status kvx_restore_from_staging(kvx_ring* ring, const int32_t* block_table,
 
 kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hipStream_t stream) {
   if (!ring) return KVX_EINVAL;
+  if (ring->async_busy.load()) return KVX_EBUSY;
   try {
     return run(ring, Dir::kOffload, block_table, stream);
   } catch (...) {
@@ -1274,8 +1327,51 @@ kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hi
   }
 }
 
+kvx_status kvx_offload_begin(kvx_ring* ring, const int32_t* block_table, hipStream_t stream) {
+  if (!ring) return KVX_EINVAL;
+  if (ring->async_busy.load()) return KVX_EBUSY;
+  if (ring->dir != Dir::kOffload) return KVX_EINVAL;
+  if (ring->closed.load()) return KVX_ECLOSED;
+  if (!block_table && !ring->plan.pieces.empty()) return KVX_EINVAL;
+  try {
+    DeviceGuard dg(ring->device);
+    if (!dg.ok) return KVX_EHIP;
+    if (!ring->store_stream && !make_store_stream(ring)) return KVX_EHIP;
+    // the gathers follow the work already enqueued on the caller's stream
+    if (hipEventRecord(ring->store_begin, stream) != hipSuccess ||
+        hipStreamWaitEvent(ring->store_stream, ring->store_begin, 0) != hipSuccess)
+      return KVX_EHIP;
+    hipStream_t gather_stream = ring->store_stream;
+    ring->async_status = KVX_OK;
+    ring->async_busy.store(true);
+    ring->async_th = std::thread([ring, block_table, gather_stream] {
+      kvx_status st;
+      try {
+        st = run(ring, Dir::kOffload, block_table, gather_stream);
+      } catch (...) {
+        st = KVX_EINTERNAL;
+      }
+      ring->async_status = st;
+    });
+    return KVX_OK;
+  } catch (...) {
+    ring->async_busy.store(false);
+    return KVX_EINTERNAL;
+  }
+}
+
+kvx_status kvx_offload_wait(kvx_ring* ring) {
+  if (!ring) return KVX_EINVAL;
+  if (!ring->async_busy.load()) return KVX_OK;
+  if (ring->async_th.joinable()) ring->async_th.join();
+  const kvx_status st = ring->async_status;
+  ring->async_busy.store(false);
+  return st;
+}
+
 kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t flags) {
   if (!ring || max_delay_us < 0 || max_delay_us > 1000000 || (flags & ~3)) return KVX_EINVAL;
+  if (ring->async_busy.load()) return KVX_EBUSY;
   const bool hip_copies = (flags & 2) != 0;
   if (hip_copies != ring->hook_hip_copies) {
     // A restore through the HIP runtime returns with copies still in flight;
@@ -1296,6 +1392,7 @@ kvx_status kvx_ring_set_test_hooks(kvx_ring* ring, int32_t max_delay_us, int32_t
 
 kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out) {
   if (!ring || !out) return KVX_EINVAL;
+  if (ring->async_busy.load()) return KVX_EBUSY;
   *out = ring->stats;
   return KVX_OK;
 }
@@ -1309,6 +1406,7 @@ kvx_status kvx_ring_abort(kvx_ring* ring) {
 
 kvx_status kvx_ring_destroy(kvx_ring* ring) {
   if (!ring) return KVX_OK;
+  if (ring->async_th.joinable()) ring->async_th.join();  // a deferred store still running
   try {
     DeviceGuard dg(ring->device);
     destroy_resources(ring);
