@@ -452,6 +452,8 @@ typedef struct kvx_preload_stats {
   int64_t hits_inflight;   /* of those, joined a speculative read in progress */
   int64_t demand_reads;    /* files whose read completed as demand work */
   int64_t evictions;       /* staged files whose slot was taken for another file */
+  int64_t spec_preempted;  /* speculative reads stopped to give their slot to a demand file
+                              (the file is queued to be read again) */
   int64_t bytes_read;      /* file bytes read into the pool */
   int64_t staged;          /* files staged now */
   int64_t held;            /* files held by fetches now */
@@ -472,7 +474,9 @@ kvx_status kvx_preloader_create(int32_t n_slots, int64_t slot_bytes, int32_t io_
 kvx_status kvx_preload_hint(kvx_preloader* p, const char* const* paths, int32_t n);
 
 /* Demand: make every named file staged (claiming staged images, joining reads
- * in progress, reading the rest before any speculative work) and hold it:
+ * in progress, reading the rest before any speculative work; a file that
+ * finds no slot takes that of a staged image nobody holds, else stops a
+ * speculative read and takes its slot) and hold it:
  * images[i] / sizes[i] receive the host address and byte size of paths[i]'s
  * image, valid until kvx_preload_release. Blocks until all are staged.
  * KVX_ENOMEM if the files held after the call would exceed n_slots (nothing is
@@ -492,6 +496,11 @@ kvx_status kvx_preload_stats_get(kvx_preloader* p, kvx_preload_stats* out);
 
 /* Stop the reactor (reads in flight complete first) and free the pool. */
 kvx_status kvx_preloader_destroy(kvx_preloader* p);
+
+/* Testing hook: the reactor pauses delay_us (0 .. 1000000; else KVX_EINVAL)
+ * after each batch of completed pieces, which holds reads in progress long
+ * enough for a test to act in the middle of one. Off (0) by default. */
+kvx_status kvx_preload_set_test_hooks(kvx_preloader* p, int32_t delay_us);
 
 /* Fault-injection hooks for testing the slot-reuse protocol from the host.
  * max_delay_us > 0: each fill or drain thread pauses a pseudo-random 0 ..

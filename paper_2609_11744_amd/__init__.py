@@ -565,6 +565,11 @@ class Preloader:
     def wait_idle(self) -> None:
         _ok(_native.lib().kvx_preload_wait_idle(self.handle), "kvx_preload_wait_idle")
 
+    def set_test_hooks(self, delay_us: int = 0) -> None:
+        """Pause the reactor delay_us after each batch of completed pieces."""
+        _ok(_native.lib().kvx_preload_set_test_hooks(self.handle, delay_us),
+            "kvx_preload_set_test_hooks")
+
     def stats(self) -> dict:
         s = _native.KvxPreloadStats()
         _ok(_native.lib().kvx_preload_stats_get(self.handle, ctypes.byref(s)),

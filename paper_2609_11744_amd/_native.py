@@ -48,7 +48,8 @@ class KvxFileIo(ctypes.Structure):
 class KvxPreloadStats(ctypes.Structure):
     _fields_ = [(n, c_i64) for n in ("hints", "spec_deduped", "spec_dropped", "spec_reads",
                                      "demand_fetches", "hits_ready", "hits_inflight",
-                                     "demand_reads", "evictions", "bytes_read", "staged", "held")]
+                                     "demand_reads", "evictions", "spec_preempted", "bytes_read",
+                                     "staged", "held")]
 
 
 class KvxCurve(ctypes.Structure):
@@ -119,6 +120,7 @@ SIGNATURES = {
     "kvx_preload_release": (ctypes.c_int, [c_vp, ctypes.POINTER(ctypes.c_char_p), c_i32]),
     "kvx_preload_wait_idle": (ctypes.c_int, [c_vp]),
     "kvx_preload_stats_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxPreloadStats)]),
+    "kvx_preload_set_test_hooks": (ctypes.c_int, [c_vp, c_i32]),
     "kvx_preloader_destroy": (ctypes.c_int, [c_vp]),
     "kvx_pinned_alloc": (ctypes.c_int, [c_i64, ctypes.POINTER(c_vp)]),
     "kvx_pinned_free": (ctypes.c_int, [c_vp]),

@@ -8,6 +8,11 @@
 //     file has pieces left to issue, so a demand arriving in the middle of a
 //     speculative read takes the engine from it at the next piece (the
 //     speculative file keeps what it has read and resumes later);
+//   * a demand file that finds no slot (none free, no staged image nobody
+//     holds) takes one from speculation: if no speculative file has all its
+//     pieces issued (which soon frees a slot by staging), the speculative
+//     file with the least read stops, hands its slot over once its pieces in
+//     flight have landed and is queued to be read again later;
 //   * one speculative preload at a time: the files of one hint call (one
 //     waiting request) are read concurrently, and the next hint call's files
 //     start only when none of them is left; speculative reads take only
@@ -20,13 +25,15 @@
 //     holds (least recently used first), but never that of a preloaded image
 //     not yet fetched; a demand fetch may take either (cached images first).
 // A file is read in pieces of kPiece bytes into its slot, with at most
-// io_depth pieces in flight. Slots are host memory (pinned for the staged
+// io_depth pieces in flight (without io_uring, where each piece is read inside
+// the issuing call, at most io_depth pieces per hold of the lock). Slots are host memory (pinned for the staged
 // restore; plain for host-only use).
 #include <hip/hip_runtime_api.h>
 #include <sys/stat.h>
 #include <unistd.h>
 
 #include <algorithm>
+#include <chrono>
 #include <condition_variable>
 #include <cstdlib>
 #include <deque>
@@ -60,6 +67,7 @@ struct Entry {
   kvx::TierFile file;
   int64_t pieces = 0, issued = 0, completed = 0, inflight = 0;
   bool io_error = false;
+  bool preempted = false;  // gives its slot to demand once its pieces in flight land
 };
 
 }  // namespace
@@ -84,6 +92,7 @@ struct kvx_preloader {
   uint64_t groups = 0;          // hint calls so far
   std::vector<int32_t> free_slots;
   uint64_t clock = 0;
+  int32_t test_delay_us = 0;  // kvx_preload_set_test_hooks
   kvx_preload_stats stats{};
   std::thread reactor;
 };
@@ -175,11 +184,47 @@ void finish_entry(kvx_preloader* p, Entry* e, bool ok) {
   p->cv_done.notify_all();
 }
 
+// A preempted speculative entry whose pieces have all landed: its slot is
+// freed and it is queued to be read again from the start, ahead of the
+// speculative files not yet started.
+void requeue_preempted(kvx_preloader* p, Entry* e) {
+  kvx::close_tier_file(&e->file);
+  p->free_slots.push_back(e->slot);
+  e->slot = -1;
+  e->st = St::kQueued;
+  e->preempted = false;
+  e->io_error = false;
+  e->size = e->pieces = e->issued = e->completed = 0;
+  p->spec_q.push_front(e);
+}
+
+// A demand file found no slot. If a speculative file has all its pieces
+// issued, it is staged soon and then gives up its slot: wait for that.
+// Otherwise stop the speculative file with the least read. True if that
+// freed a slot at once (nothing of it was in flight).
+bool preempt_for_demand(kvx_preloader* p) {
+  Entry* pick = nullptr;
+  for (Entry* e : p->spec_reading) {
+    if (e->issued == e->pieces) return false;
+    if (!pick || e->completed < pick->completed) pick = e;
+  }
+  if (!pick) return false;
+  ++p->stats.spec_preempted;
+  p->spec_reading.erase(std::remove(p->spec_reading.begin(), p->spec_reading.end(), pick),
+                        p->spec_reading.end());
+  if (pick->inflight > 0) {
+    pick->preempted = true;
+    return false;
+  }
+  requeue_preempted(p, pick);
+  return true;
+}
+
 // Issue pieces (under the lock) while the engine has room: demand entries
 // first, then the active speculative entry, then a new speculative entry.
 void schedule(kvx_preloader* p, kvx::IoEngine* io) {
   auto issue = [&](Entry* e) {
-    while (io->inflight() < io->depth() && e->issued < e->pieces && e->st == St::kReading) {
+    while (io->pending() < io->depth() && e->issued < e->pieces && e->st == St::kReading) {
       const int64_t off = e->issued * kPiece;
       const int64_t len = std::min(kPiece, e->size - off);
       if (io->start(&e->file, p->pool + (int64_t)e->slot * p->slot_bytes + off, off, len,
@@ -194,12 +239,23 @@ void schedule(kvx_preloader* p, kvx::IoEngine* io) {
     if (e->issued == e->pieces && e->inflight == 0 && e->st == St::kReading)
       finish_entry(p, e, !e->io_error && e->completed == e->pieces);
   };
-  // demand
-  while (!p->demand_q.empty() && io->inflight() < io->depth()) {
-    Entry* e = p->demand_q.front();
+  // demand, slots in arrival order; the demand files already being read go
+  // on while an earlier one waits for a slot
+  bool waiting = false;
+  for (size_t i = 0; i < p->demand_q.size() && io->pending() < io->depth();) {
+    Entry* e = p->demand_q[i];
     if (e->st == St::kQueued) {
-      const int32_t s = take_slot(p, true);
-      if (s < 0) break;  // every slot held or being read: wait for a completion
+      if (waiting) {
+        ++i;
+        continue;
+      }
+      int32_t s = take_slot(p, true);
+      if (s < 0 && preempt_for_demand(p)) s = take_slot(p, true);
+      if (s < 0) {  // wait for a completion or a release
+        waiting = true;
+        ++i;
+        continue;
+      }
       e->slot = s;
       if (!open_entry(p, e)) {
         finish_entry(p, e, false);  // leaves the demand queue
@@ -208,18 +264,19 @@ void schedule(kvx_preloader* p, kvx::IoEngine* io) {
       e->st = St::kReading;
     }
     issue(e);  // (a failure inside removes e from the queue itself)
-    if (!p->demand_q.empty() && p->demand_q.front() == e &&
-        (e->st != St::kReading || e->issued == e->pieces))
-      p->demand_q.pop_front();
+    if (i < p->demand_q.size() && p->demand_q[i] == e) {
+      if (e->st != St::kReading || e->issued == e->pieces) p->demand_q.erase(p->demand_q.begin() + (long)i);
+      else ++i;
+    }
   }
   if (!p->demand_q.empty()) return;  // demand first
   // speculative: the active preload's files being read, then more of its files
-  for (size_t i = 0; i < p->spec_reading.size() && io->inflight() < io->depth();) {
+  for (size_t i = 0; i < p->spec_reading.size() && io->pending() < io->depth();) {
     Entry* e = p->spec_reading[i];
     issue(e);  // (finishing removes e from spec_reading)
     if (i < p->spec_reading.size() && p->spec_reading[i] == e) ++i;
   }
-  while (!p->spec_q.empty() && io->inflight() < io->depth()) {
+  while (!p->spec_q.empty() && io->pending() < io->depth()) {
     Entry* e = p->spec_q.front();
     if (e->st != St::kQueued || e->demand) {  // claimed by a demand in the meantime
       p->spec_q.pop_front();
@@ -240,22 +297,21 @@ void schedule(kvx_preloader* p, kvx::IoEngine* io) {
   }
 }
 
-// Whether the front demand entry can make progress now: it is being read,
-// or a slot is free or held by a staged file nobody holds.
-bool demand_can_run(kvx_preloader* p) {
-  if (p->demand_q.empty()) return false;
-  if (p->demand_q.front()->st != St::kQueued || !p->free_slots.empty()) return true;
-  return victim_of(p, true) != nullptr;
-}
-
 // Whether a speculative read could get a slot now.
 bool spec_slot_available(kvx_preloader* p) {
   return (int32_t)p->free_slots.size() > p->reserve || victim_of(p, false) != nullptr;
 }
 
+// Whether schedule() can make progress now (called with nothing in flight).
 bool has_work(kvx_preloader* p) {
-  if (demand_can_run(p)) return true;
-  if (!p->demand_q.empty()) return false;  // demand waits for a slot; speculative work waits too
+  if (!p->demand_q.empty()) {
+    for (Entry* e : p->demand_q)
+      if (e->st != St::kQueued) return true;  // pieces to issue, or an entry to drop
+    // a demand file waits for a slot: a free one, a staged image to evict or
+    // a speculative read to stop (with nothing in flight, every speculative
+    // file being read has pieces left)
+    return !p->free_slots.empty() || victim_of(p, true) != nullptr || !p->spec_reading.empty();
+  }
   for (Entry* e : p->spec_reading)
     if (e->issued < e->pieces) return true;
   if (p->spec_q.empty()) return false;
@@ -283,10 +339,12 @@ void reactor_main(kvx_preloader* p) {
       p->cv_work.wait(lock, [&] { return p->stop || has_work(p); });
       continue;
     }
+    const int32_t delay_us = p->test_delay_us;
     lock.unlock();
     done.clear();
     failed.clear();
     const kvx_status st = io.wait(&done, &failed);
+    if (delay_us > 0) std::this_thread::sleep_for(std::chrono::microseconds(delay_us));
     lock.lock();
     for (uint64_t t : failed) {
       Entry* e = reinterpret_cast<Entry*>((uintptr_t)t);
@@ -299,15 +357,13 @@ void reactor_main(kvx_preloader* p) {
       --e->inflight;
       ++e->completed;
     }
-    for (uint64_t t : failed) {
-      Entry* e = reinterpret_cast<Entry*>((uintptr_t)t);
-      if (e->inflight == 0 && e->st == St::kReading) finish_entry(p, e, false);
-    }
-    for (uint64_t t : done) {
-      Entry* e = reinterpret_cast<Entry*>((uintptr_t)t);
-      if (e->inflight == 0 && e->issued == e->pieces && e->st == St::kReading)
-        finish_entry(p, e, !e->io_error && e->completed == e->pieces);
-    }
+    for (std::vector<uint64_t>* tags : {&failed, &done})
+      for (uint64_t t : *tags) {
+        Entry* e = reinterpret_cast<Entry*>((uintptr_t)t);
+        if (e->inflight != 0 || e->st != St::kReading) continue;
+        if (e->preempted) requeue_preempted(p, e);
+        else if (e->issued == e->pieces) finish_entry(p, e, !e->io_error && e->completed == e->pieces);
+      }
     if (st != KVX_OK) {
       // the engine itself failed (not a transfer): fail everything being read
       // and stop; the engine's teardown waits for what is still in flight
@@ -457,6 +513,7 @@ kvx_status kvx_preload_fetch(kvx_preloader* p, const char* const* paths, int32_t
           ++p->stats.hits_inflight;
           if (e->issued < e->pieces) p->demand_q.push_back(e);  // its remaining pieces now have priority
           e->demand = true;
+          e->preempted = false;  // stopped for another demand file: it keeps its slot after all
           p->spec_reading.erase(
               std::remove(p->spec_reading.begin(), p->spec_reading.end(), e),
               p->spec_reading.end());
@@ -552,6 +609,13 @@ kvx_status kvx_preload_wait_idle(kvx_preloader* p) {
     return !queued || !spec_slot_available(p);
   });
   return p->engine_failed ? KVX_EIO : KVX_OK;
+}
+
+kvx_status kvx_preload_set_test_hooks(kvx_preloader* p, int32_t delay_us) {
+  if (!p || delay_us < 0 || delay_us > 1000000) return KVX_EINVAL;
+  std::lock_guard<std::mutex> lock(p->mu);
+  p->test_delay_us = delay_us;
+  return KVX_OK;
 }
 
 kvx_status kvx_preloader_destroy(kvx_preloader* p) {

@@ -6,6 +6,7 @@ for demand, and the error paths. Pools here are plain host memory (no GPU);
 every case runs on io_uring and on the synchronous fallback
 (KVX_IO_NO_URING=1)."""
 import threading
+import time
 
 import numpy as np
 import pytest
@@ -275,5 +276,56 @@ def test_invalid_arguments(tmp_path):
             p.hint([""])
         with pytest.raises(kvx.KvxError):
             p.fetch([""])
+    finally:
+        p.close()
+
+
+def test_demand_preempts_a_speculative_read_holding_the_last_slot(tmp_path, engine):
+    # One slot, taken by a speculative read with pieces still to issue: the
+    # demand file takes it over once the pieces in flight have landed, and the
+    # speculative file is read again after the demand image is released.
+    files = _files(tmp_path, [64 << 20, 1 << 20], seed=11)  # 4 pieces, 1 piece
+    (a, data_a), (b, data_b) = files
+    p = _pre(n_slots=1, slot_bytes=64 << 20, io_depth=1)
+    got = {}
+    try:
+        p.set_test_hooks(delay_us=50000)  # each piece takes >= 50 ms
+        p.hint([a])
+        time.sleep(0.06)                  # a's read has started; pieces remain
+        th = threading.Thread(target=lambda: got.setdefault("b", p.fetch([b])))
+        th.start()
+        th.join(timeout=30)
+        assert "b" in got, "the demand fetch never got the slot"
+        assert np.array_equal(got["b"][0], data_b)
+        st = p.stats()
+        assert st["spec_preempted"] == 1 and st["demand_reads"] == 1
+        assert st["spec_reads"] == 0 and st["evictions"] == 0
+        p.set_test_hooks(delay_us=0)
+        p.release([b])                    # b is cached now: a takes its slot
+        p.wait_idle()
+        st = p.stats()
+        assert st["spec_reads"] == 1 and st["evictions"] == 1 and st["staged"] == 1
+        (img_a,) = p.fetch([a])
+        assert np.array_equal(img_a, data_a) and p.stats()["hits_ready"] == 1
+        p.release([a])
+    finally:
+        p.close()
+
+
+def test_demand_waits_for_a_speculative_read_about_to_stage(tmp_path, engine):
+    # Every piece of the speculative file is already issued: it is staged,
+    # then evicted for the demand file, and nothing is preempted.
+    files = _files(tmp_path, [2 << 20, 1 << 20], seed=12)  # one piece each
+    (a, _), (b, data_b) = files
+    p = _pre(n_slots=1, io_depth=2)
+    try:
+        p.set_test_hooks(delay_us=50000)
+        p.hint([a])
+        time.sleep(0.02)                  # a's only piece is in flight
+        (img_b,) = p.fetch([b])
+        assert np.array_equal(img_b, data_b)
+        st = p.stats()
+        assert st["spec_preempted"] == 0 and st["spec_reads"] == 1 and st["evictions"] == 1
+        p.release([b])
     finally:
         p.close()
