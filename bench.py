@@ -805,8 +805,8 @@ def run_preload(args):
     reps = max(3, args.steps)
     probe = probes(dev, 5)
     reserve = args.io_depth
-    res = {"demand": [], "preloaded": [], "half": []}
-    read_s, half_stats, pre_stats = [], None, None
+    res = {"demand": [], "preloaded": [], "half": [], "half_overlapped": [], "pool_demand": []}
+    read_s, mode_stats = [], {}
     try:
         ring = kvx.StagingRing(dev, args.slots, args.slot_mib << 20)
         try:
@@ -837,26 +837,39 @@ def run_preload(args):
                 pre.release(paths)
                 return dt
 
+            def request_overlapped(pre):
+                """The request path through a ring bound to the preloader: the
+                restore holds the files and copies each piece as soon as its
+                files are staged, while the rest are still being read."""
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                ring.bind_preloaded(cache, 0, L, ct, pre, chunks)
+                kvx.kvx_restore_from_staging(ring, bt_dst)
+                torch.cuda.synchronize()
+                return time.perf_counter() - t0
+
             half = statistics.median(res["demand"]) / 2
-            for _ in range(reps):
-                for mode in ("preloaded", "half"):
+            for rep_i in range(reps):
+                for mode in ("preloaded", "half", "half_overlapped", "pool_demand"):
                     pre = kvx.Preloader(len(paths) + reserve, chunk_bytes, io_depth=args.io_depth,
                                         reserve=reserve, pinned=True)
                     try:
                         t0 = time.perf_counter()
-                        pre.hint(paths)  # the request is still waiting
+                        if mode != "pool_demand":
+                            pre.hint(paths)  # the request is still waiting
                         if mode == "preloaded":
                             pre.wait_idle()
                             read_s.append(time.perf_counter() - t0)
-                        else:
+                        elif mode != "pool_demand":
                             time.sleep(half)
-                        res[mode].append(request(pre))
-                        if mode == "preloaded":
-                            pre_stats = pre.stats()
+                        if mode in ("preloaded", "half"):
+                            res[mode].append(request(pre))
                         else:
-                            half_stats = pre.stats()
+                            res[mode].append(request_overlapped(pre))
+                        mode_stats[mode] = pre.stats()
                     finally:
                         pre.close()
+                log(f"preload repetition {rep_i + 1} of {reps} done")
             kvx.kvx_check()
         finally:
             ring.close()
@@ -876,16 +889,20 @@ def run_preload(args):
         "request_path_ms": {k: round(v * 1e3, 2) for k, v in med.items()},
         "speedup_preloaded_vs_demand": round(med["demand"] / med["preloaded"], 2),
         "speedup_half_vs_demand": round(med["demand"] / med["half"], 2),
+        "speedup_half_overlapped_vs_demand": round(med["demand"] / med["half_overlapped"], 2),
         "preloaded_restore_GBps": round(payload / med["preloaded"] / 1e9, 2),
         "preloaded_frac_of_h2d": round(payload / med["preloaded"] / 1e9 / probe["h2d_GBps"], 4),
         "demand_restore_GBps": round(payload / med["demand"] / 1e9, 2),
         "preload_read_GBps": round(payload / statistics.median(read_s) / 1e9, 2),
-        "stats_preloaded": pre_stats, "stats_half": half_stats,
+        "stats": mode_stats,
         "probes": {"h2d_GBps": round(probe["h2d_GBps"], 2)}, "reps": reps,
         "note": "each request path starts from files whose pages were dropped from the page "
                 "cache; 'half' starts the request after half the demand restore time of "
                 "preloading, so its fetch claims what is staged, joins what is being read and "
-                "reads the rest on demand before the restore"})
+                "reads the rest on demand before the restore; 'half_overlapped' starts at the "
+                "same time but restores through a ring bound to the preloader, copying each "
+                "piece as soon as its files are staged; 'pool_demand' does the same with "
+                "nothing hinted (every file read on demand, overlapped with the copies)"})
     print(json.dumps(out), flush=True)
 
 

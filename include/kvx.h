@@ -489,6 +489,25 @@ kvx_status kvx_preload_fetch(kvx_preloader* p, const char* const* paths, int32_t
  * not held). Released images stay staged until their slot is needed. */
 kvx_status kvx_preload_release(kvx_preloader* p, const char* const* paths, int32_t n);
 
+/* Bind the next restores of `ring` to chunk files held in preloader p's pool
+ * (pinned; else KVX_EINVAL), with the chunk list of kvx_ring_bind_files
+ * (paths copied; a path may name several chunks of one size). Each
+ * kvx_restore_from_staging then holds every named file as kvx_preload_fetch
+ * does (claiming staged images, joining reads in progress, reading the rest
+ * as demand work in chunk order; KVX_ENOMEM as for the fetch, nothing held)
+ * but does not wait for all of them: a piece's host-to-device copies run
+ * straight out of the pool as soon as its files are staged, while the later
+ * files are still being read (Sec. 6.5: the demand load claims what the
+ * preload staged and joins what it is reading). The restore returns once
+ * every copy out of the pool has landed and drops its holds (the images stay
+ * staged as cached images). A file that cannot be read, or whose size is not
+ * its chunk's image size ((l1 - l0) * 2 * n_blocks * slab bytes), makes the
+ * restore return KVX_EIO (pieces already scattered stay scattered). p must
+ * outlive the binding. */
+kvx_status kvx_ring_bind_preloaded(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int32_t l1,
+                                   int32_t chunk_tokens, kvx_preloader* p,
+                                   const kvx_file_chunk* chunks, int32_t n_chunks);
+
 /* Block until no read is in progress and no queued hint can start. */
 kvx_status kvx_preload_wait_idle(kvx_preloader* p);
 

@@ -408,6 +408,18 @@ class StagingRing:
         self._source, self._cache = keep, cache
         self.n_blocks = max((bt0 + nb for _, bt0, nb in chunks), default=0)
 
+    def bind_preloaded(self, cache, l0, l1, chunk_tokens, preloader, chunks):
+        """Restore binding over chunk files [(path, bt_offset, n_blocks)] held in a
+        preloader's pool: each restore holds the files and copies every piece as
+        soon as its files are staged."""
+        arr, keep = self._file_chunks(chunks)
+        _ok(_native.lib().kvx_ring_bind_preloaded(self.handle, ctypes.byref(cache.c_struct()), l0,
+                                                  l1, chunk_tokens, preloader.handle, arr,
+                                                  len(chunks)),
+            "kvx_ring_bind_preloaded")
+        self._source, self._cache = (keep, preloader), cache
+        self.n_blocks = max((bt0 + nb for _, bt0, nb in chunks), default=0)
+
     def stats(self) -> dict:
         s = KvxRingStats()
         _ok(_native.lib().kvx_ring_stats_get(self.handle, ctypes.byref(s)), "kvx_ring_stats_get")

@@ -121,6 +121,8 @@ SIGNATURES = {
     "kvx_preload_wait_idle": (ctypes.c_int, [c_vp]),
     "kvx_preload_stats_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxPreloadStats)]),
     "kvx_preload_set_test_hooks": (ctypes.c_int, [c_vp, c_i32]),
+    "kvx_ring_bind_preloaded": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32,
+                                               c_vp, ctypes.POINTER(KvxFileChunk), c_i32]),
     "kvx_preloader_destroy": (ctypes.c_int, [c_vp]),
     "kvx_pinned_alloc": (ctypes.c_int, [c_i64, ctypes.POINTER(c_vp)]),
     "kvx_pinned_free": (ctypes.c_int, [c_vp]),

@@ -33,6 +33,7 @@
 #include <unistd.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <condition_variable>
 #include <cstdlib>
@@ -43,10 +44,12 @@
 #include <string>
 #include <thread>
 #include <unordered_map>
+#include <unordered_set>
 #include <vector>
 
 #include "kvx.h"
 #include "kvx_io.h"
+#include "kvx_preload.h"
 
 namespace {
 
@@ -112,6 +115,14 @@ void forget(kvx_preloader* p, Entry* e) {
   kvx::close_tier_file(&e->file);
   const std::string path = e->path;
   p->entries.erase(path);
+}
+
+// Forget a failed entry nobody holds, freeing the slot it may still have (an
+// image discarded as not matching what its holder expected).
+void drop_failed(kvx_preloader* p, Entry* e) {
+  if (e->slot >= 0) p->free_slots.push_back(e->slot);
+  e->slot = -1;
+  forget(p, e);
 }
 
 // The least recently used staged entry nobody holds: a cached one (fetched
@@ -386,6 +397,89 @@ bool valid_paths(const char* const* paths, int32_t n) {
   return true;
 }
 
+// The distinct paths, in the order of their first occurrence.
+std::vector<std::string> distinct(const char* const* paths, int32_t n) {
+  std::vector<std::string> out;
+  std::unordered_set<std::string> seen;
+  for (int32_t i = 0; i < n; ++i)
+    if (seen.insert(paths[i]).second) out.emplace_back(paths[i]);
+  return out;
+}
+
+// Hold each of the distinct files (all or none), in order: staged images are
+// claimed, speculative reads in progress joined (their remaining pieces become
+// demand), queued hints promoted, other files queued as demand reads. Called
+// with the lock held; KVX_ENOMEM if the files held afterwards would exceed the
+// pool, KVX_EIO if a file failed and is still held or draining elsewhere.
+kvx_status hold_locked(kvx_preloader* p, const std::vector<std::string>& uniq,
+                       std::vector<Entry*>* out) {
+  if (p->engine_failed) return KVX_EIO;
+  int32_t held = 0, held_here = 0;
+  for (auto& kv : p->entries)
+    if (kv.second->claims > 0) ++held;
+  for (const auto& path : uniq) {
+    auto it = p->entries.find(path);
+    if (it != p->entries.end() && it->second->claims > 0) ++held_here;
+  }
+  if (held + (int32_t)uniq.size() - held_here > p->n_slots) return KVX_ENOMEM;
+  std::vector<Entry*> es;
+  for (const auto& path : uniq) {
+    auto it = p->entries.find(path);
+    Entry* e;
+    if (it == p->entries.end() || it->second->st == St::kFailed) {
+      // a failed entry another holder still holds, or whose reads still
+      // drain, is left alone: that holder reports the failure
+      if (it != p->entries.end() && (it->second->inflight > 0 || it->second->claims > 0)) {
+        for (Entry* h : es) --h->claims;
+        return KVX_EIO;
+      }
+      if (it != p->entries.end()) drop_failed(p, it->second.get());  // a failed entry nobody holds
+      auto ne = std::make_unique<Entry>();
+      ne->path = path;
+      e = ne.get();
+      p->entries[path] = std::move(ne);
+      e->demand = true;
+      p->demand_q.push_back(e);
+    } else {
+      e = it->second.get();
+      if (e->st == St::kReady) {
+        ++p->stats.hits_ready;
+      } else if (e->st == St::kReading && !e->demand) {
+        ++p->stats.hits_inflight;
+        if (e->issued < e->pieces) p->demand_q.push_back(e);  // its remaining pieces now have priority
+        e->demand = true;
+        e->preempted = false;  // stopped for another demand file: it keeps its slot after all
+        p->spec_reading.erase(std::remove(p->spec_reading.begin(), p->spec_reading.end(), e),
+                              p->spec_reading.end());
+      } else if (e->st == St::kQueued && !e->demand) {
+        e->demand = true;  // a hinted file not yet started: read it now
+        for (auto q = p->spec_q.begin(); q != p->spec_q.end();)
+          q = *q == e ? p->spec_q.erase(q) : q + 1;
+        p->demand_q.push_back(e);
+      }
+    }
+    ++e->claims;
+    e->used = true;
+    es.push_back(e);
+  }
+  p->stats.demand_fetches += (int64_t)uniq.size();
+  p->cv_work.notify_one();
+  *out = std::move(es);
+  return KVX_OK;
+}
+
+// Drop one hold of each entry (distinct, each held). Failed entries nobody
+// holds any more are forgotten, so that a later fetch reads them again.
+void unhold_locked(kvx_preloader* p, const std::vector<Entry*>& es) {
+  for (Entry* e : es) {
+    --e->claims;
+    e->last_use = ++p->clock;
+  }
+  for (Entry* e : es)
+    if (e->st == St::kFailed && e->claims == 0 && e->inflight == 0) drop_failed(p, e);
+  p->cv_work.notify_one();
+}
+
 }  // namespace
 
 extern "C" {
@@ -452,7 +546,7 @@ kvx_status kvx_preload_hint(kvx_preloader* p, const char* const* paths, int32_t 
         ++p->stats.spec_dropped;
         continue;
       }
-      if (it != p->entries.end()) forget(p, it->second.get());  // a failed entry nobody holds
+      if (it != p->entries.end()) drop_failed(p, it->second.get());  // a failed entry nobody holds
       auto e = std::make_unique<Entry>();
       e->path = path;
       e->group = group;
@@ -472,64 +566,9 @@ kvx_status kvx_preload_fetch(kvx_preloader* p, const char* const* paths, int32_t
   if (!p || !valid_paths(paths, n) || (n > 0 && (!images || !sizes))) return KVX_EINVAL;
   try {
     std::unique_lock<std::mutex> lock(p->mu);
-    if (p->engine_failed) return KVX_EIO;
-    // distinct files of this fetch, and whether the pool can hold them
-    std::vector<std::string> want;
-    for (int32_t i = 0; i < n; ++i) want.emplace_back(paths[i]);
-    std::vector<std::string> uniq = want;
-    std::sort(uniq.begin(), uniq.end());
-    uniq.erase(std::unique(uniq.begin(), uniq.end()), uniq.end());
-    int32_t held = 0, held_here = 0;
-    for (auto& kv : p->entries)
-      if (kv.second->claims > 0) ++held;
-    for (const auto& path : uniq) {
-      auto it = p->entries.find(path);
-      if (it != p->entries.end() && it->second->claims > 0) ++held_here;
-    }
-    if (held + (int32_t)uniq.size() - held_here > p->n_slots) return KVX_ENOMEM;
     std::vector<Entry*> es;
-    for (const auto& path : uniq) {
-      auto it = p->entries.find(path);
-      Entry* e;
-      if (it == p->entries.end() || it->second->st == St::kFailed) {
-        // a failed entry another fetch still holds, or whose reads still
-        // drain, is left alone: that fetch reports the failure
-        if (it != p->entries.end() && (it->second->inflight > 0 || it->second->claims > 0)) {
-          for (Entry* h : es) --h->claims;
-          return KVX_EIO;
-        }
-        if (it != p->entries.end()) forget(p, it->second.get());  // a failed entry nobody holds
-        auto ne = std::make_unique<Entry>();
-        ne->path = path;
-        e = ne.get();
-        p->entries[path] = std::move(ne);
-        e->demand = true;
-        p->demand_q.push_back(e);
-      } else {
-        e = it->second.get();
-        if (e->st == St::kReady) {
-          ++p->stats.hits_ready;
-        } else if (e->st == St::kReading && !e->demand) {
-          ++p->stats.hits_inflight;
-          if (e->issued < e->pieces) p->demand_q.push_back(e);  // its remaining pieces now have priority
-          e->demand = true;
-          e->preempted = false;  // stopped for another demand file: it keeps its slot after all
-          p->spec_reading.erase(
-              std::remove(p->spec_reading.begin(), p->spec_reading.end(), e),
-              p->spec_reading.end());
-        } else if (e->st == St::kQueued && !e->demand) {
-          e->demand = true;  // a hinted file not yet started: read it now
-          for (auto q = p->spec_q.begin(); q != p->spec_q.end();)
-            q = *q == e ? p->spec_q.erase(q) : q + 1;
-          p->demand_q.push_back(e);
-        }
-      }
-      ++e->claims;
-      e->used = true;
-      es.push_back(e);
-    }
-    p->stats.demand_fetches += (int64_t)uniq.size();
-    p->cv_work.notify_one();
+    kvx_status st = hold_locked(p, distinct(paths, n), &es);
+    if (st != KVX_OK) return st;
     p->cv_done.wait(lock, [&] {
       if (p->engine_failed) return true;
       for (Entry* e : es)
@@ -539,16 +578,11 @@ kvx_status kvx_preload_fetch(kvx_preloader* p, const char* const* paths, int32_t
     bool ok = !p->engine_failed;
     for (Entry* e : es) ok = ok && e->st == St::kReady;
     if (!ok) {
-      for (Entry* e : es) --e->claims;
-      // failed entries nobody else holds are forgotten (a later fetch retries)
-      std::vector<Entry*> gone;
-      for (Entry* e : es)
-        if (e->st == St::kFailed && e->claims == 0 && e->inflight == 0) gone.push_back(e);
-      for (Entry* e : gone) forget(p, e);
+      unhold_locked(p, es);
       return KVX_EIO;
     }
     for (int32_t i = 0; i < n; ++i) {
-      const Entry* e = p->entries.at(want[(size_t)i]).get();
+      const Entry* e = p->entries.at(paths[i]).get();
       images[i] = p->pool + (int64_t)e->slot * p->slot_bytes;
       sizes[i] = e->size;
     }
@@ -562,20 +596,13 @@ kvx_status kvx_preload_release(kvx_preloader* p, const char* const* paths, int32
   if (!p || !valid_paths(paths, n)) return KVX_EINVAL;
   try {
     std::lock_guard<std::mutex> lock(p->mu);
-    std::vector<std::string> uniq;
-    for (int32_t i = 0; i < n; ++i) uniq.emplace_back(paths[i]);
-    std::sort(uniq.begin(), uniq.end());
-    uniq.erase(std::unique(uniq.begin(), uniq.end()), uniq.end());
-    for (const auto& path : uniq) {
+    std::vector<Entry*> es;
+    for (const auto& path : distinct(paths, n)) {
       auto it = p->entries.find(path);
       if (it == p->entries.end() || it->second->claims <= 0) return KVX_EINVAL;
+      es.push_back(it->second.get());
     }
-    for (const auto& path : uniq) {
-      Entry* e = p->entries.at(path).get();
-      --e->claims;
-      e->last_use = ++p->clock;
-    }
-    p->cv_work.notify_one();
+    unhold_locked(p, es);
     return KVX_OK;
   } catch (...) {
     return KVX_EINTERNAL;
@@ -634,3 +661,57 @@ kvx_status kvx_preloader_destroy(kvx_preloader* p) {
 }
 
 }  // extern "C"
+
+// ---- holds for a restore that copies each image as soon as it is staged ----
+
+namespace kvx {
+
+bool preload_pinned(const kvx_preloader* p) { return p->pinned; }
+
+kvx_status preload_hold(kvx_preloader* p, const std::vector<std::string>& paths,
+                        std::vector<void*>* handles) {
+  try {
+    std::lock_guard<std::mutex> lock(p->mu);
+    std::vector<Entry*> es;
+    const kvx_status st = hold_locked(p, paths, &es);
+    if (st != KVX_OK) return st;
+    handles->assign(es.begin(), es.end());
+    return KVX_OK;
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}
+
+kvx_status preload_image(kvx_preloader* p, void* handle, bool wait,
+                         const std::atomic<bool>* cancel, uint8_t** image, int64_t* size) {
+  Entry* e = static_cast<Entry*>(handle);
+  std::unique_lock<std::mutex> lock(p->mu);
+  auto settled = [&] { return p->engine_failed || e->st == St::kReady || e->st == St::kFailed; };
+  while (wait && !settled()) {
+    if (cancel && cancel->load()) return KVX_ECLOSED;
+    p->cv_done.wait_for(lock, std::chrono::milliseconds(5), settled);
+  }
+  if (e->st == St::kReady) {
+    *image = p->pool + (int64_t)e->slot * p->slot_bytes;
+    *size = e->size;
+    return KVX_OK;
+  }
+  if (p->engine_failed || e->st == St::kFailed) return KVX_EIO;
+  *image = nullptr;
+  return KVX_OK;
+}
+
+void preload_discard(kvx_preloader* p, void* handle) {
+  std::lock_guard<std::mutex> lock(p->mu);
+  Entry* e = static_cast<Entry*>(handle);
+  if (e->st == St::kReady) e->st = St::kFailed;  // read again by the next holder
+}
+
+void preload_unhold(kvx_preloader* p, const std::vector<void*>& handles) {
+  std::lock_guard<std::mutex> lock(p->mu);
+  std::vector<Entry*> es;
+  for (void* h : handles) es.push_back(static_cast<Entry*>(h));
+  unhold_locked(p, es);
+}
+
+}  // namespace kvx

@@ -50,13 +50,16 @@
 #include <cstring>
 #include <mutex>
 #include <new>
+#include <string>
 #include <thread>
+#include <unordered_map>
 #include <utility>
 #include <vector>
 
 #include "kvx.h"
 #include "kvx_internal.h"
 #include "kvx_io.h"
+#include "kvx_preload.h"
 
 namespace {
 enum class Dir { kNone, kRestore, kOffload };
@@ -121,6 +124,14 @@ struct kvx_ring {
   bool files_mode = false;
   int32_t io_depth = 0;
   std::vector<kvx::TierFile> files;
+
+  // restore out of a preloader's pool (kvx_ring_bind_preloaded): bound chunk c
+  // is the image of file pre_paths[pre_file[c]], held for each restore and
+  // copied to the device as soon as it is staged
+  kvx_preloader* pre = nullptr;
+  std::vector<std::string> pre_paths;  // distinct files, in chunk order
+  std::vector<int32_t> pre_file;       // per bound chunk
+  std::vector<int64_t> pre_bytes;      // per distinct file: its image bytes
 };
 
 namespace {
@@ -577,6 +588,34 @@ kvx_status scatter_copied(kvx_ring* r, int64_t j, const int32_t* bt, hipStream_t
   return hipEventRecord(r->dev_done[(size_t)s], stream) == hipSuccess ? KVX_OK : KVX_EHIP;
 }
 
+// Restore out of a preloader's pool: piece p with the notional addresses of
+// its spans replaced by the images of the held files (imgs caches those already
+// staged). Without `wait`, *ready is false if a file is not staged yet;
+// with it, blocks until every file is (KVX_ECLOSED on an abort meanwhile).
+kvx_status resolve_piece(kvx_ring* r, const kvx::Piece& p, const std::vector<void*>& holds,
+                         std::vector<uint8_t*>* imgs, bool wait, kvx::Piece* out, bool* ready) {
+  *ready = false;
+  *out = p;
+  for (kvx::Span& sp : out->spans) {
+    const int32_t u = r->pre_file[(size_t)span_file(sp)];
+    uint8_t*& img = (*imgs)[(size_t)u];
+    if (!img) {
+      int64_t size = 0;
+      const kvx_status st = kvx::preload_image(r->pre, holds[(size_t)u], wait, &r->closed, &img, &size);
+      if (st != KVX_OK) return st;
+      if (!img) return KVX_OK;
+      if (size != r->pre_bytes[(size_t)u]) {  // not this chunk's image: never use it again
+        kvx::preload_discard(r->pre, holds[(size_t)u]);
+        img = nullptr;
+        return KVX_EIO;
+      }
+    }
+    sp.host = img + span_offset(sp);
+  }
+  *ready = true;
+  return KVX_OK;
+}
+
 kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
   if (r->dir != dir) return KVX_EINVAL;
   if (r->closed.load()) return KVX_ECLOSED;
@@ -598,6 +637,17 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
   std::vector<std::thread> workers;
   kvx_status st = KVX_OK;
   double wait_ms = 0;
+  // restore out of a preloader's pool: hold every file now (those not staged
+  // are read as demand work, in chunk order) and copy each piece once its
+  // files are staged
+  std::vector<void*> holds;
+  std::vector<uint8_t*> imgs;
+  kvx::Piece resolved;
+  if (r->pre) {
+    st = kvx::preload_hold(r->pre, r->pre_paths, &holds);
+    if (st != KVX_OK) return st;
+    imgs.assign(r->pre_paths.size(), nullptr);
+  }
   try {
     if (r->files_mode)
       workers.emplace_back(dir == Dir::kRestore ? file_fill_worker : file_drain_worker, r);
@@ -619,6 +669,24 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
     const kvx::Piece& p = r->plan.pieces[(size_t)i];
     uint8_t* dslot = r->landing + (int64_t)s * r->slot_bytes;
     uint8_t* hslot = r->host + (int64_t)s * r->slot_bytes;
+    const kvx::Piece* pp = &p;  // p, or p resolved to the held images
+    if (dir == Dir::kRestore && r->pre) {
+      bool ready = false;
+      st = resolve_piece(r, p, holds, &imgs, false, &resolved, &ready);
+      if (st == KVX_OK && !ready) {
+        // a file of this piece is still being read: scatter the copied piece
+        // meanwhile, then wait
+        if (copied >= 0) {
+          st = scatter_copied(r, copied, bt, stream);
+          copied = -1;
+        }
+        const auto t0 = clk::now();
+        if (st == KVX_OK) st = resolve_piece(r, p, holds, &imgs, true, &resolved, &ready);
+        wait_ms += ms_since(t0);
+      }
+      if (st != KVX_OK) break;
+      pp = &resolved;
+    }
     if (dir == Dir::kRestore && use_dma(r)) {
       if (T > 0) wait_parts(i);
       if (r->stop.load() || r->closed.load()) {
@@ -637,7 +705,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
         st = KVX_EHIP;
         break;
       }
-      st = issue_dma(r, p, s, dslot, hslot, true);
+      st = issue_dma(r, *pp, s, dslot, hslot, true);
       if (st != KVX_OK) break;
       {
         std::lock_guard<std::mutex> lock(r->mu);
@@ -659,7 +727,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
         ok = ok && hipMemcpyAsync(dslot, hslot, (size_t)p.bytes, hipMemcpyHostToDevice, r->side) ==
                        hipSuccess;
       } else {
-        for (const kvx::Span& sp : p.spans)
+        for (const kvx::Span& sp : pp->spans)
           ok = ok && hipMemcpyAsync(dslot + sp.slot_off, sp.host, (size_t)sp.bytes,
                                     hipMemcpyHostToDevice, r->side) == hipSuccess;
       }
@@ -782,6 +850,11 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
     }
   }
   for (auto& th : workers) th.join();
+  if (!holds.empty()) {
+    // the images may be evicted once released: the copies out of them first
+    if (!use_dma(r) && hipStreamSynchronize(r->side) != hipSuccess && st == KVX_OK) st = KVX_EHIP;
+    kvx::preload_unhold(r->pre, holds);
+  }
   r->stop.store(false);
   r->stats.pieces = st == KVX_OK ? P : 0;
   r->stats.bytes = 0;
@@ -1029,7 +1102,8 @@ bool is_pinned(const void* p) {
 
 // Common part of every bind: validate, plan, upload the chunk table.
 kvx_status bind(kvx_ring* r, Dir dir, const kvx_cache* cache, int32_t l0, int32_t l1,
-                int32_t chunk_tokens, std::vector<kvx::HostChunk> chunks, int32_t threads) {
+                int32_t chunk_tokens, std::vector<kvx::HostChunk> chunks, int32_t threads,
+                bool notional = false) {
   if (threads < 0 || threads > 64) return KVX_EINVAL;
   kvx::Geometry g;
   kvx_status st = kvx::validate(cache, l0, l1, 0, chunk_tokens, false, &g);
@@ -1052,7 +1126,7 @@ kvx_status bind(kvx_ring* r, Dir dir, const kvx_cache* cache, int32_t l0, int32_
   kvx::Plan plan;
   st = kvx::plan_chunks(chunks, l0, l1, g.slab, bpc, r->slot_bytes, &plan);
   if (st != KVX_OK) return st;
-  if (threads == 0)
+  if (threads == 0 && !notional)
     for (const auto& p : plan.pieces)
       for (const auto& sp : p.spans)
         if (!is_pinned(sp.host)) return KVX_EINVAL;  // direct copies need pinned memory
@@ -1092,6 +1166,10 @@ kvx_status bind(kvx_ring* r, Dir dir, const kvx_cache* cache, int32_t l0, int32_
   r->files.clear();
   r->files_mode = false;
   r->io_depth = 0;
+  r->pre = nullptr;
+  r->pre_paths.clear();
+  r->pre_file.clear();
+  r->pre_bytes.clear();
   return KVX_OK;
 }
 
@@ -1116,7 +1194,7 @@ kvx_status bind_files(kvx_ring* r, Dir dir, const kvx_cache* cache, int32_t l0, 
     hc[(size_t)f] = kvx::HostChunk{reinterpret_cast<uint8_t*>((uintptr_t)(f + 1) << kFileShift),
                                    c.bt_offset, c.n_blocks};
   }
-  st = bind(r, dir, cache, l0, l1, chunk_tokens, std::move(hc), 1);
+  st = bind(r, dir, cache, l0, l1, chunk_tokens, std::move(hc), 1, true);
   if (st != KVX_OK) return st;
   // The staging slots are pinned host memory, which cannot be the target of a
   // direct transfer here (EFAULT): the ring's files use buffered I/O, flushed
@@ -1125,6 +1203,48 @@ kvx_status bind_files(kvx_ring* r, Dir dir, const kvx_cache* cache, int32_t l0, 
   r->files = std::move(files);
   r->files_mode = true;
   r->io_depth = io_depth;
+  return KVX_OK;
+}
+
+// Bind a restore to chunk files held in a preloader's pool: chunks planned at
+// notional addresses like files, no fill threads (the DMA engine copies out of
+// the pool).
+kvx_status bind_preloaded(kvx_ring* r, const kvx_cache* cache, int32_t l0, int32_t l1,
+                          int32_t chunk_tokens, kvx_preloader* pre, const kvx_file_chunk* chunks,
+                          int32_t n_chunks) {
+  if (!pre || !kvx::preload_pinned(pre) || n_chunks < 0 || (n_chunks > 0 && !chunks) ||
+      n_chunks >= (1 << 22))
+    return KVX_EINVAL;
+  kvx::Geometry g;
+  kvx_status st = kvx::validate(cache, l0, l1, 0, chunk_tokens, false, &g);
+  if (st != KVX_OK) return st;
+  std::vector<kvx::HostChunk> hc((size_t)n_chunks);
+  std::vector<std::string> paths;
+  std::unordered_map<std::string, int32_t> index;
+  std::vector<int32_t> file_of((size_t)n_chunks);
+  std::vector<int64_t> bytes;
+  for (int32_t f = 0; f < n_chunks; ++f) {
+    const kvx_file_chunk& c = chunks[f];
+    if (!c.path || !c.path[0] || c.n_blocks < 1) return KVX_EINVAL;
+    const int64_t size = (int64_t)(l1 - l0) * 2 * c.n_blocks * g.slab;
+    if (size >= ((int64_t)1 << kFileShift)) return KVX_EINVAL;
+    const auto ins = index.emplace(c.path, (int32_t)paths.size());
+    file_of[(size_t)f] = ins.first->second;
+    if (ins.second) {
+      paths.emplace_back(c.path);
+      bytes.push_back(size);
+    } else if (bytes[(size_t)ins.first->second] != size) {
+      return KVX_EINVAL;  // one file named for chunks of two sizes
+    }
+    hc[(size_t)f] = kvx::HostChunk{reinterpret_cast<uint8_t*>((uintptr_t)(f + 1) << kFileShift),
+                                   c.bt_offset, c.n_blocks};
+  }
+  st = bind(r, Dir::kRestore, cache, l0, l1, chunk_tokens, std::move(hc), 0, true);
+  if (st != KVX_OK) return st;
+  r->pre = pre;
+  r->pre_paths = std::move(paths);
+  r->pre_file = std::move(file_of);
+  r->pre_bytes = std::move(bytes);
   return KVX_OK;
 }
 
@@ -1301,6 +1421,18 @@ kvx_status kvx_ring_bind_offload_files(kvx_ring* r, const kvx_cache* cache, int3
   if (r->async_busy.load()) return KVX_EBUSY;
   try {
     return bind_files(r, Dir::kOffload, cache, l0, l1, chunk_tokens, chunks, n_chunks, io_depth);
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}
+
+kvx_status kvx_ring_bind_preloaded(kvx_ring* r, const kvx_cache* cache, int32_t l0, int32_t l1,
+                                   int32_t chunk_tokens, kvx_preloader* preloader,
+                                   const kvx_file_chunk* chunks, int32_t n_chunks) {
+  if (!r || !cache) return KVX_EINVAL;
+  if (r->async_busy.load()) return KVX_EBUSY;
+  try {
+    return bind_preloaded(r, cache, l0, l1, chunk_tokens, preloader, chunks, n_chunks);
   } catch (...) {
     return KVX_EINTERNAL;
   }
