@@ -424,7 +424,7 @@ kvx_status kvx_write_files(const kvx_file_io* ops, int32_t n, int32_t io_depth);
  * request runs only the host-to-device copy is left on its path: its demand
  * fetch claims the staged images, which a ring restores straight from the pool
  * (kvx_ring_bind_chunks with fill_threads 0). One reactor thread reads files
- * in 16 MiB pieces through io_uring, at most io_depth in flight, and always
+ * in 32 MiB pieces through io_uring, at most io_depth in flight, and always
  * serves demand before speculation: speculative pieces are issued only while
  * no demand file has pieces left to issue; one preload runs at a time (the
  * files of one kvx_preload_hint call, read concurrently; the next call's

@@ -13,7 +13,7 @@ import pytest
 
 import paper_2609_11744_amd as kvx
 
-SLOT = 24 << 20
+SLOT = 48 << 20
 
 
 @pytest.fixture(params=["uring", "sync"])
@@ -43,7 +43,7 @@ def _pre(**kw):
 
 
 def test_hint_then_fetch_returns_staged_images(tmp_path, engine):
-    files = _files(tmp_path, [20 << 20, 4096, 12345])  # 2 pieces, one page, a ragged size
+    files = _files(tmp_path, [40 << 20, 4096, 12345])  # 2 pieces, one page, a ragged size
     p = _pre()
     try:
         p.hint([f for f, _ in files])
@@ -284,9 +284,9 @@ def test_demand_preempts_a_speculative_read_holding_the_last_slot(tmp_path, engi
     # One slot, taken by a speculative read with pieces still to issue: the
     # demand file takes it over once the pieces in flight have landed, and the
     # speculative file is read again after the demand image is released.
-    files = _files(tmp_path, [64 << 20, 1 << 20], seed=11)  # 4 pieces, 1 piece
+    files = _files(tmp_path, [128 << 20, 1 << 20], seed=11)  # 4 pieces, 1 piece
     (a, data_a), (b, data_b) = files
-    p = _pre(n_slots=1, slot_bytes=64 << 20, io_depth=1)
+    p = _pre(n_slots=1, slot_bytes=128 << 20, io_depth=1)
     got = {}
     try:
         p.set_test_hooks(delay_us=50000)  # each piece takes >= 50 ms
