@@ -12,6 +12,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <chrono>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
@@ -114,6 +115,7 @@ void close_tier_file(TierFile* f) {
 // ---- IoEngine ------------------------------------------------------------------
 
 IoEngine::~IoEngine() {
+  drain();
   if (sqe_map_) munmap(sqe_map_, sqe_map_len_);
   if (cq_map_ && cq_map_ != sq_map_) munmap(cq_map_, cq_map_len_);
   if (sq_map_) munmap(sq_map_, sq_map_len_);
@@ -161,6 +163,33 @@ kvx_status IoEngine::init(int32_t depth, bool write) {
   sq_entries_ = p.sq_entries;
   ring_fd_ = fd;
   return KVX_OK;
+}
+
+// After a failure, transfers the kernel still holds keep writing into (or
+// reading from) their buffers until they complete, and closing the ring does
+// not wait for them: reap completions (submitting what is queued) until none
+// is in flight, for at most 30 s, so that the caller may free the buffers.
+void IoEngine::drain() {
+  if (ring_fd_ < 0 || inflight_ == 0) return;
+  const auto deadline = std::chrono::steady_clock::now() + std::chrono::seconds(30);
+  while (inflight_ > 0 && std::chrono::steady_clock::now() < deadline) {
+    unsigned head = *cq_head_;
+    const unsigned tail = __atomic_load_n(cq_tail_, __ATOMIC_ACQUIRE);
+    for (; head != tail; ++head) {
+      const io_uring_cqe* cqe = static_cast<const io_uring_cqe*>(cqes_) + (head & *cq_mask_);
+      const uint64_t slot = cqe->user_data;
+      if (slot < (uint64_t)depth_ && ops_[(size_t)slot].live) {
+        ops_[(size_t)slot].live = false;
+        --inflight_;
+      }
+    }
+    __atomic_store_n(cq_head_, head, __ATOMIC_RELEASE);
+    if (inflight_ == 0) break;
+    const long n = syscall(__NR_io_uring_enter, ring_fd_, to_submit_, 1u, IORING_ENTER_GETEVENTS,
+                           nullptr, 0);
+    if (n >= 0) to_submit_ -= (unsigned)n < to_submit_ ? (unsigned)n : to_submit_;
+    else usleep(1000);
+  }
 }
 
 bool IoEngine::enter(unsigned min_complete) {

@@ -66,6 +66,7 @@ constexpr uint64_t kSyncTag = (uint64_t)1 << 63;
 class IoEngine {
  public:
   IoEngine() = default;
+  // Waits (at most 30 s) for transfers a failure left in the kernel.
   ~IoEngine();
   IoEngine(const IoEngine&) = delete;
   IoEngine& operator=(const IoEngine&) = delete;
@@ -107,6 +108,7 @@ class IoEngine {
   int32_t take_slot();
   kvx_status submit(int32_t slot);
   bool enter(unsigned min_complete);
+  void drain();
 
   bool write_ = false;
   int32_t depth_ = 0, inflight_ = 0;

@@ -379,7 +379,7 @@ void reactor_main(kvx_preloader* p) {
       }
     if (st != KVX_OK) {
       // the engine itself failed (not a transfer): fail everything being read
-      // and stop; the engine's teardown waits for what is still in flight
+      // and stop; the engine's destructor waits for what is still in flight
       p->engine_failed = true;
       for (auto& kv : p->entries)
         if (kv.second->st == St::kReading) {
