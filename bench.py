@@ -71,6 +71,9 @@ def parse():
                     choices=["8b-80k", "8b-32k-sweep", "70b-batch", "8b-files", "8b-preload"])
     ap.add_argument("--num-blocks", type=int, default=20000)
     ap.add_argument("--prefix-blocks", type=int, default=5000)
+    ap.add_argument("--kv-heads", type=int, default=8,
+                    help="default workload: KV heads held by this GPU (8: the whole 8B-shaped "
+                         "cache; 1: one tensor-parallel shard at tp = 8)")
     ap.add_argument("--chunk-tokens", type=int, default=256)
     ap.add_argument("--slots", type=int, default=4)
     ap.add_argument("--slot-mib", type=int, default=64)
@@ -197,7 +200,9 @@ def run_80k(args):
     import paper_2609_11744_amd as kvx
 
     dev = torch.device("cuda:0")
-    L, BS, H, D, E = 32, 16, 8, 128, 2
+    L, BS, H, D, E = 32, 16, args.kv_heads, 128, 2
+    if H < 1 or 8 % H:
+        raise SystemExit("--kv-heads must divide the 8B shape's 8 KV heads")
     NB, n, ct = args.num_blocks, args.prefix_blocks, args.chunk_tokens
     if 3 * n > NB:
         raise SystemExit("pool too small for three disjoint prefixes")
@@ -275,15 +280,17 @@ def run_80k(args):
     cpu = None if args.no_cpu_baseline else cpu_baseline(args, L, BS, H, D, E, perm)
     traffic = None
     if GATHER_TRAFFIC["kernels_sha256"] == kernels_sha256() and args.layout in GATHER_TRAFFIC and \
-            (args.num_blocks, args.prefix_blocks, args.chunk_tokens) == (20000, 5000, 256):
+            (args.num_blocks, args.prefix_blocks, args.chunk_tokens, H) == (20000, 5000, 256, 8):
         traffic = sum(GATHER_TRAFFIC[args.layout])
 
     out = base_record(
         args, "KV gather/scatter GB/s & % HBM peak; 80k-token prefix restore ms",
         "GB/s", round(gs_GBps, 1), round(wall_ms / args.steps, 3),
         {"workload": "llama-3-8b-shaped paged KV, 80k-token prefix (5000 blocks), "
-                     "256-token chunks, 4 x 64 MiB pinned staging ring",
-         "num_blocks": NB, "prefix_tokens": n * BS, "chunk_tokens": ct,
+                     "256-token chunks, 4 x 64 MiB pinned staging ring" +
+                     ("" if H == 8 else f"; one GPU's share under tensor parallelism over KV "
+                                        f"heads: {H} of 8 heads (tp = {8 // H})"),
+         "num_blocks": NB, "prefix_tokens": n * BS, "chunk_tokens": ct, "kv_heads": H,
          "cache_layout": args.layout, "slots": args.slots, "slot_mib": args.slot_mib,
          "fill_threads": args.fill_threads, "parallelism": "single GPU"})
     out.update({
