@@ -112,6 +112,8 @@ OVERLAP_CASES = [
     ((4, 400, 16, 2, 64, 2), 100, 64, 5, 2, False, 3000),   # slow reads: pieces wait for files
     ((4, 400, 16, 2, 64, 2), 100, 64, 5, 1, False, 3000),   # one slot, slow reads
     ((3, 300, 5, 2, 16, 2), 70, 15, 7, 3, False, 1000),     # 320-byte slabs, 2 KiB files
+    ((4, 400, 16, 2, 64, 2, 1), 90, 64, 9, 2, False, 1000),  # HND cache layout
+    ((4, 400, 16, 2, 64, 2, 2), 90, 64, 3, 2, False, 1000),  # paged-attention cache layout
 ]
 
 
