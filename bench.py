@@ -41,7 +41,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
-KERNELS_SRC = os.path.join(ROOT, "paper_2609_11744_amd", "csrc", "kvx_kernels.hip")
+# The copy kernels' sources: the kernels and the store they issue.
+KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
+               for f in ("kvx_kernels.hip", "kvx_store.h")]
 
 # HBM bytes of one gather launch on the 80k workload, from two rocprofv3 --pmc
 # runs (FETCH_SIZE, then WRITE_SIZE; profiles/copy_units_8b_80k_pmc.md), each
@@ -93,8 +95,11 @@ def parse():
 
 
 def kernels_sha256() -> str:
-    with open(KERNELS_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for path in KERNELS_SRC:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def copies_desc(stats):

@@ -40,11 +40,14 @@
 #include <type_traits>
 
 #include "kvx_internal.h"
+#include "kvx_store.h"
 
 namespace kvx {
 namespace {
 
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+using kvx_dev::store_stream;
+using kvx_dev::stream_dst;
+using kvx_dev::v4u;
 
 constexpr int kErrBadBlock = 1;
 constexpr int kErrBadChunk = 2;
@@ -112,6 +115,7 @@ __device__ __forceinline__ uint32_t xcd_contiguous(uint32_t b, uint32_t n) {
 template <int T, int V>
 __device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __restrict__ d,
                                           uint32_t n16) {
+  const auto out = stream_dst(d, n16 * 16u);
   uint32_t i = threadIdx.x;
   // Main body: V vectors per thread per pass, loads first.
   for (; i + (V - 1) * T < n16; i += V * T) {
@@ -119,9 +123,9 @@ __device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __rest
 #pragma unroll
     for (int q = 0; q < V; ++q) r[q] = __builtin_nontemporal_load(s + i + q * T);
 #pragma unroll
-    for (int q = 0; q < V; ++q) __builtin_nontemporal_store(r[q], d + i + q * T);
+    for (int q = 0; q < V; ++q) store_stream(out, i + q * T, r[q]);
   }
-  for (; i < n16; i += T) __builtin_nontemporal_store(__builtin_nontemporal_load(s + i), d + i);
+  for (; i < n16; i += T) store_stream(out, i, __builtin_nontemporal_load(s + i));
 }
 
 // ---- cache layouts that reorder a slab ---------------------------------------
@@ -170,6 +174,13 @@ __device__ __forceinline__ uint32_t divmod(uint32_t n, FastDiv f, uint32_t& rem)
   return q;
 }
 
+// Bytes a head's moves write from the destination's first vector: the head's
+// packed rows (a gather) or its nh contiguous cache vectors (a scatter).
+template <bool kToPacked>
+__device__ __forceinline__ uint32_t head_dst_bytes(const SlabGeom& g) {
+  return (kToPacked ? (g.bs.d - 1) * g.prow + g.v16.d : g.nh) * 16u;
+}
+
 // Packed-side offset (in vectors, from the head's first row) of local packed
 // vector w = t * v16 + dv.
 __device__ __forceinline__ uint32_t packed_at(uint32_t w, const SlabGeom& g) {
@@ -188,10 +199,11 @@ __device__ __forceinline__ void move_head_rows(const v4u* __restrict__ src, v4u*
     const uint32_t w = threadIdx.x + q * T;
     if (w < g.nh) r[q] = __builtin_nontemporal_load(src + (kToPacked ? w : packed_at(w, g)));
   }
+  const auto out = stream_dst(dst, head_dst_bytes<kToPacked>(g));
 #pragma unroll
   for (int q = 0; q < V; ++q) {
     const uint32_t w = threadIdx.x + q * T;
-    if (w < g.nh) __builtin_nontemporal_store(r[q], dst + (kToPacked ? packed_at(w, g) : w));
+    if (w < g.nh) store_stream(out, kToPacked ? packed_at(w, g) : w, r[q]);
   }
 }
 
@@ -224,10 +236,11 @@ __device__ __forceinline__ void stage_out(v4u* __restrict__ dst, const SlabGeom&
     const uint32_t w = threadIdx.x + q * T;
     if (w < g.nh) r[q] = f(w);
   }
+  const auto out = stream_dst(dst, head_dst_bytes<kToPacked>(g));
 #pragma unroll
   for (int q = 0; q < V; ++q) {
     const uint32_t w = threadIdx.x + q * T;
-    if (w < g.nh) __builtin_nontemporal_store(r[q], dst + (kToPacked ? packed_at(w, g) : w));
+    if (w < g.nh) store_stream(out, kToPacked ? packed_at(w, g) : w, r[q]);
   }
 }
 

@@ -1,5 +1,6 @@
 // Measurement helper: the HBM rate that a kernel shaped like the slab mover
-// (one workgroup per 4 KiB, 256 threads x one 16-byte non-temporal vector,
+// (one workgroup per 4 KiB, 256 threads x one 16-byte vector, non-temporal
+// loads and the kernels' streaming store,
 // XCD-contiguous workgroup order) reaches on contiguous memory when it only
 // reads, only writes, or copies. The bench reports these beside the spec peak,
 // so the gap between a gather and 8 TB/s can be split into what any copy of
@@ -8,10 +9,13 @@
 #include <hip/hip_runtime.h>
 
 #include "kvx.h"
+#include "kvx_store.h"
 
 namespace {
 
-typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+using kvx_dev::store_stream;
+using kvx_dev::stream_dst;
+using kvx_dev::v4u;
 
 constexpr int kThreads = 256;
 constexpr int kVec = 1;
@@ -32,10 +36,12 @@ __global__ void __launch_bounds__(kThreads)
                  uint32_t unit_count) {
   const uint64_t u = unit_base + xcd_contiguous(blockIdx.x, unit_count);
   const uint64_t base = u * (uint64_t)(kThreads * kVec) + threadIdx.x;
+  const auto out = stream_dst(dst + u * (uint64_t)(kThreads * kVec), (uint32_t)kUnit);
   if (kMode == 1) {
     const v4u val = {(uint32_t)u, threadIdx.x, 0x9E3779B9u, 0x7F4A7C15u};
 #pragma unroll
-    for (int q = 0; q < kVec; ++q) __builtin_nontemporal_store(val, dst + base + q * kThreads);
+    for (int q = 0; q < kVec; ++q)
+      store_stream(out, threadIdx.x + q * kThreads, val);
     return;
   }
   v4u r[kVec];
@@ -43,7 +49,8 @@ __global__ void __launch_bounds__(kThreads)
   for (int q = 0; q < kVec; ++q) r[q] = __builtin_nontemporal_load(src + base + q * kThreads);
   if (kMode == 2) {
 #pragma unroll
-    for (int q = 0; q < kVec; ++q) __builtin_nontemporal_store(r[q], dst + base + q * kThreads);
+    for (int q = 0; q < kVec; ++q)
+      store_stream(out, threadIdx.x + q * kThreads, r[q]);
   } else {
     v4u acc = r[0];
 #pragma unroll
