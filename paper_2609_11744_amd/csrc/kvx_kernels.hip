@@ -87,6 +87,24 @@ struct SlabGeom {
   uint32_t pad_;
 };
 
+// Division of any 32-bit numerator by a divisor fixed for the launch, as a
+// multiply (Granlund and Montgomery, "Division by invariant integers using
+// multiplication", 1994): with l = ceil(log2 d), m = floor(2^32 (2^l - d) / d)
+// + 1 and t = umulhi(n, m), n / d = (t + ((n - t) >> 1)) >> (l - 1) for d >= 2;
+// m = 0 stands for d = 1. The workgroup index decode divides unit indexes (up
+// to 2^31) by slab and chunk counts, so the narrower FastDiv does not apply.
+struct DivU32 {
+  uint32_t d;
+  uint32_t m;
+  uint32_t s;
+};
+
+__device__ __forceinline__ uint32_t divu(uint32_t n, DivU32 f) {
+  if (f.m == 0) return n;
+  const uint32_t t = __umulhi(n, f.m);
+  return (t + ((n - t) >> 1)) >> f.s;
+}
+
 struct UnitGeom {
   uint32_t units_per_chunk;  // (l1 - l0) * 2 * bpc
   uint32_t bpc;
@@ -95,6 +113,11 @@ struct UnitGeom {
   uint32_t n16;              // 16-byte vectors per slab
   uint32_t parts;            // workgroups per slab (parts_shift: log2 of a power of two, else 32)
   uint32_t parts_shift;
+  DivU32 parts_div;
+  DivU32 upc_div;            // by units_per_chunk
+  DivU32 bpc_div;            // by bpc
+  DivU32 last_div;           // by the last chunk's block count
+  DivU32 nb_div;             // by n_blocks
   uint64_t slab;
   SlabGeom sg;
 };
@@ -347,8 +370,8 @@ __device__ __forceinline__ void move_unit(char* paged, char* pk, uint32_t n16, c
 
 // Work item w of a launch -> (unit, part of the unit).
 __device__ __forceinline__ uint32_t split_work(uint32_t w, uint32_t parts, uint32_t shift,
-                                               uint32_t* part) {
-  const uint32_t u = shift < 32 ? w >> shift : w / parts;
+                                               DivU32 parts_div, uint32_t* part) {
+  const uint32_t u = shift < 32 ? w >> shift : divu(w, parts_div);
   *part = w - u * parts;
   return u;
 }
@@ -366,24 +389,24 @@ __global__ void __launch_bounds__(T)
                       int* __restrict__ err) {
   uint32_t part;
   uint32_t u = split_work(work_base + xcd_contiguous(blockIdx.x, work_count), g.parts,
-                          g.parts_shift, &part);
+                          g.parts_shift, g.parts_div, &part);
   uint32_t c, first, nc, lk, j;
   if (kOrdered) {
-    lk = u / g.n_blocks;
+    lk = divu(u, g.nb_div);
     const uint32_t i = order[u - lk * g.n_blocks];  // < n_blocks (a permutation)
-    c = i / g.bpc;
+    c = divu(i, g.bpc_div);
     first = c * g.bpc;
     j = i - first;
     const uint32_t left = g.n_blocks - first;
     nc = left < g.bpc ? left : g.bpc;
     u = c * g.units_per_chunk + lk * nc + j;
   } else {
-    c = u / g.units_per_chunk;
+    c = divu(u, g.upc_div);
     const uint32_t r = u - c * g.units_per_chunk;
     first = c * g.bpc;
     const uint32_t left = g.n_blocks - first;
-    nc = left < g.bpc ? left : g.bpc;  // blocks in this chunk
-    lk = r / nc;                       // 2 * (l - l0) + kv
+    nc = left < g.bpc ? left : g.bpc;                   // blocks in this chunk
+    lk = divu(r, nc == g.bpc ? g.bpc_div : g.last_div);  // 2 * (l - l0) + kv
     j = r - lk * nc;
   }
   const int32_t id = block_table[first + j];
@@ -412,6 +435,9 @@ struct ChunkGeom {
   uint32_t n16;
   uint32_t parts;        // workgroups per slab, as in UnitGeom
   uint32_t parts_shift;
+  DivU32 parts_div;
+  DivU32 upc_div;
+  DivU32 bpc_div;
   int32_t table_len;
   uint64_t slab;
   int64_t packed_bytes;
@@ -425,10 +451,10 @@ __global__ void __launch_bounds__(T)
                        uint32_t work_count, char* __restrict__ packed, int* __restrict__ err) {
   uint32_t part;
   const uint32_t u = split_work(work_base + xcd_contiguous(blockIdx.x, work_count), g.parts,
-                                g.parts_shift, &part);
-  const uint32_t c = u / g.upc;
+                                g.parts_shift, g.parts_div, &part);
+  const uint32_t c = divu(u, g.upc_div);
   const uint32_t r = u - c * g.upc;
-  const uint32_t lk = r / g.bpc;
+  const uint32_t lk = divu(r, g.bpc_div);
   const uint32_t j = r - lk * g.bpc;
   const kvx_chunk_ref ref = refs[c];
   const bool ok = ref.n_blocks >= 1 && (uint32_t)ref.n_blocks <= g.bpc && ref.bt_offset >= 0 &&
@@ -605,6 +631,16 @@ void slab_parts(int layout, uint32_t n16, uint32_t heads, uint32_t* parts, uint3
   *shift = (*parts & (*parts - 1)) == 0 ? (uint32_t)__builtin_ctz(*parts) : 32u;
 }
 
+DivU32 div_u32(uint32_t d) {
+  DivU32 f{d, 0u, 0u};
+  if (d <= 1) return f;
+  uint32_t l = 0;
+  while (l < 32 && (1ull << l) < d) ++l;  // ceil(log2 d)
+  f.m = (uint32_t)(((1ull << 32) * ((1ull << l) - d)) / d + 1);
+  f.s = l - 1;
+  return f;
+}
+
 FastDiv fast_div(uint32_t d) {
   FastDiv f;
   f.d = d;
@@ -670,6 +706,11 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.n16 = (uint32_t)(g.slab / 16);
   const int layout = cache->layout, elem = cache->elem_bytes;
   slab_parts(layout, ug.n16, (uint32_t)cache->num_kv_heads, &ug.parts, &ug.parts_shift);
+  ug.parts_div = div_u32(ug.parts);
+  ug.upc_div = div_u32(ug.units_per_chunk);
+  ug.bpc_div = div_u32(ug.bpc);
+  ug.last_div = div_u32((uint32_t)(g.n_blocks - (g.n_blocks - 1) / g.bpc * g.bpc));
+  ug.nb_div = div_u32(ug.n_blocks);
   ug.slab = (uint64_t)g.slab;
   ug.sg = slab_geom(cache, to_packed);
   if ((uint64_t)g.n_units * ug.parts > 0x7FFFFFFF) return KVX_EINTERNAL;
@@ -730,6 +771,9 @@ kvx_status launch_copy_chunks(bool to_packed, const kvx_cache* cache, int32_t l0
   cg.n16 = (uint32_t)(slab / 16);
   const int layout = cache->layout, elem = cache->elem_bytes;
   slab_parts(layout, cg.n16, (uint32_t)cache->num_kv_heads, &cg.parts, &cg.parts_shift);
+  cg.parts_div = div_u32(cg.parts);
+  cg.upc_div = div_u32(cg.upc);
+  cg.bpc_div = div_u32(cg.bpc);
   cg.table_len = table_len;
   cg.slab = (uint64_t)slab;
   cg.packed_bytes = packed_bytes;

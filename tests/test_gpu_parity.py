@@ -139,6 +139,8 @@ EDGE = [
     (2, 30, 8, 1, 32, 8, 0, 2, 6, 24),        # 8-byte elements
     (5, 25, 2, 1, 8, 2, 2, 5, 1, 2),          # a single block
     (130, 12, 2, 1, 8, 2, 1, 129, 5, 4),      # the largest layer range a call takes (128)
+    (3, 40, 16, 3, 128, 2, 0, 3, 7, 48),      # 12 KiB slabs: 3 parts; chunks of 3, 3, 1 blocks
+    (2, 3000, 16, 3, 128, 2, 0, 2, 1100, 80), # the same, ordered scatter (1,100 blocks, 5 per chunk)
 ]
 
 
