@@ -53,6 +53,13 @@ constexpr int kErrBadBlock = 1;
 constexpr int kErrBadChunk = 2;
 constexpr unsigned kXcds = 8;  // MI355X: 8 XCDs, workgroups dispatched round-robin
 
+// One entry of a scatter's destination order: a block-table index and the
+// block id found there (read once by the ordering kernel).
+struct OrderEntry {
+  uint32_t index;
+  int32_t id;
+};
+
 // Device pointers of the call's layers, in image order: p[2 * (l - l0) + kv].
 // Passed by value as a kernel argument (2 KiB for KVX_MAX_LAYERS = 128).
 struct LayerPtrs {
@@ -378,22 +385,34 @@ __device__ __forceinline__ uint32_t split_work(uint32_t w, uint32_t parts, uint3
 
 // Work item w = unit * parts + part.
 // kOrdered = false: units in image order (u -> chunk, layer|K|V, block).
-// kOrdered = true: unit v -> lk = v / n_blocks, k = v % n_blocks, block index
-// i = order[k] (destinations ascending by bucket); the image position u of
-// (chunk i / bpc, lk, block i % bpc) follows.
+// kOrdered = true: unit v -> lk = v / n_blocks, k = v % n_blocks, (block index
+// i, its block id) = order[k] (destinations ascending by bucket); the image
+// position u of (chunk i / bpc, lk, block i % bpc) follows.
+// A workgroup moves only 4 KiB, so the scalar loads before its first data
+// load matter: the block id and the layer pointer (or, ordered, the order
+// entry, which carries the id, and the layer pointer) are issued together
+// and waited for once. The empty asm statements take the loaded values,
+// which keeps the compiler from moving the layer pointer's load past the
+// block-id check.
 template <bool kToPacked, bool kOrdered, int kLayout, int kElem, int T, int V>
 __global__ void __launch_bounds__(T)
     copy_units_kernel(LayerPtrs layers, const int32_t* __restrict__ block_table, UnitGeom g,
                       uint32_t work_base, uint32_t work_count,
-                      const uint32_t* __restrict__ order, char* __restrict__ packed,
+                      const OrderEntry* __restrict__ order, char* __restrict__ packed,
                       int* __restrict__ err) {
   uint32_t part;
   uint32_t u = split_work(work_base + xcd_contiguous(blockIdx.x, work_count), g.parts,
                           g.parts_shift, g.parts_div, &part);
   uint32_t c, first, nc, lk, j;
+  int32_t id;
+  char* layer;
   if (kOrdered) {
     lk = divu(u, g.nb_div);
-    const uint32_t i = order[u - lk * g.n_blocks];  // < n_blocks (a permutation)
+    const OrderEntry e = order[u - lk * g.n_blocks];  // e.index < n_blocks (a permutation)
+    layer = layers.p[lk];
+    __asm__ volatile("" : : "s"(e.index), "s"(e.id), "s"(layer));
+    const uint32_t i = e.index;
+    id = e.id;
     c = divu(i, g.bpc_div);
     first = c * g.bpc;
     j = i - first;
@@ -408,13 +427,15 @@ __global__ void __launch_bounds__(T)
     nc = left < g.bpc ? left : g.bpc;                   // blocks in this chunk
     lk = divu(r, nc == g.bpc ? g.bpc_div : g.last_div);  // 2 * (l - l0) + kv
     j = r - lk * nc;
+    id = block_table[first + j];
+    layer = layers.p[lk];
+    __asm__ volatile("" : : "s"(id), "s"(layer));
   }
-  const int32_t id = block_table[first + j];
   if ((uint32_t)id >= g.num_blocks) {
     if (threadIdx.x == 0) atomicOr(err, kErrBadBlock);
     return;
   }
-  char* paged = layers.p[lk] + (uint64_t)(uint32_t)id * g.slab;
+  char* paged = layer + (uint64_t)(uint32_t)id * g.slab;
   char* pk = packed + (uint64_t)u * g.slab;
   move_unit<kToPacked, kLayout, kElem, T, V>(paged, pk, g.n16, g.sg, lk & 1, part);
 }
@@ -478,8 +499,8 @@ __global__ void __launch_bounds__(T)
   move_unit<kToPacked, kLayout, kElem, T, V>(paged, pk, g.n16, g.sg, lk & 1, part);
 }
 
-// Destination order for a scatter: order[] lists the block-table indexes
-// bucketed by destination id, buckets ascending. The id range [0, num_blocks)
+// Destination order for a scatter: order[] lists the block-table indexes,
+// each with the id it holds, bucketed by destination id, buckets ascending. The id range [0, num_blocks)
 // is cut into kBins equal bins (ids outside it go to the last bin; the copy
 // kernel skips them). One workgroup counts bin sizes in LDS, scans them into
 // bin starts and places each index with an LDS atomic, so order[] is a
@@ -496,7 +517,7 @@ __device__ __forceinline__ uint32_t bin_of(int32_t id, uint32_t num_blocks, uint
 
 __global__ void __launch_bounds__(kOrderThreads)
     order_kernel(const int32_t* __restrict__ block_table, uint32_t n, uint32_t num_blocks,
-                 uint32_t* __restrict__ order) {
+                 OrderEntry* __restrict__ order) {
   __shared__ uint32_t cnt[kBins];
   __shared__ uint32_t wave_total[kOrderThreads / 64];
   const uint32_t t = threadIdx.x, lane = t % 64, wave = t / 64;
@@ -531,8 +552,10 @@ __global__ void __launch_bounds__(kOrderThreads)
   cnt[4 * t + 2] = base + c0 + c1;
   cnt[4 * t + 3] = base + c0 + c1 + c2;
   __syncthreads();
-  for (uint32_t i = t; i < n; i += kOrderThreads)
-    order[atomicAdd(&cnt[bin_of(block_table[i], num_blocks, bins)], 1u)] = i;
+  for (uint32_t i = t; i < n; i += kOrderThreads) {
+    const int32_t id = block_table[i];
+    order[atomicAdd(&cnt[bin_of(id, num_blocks, bins)], 1u)] = OrderEntry{i, id};
+  }
 }
 
 // A dispatch's grid is counted in work-items in 32 bits, so one launch covers
@@ -594,7 +617,7 @@ inline size_t lds_bytes(int layout, const SlabGeom& sg) {
 
 template <bool kToPacked, bool kOrdered>
 hipError_t launch(const LayerPtrs& lp, const int32_t* bt, const UnitGeom& ug, uint32_t n_work,
-                  const uint32_t* order, char* packed, int* err, int layout, int elem,
+                  const OrderEntry* order, char* packed, int* err, int layout, int elem,
                   hipStream_t stream) {
   const SlabGeom& sg = ug.sg;
   for (uint32_t base = 0; base < n_work; base += kMaxWorkPerLaunch) {
@@ -723,9 +746,9 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   // Destination-ordered scatter for large calls; the order lives in
   // stream-ordered scratch. If that allocation fails, fall back to image
   // order (same result, slower).
-  uint32_t* order = nullptr;
+  OrderEntry* order = nullptr;
   if (g.n_blocks >= kOrderedScatterMinBlocks &&
-      hipMallocAsync((void**)&order, (size_t)g.n_blocks * sizeof(uint32_t), stream) != hipSuccess)
+      hipMallocAsync((void**)&order, (size_t)g.n_blocks * sizeof(OrderEntry), stream) != hipSuccess)
     order = nullptr;
   (void)hipGetLastError();
   hipError_t e;
