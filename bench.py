@@ -51,12 +51,12 @@ KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
 # only for the kernel source they were taken on (sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "a8e3e2bac289423f9390672d9e044ae3b44fb5491ea8d7448d8111fe773013dc",
+    "kernels_sha256": "8cf1ac28614e0ef5975b416b297c1a9adb9b3b51b5f159c60496f38c54b77c9c",
     # cache layout -> (fetched, written) HBM bytes of one gather launch at the
-    # default 80k-token workload: FETCH_SIZE KiB x 1.9999886 (copy calibration),
+    # default 80k-token workload: FETCH_SIZE KiB x 1.9999877 (copy calibration),
     # WRITE_SIZE KiB x 1.0
-    "nhd": (10488886875, 10485760000),         # 5,121,556.1 / 10,240,000.0 KiB
-    "paged_attn": (10489081138, 10485760000),  # 5,121,651.2 / 10,240,000.0 KiB
+    "nhd": (10488918828, 10485760000),         # 5,121,573.9 / 10,240,000.0 KiB
+    "paged_attn": (10489089106, 10485760000),  # 5,121,656.8 / 10,240,000.0 KiB
 }
 
 
