@@ -602,8 +602,8 @@ kvx_status kvx_max_io(const kvx_curve* cold, const kvx_curve* hit, const kvx_cur
 /* ---- measurement helper --------------------------------------------------------- */
 
 /* HBM probe with the slab mover's shape (one workgroup per 4 KiB of
- * contiguous memory, 256 threads x one 16-byte non-temporal vector,
- * XCD-contiguous order), enqueued on `stream`. mode 0 reads `bytes` of src,
+ * contiguous memory, 256 threads x one 16-byte vector, non-temporal loads and
+ * the copy kernels' streaming stores, XCD-contiguous order), enqueued on `stream`. mode 0 reads `bytes` of src,
  * 1 writes `bytes` of dst, 2 copies src to dst. `bytes` a multiple of 4 KiB,
  * device pointers 16-byte aligned (src unused for mode 1, dst for mode 0);
  * else KVX_EINVAL. Mode 1 overwrites dst with a pattern. For roofline context

@@ -19,7 +19,8 @@
 //     workgroup;
 //   * the slab moves as 16-byte vectors, consecutive lanes on consecutive
 //     addresses, so every wave instruction reads or writes 1 KiB contiguous;
-//   * both streams are touched once, so loads and stores are non-temporal;
+//   * both streams are touched once, so loads are non-temporal and stores
+//     stream to memory at device scope (kvx_store.h);
 //   * workgroups are dispatched round-robin over the 8 XCDs, so workgroup b
 //     is mapped to a (unit, part) such that each XCD walks one contiguous
 //     range of them. The packed side of an XCD's work is then one sequential
