@@ -51,12 +51,12 @@ KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
 # only for the kernel code they were taken on (kernels_sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "2a49d6215b755e05de81f284f4624c8d7170b104df68379e062567df2aee366a",
+    "kernels_sha256": "515467bf68c9cf847544598f46f35bc405796daee7e9d75e08bd781a052ec155",
     # cache layout -> (fetched, written) HBM bytes of one gather launch at the
-    # default 80k-token workload: FETCH_SIZE KiB x 1.9999877 (copy calibration),
+    # default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy calibration),
     # WRITE_SIZE KiB x 1.0
-    "nhd": (10488918828, 10485760000),         # 5,121,573.9 / 10,240,000.0 KiB
-    "paged_attn": (10489089106, 10485760000),  # 5,121,656.8 / 10,240,000.0 KiB
+    "nhd": (10488912457, 10485760000),         # 5,121,569.8 / 10,240,000.0 KiB
+    "paged_attn": (10489087358, 10485760000),  # 5,121,653.7 / 10,240,000.0 KiB
 }
 
 
