@@ -57,6 +57,7 @@ GATHER_TRAFFIC = {
     # WRITE_SIZE KiB x 1.0
     "nhd": (10488912457, 10485760000),         # 5,121,569.8 / 10,240,000.0 KiB
     "paged_attn": (10489087358, 10485760000),  # 5,121,653.7 / 10,240,000.0 KiB
+    "hnd": (10488876322, 10485760000),         # 5,121,554.0 / 10,240,000.0 KiB (x 1.9999874)
 }
 
 
