@@ -86,8 +86,11 @@ struct Plan {
 };
 
 // Cut a chunk list into staging pieces of at most slot_bytes (see kvx_plan.cpp).
+// With `ramp`, the first three pieces are limited to 1/8, 1/4 and 1/2 of a
+// slot (chunks larger than that are cut into layer ranges), so that a restore's
+// first host-to-device copy starts after a small first fill.
 kvx_status plan_chunks(const std::vector<HostChunk>& chunks, int32_t l0, int32_t l1, int64_t slab,
-                       int32_t bpc, int64_t slot_bytes, Plan* out);
+                       int32_t bpc, int64_t slot_bytes, Plan* out, bool ramp);
 
 // The chunks of one contiguous packed image at `base` (geometry g).
 std::vector<HostChunk> image_chunks(uint8_t* base, const Geometry& g);

@@ -19,14 +19,23 @@
 namespace kvx {
 
 kvx_status plan_chunks(const std::vector<HostChunk>& chunks, int32_t l0, int32_t l1, int64_t slab,
-                       int32_t bpc, int64_t slot_bytes, Plan* out) {
+                       int32_t bpc, int64_t slot_bytes, Plan* out, bool ramp) {
   out->pieces.clear();
   out->refs.clear();
   out->table_len = 0;
   if (slot_bytes <= 0 || slab <= 0 || bpc <= 0 || l1 < l0) return KVX_EINVAL;
   if (l1 == l0) return KVX_OK;
   const int64_t lr = l1 - l0;
+  // Size limit of the next piece: the slot, or with the ramp 1/8, 1/4 and
+  // 1/2 of it for the first three pieces.
+  auto cap = [&]() -> int64_t {
+    const size_t k = out->pieces.size();
+    if (!ramp || k >= 3) return slot_bytes;
+    const int64_t c = slot_bytes >> (3 - k);
+    return c > 0 ? c : slot_bytes;
+  };
   Piece cur{};
+  int64_t cur_cap = 0;
   bool open = false;
   auto flush = [&]() {
     if (open) out->pieces.push_back(cur);
@@ -39,34 +48,38 @@ kvx_status plan_chunks(const std::vector<HostChunk>& chunks, int32_t l0, int32_t
     if (end > out->table_len) out->table_len = (int32_t)end;
     const int64_t layer_bytes = (int64_t)c.n_blocks * 2 * slab;  // one layer, K and V
     const int64_t chunk_bytes = lr * layer_bytes;
-    if (chunk_bytes > slot_bytes) {
+    if (!(open && cur.bytes + chunk_bytes <= cur_cap)) {
       flush();
-      if (layer_bytes > slot_bytes) {
-        out->pieces.clear();
-        out->refs.clear();
-        return KVX_EINVAL;
+      if (chunk_bytes > cap()) {
+        // Too large for the next piece: contiguous layer ranges, each as many
+        // layers as the piece it becomes allows (at least one).
+        if (layer_bytes > slot_bytes) {
+          out->pieces.clear();
+          out->refs.clear();
+          return KVX_EINVAL;
+        }
+        for (int64_t a = l0; a < l1;) {
+          const int64_t fit = cap() / layer_bytes;
+          const int64_t per = fit > 0 ? fit : 1;
+          const int64_t b = a + per < l1 ? a + per : l1;
+          Piece p{};
+          p.l_begin = (int32_t)a;
+          p.l_end = (int32_t)b;
+          p.bytes = (b - a) * layer_bytes;
+          p.ref_first = (int32_t)out->refs.size();
+          p.ref_count = 1;
+          p.spans.push_back(Span{c.host + (a - l0) * layer_bytes, p.bytes, 0});
+          out->refs.push_back(kvx_chunk_ref{0, c.bt_offset, c.n_blocks});
+          out->pieces.push_back(p);
+          a = b;
+        }
+        continue;
       }
-      const int64_t per = slot_bytes / layer_bytes;  // layers per piece
-      for (int64_t a = l0; a < l1; a += per) {
-        const int64_t b = a + per < l1 ? a + per : l1;
-        Piece p{};
-        p.l_begin = (int32_t)a;
-        p.l_end = (int32_t)b;
-        p.bytes = (b - a) * layer_bytes;
-        p.ref_first = (int32_t)out->refs.size();
-        p.ref_count = 1;
-        p.spans.push_back(Span{c.host + (a - l0) * layer_bytes, p.bytes, 0});
-        out->refs.push_back(kvx_chunk_ref{0, c.bt_offset, c.n_blocks});
-        out->pieces.push_back(p);
-      }
-      continue;
-    }
-    if (open && cur.bytes + chunk_bytes > slot_bytes) flush();
-    if (!open) {
       cur = Piece{};
       cur.l_begin = l0;
       cur.l_end = l1;
       cur.ref_first = (int32_t)out->refs.size();
+      cur_cap = cap();
       open = true;
     }
     out->refs.push_back(kvx_chunk_ref{cur.bytes, c.bt_offset, c.n_blocks});
@@ -108,7 +121,8 @@ extern "C" kvx_status kvx_plan_pieces(const kvx_cache* cache, int32_t l0, int32_
     // report each piece as (image offset, bytes, block-table slice, layers).
     uint8_t* const base = reinterpret_cast<uint8_t*>(4096);
     kvx::Plan plan;
-    st = kvx::plan_chunks(kvx::image_chunks(base, g), l0, l1, g.slab, g.bpc, slot_bytes, &plan);
+    st = kvx::plan_chunks(kvx::image_chunks(base, g), l0, l1, g.slab, g.bpc, slot_bytes, &plan,
+                         false);
     if (st != KVX_OK) return st;
     if (plan.pieces.size() > (size_t)INT32_MAX) return KVX_EINVAL;
     *n_pieces = (int32_t)plan.pieces.size();

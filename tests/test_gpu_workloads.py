@@ -117,7 +117,10 @@ def test_80k_staged_restore_4x64MiB(w80k):
         ring.bind(w.cache, 0, 32, 5000, 256, image, fill_threads=8)
         kvx.kvx_restore_from_staging(ring, _bt(w.bt_rst))
         _check()
-        assert ring.stats()["pieces"] == 157
+        # the plain plan's 157 pieces, with the restore's ramp cutting the
+        # first 32 MiB chunk into 8, 16 and 8 MiB pieces (1/8, 1/4, 1/2 slot):
+        # 3 + 156 two-chunk pieces (the last one 32 + 16 MiB)
+        assert ring.stats()["pieces"] == 159
     finally:
         ring.close()
     # round trip on the device: gather the restored blocks back
