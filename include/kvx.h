@@ -240,7 +240,8 @@ kvx_status kvx_ring_create(int device, int32_t n_slots, int64_t slot_bytes, void
  * the data already sits in pinned memory). Plans the pieces as
  * kvx_plan_pieces does, except that a restore's first three pieces are held
  * to 1/8, 1/4 and 1/2 of a slot (larger chunks cut into layer ranges), so
- * its first host-to-device copy starts after a small first fill. */
+ * its first host-to-device copy starts after a small first fill; an offload's
+ * last three pieces are held to 1/2, 1/4 and 1/8 of a slot. */
 kvx_status kvx_ring_bind(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int32_t l1,
                          int32_t n_blocks, int32_t chunk_tokens, const void* host_source,
                          int32_t fill_threads);

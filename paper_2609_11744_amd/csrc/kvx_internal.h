@@ -85,12 +85,16 @@ struct Plan {
   int32_t table_len = 0;  // block-table entries the chunks reference
 };
 
-// Cut a chunk list into staging pieces of at most slot_bytes (see kvx_plan.cpp).
-// With `ramp`, the first three pieces are limited to 1/8, 1/4 and 1/2 of a
-// slot (chunks larger than that are cut into layer ranges), so that a restore's
-// first host-to-device copy starts after a small first fill.
+// Where a plan's pieces ramp up to the slot size: nowhere, over the first
+// three pieces (1/8, 1/4, 1/2 of a slot; a restore's first copy then starts
+// after a small fill) or, mirrored, over the last three (an offload's last
+// copy and drain are then short).
+enum class Ramp { kNone, kFirst, kLast };
+
+// Cut a chunk list into staging pieces of at most slot_bytes (see kvx_plan.cpp);
+// a chunk larger than its piece's limit is cut into layer ranges.
 kvx_status plan_chunks(const std::vector<HostChunk>& chunks, int32_t l0, int32_t l1, int64_t slab,
-                       int32_t bpc, int64_t slot_bytes, Plan* out, bool ramp);
+                       int32_t bpc, int64_t slot_bytes, Plan* out, Ramp ramp_at);
 
 // The chunks of one contiguous packed image at `base` (geometry g).
 std::vector<HostChunk> image_chunks(uint8_t* base, const Geometry& g);

@@ -9,6 +9,7 @@
 // themselves that chunk's image over [a, b). Every piece is one fused
 // chunk-list copy (one launch) of the chunk references it carries, at
 // slot-relative offsets, over its layer range.
+#include <algorithm>
 #include <cstdint>
 #include <unordered_map>
 #include <vector>
@@ -19,7 +20,17 @@
 namespace kvx {
 
 kvx_status plan_chunks(const std::vector<HostChunk>& chunks, int32_t l0, int32_t l1, int64_t slab,
-                       int32_t bpc, int64_t slot_bytes, Plan* out, bool ramp) {
+                       int32_t bpc, int64_t slot_bytes, Plan* out, Ramp ramp_at) {
+  if (ramp_at == Ramp::kLast) {
+    // The same ramp at the end: plan the chunks in reverse order with the ramp
+    // first, then reverse the pieces. Each piece carries its own chunk
+    // references and host spans, so the pieces keep their meaning in any order.
+    const std::vector<HostChunk> rev(chunks.rbegin(), chunks.rend());
+    const kvx_status st = plan_chunks(rev, l0, l1, slab, bpc, slot_bytes, out, Ramp::kFirst);
+    if (st == KVX_OK) std::reverse(out->pieces.begin(), out->pieces.end());
+    return st;
+  }
+  const bool ramp = ramp_at == Ramp::kFirst;
   out->pieces.clear();
   out->refs.clear();
   out->table_len = 0;
@@ -122,7 +133,7 @@ extern "C" kvx_status kvx_plan_pieces(const kvx_cache* cache, int32_t l0, int32_
     uint8_t* const base = reinterpret_cast<uint8_t*>(4096);
     kvx::Plan plan;
     st = kvx::plan_chunks(kvx::image_chunks(base, g), l0, l1, g.slab, g.bpc, slot_bytes, &plan,
-                         false);
+                          kvx::Ramp::kNone);
     if (st != KVX_OK) return st;
     if (plan.pieces.size() > (size_t)INT32_MAX) return KVX_EINVAL;
     *n_pieces = (int32_t)plan.pieces.size();

@@ -1124,7 +1124,8 @@ kvx_status bind(kvx_ring* r, Dir dir, const kvx_cache* cache, int32_t l0, int32_
     if (c.n_blocks > bpc) return KVX_EINVAL;
   bpc = std::min(bpc, most);
   kvx::Plan plan;
-  st = kvx::plan_chunks(chunks, l0, l1, g.slab, bpc, r->slot_bytes, &plan, dir == Dir::kRestore);
+  st = kvx::plan_chunks(chunks, l0, l1, g.slab, bpc, r->slot_bytes, &plan,
+                        dir == Dir::kRestore ? kvx::Ramp::kFirst : kvx::Ramp::kLast);
   if (st != KVX_OK) return st;
   if (threads == 0 && !notional)
     for (const auto& p : plan.pieces)
