@@ -231,3 +231,35 @@ def test_abort_while_the_restore_waits_for_a_file(tmp_path):
     finally:
         ring.close()
         pre.close()
+
+
+def test_preloaded_restore_with_a_file_named_twice(tmp_path):
+    # Two chunks restore the same file into different block ranges (identical
+    # content restored twice): the file is held and read once, and both ranges
+    # receive its image.
+    s = oracle.Shape(2, 300, 16, 2, 64, 2)
+    n, ct = 32, 64
+    chunks, cache, mirror, bt_dst = _offloaded_files(tmp_path, 811, s, n, ct)
+    twice = chunks + [(chunks[0][0], n, 4)]            # chunk 0's file again, for 4 more blocks
+    extra = [b for b in range(s.num_blocks) if b not in set(bt_dst)][:4]
+    bt = np.concatenate([bt_dst, np.asarray(extra, np.int32)])
+    slot = 4 * oracle.packed_bytes(s, 0, 2, 1)
+    ring = kvx.StagingRing(DEV, 2, 64 << 10)
+    pre = kvx.Preloader(len(chunks) + 1, slot, io_depth=2, pinned=True)
+    try:
+        ring.bind_preloaded(cache, 0, 2, ct, pre, twice)
+        kvx.kvx_restore_from_staging(ring, _bt(bt))
+        torch.cuda.synchronize()
+        kvx.kvx_check()
+        st = pre.stats()
+        assert st["demand_fetches"] == len(chunks) and st["bytes_read"] == sum(
+            np.fromfile(p, np.uint8).size for p, _, _ in chunks)
+        assert st["held"] == 0
+    finally:
+        ring.close()
+        pre.close()
+    for path, b0, nb in twice:
+        oracle.scatter(s, *mirror, 0, 2, bt[b0:b0 + nb], ct, np.fromfile(path, np.uint8))
+    for l in range(2):
+        assert np.array_equal(to_host(cache.k[l]), mirror[0][l]), f"K layer {l}"
+        assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
