@@ -36,8 +36,9 @@
  * Asynchrony: gather and scatter validate, enqueue on the caller's stream and
  * return; results are defined once that stream has completed. Block ids live
  * in device memory and are checked by the kernels: a unit whose id is outside
- * [0, num_blocks) is skipped (nothing is written for it) and a sticky
- * per-device flag is set, which kvx_check() reports as KVX_EBADBLOCK.
+ * [0, num_blocks) is skipped (nothing is written for it) and a sticky error
+ * word of the stream the call was given is set, which kvx_check() on that
+ * stream reports as KVX_EBADBLOCK.
  * Scatter destinations must be distinct; duplicates make the result depend
  * on execution order (not checked).
  *
@@ -116,6 +117,15 @@ int64_t kvx_bytes_per_token(int32_t layers, int32_t kv_heads, int32_t head_dim,
  * n_blocks * (l1 - l0) * 2 * slab. Returns -1 on an invalid shape or range. */
 int64_t kvx_packed_bytes(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t n_blocks);
 
+/* Byte distance between the starts of consecutive chunks of a packed image:
+ * the size of a full chunk, (l1 - l0) * 2 * chunk_tokens * row bytes with
+ * row = num_kv_heads * head_dim * elem_bytes (Sec. 6.4: a storage block
+ * groups chunk_tokens / block_size GPU blocks). Chunk c starts at c times
+ * this; only the last chunk of an image may be shorter. Returns -1 on an
+ * invalid shape or range, or chunk_tokens not a positive multiple of
+ * block_size. Cache pointers are not read. */
+int64_t kvx_chunk_stride(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t chunk_tokens);
+
 /* Gather (offload side): for every chunk c, layer l in [l0, l1), K|V and block
  * j of the chunk, copy slab cache[l][K|V][block_table[c*bpc + j]] to its place
  * in the packed image at dst (layout above).
@@ -179,10 +189,17 @@ kvx_status kvx_scatter_chunks(const kvx_cache* cache, int32_t l0, int32_t l1,
                               const kvx_chunk_ref* chunks, int32_t n_chunks, int32_t chunk_tokens,
                               const void* packed, int64_t packed_bytes, hipStream_t stream);
 
-/* Wait for `stream`, then read and clear the calling device's sticky error
- * flag: KVX_EINVAL if a kernel met an invalid device-resident chunk
- * reference, else KVX_EBADBLOCK if one met a bad block id, KVX_EHIP if the
- * stream reported an error, else KVX_OK. */
+/* Wait for `stream`, then read and clear its sticky error word on the calling
+ * device: KVX_EINVAL if a kernel of a call given this stream met an invalid
+ * device-resident chunk reference, else KVX_EBADBLOCK if one met a bad block
+ * id, KVX_EHIP if the stream reported an error, else KVX_OK. Each stream has a
+ * word of its own (errors on one stream are never reported to, or cleared by,
+ * a check of another), kept in a fixed table of 1,024 words per device: the
+ * null stream and streams beyond the first 1,023 distinct handles seen on a
+ * device share the table's first word. Work a ring or a deferred call runs on
+ * a stream of its own reports to the stream the caller passed. An error left
+ * unchecked when a stream is destroyed is reported to a later stream that
+ * receives the same handle. */
 kvx_status kvx_check(hipStream_t stream);
 
 const char* kvx_strerror(kvx_status status);
@@ -202,18 +219,32 @@ typedef struct kvx_piece {
   int32_t l_begin;
   int32_t l_end;
   int32_t chunk_tokens;
-  int32_t reserved;
+  int32_t n_spans;  /* host-link copies the piece takes (runs of chunks adjacent in the image) */
 } kvx_piece;
 
+/* Where a plan's piece sizes ramp up to the slot size. */
+#define KVX_RAMP_NONE 0   /* every piece up to slot_bytes */
+#define KVX_RAMP_FIRST 1  /* the first three pieces at most 1/8, 1/4 and 1/2 of a slot
+                             (a restore: its first copy starts after a small fill) */
+#define KVX_RAMP_LAST 2   /* the last three at most 1/2, 1/4 and 1/8 of a slot (an
+                             offload: its last copy and drain are short); the pieces
+                             of the first-ramp plan of the reversed chunk list, in
+                             reverse order, each carrying its chunks in image order */
+
 /* Split the packed image of (cache shape, [l0, l1), n_blocks, chunk_tokens)
- * into pieces of at most slot_bytes: as many whole chunks per piece as fit;
- * a chunk larger than a slot is split into contiguous layer ranges, as many
- * layers per piece as fit. Pure host computation (no HIP call). Writes at
- * most max_pieces entries to out (out may be NULL to count) and the total
- * count to *n_pieces. KVX_EINVAL if a single layer of a chunk exceeds
- * slot_bytes or the arguments are invalid (cache pointers are not read). */
+ * into pieces: as many consecutive whole chunks per piece as fit its size
+ * limit (slot_bytes, or less under the ramp); a chunk larger than its piece's
+ * limit is split into contiguous layer ranges, as many layers per piece as its
+ * limit allows (at least one), and the next chunk starts a new piece. So a
+ * ramped piece may hold less than its limit. This is the planner the ring
+ * runs (kvx_ring_bind: KVX_RAMP_FIRST for restores, KVX_RAMP_LAST for
+ * offloads). Pure host computation (no HIP call). Writes at most max_pieces
+ * entries to out (out may be NULL to count) and the total count to *n_pieces.
+ * KVX_EINVAL if a single layer of a chunk exceeds slot_bytes, ramp is not a
+ * KVX_RAMP_* value or the arguments are invalid (cache pointers are not
+ * read). */
 kvx_status kvx_plan_pieces(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t n_blocks,
-                           int32_t chunk_tokens, int64_t slot_bytes, kvx_piece* out,
+                           int32_t chunk_tokens, int64_t slot_bytes, int32_t ramp, kvx_piece* out,
                            int32_t max_pieces, int32_t* n_pieces);
 
 typedef struct kvx_ring kvx_ring;
@@ -238,10 +269,10 @@ kvx_status kvx_ring_create(int device, int32_t n_slots, int64_t slot_bytes, void
  * into staging slots. fill_threads == 0 skips staging: the H2D copies then
  * read the image directly, which must be pinned (the preloaded case, where
  * the data already sits in pinned memory). Plans the pieces as
- * kvx_plan_pieces does, except that a restore's first three pieces are held
- * to 1/8, 1/4 and 1/2 of a slot (larger chunks cut into layer ranges), so
- * its first host-to-device copy starts after a small first fill; an offload's
- * last three pieces are held to 1/2, 1/4 and 1/8 of a slot. */
+ * kvx_plan_pieces does with KVX_RAMP_FIRST: a restore's first three pieces
+ * hold at most 1/8, 1/4 and 1/2 of a slot (larger chunks cut into layer
+ * ranges), so its first host-to-device copy starts after a small first fill;
+ * offloads (kvx_ring_bind_offload) plan with KVX_RAMP_LAST. */
 kvx_status kvx_ring_bind(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int32_t l1,
                          int32_t n_blocks, int32_t chunk_tokens, const void* host_source,
                          int32_t fill_threads);
@@ -327,8 +358,28 @@ kvx_status kvx_offload_begin(kvx_ring* ring, const int32_t* block_table, hipStre
 
 /* Wait for the offload started by kvx_offload_begin and return its status
  * (KVX_OK at once if none was started). On return every destination holds
- * its image, as after kvx_offload_to_staging. */
+ * its image, as after kvx_offload_to_staging. Bad block ids met by its
+ * gathers are reported by kvx_check on the stream given to kvx_offload_begin. */
 kvx_status kvx_offload_wait(kvx_ring* ring);
+
+/* Asynchronous restore (Sec. 6.4: the worker turns load plans into transfers
+ * without blocking the engine; Sec. 6.2): start the restore of the bound
+ * transfer into the blocks named by block_table on a thread the ring owns,
+ * and return at once. Its scatters run after the work already enqueued on
+ * `stream`, on a stream the ring owns; fills, host-link copies and slot reuse
+ * are those of kvx_restore_from_staging. Until kvx_restore_wait has returned,
+ * every other call on the ring except kvx_ring_abort and kvx_ring_destroy
+ * returns KVX_EBUSY, and block_table and the bound sources must stay valid.
+ * Argument errors found before the start are returned here; errors of the
+ * transfer by kvx_restore_wait; bad block ids by kvx_check on `stream`. */
+kvx_status kvx_restore_begin(kvx_ring* ring, const int32_t* block_table, hipStream_t stream);
+
+/* Wait until the restore started by kvx_restore_begin has enqueued every
+ * scatter, then order `stream` after all of them (no host wait for the
+ * device): work enqueued on `stream` after this call sees the restored
+ * blocks. Returns the transfer's status (KVX_OK at once if none was started;
+ * KVX_ECLOSED after kvx_ring_abort). */
+kvx_status kvx_restore_wait(kvx_ring* ring, hipStream_t stream);
 
 typedef struct kvx_ring_stats {
   int64_t pieces;         /* pieces moved by the last restore or offload */
@@ -558,6 +609,80 @@ int64_t kvx_block_hashes(const int32_t* tokens, int64_t n_tokens, int32_t block_
  * first_of[i] == i. Pure host code. */
 kvx_status kvx_dedupe_keys(const uint64_t* keys, int32_t n, int32_t* first_of);
 
+/* One request of a batched engine step (caller-owned arrays, read during the
+ * call only). */
+typedef struct kvx_step_request {
+  const uint64_t* block_hashes;  /* n_blocks hashes of the prompt's full blocks, as
+                                    kvx_block_hashes computes them */
+  const uint8_t* resident;       /* one flag per chunk of the prompt: nonzero if the GPU
+                                    holds that chunk (the engine's prefix lookup) */
+  int32_t n_blocks;
+  int32_t n_resident;            /* ceil(n_blocks / (chunk_tokens / block_size)) */
+  int32_t new_blocks;            /* newly computed blocks to offload */
+  int32_t reserved;
+} kvx_step_request;
+
+/* A chunk the step restores: its key (the hash of its last block), its
+ * blocks, its origin (the first request, in order, that loads and needs it,
+ * and the chunk's index in that request's prompt) and its slice of the
+ * restore block table. */
+typedef struct kvx_step_restore {
+  uint64_t key;
+  int32_t n_blocks;
+  int32_t request;
+  int32_t chunk;
+  int32_t bt_offset;
+} kvx_step_restore;
+
+/* A chunk of one request's newly computed blocks (the store path): chunk
+ * index among that request's new-block chunks, its blocks, its slice of the
+ * offload block table and the request's first new block in it. */
+typedef struct kvx_step_offload {
+  int32_t request;
+  int32_t chunk;
+  int32_t n_blocks;
+  int32_t bt_offset;
+  int32_t new_first;
+} kvx_step_offload;
+
+/* chunk_states entries: >= 0 is an index into the restore list. */
+#define KVX_CHUNK_RESIDENT (-1)
+#define KVX_CHUNK_RECOMPUTE (-2)
+
+/* Output of kvx_plan_step: caller-owned arrays with their capacities
+ * (entries), then the counts and sums the call writes. */
+typedef struct kvx_step_plan {
+  kvx_step_restore* restore;
+  kvx_step_offload* offload;
+  int32_t* chunk_states;      /* per (request, chunk of its prompt), in order */
+  int32_t* declined;          /* requests under the gate that had something to load */
+  int32_t restore_cap, offload_cap, chunk_states_cap, declined_cap;
+  int32_t n_restore, n_offload, n_chunk_states, n_declined;
+  int32_t resident_hits;      /* distinct chunks the GPU already holds */
+  int32_t reserved;
+  int64_t restore_blocks, offload_blocks;
+  int64_t recompute_blocks;   /* blocks of needed chunks nobody restores, per request */
+} kvx_step_plan;
+
+/* Plan one batched step (Secs. 6.2, 6.4-6.6): every chunk of every prompt
+ * (chunk_tokens / block_size blocks; a prompt's last chunk may be shorter) is
+ * keyed by the hash of its last full block, so a chunk that extends another
+ * prompt's partial last chunk is a different chunk; a chunk's residency is
+ * that of its first occurrence. A request loads when the tokens of its chunks
+ * the GPU does not hold reach gate_tokens (the tier's break-even threshold,
+ * Sec. 6.6; 0 loads everything; a request with nothing to load counts as
+ * loading). A missing chunk is restored once, the first time a loading
+ * request needs it (identical prefixes share one read, Sec. 6.5), and is
+ * recomputed for each request that needs it otherwise. Each request's new
+ * blocks are cut into chunks, in request order, for the store path. Restore
+ * and offload block-table slices follow list order from 0.
+ * With all four arrays NULL only the counts and sums are written (size query);
+ * otherwise every array must hold its count (else KVX_EINVAL). KVX_EINVAL also
+ * for a bad argument, a residency count other than the prompt's chunk count,
+ * or a total over INT32_MAX blocks. Pure host code. */
+kvx_status kvx_plan_step(const kvx_step_request* reqs, int32_t n_requests, int32_t block_size,
+                         int32_t chunk_tokens, int64_t gate_tokens, kvx_step_plan* plan);
+
 /* ---- break-even gate (host) --------------------------------------------------- */
 
 /* A timing curve from an offline calibration sweep (Sec. 4.1, Pareto capture):
@@ -601,6 +726,33 @@ kvx_status kvx_break_even_tokens(const kvx_curve* cold, const kvx_curve* hit, in
  * path must sustain to match recomputation. */
 kvx_status kvx_max_io(const kvx_curve* cold, const kvx_curve* hit, const kvx_curve* copy,
                       int64_t doc_tokens, double* out_seconds);
+
+/* The hit curve of a tier from a measured restore rate (Secs. 5.2, 6.6: the
+ * hit path's time is its non-transfer part plus the KV transfer):
+ * out_seconds[i] = non_transfer.seconds[i] + non_transfer.tokens[i] *
+ * bytes_per_token / (restore_GBps * 1e9), for the n knots of non_transfer
+ * (out_seconds holds n doubles, caller-owned). The added term is linear in
+ * tokens, so the curve through these knots is exact between and beyond them.
+ * KVX_EINVAL for an invalid curve, bytes_per_token <= 0 or a rate that is not
+ * positive and finite. */
+kvx_status kvx_hit_curve_from_rate(const kvx_curve* non_transfer, int64_t bytes_per_token,
+                                   double restore_GBps, double* out_seconds);
+
+/* The bandwidth a cache path must sustain for a fully cached document of
+ * doc_tokens to match recomputing it (Sec. 5.2): its KV bytes (doc_tokens *
+ * bytes_per_token) over kvx_max_io, in GB/s (1e9 B/s); +infinity when the
+ * budget is not positive. */
+kvx_status kvx_required_GBps(const kvx_curve* cold, const kvx_curve* hit, const kvx_curve* copy,
+                             int64_t doc_tokens, int64_t bytes_per_token, double* out_GBps);
+
+/* The gate threshold of a source tier from its measured restore rate (Sec.
+ * 6.6): kvx_break_even_tokens of the cold curve against the hit curve
+ * kvx_hit_curve_from_rate builds from non_transfer, bytes_per_token and
+ * restore_GBps. *out as for kvx_break_even_tokens (-1: loading never pays up
+ * to max_tokens). */
+kvx_status kvx_tier_threshold(const kvx_curve* cold, const kvx_curve* non_transfer,
+                              int64_t bytes_per_token, double restore_GBps, int64_t max_tokens,
+                              int32_t granularity, int64_t* out);
 
 /* ---- measurement helper --------------------------------------------------------- */
 

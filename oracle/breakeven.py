@@ -24,11 +24,16 @@ Written from the definitions, in float64:
   * Step planning under the gate: a request loads its missing chunks when
     their tokens reach the threshold; otherwise it declines, and a chunk is
     restored when at least one request that needs it loads.
+  * Secs. 5.2, 6.6: a tier's hit time is its non-transfer part plus the KV
+    bytes moved at the tier's restore rate; the bandwidth a path must
+    sustain is a document's KV bytes over max_io.
 
 Pinned against closed forms on linear curves (the two break-even points
 have different closed forms), special cases, and brute force.
 """
 from __future__ import annotations
+
+import math
 
 
 def curve(tokens, seconds, x):
@@ -73,3 +78,15 @@ def plan_gate(load_blocks_per_request, block_size, gate_tokens):
     """Per request: True = loads its missing chunks, False = declines. A
     request with nothing to load counts as loading (nothing to decide)."""
     return [lb == 0 or lb * block_size >= gate_tokens for lb in load_blocks_per_request]
+
+
+def hit_from_rate(non_transfer, bytes_per_token, restore_GBps):
+    """Hit time of a tier restoring at restore_GBps (1e9 bytes per second):
+    the non-transfer part plus the prompt's KV bytes at that rate."""
+    return lambda x: non_transfer(x) + x * bytes_per_token / (restore_GBps * 1e9)
+
+
+def required_GBps(f, g, copy, D, bytes_per_token):
+    """D's KV bytes over max_io(D), in GB/s; infinite without a budget."""
+    budget = max_io(f, g, copy, D)
+    return D * bytes_per_token / budget / 1e9 if budget > 0 else math.inf

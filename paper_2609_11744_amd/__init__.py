@@ -193,6 +193,12 @@ def _buffer_ptr(cache, buf, need):
     return buf.data_ptr()
 
 
+def kvx_chunk_stride(cache, l0, l1, chunk_tokens) -> int:
+    """Bytes from one chunk of a packed image to the next (-1 if invalid)."""
+    c = _cstruct(cache)
+    return int(_native.lib().kvx_chunk_stride(ctypes.byref(c), l0, l1, chunk_tokens))
+
+
 def kvx_gather_blocks(cache: PagedKVCache, l0, l1, block_table, n_blocks, chunk_tokens, dst,
                       stream=None) -> None:
     need = max(kvx_packed_bytes(cache, l0, l1, n_blocks), 0)
@@ -261,18 +267,21 @@ def kvx_check(stream=None) -> None:
     _ok(_native.lib().kvx_check(_stream_handle(stream)), "kvx_check")
 
 
-def kvx_plan_pieces(cache, l0, l1, n_blocks, chunk_tokens, slot_bytes):
+KVX_RAMP_NONE, KVX_RAMP_FIRST, KVX_RAMP_LAST = 0, 1, 2
+
+
+def kvx_plan_pieces(cache, l0, l1, n_blocks, chunk_tokens, slot_bytes, ramp=KVX_RAMP_NONE):
     """Staging pieces as a list of dicts (pure host computation)."""
     c = _cstruct(cache)
     n = ctypes.c_int32(0)
     _ok(_native.lib().kvx_plan_pieces(ctypes.byref(c), l0, l1, n_blocks, chunk_tokens,
-                                      slot_bytes, None, 0, ctypes.byref(n)), "kvx_plan_pieces")
+                                      slot_bytes, ramp, None, 0, ctypes.byref(n)),
+        "kvx_plan_pieces")
     arr = (KvxPiece * max(n.value, 1))()
     _ok(_native.lib().kvx_plan_pieces(ctypes.byref(c), l0, l1, n_blocks, chunk_tokens,
-                                      slot_bytes, arr, n.value, ctypes.byref(n)),
+                                      slot_bytes, ramp, arr, n.value, ctypes.byref(n)),
         "kvx_plan_pieces")
-    return [{f: getattr(arr[i], f) for f, _ in KvxPiece._fields_ if f != "reserved"}
-            for i in range(n.value)]
+    return [{f: getattr(arr[i], f) for f, _ in KvxPiece._fields_} for i in range(n.value)]
 
 
 class PinnedBuffer:
@@ -621,6 +630,21 @@ def kvx_offload_wait(ring: StagingRing) -> None:
     _ok(st, "kvx_offload_wait")
 
 
+def kvx_restore_begin(ring: StagingRing, block_table, stream=None) -> None:
+    """Start the bound restore in the background; kvx_restore_wait orders a
+    stream after its scatters. The block table is kept alive until then."""
+    ptr = _table_ptr(ring._cache, block_table, ring.n_blocks) if ring._cache is not None else None
+    st = _native.lib().kvx_restore_begin(ring.handle, ptr, _stream_handle(stream))
+    _ok(st, "kvx_restore_begin")
+    ring._pending = block_table
+
+
+def kvx_restore_wait(ring: StagingRing, stream=None) -> None:
+    st = _native.lib().kvx_restore_wait(ring.handle, _stream_handle(stream))
+    ring._pending = None
+    _ok(st, "kvx_restore_wait")
+
+
 __all__ = [
     "KvxError", "PagedKVCache", "PinnedBuffer", "StagingRing", "kvx_bytes_per_token",
     "kvx_packed_bytes", "kvx_gather_blocks", "kvx_scatter_blocks", "kvx_check",
@@ -629,5 +653,6 @@ __all__ = [
     "kvx_block_hashes", "kvx_dedupe_keys", "KVX_LAYOUT_NHD", "KVX_LAYOUT_HND",
     "KVX_LAYOUT_PAGED_ATTN", "layer_shapes", "kvx_probe_stream", "kvx_chunk_path", "Preloader",
     "kvx_read_files", "kvx_write_files", "KVX_EIO", "KVX_EBUSY", "kvx_offload_begin",
-    "kvx_offload_wait",
+    "kvx_offload_wait", "kvx_restore_begin", "kvx_restore_wait", "kvx_chunk_stride",
+    "KVX_RAMP_NONE", "KVX_RAMP_FIRST", "KVX_RAMP_LAST",
 ]

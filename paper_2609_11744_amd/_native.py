@@ -20,7 +20,7 @@ class KvxCache(ctypes.Structure):
 class KvxPiece(ctypes.Structure):
     _fields_ = [("src_offset", c_i64), ("bytes", c_i64), ("bt_first", c_i32),
                 ("n_blocks", c_i32), ("l_begin", c_i32), ("l_end", c_i32),
-                ("chunk_tokens", c_i32), ("reserved", c_i32)]
+                ("chunk_tokens", c_i32), ("n_spans", c_i32)]
 
 
 class KvxChunkRef(ctypes.Structure):
@@ -57,10 +57,37 @@ class KvxCurve(ctypes.Structure):
                 ("seconds", ctypes.POINTER(ctypes.c_double)), ("n", c_i32)]
 
 
+class KvxStepRequest(ctypes.Structure):
+    _fields_ = [("block_hashes", c_vp), ("resident", c_vp), ("n_blocks", c_i32),
+                ("n_resident", c_i32), ("new_blocks", c_i32), ("reserved", c_i32)]
+
+
+class KvxStepRestore(ctypes.Structure):
+    _fields_ = [("key", ctypes.c_uint64), ("n_blocks", c_i32), ("request", c_i32),
+                ("chunk", c_i32), ("bt_offset", c_i32)]
+
+
+class KvxStepOffload(ctypes.Structure):
+    _fields_ = [("request", c_i32), ("chunk", c_i32), ("n_blocks", c_i32), ("bt_offset", c_i32),
+                ("new_first", c_i32)]
+
+
+class KvxStepPlan(ctypes.Structure):
+    _fields_ = [("restore", ctypes.POINTER(KvxStepRestore)),
+                ("offload", ctypes.POINTER(KvxStepOffload)),
+                ("chunk_states", ctypes.POINTER(c_i32)), ("declined", ctypes.POINTER(c_i32)),
+                ("restore_cap", c_i32), ("offload_cap", c_i32), ("chunk_states_cap", c_i32),
+                ("declined_cap", c_i32), ("n_restore", c_i32), ("n_offload", c_i32),
+                ("n_chunk_states", c_i32), ("n_declined", c_i32), ("resident_hits", c_i32),
+                ("reserved", c_i32), ("restore_blocks", c_i64), ("offload_blocks", c_i64),
+                ("recompute_blocks", c_i64)]
+
+
 # name -> (restype, argtypes); every symbol include/kvx.h declares.
 SIGNATURES = {
     "kvx_bytes_per_token": (c_i64, [c_i32, c_i32, c_i32, c_i32]),
     "kvx_packed_bytes": (c_i64, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32]),
+    "kvx_chunk_stride": (c_i64, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32]),
     "kvx_gather_blocks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
                                          c_i32, c_vp, c_vp]),
     "kvx_scatter_blocks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
@@ -72,7 +99,7 @@ SIGNATURES = {
     "kvx_check": (ctypes.c_int, [c_vp]),
     "kvx_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "kvx_plan_pieces": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32, c_i32,
-                                       c_i64, ctypes.POINTER(KvxPiece), c_i32,
+                                       c_i64, c_i32, ctypes.POINTER(KvxPiece), c_i32,
                                        ctypes.POINTER(c_i32)]),
     "kvx_ring_create": (ctypes.c_int, [ctypes.c_int, c_i32, c_i64, c_vp, ctypes.POINTER(c_vp)]),
     "kvx_ring_bind": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32, c_i32,
@@ -85,12 +112,16 @@ SIGNATURES = {
     "kvx_offload_to_staging": (ctypes.c_int, [c_vp, c_vp, c_vp]),
     "kvx_offload_begin": (ctypes.c_int, [c_vp, c_vp, c_vp]),
     "kvx_offload_wait": (ctypes.c_int, [c_vp]),
+    "kvx_restore_begin": (ctypes.c_int, [c_vp, c_vp, c_vp]),
+    "kvx_restore_wait": (ctypes.c_int, [c_vp, c_vp]),
     "kvx_ring_stats_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxRingStats)]),
     "kvx_ring_abort": (ctypes.c_int, [c_vp]),
     "kvx_ring_set_test_hooks": (ctypes.c_int, [c_vp, c_i32, c_i32]),
     "kvx_ring_destroy": (ctypes.c_int, [c_vp]),
     "kvx_block_hashes": (c_i64, [c_vp, c_i64, c_i32, ctypes.c_uint64, c_vp]),
     "kvx_dedupe_keys": (ctypes.c_int, [c_vp, c_i32, c_vp]),
+    "kvx_plan_step": (ctypes.c_int, [ctypes.POINTER(KvxStepRequest), c_i32, c_i32, c_i32, c_i64,
+                                     ctypes.POINTER(KvxStepPlan)]),
     "kvx_curve_eval": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.c_double,
                                       ctypes.POINTER(ctypes.c_double)]),
     "kvx_load_beats_recompute": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.POINTER(KvxCurve),
@@ -102,6 +133,14 @@ SIGNATURES = {
     "kvx_max_io": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.POINTER(KvxCurve),
                                   ctypes.POINTER(KvxCurve), c_i64,
                                   ctypes.POINTER(ctypes.c_double)]),
+    "kvx_hit_curve_from_rate": (ctypes.c_int, [ctypes.POINTER(KvxCurve), c_i64, ctypes.c_double,
+                                               ctypes.POINTER(ctypes.c_double)]),
+    "kvx_required_GBps": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.POINTER(KvxCurve),
+                                         ctypes.POINTER(KvxCurve), c_i64, c_i64,
+                                         ctypes.POINTER(ctypes.c_double)]),
+    "kvx_tier_threshold": (ctypes.c_int, [ctypes.POINTER(KvxCurve), ctypes.POINTER(KvxCurve),
+                                          c_i64, ctypes.c_double, c_i64, c_i32,
+                                          ctypes.POINTER(c_i64)]),
     "kvx_probe_stream": (ctypes.c_int, [c_vp, c_vp, c_i64, c_i32, c_vp]),
     "kvx_ring_bind_files": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32,
                                            ctypes.POINTER(KvxFileChunk), c_i32, c_i32]),

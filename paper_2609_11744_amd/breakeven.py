@@ -38,11 +38,24 @@ class Curve:
 
 def hit_curve_from_restore(non_transfer: Curve, bytes_per_token: int, restore_GBps: float) -> Curve:
     """Hit TTFT = its non-transfer part + the KV bytes at the measured restore
-    rate. The added term is linear, so the sum is exact at the same knots."""
-    rate = restore_GBps * 1e9
-    return Curve(non_transfer.tokens,
-                 [s + t * bytes_per_token / rate
-                  for t, s in zip(non_transfer.tokens, non_transfer.seconds)])
+    rate (kvx_hit_curve_from_rate), on the same knots."""
+    n = len(non_transfer.tokens)
+    out = (ctypes.c_double * max(n, 1))()
+    _ok(_native.lib().kvx_hit_curve_from_rate(ctypes.byref(non_transfer.c), bytes_per_token,
+                                              float(restore_GBps), out),
+        "kvx_hit_curve_from_rate")
+    return Curve(non_transfer.tokens, list(out[:n]))
+
+
+def tier_threshold(cold: Curve, non_transfer: Curve, bytes_per_token: int, restore_GBps: float,
+                   max_tokens: int, granularity: int):
+    """The gate threshold of a tier restoring at restore_GBps (kvx_tier_threshold);
+    None if loading never pays up to max_tokens."""
+    out = ctypes.c_int64()
+    _ok(_native.lib().kvx_tier_threshold(ctypes.byref(cold.c), ctypes.byref(non_transfer.c),
+                                         bytes_per_token, float(restore_GBps), max_tokens,
+                                         granularity, ctypes.byref(out)), "kvx_tier_threshold")
+    return None if out.value < 0 else out.value
 
 
 def load_beats_recompute(cold: Curve, hit: Curve, doc_tokens: int, prefix_tokens: int) -> bool:
@@ -81,12 +94,13 @@ def max_io(cold: Curve, hit: Curve, copy: Curve, doc_tokens: int) -> float:
 def required_GBps(cold: Curve, hit: Curve, copy: Curve, doc_tokens: int,
                   bytes_per_token: int) -> float:
     """Bandwidth a cache path must sustain for a fully cached document to match
-    recomputing it: its KV bytes over max_io (Sec. 5.2)."""
-    budget = max_io(cold, hit, copy, doc_tokens)
-    if budget <= 0:
-        return float("inf")
-    return doc_tokens * bytes_per_token / budget / 1e9
+    recomputing it (kvx_required_GBps, Sec. 5.2)."""
+    out = ctypes.c_double()
+    _ok(_native.lib().kvx_required_GBps(ctypes.byref(cold.c), ctypes.byref(hit.c),
+                                        ctypes.byref(copy.c), doc_tokens, bytes_per_token,
+                                        ctypes.byref(out)), "kvx_required_GBps")
+    return out.value
 
 
 __all__ = ["Curve", "hit_curve_from_restore", "load_beats_recompute", "break_even_prefix",
-           "break_even_tokens", "max_io", "required_GBps", "KvxError"]
+           "break_even_tokens", "max_io", "required_GBps", "tier_threshold", "KvxError"]

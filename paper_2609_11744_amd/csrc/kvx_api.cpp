@@ -91,7 +91,8 @@ static kvx_status copy_entry(bool to_packed, const kvx_cache* cache, int32_t l0,
   if (g.n_units == 0) return KVX_OK;
   if (!block_table || !packed || ((uintptr_t)packed & 15)) return KVX_EINVAL;
   if (overlaps_cache(cache, l0, l1, packed, g.packed)) return KVX_EINVAL;
-  return launch_copy(to_packed, cache, l0, l1, block_table, g, const_cast<void*>(packed), stream);
+  return launch_copy(to_packed, cache, l0, l1, block_table, g, const_cast<void*>(packed), stream,
+                     stream_error_word(stream));
 }
 
 static kvx_status chunks_entry(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
@@ -115,7 +116,8 @@ static kvx_status chunks_entry(bool to_packed, const kvx_cache* cache, int32_t l
   if (units > INT32_MAX) return KVX_EINVAL;
   if (overlaps_cache(cache, l0, l1, packed, packed_bytes)) return KVX_EINVAL;
   return launch_copy_chunks(to_packed, cache, l0, l1, block_table, table_len, chunks, n_chunks,
-                            chunk_tokens, const_cast<void*>(packed), packed_bytes, stream);
+                            chunk_tokens, const_cast<void*>(packed), packed_bytes, stream,
+                            stream_error_word(stream));
 }
 
 }  // namespace kvx
@@ -133,6 +135,14 @@ int64_t kvx_packed_bytes(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t
   const int32_t ct = cache ? cache->block_size : 0;
   if (kvx::validate(cache, l0, l1, n_blocks, ct, false, &g) != KVX_OK) return -1;
   return g.packed;
+}
+
+int64_t kvx_chunk_stride(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t chunk_tokens) {
+  kvx::Geometry g;
+  if (kvx::validate(cache, l0, l1, 0, chunk_tokens, false, &g) != KVX_OK) return -1;
+  int64_t s = 0;
+  if (__builtin_mul_overflow((int64_t)g.lr * 2 * g.bpc, g.slab, &s)) return -1;
+  return s;
 }
 
 kvx_status kvx_gather_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
@@ -181,13 +191,19 @@ kvx_status kvx_scatter_chunks(const kvx_cache* cache, int32_t l0, int32_t l1,
 
 kvx_status kvx_check(hipStream_t stream) {
   if (hipStreamSynchronize(stream) != hipSuccess) return KVX_EHIP;
-  int* w = kvx::device_error_word();
+  int* w = kvx::stream_error_word(stream);
   if (!w) return KVX_EHIP;
+  // read and clear the word through the stream itself, so that the check
+  // waits for no other stream
   int v = 0;
-  if (hipMemcpy(&v, w, sizeof(int), hipMemcpyDeviceToHost) != hipSuccess) return KVX_EHIP;
+  if (hipMemcpyAsync(&v, w, sizeof(int), hipMemcpyDeviceToHost, stream) != hipSuccess ||
+      hipStreamSynchronize(stream) != hipSuccess)
+    return KVX_EHIP;
   if (v != 0) {
     const int zero = 0;
-    if (hipMemcpy(w, &zero, sizeof(int), hipMemcpyHostToDevice) != hipSuccess) return KVX_EHIP;
+    if (hipMemcpyAsync(w, &zero, sizeof(int), hipMemcpyHostToDevice, stream) != hipSuccess ||
+        hipStreamSynchronize(stream) != hipSuccess)
+      return KVX_EHIP;
     return (v & 2) ? KVX_EINVAL : KVX_EBADBLOCK;  // bit 1: bad chunk ref, bit 0: bad block id
   }
   return KVX_OK;

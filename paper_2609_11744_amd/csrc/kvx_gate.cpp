@@ -10,6 +10,8 @@
 // length per source tier; at lookup a reusable prefix below it is recomputed.
 #include <cmath>
 #include <cstdint>
+#include <limits>
+#include <vector>
 
 #include "kvx.h"
 
@@ -91,6 +93,41 @@ kvx_status kvx_max_io(const kvx_curve* cold, const kvx_curve* hit, const kvx_cur
   const double d = (double)doc_tokens;
   *out_seconds = eval(cold, d) - (eval(hit, d) - eval(copy, d));
   return KVX_OK;
+}
+
+kvx_status kvx_hit_curve_from_rate(const kvx_curve* non_transfer, int64_t bytes_per_token,
+                                   double restore_GBps, double* out_seconds) {
+  if (!valid(non_transfer) || !out_seconds || bytes_per_token <= 0 ||
+      !std::isfinite(restore_GBps) || !(restore_GBps > 0))
+    return KVX_EINVAL;
+  const double rate = restore_GBps * 1e9;  // bytes per second
+  for (int32_t i = 0; i < non_transfer->n; ++i)
+    out_seconds[i] =
+        non_transfer->seconds[i] + non_transfer->tokens[i] * (double)bytes_per_token / rate;
+  return KVX_OK;
+}
+
+kvx_status kvx_required_GBps(const kvx_curve* cold, const kvx_curve* hit, const kvx_curve* copy,
+                             int64_t doc_tokens, int64_t bytes_per_token, double* out_GBps) {
+  if (!out_GBps || bytes_per_token <= 0) return KVX_EINVAL;
+  double budget = 0;
+  const kvx_status st = kvx_max_io(cold, hit, copy, doc_tokens, &budget);
+  if (st != KVX_OK) return st;
+  *out_GBps = budget > 0 ? (double)doc_tokens * (double)bytes_per_token / budget / 1e9
+                         : std::numeric_limits<double>::infinity();
+  return KVX_OK;
+}
+
+kvx_status kvx_tier_threshold(const kvx_curve* cold, const kvx_curve* non_transfer,
+                              int64_t bytes_per_token, double restore_GBps, int64_t max_tokens,
+                              int32_t granularity, int64_t* out) {
+  if (!valid(non_transfer)) return KVX_EINVAL;
+  std::vector<double> sec((size_t)non_transfer->n);
+  const kvx_status st =
+      kvx_hit_curve_from_rate(non_transfer, bytes_per_token, restore_GBps, sec.data());
+  if (st != KVX_OK) return st;
+  const kvx_curve hit{non_transfer->tokens, sec.data(), non_transfer->n};
+  return kvx_break_even_tokens(cold, &hit, max_tokens, granularity, out);
 }
 
 }  // extern "C"

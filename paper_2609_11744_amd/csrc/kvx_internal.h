@@ -41,10 +41,11 @@ bool overlaps_cache(const kvx_cache* cache, int32_t l0, int32_t l1, const void* 
                     int64_t bytes);
 
 // Enqueue the gather (to_packed = true) or scatter kernel on `stream`.
-// `block_table` is a device pointer to the call's n_blocks ids.
+// `block_table` is a device pointer to the call's n_blocks ids; the kernels
+// report bad ids in the error word err (stream_error_word).
 kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
                        const int32_t* block_table, const Geometry& g, void* packed,
-                       hipStream_t stream);
+                       hipStream_t stream, int* err);
 
 // Enqueue the chunk-list gather (to_packed) or scatter on `stream`: refs is a
 // device array of n_chunks references, validated by the kernel against
@@ -52,7 +53,8 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
 kvx_status launch_copy_chunks(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
                               const int32_t* block_table, int32_t table_len,
                               const kvx_chunk_ref* refs, int32_t n_chunks, int32_t chunk_tokens,
-                              void* packed, int64_t packed_bytes, hipStream_t stream);
+                              void* packed, int64_t packed_bytes, hipStream_t stream,
+                              int* err);
 
 // A chunk image in host memory (restore source or offload destination) and the
 // block-table slice it belongs to.
@@ -99,8 +101,9 @@ kvx_status plan_chunks(const std::vector<HostChunk>& chunks, int32_t l0, int32_t
 // The chunks of one contiguous packed image at `base` (geometry g).
 std::vector<HostChunk> image_chunks(uint8_t* base, const Geometry& g);
 
-// Device address of the calling device's sticky error word (resolved once per
-// device with hipGetSymbolAddress). Null on failure.
-int* device_error_word();
+// Device address of the sticky error word of `stream` on the calling device
+// (a fixed table per device, resolved once with hipGetSymbolAddress; the null
+// stream and streams beyond the table share its first word). Null on failure.
+int* stream_error_word(hipStream_t stream);
 
 }  // namespace kvx

@@ -52,6 +52,7 @@ using kvx_dev::v4u;
 
 constexpr int kErrBadBlock = 1;
 constexpr int kErrBadChunk = 2;
+constexpr int kErrorWords = 1024;  // word 0: the null stream, and streams beyond the table
 constexpr unsigned kXcds = 8;  // MI355X: 8 XCDs, workgroups dispatched round-robin
 
 // One entry of a scatter's destination order: a block-table index and the
@@ -130,9 +131,11 @@ struct UnitGeom {
   SlabGeom sg;
 };
 
-// Sticky error word, one per device. Host code reaches it only through the
-// address that hipGetSymbolAddress returns (device_error_word()).
-__device__ int g_error_word;
+// Sticky error words, a table per device: each stream that launches copies
+// gets a word of its own (stream_error_word), so that a check of one stream
+// neither reports nor clears another stream's error. Host code reaches the
+// table only through the address that hipGetSymbolAddress returns.
+__device__ int g_error_words[kErrorWords];
 
 // Workgroup b of a launch over n units -> unit index. XCD x = b % kXcds runs
 // the workgroups b = x, x + kXcds, ...; they get the contiguous range
@@ -710,25 +713,51 @@ SlabGeom slab_geom(const kvx_cache* c, bool to_packed) {
 
 }  // namespace
 
-int* device_error_word() {
-  static std::mutex mu;
-  static int* addr[64] = {};
+namespace {
+
+// Per device: the table's device address and which stream owns each word.
+// Fixed-size (no allocation), open addressing on the stream handle.
+constexpr int kMaxDevices = 64;
+struct ErrorTable {
+  int* base = nullptr;
+  hipStream_t owner[kErrorWords] = {};
+  bool used[kErrorWords] = {};
+};
+ErrorTable g_tables[kMaxDevices];
+std::mutex g_tables_mu;
+
+}  // namespace
+
+int* stream_error_word(hipStream_t stream) {
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
-  std::lock_guard<std::mutex> lock(mu);
-  if (!addr[dev]) {
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_tables_mu);
+  ErrorTable& t = g_tables[dev];
+  if (!t.base) {
     void* p = nullptr;
-    if (hipGetSymbolAddress(&p, HIP_SYMBOL(g_error_word)) == hipSuccess) addr[dev] = (int*)p;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(g_error_words)) != hipSuccess) return nullptr;
+    t.base = (int*)p;
   }
-  return addr[dev];
+  if (!stream) return t.base;
+  const uint64_t h = (uint64_t)(uintptr_t)stream * 0x9E3779B97F4A7C15ull;
+  uint32_t w = 1 + (uint32_t)(h >> 40) % (kErrorWords - 1);
+  for (int probe = 0; probe < kErrorWords - 1; ++probe) {
+    if (!t.used[w]) {
+      t.used[w] = true;
+      t.owner[w] = stream;
+      return t.base + w;
+    }
+    if (t.owner[w] == stream) return t.base + w;
+    w = w + 1 == (uint32_t)kErrorWords ? 1u : w + 1;
+  }
+  return t.base;  // table full: the shared word
 }
 
 kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
                        const int32_t* block_table, const Geometry& g, void* packed,
-                       hipStream_t stream) {
+                       hipStream_t stream, int* err) {
   if (g.n_units == 0) return KVX_OK;
   if (g.n_units > 0x7FFFFFFF || g.slab % 16 != 0) return KVX_EINTERNAL;
-  int* err = device_error_word();
   if (!err) return KVX_EHIP;
   LayerPtrs lp = {};
   for (int32_t l = l0; l < l1; ++l) {
@@ -785,9 +814,9 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
 kvx_status launch_copy_chunks(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
                               const int32_t* block_table, int32_t table_len,
                               const kvx_chunk_ref* refs, int32_t n_chunks, int32_t chunk_tokens,
-                              void* packed, int64_t packed_bytes, hipStream_t stream) {
+                              void* packed, int64_t packed_bytes, hipStream_t stream,
+                              int* err) {
   if (n_chunks <= 0 || l1 <= l0) return KVX_OK;
-  int* err = device_error_word();
   if (!err) return KVX_EHIP;
   const int64_t slab = (int64_t)cache->block_size * cache->num_kv_heads * cache->head_dim *
                        cache->elem_bytes;

@@ -110,12 +110,20 @@ struct kvx_ring {
   bool hook_poison = false;
   bool hook_hip_copies = false;  // copies through the HIP runtime even with the DMA engines set up
 
-  // deferred store (kvx_offload_begin / kvx_offload_wait): its gathers run on
-  // store_stream after store_begin (recorded on the caller's stream)
+  // the running transfer's kernels report bad block ids here: the error word
+  // of the stream the caller passed
+  int* err_word = nullptr;
+
+  // deferred store (kvx_offload_begin / kvx_offload_wait) and asynchronous
+  // restore (kvx_restore_begin / kvx_restore_wait): the gathers or scatters
+  // run on store_stream after store_begin (recorded on the caller's stream);
+  // an asynchronous restore records restore_end on it after its last scatter
   hipStream_t store_stream = nullptr;
   hipEvent_t store_begin = nullptr;
+  hipEvent_t restore_end = nullptr;
   std::thread async_th;
   std::atomic<bool> async_busy{false};
+  Dir async_dir = Dir::kNone;
   kvx_status async_status = KVX_OK;
 
   // storage tier: the bound chunks live in files (kvx_ring_bind_files /
@@ -208,6 +216,8 @@ void destroy_resources(kvx_ring* r) {
   r->store_stream = nullptr;
   if (r->store_begin) (void)hipEventDestroy(r->store_begin);
   r->store_begin = nullptr;
+  if (r->restore_end) (void)hipEventDestroy(r->restore_end);
+  r->restore_end = nullptr;
   if (r->host) (void)hipHostFree(r->host);
   r->host = nullptr;
   if (r->owns_landing && r->landing) (void)hipFree(r->landing);
@@ -535,7 +545,7 @@ kvx_status launch_piece(kvx_ring* r, bool to_packed, const kvx::Piece& p, const 
                         uint8_t* dslot, hipStream_t stream) {
   return kvx::launch_copy_chunks(to_packed, &r->cache, p.l_begin, p.l_end, bt, r->plan.table_len,
                                  r->d_refs + p.ref_first, p.ref_count, r->chunk_tokens, dslot,
-                                 r->slot_bytes, stream);
+                                 r->slot_bytes, stream, r->err_word);
 }
 
 // One async copy on a DMA engine (engine 0: the runtime's choice); the copy
@@ -616,13 +626,16 @@ kvx_status resolve_piece(kvx_ring* r, const kvx::Piece& p, const std::vector<voi
   return KVX_OK;
 }
 
-kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream) {
+// Run the bound transfer, its kernels on `stream` reporting bad ids to err.
+kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int* err) {
   if (r->dir != dir) return KVX_EINVAL;
   if (r->closed.load()) return KVX_ECLOSED;
   if (r->plan.pieces.empty()) return KVX_OK;
   if (!bt) return KVX_EINVAL;
   DeviceGuard dg(r->device);
   if (!dg.ok) return KVX_EHIP;
+  if (!err) return KVX_EHIP;
+  r->err_word = err;
   const auto t_start = clk::now();
   const int32_t S = r->n_slots, T = r->threads;
   const int64_t P = (int64_t)r->plan.pieces.size();
@@ -1280,13 +1293,59 @@ bool make_store_stream(kvx_ring* r) {
       return false;
     }
   }
-  if (hipEventCreateWithFlags(&r->store_begin, hipEventDisableTiming) != hipSuccess) {
+  if (hipEventCreateWithFlags(&r->store_begin, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&r->restore_end, hipEventDisableTiming) != hipSuccess) {
+    if (r->store_begin) (void)hipEventDestroy(r->store_begin);
     (void)hipStreamDestroy(r->store_stream);
     r->store_stream = nullptr;
     r->store_begin = nullptr;
+    r->restore_end = nullptr;
     return false;
   }
   return true;
+}
+
+// kvx_offload_begin / kvx_restore_begin: the bound transfer on a thread of
+// the ring's own, its kernels on the ring's stream after the work already
+// enqueued on the caller's stream, reporting bad ids to the caller's stream.
+kvx_status start_async(kvx_ring* ring, Dir dir, const int32_t* block_table, hipStream_t stream) {
+  if (!ring) return KVX_EINVAL;
+  if (ring->async_busy.load()) return KVX_EBUSY;
+  if (ring->dir != dir) return KVX_EINVAL;
+  if (ring->closed.load()) return KVX_ECLOSED;
+  if (!block_table && !ring->plan.pieces.empty()) return KVX_EINVAL;
+  try {
+    DeviceGuard dg(ring->device);
+    if (!dg.ok) return KVX_EHIP;
+    if (!ring->store_stream && !make_store_stream(ring)) return KVX_EHIP;
+    int* err = kvx::stream_error_word(stream);
+    if (!err) return KVX_EHIP;
+    if (hipEventRecord(ring->store_begin, stream) != hipSuccess ||
+        hipStreamWaitEvent(ring->store_stream, ring->store_begin, 0) != hipSuccess)
+      return KVX_EHIP;
+    hipStream_t own = ring->store_stream;
+    ring->async_status = KVX_OK;
+    ring->async_dir = dir;
+    ring->async_busy.store(true);
+    ring->async_th = std::thread([ring, dir, block_table, own, err] {
+      kvx_status st;
+      try {
+        st = run(ring, dir, block_table, own, err);
+      } catch (...) {
+        st = KVX_EINTERNAL;
+      }
+      if (dir == Dir::kRestore) {
+        DeviceGuard g(ring->device);
+        if ((!g.ok || hipEventRecord(ring->restore_end, own) != hipSuccess) && st == KVX_OK)
+          st = KVX_EHIP;
+      }
+      ring->async_status = st;
+    });
+    return KVX_OK;
+  } catch (...) {
+    ring->async_busy.store(false);
+    return KVX_EINTERNAL;
+  }
 }
 
 }  // namespace
@@ -1444,7 +1503,7 @@ kvx_status kvx_restore_from_staging(kvx_ring* ring, const int32_t* block_table,
   if (!ring) return KVX_EINVAL;
   if (ring->async_busy.load()) return KVX_EBUSY;
   try {
-    return run(ring, Dir::kRestore, block_table, stream);
+    return run(ring, Dir::kRestore, block_table, stream, kvx::stream_error_word(stream));
   } catch (...) {
     return KVX_EINTERNAL;
   }
@@ -1454,50 +1513,47 @@ kvx_status kvx_offload_to_staging(kvx_ring* ring, const int32_t* block_table, hi
   if (!ring) return KVX_EINVAL;
   if (ring->async_busy.load()) return KVX_EBUSY;
   try {
-    return run(ring, Dir::kOffload, block_table, stream);
+    return run(ring, Dir::kOffload, block_table, stream, kvx::stream_error_word(stream));
   } catch (...) {
     return KVX_EINTERNAL;
   }
 }
 
 kvx_status kvx_offload_begin(kvx_ring* ring, const int32_t* block_table, hipStream_t stream) {
-  if (!ring) return KVX_EINVAL;
-  if (ring->async_busy.load()) return KVX_EBUSY;
-  if (ring->dir != Dir::kOffload) return KVX_EINVAL;
-  if (ring->closed.load()) return KVX_ECLOSED;
-  if (!block_table && !ring->plan.pieces.empty()) return KVX_EINVAL;
-  try {
-    DeviceGuard dg(ring->device);
-    if (!dg.ok) return KVX_EHIP;
-    if (!ring->store_stream && !make_store_stream(ring)) return KVX_EHIP;
-    // the gathers follow the work already enqueued on the caller's stream
-    if (hipEventRecord(ring->store_begin, stream) != hipSuccess ||
-        hipStreamWaitEvent(ring->store_stream, ring->store_begin, 0) != hipSuccess)
-      return KVX_EHIP;
-    hipStream_t gather_stream = ring->store_stream;
-    ring->async_status = KVX_OK;
-    ring->async_busy.store(true);
-    ring->async_th = std::thread([ring, block_table, gather_stream] {
-      kvx_status st;
-      try {
-        st = run(ring, Dir::kOffload, block_table, gather_stream);
-      } catch (...) {
-        st = KVX_EINTERNAL;
-      }
-      ring->async_status = st;
-    });
-    return KVX_OK;
-  } catch (...) {
-    ring->async_busy.store(false);
-    return KVX_EINTERNAL;
-  }
+  return start_async(ring, Dir::kOffload, block_table, stream);
 }
 
 kvx_status kvx_offload_wait(kvx_ring* ring) {
   if (!ring) return KVX_EINVAL;
   if (!ring->async_busy.load()) return KVX_OK;
+  if (ring->async_dir != Dir::kOffload) return KVX_EINVAL;
   if (ring->async_th.joinable()) ring->async_th.join();
   const kvx_status st = ring->async_status;
+  ring->async_busy.store(false);
+  return st;
+}
+
+kvx_status kvx_restore_begin(kvx_ring* ring, const int32_t* block_table, hipStream_t stream) {
+  return start_async(ring, Dir::kRestore, block_table, stream);
+}
+
+kvx_status kvx_restore_wait(kvx_ring* ring, hipStream_t stream) {
+  if (!ring) return KVX_EINVAL;
+  if (!ring->async_busy.load()) return KVX_OK;
+  if (ring->async_dir != Dir::kRestore) return KVX_EINVAL;
+  if (ring->async_th.joinable()) ring->async_th.join();
+  kvx_status st = ring->async_status;
+  try {
+    // the caller's stream continues after the last scatter (restore_end was
+    // recorded on the ring's stream after it, also after a failure, so that
+    // the stream never waits on an event that was not recorded)
+    DeviceGuard dg(ring->device);
+    if (!dg.ok || hipStreamWaitEvent(stream, ring->restore_end, 0) != hipSuccess) {
+      if (st == KVX_OK) st = KVX_EHIP;
+    }
+  } catch (...) {
+    if (st == KVX_OK) st = KVX_EINTERNAL;
+  }
   ring->async_busy.store(false);
   return st;
 }

@@ -111,3 +111,50 @@ def first_mismatch(a: np.ndarray, b: np.ndarray, step: int = 1 << 28):
         if not np.array_equal(x, y):
             return s + int(np.flatnonzero(x != y)[0])
     return None
+
+
+def generator_tensor(shape: Shape, fill: Filled, layer: int, kv: int, threads=16) -> np.ndarray:
+    """The whole cache tensor (layer, K|V) as the generator filled it."""
+    buf = np.empty(shape.num_blocks * shape.slab_bytes, dtype=np.uint8)
+    kvsynth.fill_host(buf, fill.seed, kvsynth.cache_stream(fill.role, layer, kv), mode=fill.mode,
+                      threads=threads)
+    return buf
+
+
+def oracle_layer_after_scatters(shape: Shape, fill: Filled, layer: int, chunks,
+                                chunk_tokens: int):
+    """Expected cache tensors (layer, K) and (layer, V) after scattering a list
+    of chunk images into a cache the generator filled: the generator's content
+    of the whole tensor, then the oracle scatter of each chunk restricted to
+    this layer. chunks: (image, block ids, l0) with image the packed image of
+    one chunk (len(ids) blocks) over layers [l0, ...); a chunk's layer-l part
+    is one contiguous run of its K then V slabs (the layer-major chunk
+    layout), which is itself that chunk's image over [layer, layer + 1)
+    (the layer-decomposition pin; tests/test_kvtest_util.py checks this
+    function against the oracle's scatter of the whole chunks)."""
+    dummy = np.zeros(16, dtype=np.uint8)
+    k = [dummy] * shape.num_layers
+    v = [dummy] * shape.num_layers
+    k[layer] = generator_tensor(shape, fill, layer, 0)
+    v[layer] = generator_tensor(shape, fill, layer, 1)
+    u = shape.slab_bytes
+    for img, ids, l0 in chunks:
+        n = len(ids)
+        part = img[(layer - l0) * 2 * n * u:(layer - l0 + 1) * 2 * n * u]
+        oracle.scatter(shape, k, v, layer, layer + 1, ids, chunk_tokens, part)
+    return k[layer], v[layer]
+
+
+def check_layer_after_scatters(cache, shape: Shape, fill: Filled, layer: int, chunks,
+                               chunk_tokens: int, what: str) -> None:
+    """Every byte of cache tensors (layer, K) and (layer, V) on the device
+    against oracle_layer_after_scatters: the scattered slabs, and every other
+    block unchanged."""
+    u = shape.slab_bytes
+    exp = oracle_layer_after_scatters(shape, fill, layer, chunks, chunk_tokens)
+    for kv in (0, 1):
+        got = to_host((cache.k if kv == 0 else cache.v)[layer])
+        bad = first_mismatch(got, exp[kv])
+        if bad is not None:
+            raise AssertionError(f"{what}: layer {layer} kv {kv} differs at byte {bad} "
+                                 f"(block {bad // u})")

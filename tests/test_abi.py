@@ -21,7 +21,7 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def _declared_functions():
     text = open(os.path.join(ROOT, "include", "kvx.h")).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(kvx_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(kvx_[A-Za-z0-9_]+)\s*\(", text)))
 
 
 def test_header_declares_the_three_path_calls():
@@ -148,8 +148,67 @@ def test_plan_rejects_slot_smaller_than_one_layer():
         kvx.kvx_plan_pieces(c, 0, 4, 16, 256, (1 << 20) - 4096)
 
 
+def _ramp_caps(n_pieces, slot, ramp):
+    caps = [slot] * n_pieces
+    first = [slot >> 3, slot >> 2, slot >> 1]
+    for k in range(min(3, n_pieces)):
+        if ramp == kvx.KVX_RAMP_FIRST:
+            caps[k] = first[k]
+        elif ramp == kvx.KVX_RAMP_LAST:
+            caps[n_pieces - 1 - k] = first[k]
+    return caps
+
+
+@pytest.mark.parametrize("ramp", [kvx.KVX_RAMP_FIRST, kvx.KVX_RAMP_LAST])
+@pytest.mark.parametrize("case", PLAN_CASES)
+def test_ramped_plan_tiles_image_within_limits(case, ramp):
+    """The ring's ramped plans: the pieces tile the image exactly once, each
+    within its limit (or one layer of a chunk where a layer exceeds it), each
+    carries its chunks in image order (one host copy per piece of a
+    contiguous image), and the end ramp mirrors the first-piece ramp."""
+    L, H, D, BS, n, ct, slot = case
+    c = kvx.shape_only_cache(L, 4 * n + 8, BS, H, D, 2)
+    slab = BS * H * D * 2
+    pieces = kvx.kvx_plan_pieces(c, 0, L, n, ct, slot, ramp)
+    caps = _ramp_caps(len(pieces), slot, ramp)
+    bpc = ct // BS
+    covered = []
+    for p, cap in zip(pieces, caps):
+        layer = min(bpc, n) * 2 * slab  # one layer of a full chunk
+        assert 0 < p["bytes"] <= max(cap, layer if p["l_end"] - p["l_begin"] == 1 else 0), p
+        assert p["bytes"] == p["n_blocks"] * (p["l_end"] - p["l_begin"]) * 2 * slab
+        assert p["n_spans"] == 1
+        covered.append((p["src_offset"], p["bytes"]))
+    at = 0
+    for off, b in sorted(covered):
+        assert off == at
+        at += b
+    assert at == kvx.kvx_packed_bytes(c, 0, L, n)
+    if n % bpc == 0:  # all chunks alike: the end ramp is the first ramp reversed
+        other = kvx.kvx_plan_pieces(c, 0, L, n, ct, slot, 3 - ramp)
+        assert [p["bytes"] for p in pieces] == [p["bytes"] for p in reversed(other)]
+
+
+def test_ramped_80k_restore_plan():
+    """The restore's first-piece ramp at 80k: the first 32 MiB chunk is cut
+    into 8, 16 and 8 MiB layer ranges, then 156 two-chunk pieces."""
+    c = kvx.shape_only_cache(32, 20000, 16, 8, 128, 2)
+    pieces = kvx.kvx_plan_pieces(c, 0, 32, 5000, 256, 64 << 20, kvx.KVX_RAMP_FIRST)
+    assert len(pieces) == 159
+    assert [p["bytes"] >> 20 for p in pieces[:4]] == [8, 16, 8, 64]
+    assert [(p["l_begin"], p["l_end"]) for p in pieces[:3]] == [(0, 8), (8, 24), (24, 32)]
+    # the end ramp starts from the compact 16 MiB last chunk: 8 + 8 MiB
+    # layer halves, the 32 MiB chunk before it alone
+    end = kvx.kvx_plan_pieces(c, 0, 32, 5000, 256, 64 << 20, kvx.KVX_RAMP_LAST)
+    assert [p["bytes"] >> 20 for p in end[-3:]] == [32, 8, 8]
+    assert [(p["l_begin"], p["l_end"]) for p in end[-2:]] == [(16, 32), (0, 16)]
+    with pytest.raises(kvx.KvxError):
+        kvx.kvx_plan_pieces(c, 0, 32, 5000, 256, 64 << 20, 3)
+
+
+@pytest.mark.parametrize("ramp", [kvx.KVX_RAMP_NONE, kvx.KVX_RAMP_FIRST, kvx.KVX_RAMP_LAST])
 @pytest.mark.parametrize("case", PLAN_CASES[4:] + [(4, 2, 8, 4, 23, 16, 2048), (6, 1, 8, 2, 13, 8, 256)])
-def test_scattering_pieces_equals_scattering_image(case):
+def test_scattering_pieces_equals_scattering_image(case, ramp):
     """Every piece is a plain scatter of its bytes; together they reproduce the
     oracle's scatter of the whole image (restore transparency, on the CPU)."""
     L, H, D, BS, n, ct, slot = case
@@ -161,7 +220,7 @@ def test_scattering_pieces_equals_scattering_image(case):
     whole = oracle.new_mirror(s)
     oracle.scatter(s, *whole, 0, L, bt, ct, img)
     by_piece = oracle.new_mirror(s)
-    for p in kvx.kvx_plan_pieces(c, 0, L, n, ct, slot):
+    for p in kvx.kvx_plan_pieces(c, 0, L, n, ct, slot, ramp):
         part = img[p["src_offset"]:p["src_offset"] + p["bytes"]]
         oracle.scatter(s, *by_piece, p["l_begin"], p["l_end"],
                        bt[p["bt_first"]:p["bt_first"] + p["n_blocks"]], p["chunk_tokens"], part)

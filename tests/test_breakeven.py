@@ -63,6 +63,55 @@ def test_oracle_linear_closed_forms(c0, a, c1, b, gran):
         assert math.isclose(ob.max_io(f, g, cp, D), (c0 - c1) + (a - b + k) * D, rel_tol=1e-12)
 
 
+# The paper's 3B model moves 114,688 B of KV per token (Sec. 2.1); at a
+# restore rate R (GB/s) a fully cached x-token prompt takes c1 + (b + beta/R) x
+# with beta = 114,688 B/token over R * 1e9 B/s. The threshold is then the first
+# grid size above (c1 - c0) / (a - b - beta / (R * 1e9)).
+RATES = [(0.02, 2.0e-5, 0.05, 0.5e-5, 16, 55.0), (0.10, 1.0e-4, 0.30, 0.3e-4, 64, 5.2)]
+
+
+@pytest.mark.parametrize("c0,a,c1,b,gran,rate", RATES)
+def test_oracle_hit_from_rate_closed_forms(c0, a, c1, b, gran, rate):
+    beta = 114688
+    f = lambda x: ob.curve(*lin(c0, a), x)  # noqa: E731
+    g0 = lambda x: ob.curve(*lin(c1, b), x)  # noqa: E731
+    g = ob.hit_from_rate(g0, beta, rate)
+    assert math.isclose(g(81920), c1 + b * 81920 + 81920 * beta / (rate * 1e9), rel_tol=1e-12)
+    x_star = _grid_above((c1 - c0) / (a - b - beta / (rate * 1e9)), gran)
+    assert ob.break_even_tokens(f, g, 200000, gran) == x_star
+    assert x_star != _grid_above((c1 - c0) / (a - b), gran)  # the transfer term matters
+    # required bandwidth: the document's bytes over max_io, copy = k x
+    k = 1.5e-6
+    copy = lambda x: k * x  # noqa: E731
+    for D in (1024, 8192, 81920):
+        budget = c0 + a * D - (c1 + b * D + D * beta / (rate * 1e9) - k * D)
+        want = D * beta / budget / 1e9 if budget > 0 else math.inf
+        got = ob.required_GBps(f, g, copy, D, beta)
+        assert got == want or math.isclose(got, want, rel_tol=1e-9)
+    assert ob.required_GBps(f, lambda x: f(x) + 1.0, lambda x: 0.0, 1000, beta) == math.inf
+
+
+@pytest.mark.parametrize("c0,a,c1,b,gran,rate", RATES)
+def test_library_rate_calls_match_oracle(c0, a, c1, b, gran, rate):
+    beta = 114688
+    cold, base = be.Curve(*lin(c0, a)), be.Curve(*lin(c1, b))
+    f = lambda x: ob.curve(*lin(c0, a), x)  # noqa: E731
+    g = ob.hit_from_rate(lambda x: ob.curve(*lin(c1, b), x), beta, rate)
+    hit = be.hit_curve_from_restore(base, beta, rate)
+    for x in (1000.0, 5000.0, 9000.0, 81920.0):
+        assert math.isclose(hit(x), g(x), rel_tol=1e-12)
+    assert be.tier_threshold(cold, base, beta, rate, 200000, gran) == \
+        ob.break_even_tokens(f, g, 200000, gran)
+    copy = be.Curve([1000.0, 9000.0], [1.5e-3, 13.5e-3])
+    for D in (1024, 8192, 81920):
+        want = ob.required_GBps(f, g, lambda x: 1.5e-6 * x, D, beta)
+        assert math.isclose(be.required_GBps(cold, hit, copy, D, beta), want, rel_tol=1e-9)
+    with pytest.raises(be.KvxError):
+        be.hit_curve_from_restore(base, beta, 0.0)
+    with pytest.raises(be.KvxError):
+        be.tier_threshold(cold, base, 0, rate, 200000, gran)
+
+
 def test_oracle_special_cases():
     f = lambda x: ob.curve(*lin(0.05, 2e-5), x)  # noqa: E731
     # a hit that costs as much as recomputing never pays (fixed cost counted twice)

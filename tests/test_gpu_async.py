@@ -1,0 +1,291 @@
+"""Asynchronous restore (kvx_restore_begin / kvx_restore_wait), per-stream
+error words, gathers that name a block more than once, and the break-even gate
+fed by a restore rate measured on the GPU.
+
+Every data check is against the oracle on generator inputs (whole cache
+tensors: the restored slabs and every other block)."""
+import statistics
+import time
+
+import numpy as np
+import pytest
+
+import kvsynth
+import oracle
+import oracle.breakeven as ob
+from kvtest_util import Filled, device_cache, host_mirror, seeded_ids, shape_8b, to_host
+
+torch = pytest.importorskip("torch")
+import paper_2609_11744_amd as kvx  # noqa: E402
+from paper_2609_11744_amd import breakeven as be  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda:0"
+
+
+def _bt(ids):
+    return torch.from_numpy(np.ascontiguousarray(ids, dtype=np.int32)).to(DEV)
+
+
+def _image(nbytes, seed, pinned):
+    if pinned:
+        img = kvx.PinnedBuffer(nbytes)
+        kvsynth.fill_host(img.array, seed, kvsynth.image_stream(7), mode=kvsynth.MODE_RAW)
+        return img, img.array
+    a = kvsynth.host_bytes(nbytes, seed, kvsynth.image_stream(7), mode=kvsynth.MODE_RAW)
+    return a, a
+
+
+# ---- asynchronous restore ---------------------------------------------------------
+
+@pytest.mark.parametrize("threads", [3, 0])
+def test_restore_begin_wait_bit_exact(threads):
+    """The restore runs on the ring's thread; after kvx_restore_wait, work on
+    the caller's stream (here a snapshot copy, with no host wait in between)
+    sees every restored block, and nothing else changed."""
+    s = oracle.Shape(4, 800, 16, 2, 64, 2)
+    n, ct, seed = 300, 64, 71 + threads
+    (bt,) = seeded_ids(seed, s.num_blocks, n)
+    fill = Filled(seed, kvsynth.ROLE_DST, kvsynth.MODE_RAW)
+    cache = device_cache(s, fill, DEV)
+    src, img = _image(oracle.packed_bytes(s, 0, 4, n), seed, pinned=threads == 0)
+    ring = kvx.StagingRing(DEV, 2, 96 << 10)
+    stream = torch.cuda.Stream()
+    try:
+        ring.bind(cache, 0, 4, n, ct, src, fill_threads=threads)
+        torch.cuda.synchronize()
+        kvx.kvx_restore_begin(ring, _bt(bt), stream=stream)
+        for call in (lambda: kvx.kvx_restore_from_staging(ring, _bt(bt)),
+                     lambda: kvx.kvx_restore_begin(ring, _bt(bt)),
+                     lambda: ring.bind(cache, 0, 4, n, ct, src, fill_threads=threads),
+                     lambda: ring.stats()):
+            with pytest.raises(kvx.KvxError) as ei:
+                call()
+            assert ei.value.status == kvx.KVX_EBUSY
+        kvx.kvx_restore_wait(ring, stream=stream)
+        with torch.cuda.stream(stream):
+            snap_k = [t.clone() for t in cache.k]
+            snap_v = [t.clone() for t in cache.v]
+        stream.synchronize()
+        kvx.kvx_check(stream)
+        kvx.kvx_restore_wait(ring, stream=stream)  # nothing pending: returns at once
+        assert ring.stats()["pieces"] > 2
+    finally:
+        ring.close()
+    mirror = host_mirror(s, fill, range(s.num_blocks))
+    oracle.restore(s, *mirror, 0, 4, bt, ct, img)
+    for l in range(4):
+        assert np.array_equal(to_host(snap_k[l]), mirror[0][l]), f"K layer {l}"
+        assert np.array_equal(to_host(snap_v[l]), mirror[1][l]), f"V layer {l}"
+
+
+def test_restore_and_offload_started_together():
+    """One thread starts a restore on one ring and an offload on another, then
+    collects both: the restored blocks and the offloaded images are the
+    oracle's."""
+    s = oracle.Shape(3, 900, 16, 2, 64, 2)
+    ct, seed = 64, 75
+    bt_r, bt_o = seeded_ids(seed, s.num_blocks, 250, 170)
+    fill = Filled(seed, kvsynth.ROLE_NEW, kvsynth.MODE_RAW)
+    cache = device_cache(s, fill, DEV)
+    src, img = _image(oracle.packed_bytes(s, 0, 3, 250), seed, pinned=False)
+    per_block = oracle.packed_bytes(s, 0, 3, 1)
+    sinks = [(np.full(min(4, 170 - b) * per_block, 0xEE, np.uint8), b, min(4, 170 - b))
+             for b in range(0, 170, 4)]
+    r_ring, o_ring = kvx.StagingRing(DEV, 2, 64 << 10), kvx.StagingRing(DEV, 2, 64 << 10)
+    s_r, s_o = torch.cuda.Stream(), torch.cuda.Stream()
+    try:
+        r_ring.bind(cache, 0, 3, 250, ct, src, fill_threads=2)
+        o_ring.bind_offload(cache, 0, 3, ct, sinks, drain_threads=2)
+        torch.cuda.synchronize()
+        kvx.kvx_restore_begin(r_ring, _bt(bt_r), stream=s_r)
+        kvx.kvx_offload_begin(o_ring, _bt(bt_o), stream=s_o)
+        kvx.kvx_offload_wait(o_ring)
+        kvx.kvx_restore_wait(r_ring, stream=s_r)
+        s_r.synchronize()
+        kvx.kvx_check(s_r)
+        kvx.kvx_check(s_o)
+    finally:
+        r_ring.close()
+        o_ring.close()
+    mirror = host_mirror(s, fill, range(s.num_blocks))
+    for a, b0, nb in sinks:
+        assert np.array_equal(a, oracle.gather(s, *mirror, 0, 3, bt_o[b0:b0 + nb], ct)), b0
+    oracle.restore(s, *mirror, 0, 3, bt_r, ct, img)
+    for l in range(3):
+        assert np.array_equal(to_host(cache.k[l]), mirror[0][l]), f"K layer {l}"
+        assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
+
+
+def test_abort_during_async_restore():
+    s = oracle.Shape(2, 3000, 16, 2, 64, 2)
+    n = 1200
+    (bt,) = seeded_ids(77, s.num_blocks, n)
+    cache = device_cache(s, Filled(77, kvsynth.ROLE_DST), DEV)
+    src, _ = _image(oracle.packed_bytes(s, 0, 2, n), 77, pinned=False)
+    ring = kvx.StagingRing(DEV, 2, 64 << 10)
+    stream = torch.cuda.Stream()
+    try:
+        ring.set_test_hooks(max_delay_us=20000)  # slow fills: the abort lands mid-transfer
+        ring.bind(cache, 0, 2, n, 64, src, fill_threads=2)
+        kvx.kvx_restore_begin(ring, _bt(bt), stream=stream)
+        time.sleep(0.05)
+        ring.abort()
+        t0 = time.perf_counter()
+        with pytest.raises(kvx.KvxError) as ei:
+            kvx.kvx_restore_wait(ring, stream=stream)
+        assert ei.value.status == kvx.KVX_ECLOSED
+        assert time.perf_counter() - t0 < 5.0
+        stream.synchronize()
+        kvx.kvx_check(stream)
+    finally:
+        ring.close()
+
+
+# ---- error words, one per stream ----------------------------------------------------
+
+def test_error_words_are_per_stream():
+    """Two streams run gathers at the same time, only one with an id outside
+    the pool: only that stream's check reports KVX_EBADBLOCK (and clears it);
+    the other stream's check and the null stream's check report nothing, and
+    the good stream's images are the oracle's."""
+    s = oracle.Shape(2, 400, 16, 2, 64, 2)
+    n, ct = 120, 64
+    fill = Filled(81, kvsynth.ROLE_SRC, kvsynth.MODE_RAW)
+    cache = device_cache(s, fill, DEV)
+    (good,) = seeded_ids(81, s.num_blocks, n)
+    bad = good.copy()
+    bad[7] = s.num_blocks + 5
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    nbytes = oracle.packed_bytes(s, 0, 2, n)
+    d1 = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    d2 = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    bad_d, good_d = _bt(bad), _bt(good)
+    torch.cuda.synchronize()
+    for _ in range(4):
+        kvx.kvx_gather_blocks(cache, 0, 2, bad_d, n, ct, d1, stream=s1)
+        kvx.kvx_gather_blocks(cache, 0, 2, good_d, n, ct, d2, stream=s2)
+    kvx.kvx_check(s2)
+    kvx.kvx_check()
+    with pytest.raises(kvx.KvxError) as ei:
+        kvx.kvx_check(s1)
+    assert ei.value.status == kvx.KVX_EBADBLOCK
+    kvx.kvx_check(s1)  # read and cleared
+    mirror = host_mirror(s, fill, good)
+    assert np.array_equal(to_host(d2), oracle.gather(s, *mirror, 0, 2, good, ct))
+    # a bad chunk reference reports KVX_EINVAL to its own stream only
+    refs = kvx.chunk_refs([(0, 0, 4), (1 << 40, 4, 4)], DEV)
+    kvx.kvx_gather_chunks(cache, 0, 2, good_d, n, refs, 2, ct, d1, stream=s1)
+    kvx.kvx_gather_blocks(cache, 0, 2, good_d, n, ct, d2, stream=s2)
+    kvx.kvx_check(s2)
+    with pytest.raises(kvx.KvxError) as ei:
+        kvx.kvx_check(s1)
+    assert ei.value.status == kvx.KVX_EINVAL
+
+
+def test_ring_reports_to_the_callers_stream():
+    """An asynchronous restore's scatters run on the ring's own stream but
+    report a bad id to the stream the caller passed."""
+    s = oracle.Shape(2, 400, 16, 2, 64, 2)
+    n = 64
+    (bt,) = seeded_ids(83, s.num_blocks, n)
+    bt[10] = -1
+    cache = device_cache(s, Filled(83, kvsynth.ROLE_DST), DEV)
+    src, _ = _image(oracle.packed_bytes(s, 0, 2, n), 83, pinned=False)
+    ring = kvx.StagingRing(DEV, 2, 64 << 10)
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    try:
+        ring.bind(cache, 0, 2, n, 64, src, fill_threads=1)
+        kvx.kvx_restore_begin(ring, _bt(bt), stream=s1)
+        kvx.kvx_restore_wait(ring, stream=s1)
+        kvx.kvx_check(s2)
+        with pytest.raises(kvx.KvxError) as ei:
+            kvx.kvx_check(s1)
+        assert ei.value.status == kvx.KVX_EBADBLOCK
+    finally:
+        ring.close()
+
+
+# ---- gathers that name a block more than once -------------------------------------
+
+@pytest.mark.parametrize("shape,n,distinct,ct", [
+    (oracle.Shape(3, 300, 16, 2, 64, 2), 200, 50, 64),
+    (oracle.Shape(8, 2000, 16, 8, 128, 2), 1500, 400, 256),
+])
+def test_gather_with_repeated_ids_bit_exact(shape, n, distinct, ct):
+    """A gather's ids may repeat (it only reads them): every occurrence packs
+    the same block's slabs."""
+    rng = np.random.default_rng(n)
+    pool = rng.permutation(shape.num_blocks)[:distinct].astype(np.int32)
+    ids = pool[rng.integers(0, distinct, size=n)]
+    assert len(set(ids.tolist())) < n
+    fill = Filled(n, kvsynth.ROLE_SRC)
+    cache = device_cache(shape, fill, DEV)
+    mirror = host_mirror(shape, fill, pool)
+    L = shape.num_layers
+    want = oracle.gather(shape, *mirror, 0, L, ids, ct)
+    dst = torch.empty(want.size, dtype=torch.uint8, device=DEV)
+    kvx.kvx_gather_blocks(cache, 0, L, _bt(ids), n, ct, dst)
+    torch.cuda.synchronize()
+    kvx.kvx_check()
+    assert np.array_equal(to_host(dst), want)
+
+
+# ---- the gate fed by the measured restore rate (Secs. 5.2, 6.6) ----------------------
+
+# A stated synthetic calibration for an 8B-shaped model (no model runs here):
+# cold TTFT f(x) = 0.012 + 1.4e-5 x + 2.2e-10 x^2 s, the hit path's non-transfer
+# part 0.010 + 1.0e-7 x s, at knots 1k .. 128k tokens.
+KNOTS = [1024.0, 4096.0, 8192.0, 16384.0, 32768.0, 65536.0, 131072.0]
+COLD = [0.012 + 1.4e-5 * x + 2.2e-10 * x * x for x in KNOTS]
+BASE = [0.010 + 1.0e-7 * x for x in KNOTS]
+
+
+def test_gate_from_measured_restore_rate():
+    """Restore 1 GiB of an 8B-shaped cache through a 4 x 64 MiB ring, time it,
+    and feed the measured rate (and a slower tier's, a twentieth of it) to the
+    library's gate; the thresholds, transfer budgets and required bandwidths
+    equal the oracle's fed the same rate."""
+    s = shape_8b(1100)
+    n = 512
+    (bt,) = seeded_ids(85, s.num_blocks, n)
+    cache = device_cache(s, Filled(85, kvsynth.ROLE_DST), DEV)
+    nbytes = oracle.packed_bytes(s, 0, 32, n)
+    img = kvx.PinnedBuffer(nbytes)
+    kvsynth.fill_host(img.array, 85, kvsynth.image_stream(8), threads=16)
+    ring = kvx.StagingRing(DEV, 4, 64 << 20)
+    times = []
+    try:
+        ring.bind(cache, 0, 32, n, 256, img, fill_threads=8)
+        bt_d = _bt(bt)
+        for i in range(4):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            kvx.kvx_restore_from_staging(ring, bt_d)
+            torch.cuda.synchronize()
+            if i:
+                times.append(time.perf_counter() - t0)
+        kvx.kvx_check()
+    finally:
+        ring.close()
+        img.free()
+    rate = nbytes / statistics.median(times) / 1e9
+    print(f"\nmeasured restore rate {rate:.2f} GB/s", flush=True)
+    assert rate > 1.0
+    bpt = kvx.kvx_bytes_per_token(32, 8, 128, 2)
+    cold, base = be.Curve(KNOTS, COLD), be.Curve(KNOTS, BASE)
+    f = lambda x: ob.curve(KNOTS, COLD, x)  # noqa: E731
+    g0 = lambda x: ob.curve(KNOTS, BASE, x)  # noqa: E731
+    for r in (rate, rate / 20, rate / 400):
+        g = ob.hit_from_rate(g0, bpt, r)
+        assert be.tier_threshold(cold, base, bpt, r, 131072, 256) == \
+            ob.break_even_tokens(f, g, 131072, 256), r
+        hit = be.hit_curve_from_restore(base, bpt, r)
+        copy_t = [x * bpt / (r * 1e9) for x in KNOTS]
+        copy = be.Curve(KNOTS, copy_t)
+        for D in (1024, 8192, 81920):
+            assert be.break_even_prefix(cold, hit, D, 256) == ob.break_even_prefix(f, g, D, 256)
+            mi = ob.max_io(f, g, lambda x: x * bpt / (r * 1e9), D)
+            assert np.isclose(be.max_io(cold, hit, copy, D), mi, rtol=1e-9)
+            want = ob.required_GBps(f, g, lambda x: x * bpt / (r * 1e9), D, bpt)
+            assert np.isclose(be.required_GBps(cold, hit, copy, D, bpt), want, rtol=1e-9)

@@ -1,12 +1,13 @@
 """GPU parity of the batched path: fused chunk-list gather / scatter, chunk-list
 staged restore, staged offload, and one batched step (restore of the distinct
 missing chunks of a request batch concurrent with the offload of their new
-blocks), against the oracle.
+blocks, both started from one thread with kvx_restore_begin and
+kvx_offload_begin), against the oracle.
 
 The oracle's side of a chunk list is the plain definition: chunk c is the
 oracle gather of its own blocks, as one chunk, placed at its packed offset.
 """
-import threading
+import time
 
 import numpy as np
 import pytest
@@ -14,8 +15,9 @@ import pytest
 import kvsynth
 import kvsynth.prefix_tree as pt
 import oracle
-from kvtest_util import (Filled, device_cache, first_mismatch, host_mirror, mirror_slabs,
-                         read_slabs, seeded_ids, shape_70b, to_host)
+import oracle.prefix as oracle_prefix
+from kvtest_util import (Filled, check_layer_after_scatters, device_cache, first_mismatch,
+                         host_mirror, mirror_slabs, read_slabs, seeded_ids, shape_70b, to_host)
 
 torch = pytest.importorskip("torch")
 import paper_2609_11744_amd as kvx  # noqa: E402
@@ -250,47 +252,40 @@ def _run_step(s, reqs, plan, seed, slots=4, slot_bytes=64 << 20, threads=8, laye
                             drain_threads=threads)
         rbt_d, obt_d = _bt(rbt), _bt(obt)
         s_r, s_o = torch.cuda.Stream(), torch.cuda.Stream()
-        errors = []
-
-        def restore():
-            try:
-                import time
-                t0 = time.perf_counter()
-                kvx.kvx_restore_from_staging(r_ring, rbt_d, stream=s_r)
-                s_r.synchronize()
-                timings["restore_s"] = time.perf_counter() - t0
-            except Exception as e:  # noqa: BLE001
-                errors.append(e)
-
-        def offload():
-            try:
-                import time
-                t0 = time.perf_counter()
-                kvx.kvx_offload_to_staging(o_ring, obt_d, stream=s_o)
-                timings["offload_s"] = time.perf_counter() - t0
-            except Exception as e:  # noqa: BLE001
-                errors.append(e)
-
         torch.cuda.synchronize()
-        th = [threading.Thread(target=restore), threading.Thread(target=offload)]
-        for t in th:
-            t.start()
-        for t in th:
-            t.join()
-        if errors:
-            raise errors[0]
+        # both transfers run on the rings' own threads; this thread only
+        # starts and collects them
+        t0 = time.perf_counter()
+        kvx.kvx_restore_begin(r_ring, rbt_d, stream=s_r)
+        kvx.kvx_offload_begin(o_ring, obt_d, stream=s_o)
+        kvx.kvx_offload_wait(o_ring)
+        timings["offload_s"] = time.perf_counter() - t0
+        kvx.kvx_restore_wait(r_ring, stream=s_r)
+        s_r.synchronize()
+        timings["restore_s"] = time.perf_counter() - t0
         _check()
+        kvx.kvx_check(s_r)
+        kvx.kvx_check(s_o)
     finally:
         r_ring.close()
         o_ring.close()
     return cache, rbt, store, store_chunks, obt, sinks, timings
 
 
-def test_batched_step_small_shape_bit_exact():
-    """The whole step at a small shape (4 layers, 4 KiB slabs), every byte checked."""
+@pytest.mark.parametrize("share", ["chunk", "block"])
+def test_batched_step_small_shape_bit_exact(share):
+    """The whole step at a small shape (4 layers, 4 KiB slabs), every byte
+    checked; with share="block" shared prefixes end inside chunks, so a child
+    that extends its parent's partial chunk restores a chunk of its own."""
     seed = 5
-    reqs = pt.make_requests(seed, n=24, lo=256, hi=2048)
+    reqs = pt.make_requests(seed, n=24, lo=256, hi=2048, share=share)
     plan = step.plan_step(reqs, 16, 256)
+    if share == "block":
+        assert any(r.shared_tokens % 256 for r in reqs)
+        # the plan restores one chunk per distinct exact key (the oracle's plan)
+        want = oracle_prefix.plan_step(reqs, 16, 256)
+        assert [(c.n_blocks, c.origin, c.bt_offset) for c in plan.restore] == \
+            [(nb, o, bt) for _, nb, o, bt in want["restore"]]
     s = oracle.Shape(4, plan.restore_blocks + plan.offload_blocks + 32, 16, 2, 64, 2)
     cache, rbt, store, store_chunks, obt, sinks, _ = _run_step(
         s, reqs, plan, seed, slots=2, slot_bytes=192 << 10, threads=3)  # 1 layer of a full chunk = 128 KiB
@@ -323,33 +318,14 @@ def test_batched_step_70b_64_requests():
     rb, ob = plan.restore_blocks * per_block, plan.offload_blocks * per_block
     print(f"restore {rb / 1e9:.1f} GB in {t['restore_s']:.3f} s; offload {ob / 1e9:.1f} GB "
           f"in {t['offload_s']:.3f} s (concurrent)", flush=True)
-    # every restored block: gather the restore list back on the device, compare
-    # with the store, a batch of chunks at a time
-    refs = [(c.bt_offset * per_block, c.bt_offset, c.n_blocks) for c in plan.restore]
-    step_chunks = 64
-    buf = torch.empty(step_chunks * 16 * per_block, dtype=torch.uint8, device=DEV)
-    rbt_d = _bt(rbt)
-    for i in range(0, len(refs), step_chunks):
-        part = refs[i:i + step_chunks]
-        base = part[0][0]
-        rel = [(o - base, b, n) for o, b, n in part]
-        kvx.kvx_gather_chunks(cache, 0, 80, rbt_d, len(rbt), kvx.chunk_refs(rel, DEV), len(rel),
-                              256, buf)
-        end = part[-1][0] + part[-1][2] * per_block
-        want = torch.from_numpy(store[base:end]).to(DEV)
-        assert torch.equal(buf[:end - base], want), f"restored chunks {i}.. differ"
-    _check()
-    # the oracle's scatter on a seeded sample of restored chunks
-    pick = np.random.default_rng(1).choice(len(plan.restore), 24, replace=False)
-    mirror = oracle.new_mirror(s)
-    sample_ids = []
-    for i in pick:
-        img, bt0, nb = store_chunks[i]
-        oracle.scatter(s, *mirror, 0, 80, rbt[bt0:bt0 + nb], 256, img)
-        sample_ids += list(rbt[bt0:bt0 + nb])
-    _compare_blocks(cache, s, mirror, np.array(sample_ids), range(0, 80, 7), "70B restore")
-    # offload: every sink against the oracle gather of the new blocks
+    # every byte of every cache tensor against the oracle: the generator's
+    # content with each restored chunk scattered into it (restored slabs
+    # right, every other block unchanged), one layer at a time
     fill = Filled(seed, kvsynth.ROLE_NEW, kvsynth.MODE_NORMAL_BF16)
+    chunks = [(img, rbt[bt0:bt0 + nb], 0) for img, bt0, nb in store_chunks]
+    for l in range(80):
+        check_layer_after_scatters(cache, s, fill, l, chunks, 256, "70B restore")
+    # offload: every sink against the oracle gather of the new blocks
     src = host_mirror(s, fill, obt)
     for b, c in zip(sinks, plan.offload):
         exp = oracle.gather(s, *src, 0, 80, obt[c.bt_offset:c.bt_offset + c.n_blocks], 256)

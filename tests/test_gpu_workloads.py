@@ -6,8 +6,7 @@ times: the 8B-shaped 80k-token prefix (5,000 blocks of a 20,000-block pool,
 Every gathered image is compared with the oracle's image byte for byte.
 Scatters and restores are compared with the oracle's result on every slab
 they name (read back from the device), and every other block is checked
-unchanged on the device. Restores are also checked by gathering the restored
-blocks back (gather parity is established independently) against the image.
+unchanged on the device against a copy taken before the call.
 """
 import numpy as np
 import pytest
@@ -25,6 +24,8 @@ pytestmark = pytest.mark.gpu
 DEV = "cuda:0"
 NB = 20000
 SLOT = 64 << 20
+# Pieces of the ramped 80k restore plan (also checked on the CPU, test_abi).
+RAMPED_80K_PIECES = 159
 
 
 def _bt(ids):
@@ -110,30 +111,30 @@ def test_80k_staged_restore_4x64MiB(w80k):
     w = w80k
     if not hasattr(w, "packed"):
         pytest.skip("needs the gather of the first test")
+    del w.packed
+    torch.cuda.empty_cache()
     image = kvx.PinnedBuffer(w.nbytes)
     kvsynth.fill_host(image.array, w.seed, kvsynth.image_stream(1), threads=16)
+    before = ([t.clone() for t in w.cache.k], [t.clone() for t in w.cache.v])
     ring = kvx.StagingRing(DEV, 4, SLOT)
     try:
         ring.bind(w.cache, 0, 32, 5000, 256, image, fill_threads=8)
         kvx.kvx_restore_from_staging(ring, _bt(w.bt_rst))
         _check()
         # the plain plan's 157 pieces, with the restore's ramp cutting the
-        # first 32 MiB chunk into 8, 16 and 8 MiB pieces (1/8, 1/4, 1/2 slot):
-        # 3 + 156 two-chunk pieces (the last one 32 + 16 MiB)
-        assert ring.stats()["pieces"] == 159
+        # first 32 MiB chunk into 8, 16 and 8 MiB pieces (at most 1/8, 1/4,
+        # 1/2 slot): 3 + 156 two-chunk pieces (the last one 32 + 16 MiB)
+        assert ring.stats()["pieces"] == RAMPED_80K_PIECES
     finally:
         ring.close()
-    # round trip on the device: gather the restored blocks back
-    kvx.kvx_gather_blocks(w.cache, 0, 32, _bt(w.bt_rst), 5000, 256, w.packed)
-    _check()
-    bad = first_mismatch(to_host(w.packed), image.array)
-    assert bad is None, f"restored blocks gather back differently at byte {bad}"
-    # the oracle's restore, compared on a seeded sample of restored slabs
+    # the oracle's restore: every restored slab, and every other block unchanged
     oracle.restore(w.shape, *w.mirror, 0, 32, w.bt_rst, 256, image.array)
-    sample = np.random.default_rng(7).choice(w.bt_rst, 400, replace=False)
-    _compare_named_slabs(w.cache, w.shape, w.mirror, sample, "80k restore")
+    _compare_named_slabs(w.cache, w.shape, w.mirror, w.bt_rst, "80k restore")
+    _unchanged_except(w.cache, before, w.shape, w.bt_rst, "80k restore")
+    del before
+    torch.cuda.empty_cache()
     image.free()
-    del w.packed, w.expect
+    del w.expect
 
 
 # ---- 32k-token granularity sweep -------------------------------------------------
@@ -148,13 +149,16 @@ class Workload32k:
         self.mirror = host_mirror(self.shape, self.fill, self.bt_src)
         self.nbytes = oracle.packed_bytes(self.shape, 0, 32, 2048)
         self.packed = torch.empty(self.nbytes, dtype=torch.uint8, device=DEV)
+        # the cache as filled; the scatters and restores below write only the
+        # bt_dst blocks, so every other block must keep this content
+        self.before = ([t.clone() for t in self.cache.k], [t.clone() for t in self.cache.v])
 
 
 @pytest.fixture(scope="module")
 def w32k():
     w = Workload32k()
     yield w
-    del w.cache, w.packed
+    del w.cache, w.packed, w.before
     torch.cuda.empty_cache()
 
 
@@ -173,6 +177,7 @@ def test_32k_gather_then_scatter_per_chunk_size(w32k, chunk):
     # sizes still gather from unchanged sources)
     oracle.scatter(w.shape, *w.mirror, 0, 32, w.bt_dst, chunk, expect)
     _compare_named_slabs(w.cache, w.shape, w.mirror, w.bt_dst, f"chunk {chunk} scatter")
+    _unchanged_except(w.cache, w.before, w.shape, w.bt_dst, f"chunk {chunk} scatter")
 
 
 @pytest.mark.parametrize("chunk", [16, 64, 256, 1024])
@@ -188,12 +193,9 @@ def test_32k_staged_restore(w32k, chunk, slots):
         _check()
     finally:
         ring.close()
-    kvx.kvx_gather_blocks(w.cache, 0, 32, _bt(w.bt_dst), 2048, chunk, w.packed)
-    _check()
-    bad = first_mismatch(to_host(w.packed), image.array)
-    assert bad is None, f"chunk {chunk} slots {slots}: restore round trip differs at {bad}"
+    # every restored slab against the oracle's restore, every other block unchanged
     exp = oracle.new_mirror(w.shape)
     oracle.restore(w.shape, *exp, 0, 32, w.bt_dst, chunk, image.array)
-    sample = np.random.default_rng(chunk * 10 + slots).choice(w.bt_dst, 64, replace=False)
-    _compare_named_slabs(w.cache, w.shape, exp, sample, f"chunk {chunk} slots {slots} restore")
+    _compare_named_slabs(w.cache, w.shape, exp, w.bt_dst, f"chunk {chunk} slots {slots} restore")
+    _unchanged_except(w.cache, w.before, w.shape, w.bt_dst, f"chunk {chunk} slots {slots} restore")
     image.free()

@@ -73,6 +73,12 @@ BE_MUTANTS = {
                                    "for P in range(0, D + 1, granularity):"),
     "gate_declines_empty_loads": ("return [lb == 0 or lb * block_size >= gate_tokens",
                                   "return [lb * block_size >= gate_tokens"),
+    "rate_in_binary_gigabytes": ("x * bytes_per_token / (restore_GBps * 1e9)",
+                                 "x * bytes_per_token / (restore_GBps * 2**30)"),
+    "rate_transfer_dropped": ("return lambda x: non_transfer(x) + x * bytes_per_token",
+                              "return lambda x: non_transfer(x) + 0 * bytes_per_token"),
+    "required_without_copy_credit": ("    budget = max_io(f, g, copy, D)\n",
+                                     "    budget = f(D) - g(D)\n"),
 }
 
 
@@ -99,6 +105,7 @@ def test_breakeven_pins_reject_mutant(name, tmp_path, monkeypatch):
             (tb.test_oracle_special_cases, ()), (tb.test_oracle_exact_tie_does_not_pay, ()),
             (tb.test_oracle_brute_force_frontier_is_minimal, ())]
     pins += [(tb.test_oracle_linear_closed_forms, case) for case in tb.LINES]
+    pins += [(tb.test_oracle_hit_from_rate_closed_forms, case) for case in tb.RATES]
     for fn, args in pins:
         try:
             fn(*args)
@@ -106,3 +113,67 @@ def test_breakeven_pins_reject_mutant(name, tmp_path, monkeypatch):
             caught = True
             break
     assert caught, f"break-even pins did not catch mutant {name}"
+
+
+# ---- the prefix / step-plan oracle (Python): text edits of oracle/prefix.py,
+# run through the oracle pins of test_step_plan.py in-process.
+
+PREFIX_SRC = os.path.join(ROOT, "oracle", "prefix.py")
+PREFIX_MUTANTS = {
+    "chunk_keyed_by_first_block": ("out.append((keys[last], last - first + 1))",
+                                   "out.append((keys[first], last - first + 1))"),
+    "chunk_block_count_full": ("out.append((keys[last], last - first + 1))",
+                               "out.append((keys[last], bpc))"),
+    "dedupe_last_occurrence": ("return [seen.setdefault(k, i) for i, k in enumerate(keys)]",
+                               "return [max(j for j, q in enumerate(keys) if q == k) for k in keys]"),
+    "lookup_skips_misses": ("        if key not in cached:\n            break\n        n += 1",
+                            "        if key in cached:\n            n += 1"),
+    "gate_counts_resident_chunks": ("        if not resident[key]:\n            load[ri] += nb",
+                                    "        load[ri] += nb"),
+    "declined_request_restores": ("if not resident[key] and loads[ri] and key not in index_of:",
+                                  "if not resident[key] and key not in index_of:"),
+    "recompute_counted_once": ("            states.append((\"recompute\",))\n            recompute += nb",
+                               "            states.append((\"recompute\",))\n"
+                               "            recompute += nb if (ri, k) == next((c[0], c[1]) for c in chunks if c[2] == key) else 0"),
+    "offload_chunk_index_global": ("            offload.append((ri, c, nb, obt, first_new))",
+                                   "            offload.append((ri, len(offload), nb, obt, first_new))"),
+}
+
+
+@pytest.mark.parametrize("name", sorted(PREFIX_MUTANTS))
+def test_prefix_pins_reject_mutant(name, tmp_path, monkeypatch):
+    import importlib
+
+    old, new = PREFIX_MUTANTS[name]
+    text = open(PREFIX_SRC).read()
+    assert text.count(old) >= 1, f"mutation anchor for {name} not found"
+    pkg = tmp_path / "oracle_mut"
+    pkg.mkdir()
+    (pkg / "__init__.py").write_text("")
+    (pkg / "breakeven.py").write_text(open(os.path.join(ROOT, "oracle", "breakeven.py")).read())
+    (pkg / "prefix.py").write_text(text.replace(old, new, 1))
+    sys.path.insert(0, str(tmp_path))
+    try:
+        mod = importlib.import_module("oracle_mut.prefix")
+        sys.path.insert(0, os.path.join(ROOT, "tests"))
+        import test_step_plan as tsp
+    finally:
+        while str(tmp_path) in sys.path:
+            sys.path.remove(str(tmp_path))
+        if os.path.join(ROOT, "tests") in sys.path:
+            sys.path.remove(os.path.join(ROOT, "tests"))
+    monkeypatch.setattr(tsp, "op", mod)
+    caught = False
+    pins = [(tsp.test_oracle_reproduces_paper_example, ()),
+            (tsp.test_oracle_lookup_stops_at_first_miss, ()),
+            (tsp.test_oracle_chunk_identity_golden, ()),
+            (tsp.test_oracle_plan_step_golden, (0,)), (tsp.test_oracle_plan_step_golden, (1,))]
+    for fn, args in pins:
+        try:
+            fn(*args)
+        except Exception:
+            caught = True
+            break
+    for m in [m for m in sys.modules if m.startswith("oracle_mut")]:
+        del sys.modules[m]
+    assert caught, f"prefix pins did not catch mutant {name}"

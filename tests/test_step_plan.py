@@ -108,3 +108,182 @@ def test_residency_is_consistent_across_sharing_requests():
     for r in reqs:
         for (key, nb), res in zip(op.chunk_keys(r.tokens, 16, 256), r.resident):
             assert seen.setdefault(key, bool(res)) == bool(res)
+
+
+# ---- chunk identity when a shared prefix ends inside a chunk ------------------------
+
+CHUNK_GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "chunk_identity_example.json")
+
+
+def _golden_requests(ex):
+    import types
+
+    reqs = []
+    for r in ex["requests"]:
+        toks = []
+        for first, count in r["segments"]:
+            toks += list(range(first, first + count))
+        reqs.append(types.SimpleNamespace(
+            name=r["name"], tokens=np.array(toks, dtype=np.int32), new_blocks=r["new_blocks"],
+            resident=[lab in ex["resident_labels"] for lab, _ in r["chunks"]]))
+    return reqs
+
+
+def _label_map(ex, reqs, keys_of):
+    """key -> label, checking that equal labels mean equal keys and back."""
+    lab = {}
+    for r, spec in zip(reqs, ex["requests"]):
+        ck = keys_of(r)
+        assert [nb for _, nb in ck] == [nb for _, nb in spec["chunks"]], r.name
+        for (key, _), (l, _) in zip(ck, spec["chunks"]):
+            assert lab.setdefault(key, l) == l, (r.name, l)
+    assert len(set(lab.values())) == len(lab)
+    return lab
+
+
+def test_oracle_chunk_identity_golden():
+    """Sec. 2.1 / 6.5: a child extending a parent's partial last chunk, a
+    sibling diverging inside that chunk and a truncated prompt each give a
+    chunk of their own; an identical prompt shares both chunks."""
+    ex = json.load(open(CHUNK_GOLDEN))
+    reqs = _golden_requests(ex)
+    bs, ct = ex["block_size"], ex["chunk_tokens"]
+    _label_map(ex, reqs, lambda r: op.chunk_keys(r.tokens, bs, ct))
+    keys = [k for r in reqs for k, _ in op.chunk_keys(r.tokens, bs, ct)]
+    assert op.dedupe(keys) == ex["first_of"]
+    cached = set()
+    for r, spec in zip(reqs, ex["requests"]):
+        assert op.matched_blocks(r.tokens, bs, cached) == spec["matched_blocks"], r.name
+        cached.update(op.block_keys(r.tokens, bs))
+
+
+def test_oracle_lookup_stops_at_first_miss():
+    """Sec. 2.1: lookup walks the prompt's blocks from the start and stops at
+    the first block not in the cache, even if later blocks are cached (a
+    block evicted from the middle of a cached prefix)."""
+    toks = list(range(10))
+    keys = op.block_keys(toks, 2)
+    assert op.matched_blocks(toks, 2, {keys[0], keys[1], keys[3], keys[4]}) == 2
+    assert op.matched_blocks(toks, 2, {keys[1], keys[2]}) == 0
+    assert op.matched_blocks(toks, 2, set(keys)) == 5
+    assert op.matched_blocks(toks + [99], 2, set(keys)) == 5  # trailing partial block
+
+
+def _check_plan_against_golden(ex, plan, label_of, step_spec):
+    restore = [[label_of[key], nb, o[0], o[1]] for key, nb, o, _ in plan["restore"]]
+    assert restore == step_spec["restore"]
+    bt = 0
+    for _, nb, _, off in plan["restore"]:
+        assert off == bt
+        bt += nb
+    assert plan["restore_blocks"] == step_spec["restore_blocks"] == bt
+    assert plan["resident_hits"] == step_spec["resident_hits"]
+    assert plan["declined"] == step_spec["declined"]
+    assert plan["recompute_blocks"] == step_spec["recompute_blocks"]
+    assert [list(s) for s in plan["chunk_states"]] == step_spec["chunk_states"]
+    assert [list(o) for o in plan["offload"]] == ex["offload"]
+    assert plan["offload_blocks"] == ex["offload_blocks"]
+
+
+@pytest.mark.parametrize("step_i", [0, 1])
+def test_oracle_plan_step_golden(step_i):
+    ex = json.load(open(CHUNK_GOLDEN))
+    reqs = _golden_requests(ex)
+    bs, ct = ex["block_size"], ex["chunk_tokens"]
+    label_of = _label_map(ex, reqs, lambda r: op.chunk_keys(r.tokens, bs, ct))
+    spec = ex["steps"][step_i]
+    _check_plan_against_golden(ex, op.plan_step(reqs, bs, ct, spec["gate_tokens"]), label_of, spec)
+
+
+def _library_plan(reqs, bs, ct, gate):
+    p = step.plan_step(reqs, bs, ct, gate_tokens=gate)
+    return {"restore": [(c.key, c.n_blocks, c.origin, c.bt_offset) for c in p.restore],
+            "offload": [(o.request, o.chunk, o.n_blocks, o.bt_offset, o.new_first)
+                        for o in p.offload],
+            "chunk_states": p.request_chunks, "resident_hits": p.resident_hits,
+            "restore_blocks": p.restore_blocks, "offload_blocks": p.offload_blocks,
+            "declined": p.declined, "recompute_blocks": p.recompute_blocks}
+
+
+def _library_chunk_keys(r, bs, ct):
+    h = kvx.kvx_block_hashes(r.tokens, bs)
+    bpc = ct // bs
+    return [(int(h[min(f + bpc, h.size) - 1]), min(f + bpc, h.size) - f)
+            for f in range(0, h.size, bpc)]
+
+
+@pytest.mark.parametrize("step_i", [0, 1])
+def test_library_plan_step_golden(step_i):
+    ex = json.load(open(CHUNK_GOLDEN))
+    reqs = _golden_requests(ex)
+    bs, ct = ex["block_size"], ex["chunk_tokens"]
+    label_of = _label_map(ex, reqs, lambda r: _library_chunk_keys(r, bs, ct))
+    spec = ex["steps"][step_i]
+    _check_plan_against_golden(ex, _library_plan(reqs, bs, ct, spec["gate_tokens"]), label_of,
+                               spec)
+
+
+def _exact_of_hash(reqs, bs, ct):
+    m = {}
+    for r in reqs:
+        for (ek, _), (hk, _) in zip(op.chunk_keys(r.tokens, bs, ct), _library_chunk_keys(r, bs, ct)):
+            assert m.setdefault(hk, ek) == ek
+    return m
+
+
+@pytest.mark.parametrize("seed,share", [(5, "block"), (6, "block"), (7, "chunk"), (8, "block")])
+def test_library_plan_matches_oracle(seed, share):
+    """kvx_plan_step against the oracle's exact-key plan on prefix trees whose
+    shared prefixes end inside chunks, at several gate thresholds."""
+    reqs = pt.make_requests(seed, n=32, lo=64, hi=4096, share=share)
+    exact = _exact_of_hash(reqs, 16, 256)
+    load_tokens = sorted({sum(nb for (k, nb), res in zip(op.chunk_keys(r.tokens, 16, 256),
+                                                          r.resident) if not res) * 16
+                          for r in reqs})
+    for gate in (0, load_tokens[len(load_tokens) // 3], load_tokens[-1], load_tokens[-1] + 1):
+        want = op.plan_step(reqs, 16, 256, gate)
+        got = _library_plan(reqs, 16, 256, gate)
+        got["restore"] = [(exact[k], nb, o, bt) for k, nb, o, bt in got["restore"]]
+        assert got == want, gate
+
+
+def test_block_shared_generator_keys_chunks_by_owner():
+    """The generator's chunk owners (which decide the stored chunk images) are
+    in one-to-one correspondence with exact chunk keys."""
+    for seed in (5, 11):
+        reqs = pt.make_requests(seed, n=64, lo=256, hi=8192, share="block")
+        key_of_owner, owner_of_key = {}, {}
+        mid = 0
+        for r in reqs:
+            mid += r.shared_tokens % 256 != 0
+            for (key, _), owner in zip(op.chunk_keys(r.tokens, 16, 256), r.chunk_owner):
+                assert key_of_owner.setdefault(owner, key) == key
+                assert owner_of_key.setdefault(key, owner) == owner
+        assert mid > 0  # some shared prefixes end inside a chunk
+
+
+def test_plan_step_rejects_bad_requests():
+    import types
+
+    r = types.SimpleNamespace(tokens=np.arange(48, dtype=np.int32), resident=[True, False],
+                              new_blocks=0)
+    with pytest.raises(kvx.KvxError):
+        step.plan_step([r], 16, 256)  # 3 blocks = 1 chunk, 2 flags
+    r.resident = [True]
+    with pytest.raises(kvx.KvxError):
+        step.plan_step([r], 16, 100)  # chunk not a multiple of the block size
+    with pytest.raises(kvx.KvxError):
+        step.plan_step([r], 16, 256, gate_tokens=-1)
+    p = step.plan_step([], 16, 256)
+    assert p.restore == [] and p.offload == [] and p.request_chunks == []
+
+
+def test_chunk_stride():
+    c = kvx.shape_only_cache(32, 100, 16, 8, 128, 2)
+    assert kvx.kvx_chunk_stride(c, 0, 32, 256) == 32 * 2 * 256 * 8 * 128 * 2 == 32 << 20
+    assert kvx.kvx_chunk_stride(c, 4, 6, 16) == 2 * 2 * 16 * 2048
+    assert kvx.kvx_chunk_stride(c, 0, 32, 100) == -1
+    assert kvx.kvx_chunk_stride(c, 3, 2, 256) == -1
+    # the image's chunks sit at multiples of the stride: a whole-chunk prefix
+    # is n / bpc strides long
+    assert kvx.kvx_packed_bytes(c, 0, 32, 48) == 3 * kvx.kvx_chunk_stride(c, 0, 32, 256)
