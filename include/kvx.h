@@ -151,6 +151,25 @@ kvx_status kvx_scatter_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
                               const int32_t* block_table, int32_t n_blocks, int32_t chunk_tokens,
                               const void* src, hipStream_t stream);
 
+/* Largest n_blocks of kvx_scatter_blocks_noalloc. */
+#define KVX_NOALLOC_MAX_BLOCKS 65536
+
+/* kvx_scatter_blocks for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same arguments, validation, kernels and result, but the
+ * destination order a scatter of 1,024 blocks or more computes first lives in
+ * a fixed device array of the library's (512 KiB, KVX_NOALLOC_MAX_BLOCKS
+ * 8-byte entries; each GPU the library runs on holds one until the process
+ * ends) instead of stream-ordered scratch. The call allocates nothing.
+ * n_blocks above KVX_NOALLOC_MAX_BLOCKS returns KVX_EINVAL before anything is
+ * enqueued. Every call on one GPU shares that GPU's array, and each call
+ * rewrites the entries it uses before reading them: calls that may overlap on
+ * one GPU (other streams, or other threads) race on it and must be ordered by
+ * the caller. */
+kvx_status kvx_scatter_blocks_noalloc(const kvx_cache* cache, int32_t l0, int32_t l1,
+                                      const int32_t* block_table, int32_t n_blocks,
+                                      int32_t chunk_tokens, const void* src, hipStream_t stream);
+
 /* ---- batched chunk lists (several requests in one launch) ------------------ */
 
 /* One chunk of a batch: the packed image of blocks block_table[bt_offset ..

@@ -217,6 +217,20 @@ def kvx_scatter_blocks(cache: PagedKVCache, l0, l1, block_table, n_blocks, chunk
     _ok(st, "kvx_scatter_blocks")
 
 
+KVX_NOALLOC_MAX_BLOCKS = 65536
+
+
+def kvx_scatter_blocks_noalloc(cache: PagedKVCache, l0, l1, block_table, n_blocks, chunk_tokens,
+                               src, stream=None) -> None:
+    """kvx_scatter_blocks that allocates nothing (its ordering scratch is a
+    fixed device array of the library's; calls on one GPU must not overlap)."""
+    need = max(kvx_packed_bytes(cache, l0, l1, n_blocks), 0)
+    st = _native.lib().kvx_scatter_blocks_noalloc(
+        ctypes.byref(cache.c_struct()), l0, l1, _table_ptr(cache, block_table, n_blocks),
+        n_blocks, chunk_tokens, _buffer_ptr(cache, src, need), _stream_handle(stream))
+    _ok(st, "kvx_scatter_blocks_noalloc")
+
+
 CHUNK_REF_DTYPE = [("packed_offset", "<i8"), ("bt_offset", "<i4"), ("n_blocks", "<i4")]
 
 
@@ -654,5 +668,6 @@ __all__ = [
     "KVX_LAYOUT_PAGED_ATTN", "layer_shapes", "kvx_probe_stream", "kvx_chunk_path", "Preloader",
     "kvx_read_files", "kvx_write_files", "KVX_EIO", "KVX_EBUSY", "kvx_offload_begin",
     "kvx_offload_wait", "kvx_restore_begin", "kvx_restore_wait", "kvx_chunk_stride",
-    "KVX_RAMP_NONE", "KVX_RAMP_FIRST", "KVX_RAMP_LAST",
+    "KVX_RAMP_NONE", "KVX_RAMP_FIRST", "KVX_RAMP_LAST", "kvx_scatter_blocks_noalloc",
+    "KVX_NOALLOC_MAX_BLOCKS",
 ]

@@ -92,6 +92,8 @@ SIGNATURES = {
                                          c_i32, c_vp, c_vp]),
     "kvx_scatter_blocks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
                                           c_i32, c_vp, c_vp]),
+    "kvx_scatter_blocks_noalloc": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp,
+                                                  c_i32, c_i32, c_vp, c_vp]),
     "kvx_gather_chunks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
                                          c_vp, c_i32, c_i32, c_vp, c_i64, c_vp]),
     "kvx_scatter_chunks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,

@@ -42,10 +42,17 @@ bool overlaps_cache(const kvx_cache* cache, int32_t l0, int32_t l1, const void* 
 
 // Enqueue the gather (to_packed = true) or scatter kernel on `stream`.
 // `block_table` is a device pointer to the call's n_blocks ids; the kernels
-// report bad ids in the error word err (stream_error_word).
+// report bad ids in the error word err (stream_error_word). A scatter of at
+// least 1,024 blocks first orders its destinations into n_blocks 8-byte
+// entries: in order_scratch (device memory of the caller's) when given,
+// otherwise in stream-ordered scratch allocated and freed on `stream`.
 kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
                        const int32_t* block_table, const Geometry& g, void* packed,
-                       hipStream_t stream, int* err);
+                       hipStream_t stream, int* err, void* order_scratch = nullptr);
+
+// Bytes of the fixed device scratch of kvx_scatter_blocks_noalloc: one
+// 8-byte order entry per block.
+constexpr size_t kNoAllocScratchBytes = (size_t)KVX_NOALLOC_MAX_BLOCKS * 8;
 
 // Enqueue the chunk-list gather (to_packed) or scatter on `stream`: refs is a
 // device array of n_chunks references, validated by the kernel against

@@ -755,7 +755,7 @@ int* stream_error_word(hipStream_t stream) {
 
 kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32_t l1,
                        const int32_t* block_table, const Geometry& g, void* packed,
-                       hipStream_t stream, int* err) {
+                       hipStream_t stream, int* err, void* order_scratch) {
   if (g.n_units == 0) return KVX_OK;
   if (g.n_units > 0x7FFFFFFF || g.slab % 16 != 0) return KVX_EINTERNAL;
   if (!err) return KVX_EHIP;
@@ -786,13 +786,19 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
                                        layout, elem, stream);
     return e == hipSuccess ? KVX_OK : KVX_EHIP;
   }
-  // Destination-ordered scatter for large calls; the order lives in
-  // stream-ordered scratch. If that allocation fails, fall back to image
-  // order (same result, slower).
+  // Destination-ordered scatter for large calls; the order lives in the
+  // caller's scratch (order_scratch, n_blocks entries) or else in
+  // stream-ordered scratch allocated here. If that allocation fails, fall
+  // back to image order (same result, slower).
   OrderEntry* order = nullptr;
-  if (g.n_blocks >= kOrderedScatterMinBlocks &&
-      hipMallocAsync((void**)&order, (size_t)g.n_blocks * sizeof(OrderEntry), stream) != hipSuccess)
-    order = nullptr;
+  const bool own = order_scratch == nullptr;
+  if (g.n_blocks >= kOrderedScatterMinBlocks) {
+    if (!own)
+      order = static_cast<OrderEntry*>(order_scratch);
+    else if (hipMallocAsync((void**)&order, (size_t)g.n_blocks * sizeof(OrderEntry), stream) !=
+             hipSuccess)
+      order = nullptr;
+  }
   (void)hipGetLastError();
   hipError_t e;
   if (order) {
@@ -802,8 +808,10 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
     if (e == hipSuccess)
       e = launch<false, true>(lp, block_table, ug, n_work, order, (char*)packed, err, layout,
                               elem, stream);
-    const hipError_t ef = hipFreeAsync(order, stream);
-    if (e == hipSuccess) e = ef;
+    if (own) {
+      const hipError_t ef = hipFreeAsync(order, stream);
+      if (e == hipSuccess) e = ef;
+    }
   } else {
     e = launch<false, false>(lp, block_table, ug, n_work, nullptr, (char*)packed, err, layout,
                              elem, stream);
@@ -854,3 +862,56 @@ kvx_status launch_copy_chunks(bool to_packed, const kvx_cache* cache, int32_t l0
 }
 
 }  // namespace kvx
+
+// ---- scatter for callers that cannot allocate --------------------------------
+//
+// The order entries of a destination-ordered scatter live in this fixed array
+// instead of stream-ordered scratch: each GPU the library runs on holds one
+// copy (kvx::kNoAllocScratchBytes) until the process ends. Host code reaches a
+// device's copy only through the address hipGetSymbolAddress returns for that
+// device (resolved once per device, with the device current); the array's
+// name on the host is not a device address.
+static __device__ __align__(256) unsigned char scratch[kvx::kNoAllocScratchBytes];
+
+namespace {
+
+constexpr int kScratchDevices = 64;
+void* g_scratch_ptr[kScratchDevices] = {};
+std::mutex g_scratch_mu;
+
+// The calling device's copy of `scratch`, or null.
+void* device_scratch() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return nullptr;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    g_scratch_ptr[dev] = p;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+
+extern "C" kvx_status kvx_scatter_blocks_noalloc(const kvx_cache* cache, int32_t l0, int32_t l1,
+                                                 const int32_t* block_table, int32_t n_blocks,
+                                                 int32_t chunk_tokens, const void* src,
+                                                 hipStream_t stream) {
+  try {
+    kvx::Geometry g;
+    kvx_status st = kvx::validate(cache, l0, l1, n_blocks, chunk_tokens, true, &g);
+    if (st != KVX_OK) return st;
+    if (n_blocks > KVX_NOALLOC_MAX_BLOCKS) return KVX_EINVAL;
+    if (g.n_units == 0) return KVX_OK;
+    if (!block_table || !src || ((uintptr_t)src & 15)) return KVX_EINVAL;
+    if (kvx::overlaps_cache(cache, l0, l1, src, g.packed)) return KVX_EINVAL;
+    void* order = device_scratch();
+    int* err = kvx::stream_error_word(stream);
+    if (!order || !err) return KVX_EHIP;
+    return kvx::launch_copy(false, cache, l0, l1, block_table, g, const_cast<void*>(src), stream,
+                            err, order);
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
+}

@@ -325,6 +325,8 @@ def test_batched_step_70b_64_requests():
     chunks = [(img, rbt[bt0:bt0 + nb], 0) for img, bt0, nb in store_chunks]
     for l in range(80):
         check_layer_after_scatters(cache, s, fill, l, chunks, 256, "70B restore")
+        if l % 16 == 15:
+            print(f"70B restore: layers 0..{l} match the oracle", flush=True)
     # offload: every sink against the oracle gather of the new blocks
     src = host_mirror(s, fill, obt)
     for b, c in zip(sinks, plan.offload):
