@@ -89,11 +89,12 @@ struct SlabGeom {
   FastDiv bs;      // tokens per block
   FastDiv d;       // head dim (elements)
   FastDiv v16;     // 16-byte vectors per (token, head) row: d * elem_bytes / 16
-  FastDiv pad[2];  // LDS pad period of K and V parts (see lds_slot)
   uint32_t x;      // elements per 16-byte vector: 16 / elem_bytes
   uint32_t nh;     // vectors of one head: bs * v16
   uint32_t prow;   // packed row stride in vectors: heads * v16
-  uint32_t pad_;
+  FastDiv pad;       // scatter: LDS pad period (see lds_slot)
+  uint32_t v_pairs;  // paged-attention V of 2-byte words gathered as row pairs (v_pairs_gather)
+  uint32_t swz;      // gather: LDS swizzle shift (see lds_slot)
 };
 
 // Division of any 32-bit numerator by a divisor fixed for the launch, as a
@@ -184,7 +185,7 @@ __device__ __forceinline__ void move_slab(const v4u* __restrict__ s, v4u* __rest
 //     from it.
 // Both global sides stay coalesced (consecutive lanes on consecutive 16-byte
 // vectors, or whole packed rows) and only LDS sees the reordering; the LDS
-// image is padded so that a wave's strided reads land on distinct banks. A
+// image is swizzled so that a wave's strided reads land on distinct banks. A
 // thread holds V vectors of the head, all of its loads issued before it waits
 // for any of them: V = 1 when a head fits one vector per thread (the usual
 // shapes: few registers, full occupancy), else kVecPerThread, enough for the
@@ -196,10 +197,33 @@ constexpr int kVecPerThread = (int)(kMaxSlabVectors / kTransposeThreads);  // 12
 
 extern __shared__ __attribute__((aligned(16))) unsigned char kvx_lds[];
 
-// LDS slot of vector v: one pad vector after every `pad` vectors. The pad
-// period is the stride at which the head's strided LDS accesses walk (chosen
-// per layout and direction on the host).
-__device__ __forceinline__ uint32_t lds_slot(uint32_t v, FastDiv pad) { return v + fdiv(v, pad); }
+// LDS slot of vector v in the head's image; the layout differs by direction.
+// Gather (kToPacked): inside each aligned group of 16 vectors (256 bytes, one
+// pass over the 64 banks) the position is XORed with h(r), r = bits swz ..
+// swz + 3 of v, which the XOR leaves alone, so the map is a permutation of
+// every group. h(r) = r ^ (bit 3 of r moved to bit 1) is itself a permutation
+// of 0 .. 15, so a wave walking the image at a stride of 2^swz vectors (the
+// head's read stride, chosen on the host) meets 16 different positions per
+// group, and consecutive vectors stay in one group; moving bit 3 to bit 1
+// also keeps rows r and r + 8 apart modulo 8 positions (32 banks), where the
+// 32-bit reads of a half-wave meet (see lane_perm). Scatter: one pad vector
+// after every `pad` vectors (the read stride). Measured on gfx950 with the LDS
+// bank-conflict counter, a 16 x 16 transposed read of 16-byte vectors costs
+// no conflict cycles through an XOR swizzle, 4 per wave instruction with the
+// pad and 28 with neither, and linear 16-byte writes cost none either way.
+// The 80k paged-attention gather ran 1 to 2 points faster with the swizzle
+// (no conflicts left) than with the pad; the scatter ran 2 points slower
+// with it (also with no conflicts left): it is not bound by the LDS, and the
+// swizzle's extra arithmetic in its element-by-element loop costs more than
+// the conflicts it removes.
+template <bool kToPacked>
+__device__ __forceinline__ uint32_t lds_slot(uint32_t v, const SlabGeom& g) {
+  if (kToPacked) {
+    const uint32_t r = (v >> g.swz) & 15u;
+    return v ^ (r ^ ((r >> 2) & 2u));
+  }
+  return v + fdiv(v, g.pad);
+}
 
 // Quotient and remainder.
 __device__ __forceinline__ uint32_t divmod(uint32_t n, FastDiv f, uint32_t& rem) {
@@ -244,8 +268,7 @@ __device__ __forceinline__ void move_head_rows(const v4u* __restrict__ src, v4u*
 // Load the head's nh source vectors, in source order, into the padded LDS
 // image. A gather reads the cache (contiguous), a scatter the packed rows.
 template <bool kToPacked, int T, int V>
-__device__ __forceinline__ void stage_in(const v4u* __restrict__ src, const SlabGeom& g,
-                                         FastDiv pad) {
+__device__ __forceinline__ void stage_in(const v4u* __restrict__ src, const SlabGeom& g) {
   v4u* lds = reinterpret_cast<v4u*>(kvx_lds);
   v4u r[V];
 #pragma unroll
@@ -256,8 +279,23 @@ __device__ __forceinline__ void stage_in(const v4u* __restrict__ src, const Slab
 #pragma unroll
   for (int q = 0; q < V; ++q) {
     const uint32_t v = threadIdx.x + q * T;
-    if (v < g.nh) lds[lds_slot(v, pad)] = r[q];
+    if (v < g.nh) lds[lds_slot<kToPacked>(v, g)] = r[q];
   }
+}
+
+// The LDS serves 32-bit and narrower reads a half-wave (32 lanes) at a time
+// over 32 banks (measured: two extra cycles per such read when a half-wave
+// puts two words on one bank). The paired V gather below therefore lets lane
+// L of a wave handle pair lane_perm(L) of the wave's 64 pairs, a permutation
+// of the lane bits (b5 b4 b3 b2 b1 b0 -> b4 b3 b5 b2 b1 b0) that gives each
+// half-wave 4 token pairs x 8 dim groups instead of 2 x 16; the 64 pairs of a
+// wave, and so the bytes each store instruction writes, are the same as in
+// lane order. (The scatter keeps lane order: permuting which lane stores
+// which cache vector measured a point slower, the stores of a wave no longer
+// running in address order; its reads are kept apart by the swizzle.)
+__device__ __forceinline__ uint32_t lane_perm(uint32_t i) {
+  const uint32_t l = i & 63u;
+  return (i & ~63u) | (((l >> 3) & 3u) << 4) | (((l >> 5) & 1u) << 3) | (l & 7u);
 }
 
 // Write the head's nh destination vectors, in destination order, each
@@ -300,7 +338,7 @@ struct ElemRow {
 // the LDS image of the source. Cache elements inside a head are (dim, t) at
 // dim * bs + t; packed elements (t, dim) at t * d + dim.
 template <bool kToPacked, typename E>
-__device__ __forceinline__ v4u v_elements(uint32_t w, const SlabGeom& g, FastDiv pad) {
+__device__ __forceinline__ v4u v_elements(uint32_t w, const SlabGeom& g) {
   constexpr uint32_t kX = 16 / sizeof(E);
   ElemRow<E> out;
   if (kToPacked) {  // packed (t, dv * x + i) <- cache element (dv * x + i, t): stride bs
@@ -310,7 +348,7 @@ __device__ __forceinline__ v4u v_elements(uint32_t w, const SlabGeom& g, FastDiv
 #pragma unroll
     for (uint32_t i = 0; i < kX; ++i) {
       const uint32_t e = e0 + i * g.bs.d;
-      out.e[i] = reinterpret_cast<const E*>(kvx_lds + 16u * lds_slot(e / kX, pad))[e % kX];
+      out.e[i] = reinterpret_cast<const E*>(kvx_lds + 16u * lds_slot<kToPacked>(e / kX, g))[e % kX];
     }
   } else {  // cache (dim, t .. t + x - 1) <- packed elements (t + i, dim); t wraps to dim + 1
     uint32_t t;
@@ -318,7 +356,7 @@ __device__ __forceinline__ v4u v_elements(uint32_t w, const SlabGeom& g, FastDiv
 #pragma unroll
     for (uint32_t i = 0; i < kX; ++i) {
       const uint32_t e = t * g.d.d + dim;
-      out.e[i] = reinterpret_cast<const E*>(kvx_lds + 16u * lds_slot(e / kX, pad))[e % kX];
+      out.e[i] = reinterpret_cast<const E*>(kvx_lds + 16u * lds_slot<kToPacked>(e / kX, g))[e % kX];
       if (++t == g.bs.d) {
         t = 0;
         ++dim;
@@ -326,6 +364,50 @@ __device__ __forceinline__ v4u v_elements(uint32_t w, const SlabGeom& g, FastDiv
     }
   }
   return __builtin_bit_cast(v4u, out);
+}
+
+// Paged-attention V of 2-byte words in a gather, two packed rows per thread:
+// the rows of tokens t and t + 1 (t even) at one group of dims, whose
+// elements come from cache words (dim, t) and (dim, t + 1), adjacent in one
+// dword. Each 32-bit LDS read yields one element of each vector, so no two
+// lanes share a dword, and for the usual shapes (block size 16, 16 vectors
+// per row) a wave's reads of one element land on 64 distinct banks; the two
+// stores of a lane write whole token rows. A scatter does not pair its
+// vectors this way: paired dims d, d + 1 would make each store instruction
+// write every other 32-byte run of the cache lines (the 80k scatter ran at
+// half speed that way).
+template <int T, int V>
+__device__ __forceinline__ void v_pairs_gather(v4u* __restrict__ dst, const SlabGeom& g) {
+  typedef ElemRow<uint16_t> Row;
+  const uint32_t np = g.nh >> 1;
+  Row r0[V], r1[V];
+  uint32_t w0[V];
+#pragma unroll
+  for (int q = 0; q < V; ++q) {
+    // a half-wave takes 4 token pairs x 8 dim groups (16 vectors per row)
+    const uint32_t p = lane_perm(threadIdx.x + q * T);
+    if (p >= np) continue;
+    uint32_t dv;
+    const uint32_t tp = divmod(p, g.v16, dv);  // tokens 2 tp, 2 tp + 1
+    w0[q] = 2 * tp * g.v16.d + dv;
+    const uint32_t e0 = dv * 8 * g.bs.d + 2 * tp;
+#pragma unroll
+    for (uint32_t i = 0; i < 8; ++i) {
+      const uint32_t e = e0 + i * g.bs.d;
+      const uint32_t w = *reinterpret_cast<const uint32_t*>(kvx_lds + 16u * lds_slot<true>(e >> 3, g) +
+                                                            2u * (e & 7u));
+      r0[q].e[i] = (uint16_t)w;
+      r1[q].e[i] = (uint16_t)(w >> 16);
+    }
+  }
+  const auto out = stream_dst(dst, head_dst_bytes<true>(g));
+#pragma unroll
+  for (int q = 0; q < V; ++q) {
+    const uint32_t p = lane_perm(threadIdx.x + q * T);
+    if (p >= np) continue;
+    store_stream(out, packed_at(w0[q], g), __builtin_bit_cast(v4u, r0[q]));
+    store_stream(out, packed_at(w0[q] + g.v16.d, g), __builtin_bit_cast(v4u, r1[q]));
+  }
 }
 
 // One head of a slab in a reordering layout (src / dst: the head's cache
@@ -342,16 +424,17 @@ __device__ __forceinline__ void move_head(const v4u* __restrict__ src, v4u* __re
     move_head_rows<kToPacked, T, V>(src, dst, g);
     return;
   }
-  const FastDiv pad = g.pad[kv];
-  stage_in<kToPacked, T, V>(src, g, pad);
+  stage_in<kToPacked, T, V>(src, g);
   __syncthreads();
   const v4u* lds = reinterpret_cast<const v4u*>(kvx_lds);
   if (kv == 0)
     stage_out<kToPacked, T, V>(
-        dst, g, [&](uint32_t w) { return lds[lds_slot(k_source<kToPacked>(w, g), pad)]; });
+        dst, g, [&](uint32_t w) { return lds[lds_slot<kToPacked>(k_source<kToPacked>(w, g), g)]; });
+  else if (kToPacked && kElem == 2 && g.v_pairs)
+    v_pairs_gather<T, V>(dst, g);
   else
     stage_out<kToPacked, T, V>(dst, g,
-                               [&](uint32_t w) { return v_elements<kToPacked, E>(w, g, pad); });
+                               [&](uint32_t w) { return v_elements<kToPacked, E>(w, g); });
 }
 
 // Move part `part` of one slab in the direction and layout of the kernel: a
@@ -574,12 +657,13 @@ constexpr uint32_t kPartThreads = 256;
 // Scatters of at least this many blocks run in destination order.
 constexpr int32_t kOrderedScatterMinBlocks = 1024;
 
-// Dynamic LDS bytes for a reordering layout: the padded image of one head
-// (none for HND, which moves rows directly).
-inline size_t lds_bytes(int layout, const SlabGeom& sg) {
+// Dynamic LDS bytes for a reordering layout: the image of one head, rounded
+// up to whole swizzle groups of 16 vectors (gather) or with its pad vectors
+// (scatter); none for HND, which moves rows directly.
+inline size_t lds_bytes(int layout, const SlabGeom& sg, bool to_packed) {
   if (layout != KVX_LAYOUT_PAGED_ATTN) return 0;
-  const uint32_t pad = sg.pad[0].d < sg.pad[1].d ? sg.pad[0].d : sg.pad[1].d;
-  return 16u * (size_t)(sg.nh + sg.nh / pad + 1);
+  if (to_packed) return 16u * (size_t)((sg.nh + 15u) & ~15u);
+  return 16u * (size_t)(sg.nh + sg.nh / sg.pad.d + 1);
 }
 
 // Launch `cnt` workgroups of kernel K<..., layout, elem, T, V>: the default
@@ -602,17 +686,17 @@ inline size_t lds_bytes(int layout, const SlabGeom& sg) {
       if (sg.nh <= (uint32_t)kTransposeThreads) {                                      \
         hipLaunchKernelGGL(                                                            \
             (KERNEL<KVX_UNPAREN PREFIX, LAYOUT, ELEM, kTransposeThreads / 2, 2>), grid, \
-            dim3(kTransposeThreads / 2), lds_bytes(layout, sg), stream, __VA_ARGS__);  \
+            dim3(kTransposeThreads / 2), lds_bytes(layout, sg, kToPacked), stream, __VA_ARGS__);  \
         break;                                                                         \
       }                                                                                \
     }                                                                                  \
     if (sg.nh <= (uint32_t)kTransposeThreads)                                          \
       hipLaunchKernelGGL((KERNEL<KVX_UNPAREN PREFIX, LAYOUT, ELEM, kTransposeThreads, 1>), \
-                         grid, tb, lds_bytes(layout, sg), stream, __VA_ARGS__);        \
+                         grid, tb, lds_bytes(layout, sg, kToPacked), stream, __VA_ARGS__);        \
     else                                                                               \
       hipLaunchKernelGGL(                                                              \
           (KERNEL<KVX_UNPAREN PREFIX, LAYOUT, ELEM, kTransposeThreads, kVecPerThread>), \
-          grid, tb, lds_bytes(layout, sg), stream, __VA_ARGS__);                       \
+          grid, tb, lds_bytes(layout, sg, kToPacked), stream, __VA_ARGS__);                       \
   } while (0)
 
 #define KVX_DISPATCH(KERNEL, PREFIX, ...)                                                   \
@@ -688,12 +772,13 @@ FastDiv fast_div(uint32_t d) {
   return f;
 }
 
-// Head shape and LDS pad periods for a reordering layout. The pad period is
-// the stride (in vectors) of the head's strided LDS reads: a gather (cache
-// image in LDS) reads paged-attention K vectors and V elements of consecutive
-// dims at stride bs; a scatter (packed image in LDS) reads them at stride v16
-// (K: consecutive tokens; V: the x tokens of one output vector). HND uses no
-// LDS.
+// Head shape and LDS layout for a reordering layout, from the stride (in
+// vectors) of the head's strided LDS reads: a gather (cache image in LDS)
+// reads paged-attention K vectors and V elements of consecutive dims at
+// stride bs, and swizzles with shift log2 of that stride (at least 16)
+// rounded up to a power of two; a scatter (packed image in LDS) reads them at
+// stride v16 (K: consecutive tokens; V: the x tokens of one output vector)
+// and pads every v16 (at least 8) vectors. HND uses no LDS.
 SlabGeom slab_geom(const kvx_cache* c, bool to_packed) {
   const uint32_t bs = (uint32_t)c->block_size, h = (uint32_t)c->num_kv_heads,
                  d = (uint32_t)c->head_dim, x = (uint32_t)(16 / c->elem_bytes),
@@ -705,9 +790,13 @@ SlabGeom slab_geom(const kvx_cache* c, bool to_packed) {
   sg.x = x;
   sg.nh = bs * v16;
   sg.prow = h * v16;
-  sg.pad_ = 0;
-  const uint32_t p = to_packed ? bs : v16;
-  sg.pad[0] = sg.pad[1] = fast_div(p < 8 ? 8 : p);
+  // V of 2-byte words as row pairs in a gather: token pairs, so an even
+  // block size (v_pairs_gather says why not in a scatter)
+  sg.v_pairs = c->elem_bytes == 2 && to_packed && bs % 2 == 0 ? 1u : 0u;
+  const uint32_t stride = to_packed ? bs : v16;
+  sg.swz = 4;
+  while ((1u << sg.swz) < stride) ++sg.swz;
+  sg.pad = fast_div(stride < 8 ? 8 : stride);
   return sg;
 }
 

@@ -44,6 +44,9 @@ CASES = [
     (PA, 2, 16, 12, 128, 2, 0, 2, 5, 32),     # 48 KiB slabs, the largest transposed
     (HND, 2, 16, 12, 128, 2, 0, 2, 5, 32),
     (PA, 2, 32, 4, 128, 2, 0, 2, 6, 64),      # 4 token vectors per value row
+    (PA, 2, 8, 2, 64, 2, 0, 2, 9, 16),        # 1 token vector per value row
+    (PA, 2, 24, 2, 64, 2, 0, 2, 7, 48),       # 3 token vectors per value row
+    (PA, 2, 6, 3, 32, 2, 0, 2, 8, 12),        # even block size, not a multiple of 8
     (PA, 2, 16, 16, 96, 1, 0, 2, 5, 32),      # 1-byte elements, 24 KiB slabs
     (PA, 2, 1, 8, 64, 2, 0, 2, 9, 3),         # one token per block
     (PA, 2, 3, 5, 40, 2, 0, 2, 7, 9),         # odd block size and head count
