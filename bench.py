@@ -34,7 +34,6 @@ import json
 import os
 import statistics
 import sys
-import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
@@ -51,13 +50,13 @@ KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
 # only for the kernel code they were taken on (kernels_sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "515467bf68c9cf847544598f46f35bc405796daee7e9d75e08bd781a052ec155",
+    "kernels_sha256": "0cb81b2450db76088dcfd19a7ad2e821ec4d692d1c09fd1bdb0af54677945c49",
     # cache layout -> (fetched, written) HBM bytes of one gather launch at the
     # default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy calibration),
     # WRITE_SIZE KiB x 1.0
-    "nhd": (10488912457, 10485760000),         # 5,121,569.8 / 10,240,000.0 KiB
-    "paged_attn": (10489087358, 10485760000),  # 5,121,653.7 / 10,240,000.0 KiB
-    "hnd": (10488876322, 10485760000),         # 5,121,554.0 / 10,240,000.0 KiB (x 1.9999874)
+    "nhd": (10488913979, 10485760000),         # 5,121,570.8 / 10,240,000.0 KiB
+    "paged_attn": (10489059182, 10485760000),  # 5,121,641.7 / 10,240,000.0 KiB
+    "hnd": (10488915823, 10485760000),         # 5,121,571.7 / 10,240,000.0 KiB
 }
 
 
@@ -92,6 +91,9 @@ def parse():
     ap.add_argument("--io-depth", type=int, default=8, help="8b-files: storage I/O depth")
     ap.add_argument("--offload-reps", type=int, default=3,
                     help="reps of the staged offload leg (8b-80k), timed after the steps")
+    ap.add_argument("--sweep-reps", type=int, default=5,
+                    help="reps of the 32k-token gather / scatter sweep (8b-80k), timed after "
+                         "the steps; 0 skips it")
     return ap.parse_args()
 
 
@@ -285,6 +287,8 @@ def run_80k(args):
     kvx.kvx_check()
     log("timed steps done")
     offload = offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe)
+    sweep = sweep_32k(args, cache, L, perm, packed, slab, args.sweep_reps) \
+        if H == 8 and args.sweep_reps > 0 else None
 
     med = {k: statistics.median(v) for k, v in rec.items()}
     mean_g = statistics.mean(rec["gather_ms"])
@@ -294,6 +298,7 @@ def run_80k(args):
     gather_GBps = rw / mean_g / 1e6
     scatter_GBps = rw / mean_s / 1e6
     restore_GBps = payload / med["restore_ms"] / 1e6
+    gate = gate_from_rate(restore_GBps, L, H, D, E) if H == 8 else None
     cpu = None if args.no_cpu_baseline else cpu_baseline(args, L, BS, H, D, E, perm)
     traffic = None
     if GATHER_TRAFFIC["kernels_sha256"] == kernels_sha256() and args.layout in GATHER_TRAFFIC and \
@@ -316,6 +321,8 @@ def run_80k(args):
         "scatter_GBps_rw": round(scatter_GBps, 1),
         "gather_ms": round(mean_g, 4),
         "scatter_ms": round(mean_s, 4),
+        "gather_ms_stats": ms_stats(rec["gather_ms"]),
+        "scatter_ms_stats": ms_stats(rec["scatter_ms"]),
         "restore_ms": round(med["restore_ms"], 3),
         "restore_GBps": round(restore_GBps, 2),
         "restore_frac_of_h2d": round(restore_GBps / probe["h2d_GBps"], 4),
@@ -324,6 +331,8 @@ def run_80k(args):
                                  "enqueue_wait_for_fill": round(med["wait_fill_ms"], 2),
                                  "device_span": round(med["restore_dev_ms"], 2)},
         "offload": offload,
+        "sweep_32k": sweep,
+        "gate": gate,
         "probes": {k: round(v, 2) for k, v in probe.items()},
         "roofline": {"bound": "hbm",
                      "kernel": "gather (copy_units_kernel<true, false, layout %s>)" % args.layout,
@@ -337,6 +346,78 @@ def run_80k(args):
     print(json.dumps(out), flush=True)
     ring.close()
     image.free()
+
+
+def ms_stats(v):
+    """Median, min and mean of event-timed milliseconds, and how many."""
+    return {"median": round(statistics.median(v), 4), "min": round(min(v), 4),
+            "mean": round(statistics.mean(v), 4), "n": len(v)}
+
+
+def sweep_32k(args, cache, L, perm, packed, slab, reps=5):
+    """The granularity sweep's gather and scatter on the same cache, outside
+    the timed steps: a 32,768-token prefix (the first 2,048 of the seeded
+    block permutation; scatter into the next 2,048) in chunks of 16, 64, 256
+    and 1,024 tokens, each timed with events (median of reps)."""
+    import torch
+
+    import paper_2609_11744_amd as kvx
+
+    n = 2048
+    payload = n * L * 2 * slab
+    src = torch.from_numpy(perm[:n].copy()).to(cache.device)
+    dst = torch.from_numpy(perm[n:2 * n].copy()).to(cache.device)
+    rows = []
+    for ct in (16, 64, 256, 1024):
+        g = event_ms(lambda: kvx.kvx_gather_blocks(cache, 0, L, src, n, ct, packed), reps + 1)[1:]
+        sc = event_ms(lambda: kvx.kvx_scatter_blocks(cache, 0, L, dst, n, ct, packed), reps + 1)[1:]
+        rows.append({"chunk_tokens": ct,
+                     "gather_GBps_rw": round(2 * payload / statistics.median(g) / 1e6, 1),
+                     "scatter_GBps_rw": round(2 * payload / statistics.median(sc) / 1e6, 1),
+                     "gather_pct_hbm_peak": round(100 * 2 * payload / statistics.median(g) / 1e6
+                                                  / HBM_PEAK_GBPS, 2),
+                     "scatter_pct_hbm_peak": round(100 * 2 * payload / statistics.median(sc) / 1e6
+                                                   / HBM_PEAK_GBPS, 2),
+                     "gather_ms": ms_stats(g), "scatter_ms": ms_stats(sc)})
+    kvx.kvx_check()
+    log(f"32k sweep: {[(r['chunk_tokens'], r['gather_pct_hbm_peak'], r['scatter_pct_hbm_peak']) for r in rows]}")
+    return {"prefix_tokens": n * 16, "payload_bytes": payload, "reps": reps, "rows": rows}
+
+
+# A stated synthetic calibration for the gate of an 8B-shaped model (no model
+# runs here): cold TTFT 0.012 + 1.4e-5 x + 2.2e-10 x^2 s and the cache-hit
+# path's non-transfer part 0.010 + 1.0e-7 x s, at knots from 1k to 128k tokens.
+GATE_KNOTS = [1024.0, 4096.0, 8192.0, 16384.0, 32768.0, 65536.0, 131072.0]
+GATE_COLD = [0.012 + 1.4e-5 * x + 2.2e-10 * x * x for x in GATE_KNOTS]
+GATE_BASE = [0.010 + 1.0e-7 * x for x in GATE_KNOTS]
+
+
+def gate_from_rate(restore_GBps, L, H, D, E):
+    """The break-even gate of the pinned-host staging tier fed by the restore
+    rate this run measured (Secs. 5.2, 6.6), on the synthetic curves above:
+    the tier's threshold and the bandwidth a path must sustain at 1k, 8k and
+    80k tokens; also for a tier ten and a hundred times slower."""
+    from paper_2609_11744_amd import breakeven as be
+    import paper_2609_11744_amd as kvx
+
+    bpt = kvx.kvx_bytes_per_token(L, H, D, E)
+    cold, base = be.Curve(GATE_KNOTS, GATE_COLD), be.Curve(GATE_KNOTS, GATE_BASE)
+    # the required bandwidth depends on the curves only (the transfer the hit
+    # path adds is credited back), so it is computed once, at the measured rate
+    hit = be.hit_curve_from_restore(base, bpt, restore_GBps)
+    copy = be.Curve(GATE_KNOTS, [x * bpt / (restore_GBps * 1e9) for x in GATE_KNOTS])
+    need = {d: be.required_GBps(cold, hit, copy, d, bpt) for d in (1024, 8192, 81920)}
+    out = {"curves": "synthetic: cold 0.012 + 1.4e-5 x + 2.2e-10 x^2 s, hit non-transfer "
+                     "0.010 + 1.0e-7 x s (x tokens), knots 1k..128k",
+           "bytes_per_token": bpt, "granularity_tokens": 256,
+           "required_GBps": {str(d): round(v, 3) for d, v in need.items()}, "tiers": []}
+    for name, rate in (("staging (measured)", restore_GBps), ("10x slower", restore_GBps / 10),
+                       ("100x slower", restore_GBps / 100)):
+        out["tiers"].append({
+            "tier": name, "restore_GBps": round(rate, 3),
+            "threshold_tokens": be.tier_threshold(cold, base, bpt, rate, 131072, 256),
+            "sustains_required_at": [d for d, v in need.items() if rate >= v]})
+    return out
 
 
 def offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe):
@@ -427,7 +508,7 @@ def deferred_store(ring, bt_src, dev, offload_s):
         during.append(time.perf_counter() - t1)
         kvx.kvx_offload_wait(ring)
         both.append(time.perf_counter() - t0)
-    kvx.kvx_check()
+    kvx.kvx_check(side)
     t_c, t_b = statistics.median(alone), statistics.median(both)
     flops = 2.0 * 8192 ** 3 * k
     return {"gemms": k, "compute_alone_ms": round(t_c * 1e3, 2),
@@ -477,7 +558,12 @@ def cpu_baseline(args, L, BS, H, D, E, perm):
         t0 = time.perf_counter()
         one(0, m)
         times1.append(time.perf_counter() - t0)
-    cores = max(1, min(16, len(os.sched_getaffinity(0))))
+    # every core of the process's affinity mask, unless OMP_NUM_THREADS says
+    # the process's CPU share is smaller (on the GPU machine it is set to the one
+    # GPU's share of the host, 16 threads)
+    affinity = len(os.sched_getaffinity(0))
+    share = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    cores = max(1, min(affinity, share) if share > 0 else affinity)
     nch = (m + bpc - 1) // bpc
     bounds = [min(m, (nch * i // cores) * bpc) for i in range(cores + 1)]
     timesn = []
@@ -488,12 +574,39 @@ def cpu_baseline(args, L, BS, H, D, E, perm):
             timesn.append(time.perf_counter() - t0)
     rw = 2 * 2 * out.nbytes
     one_core = rw / statistics.median(times1) / 1e9
+
+    def rates(times):
+        return {"median": round(rw / statistics.median(times) / 1e9, 2),
+                "mean": round(rw / statistics.mean(times) / 1e9, 2),
+                "min": round(rw / max(times) / 1e9, 2), "max": round(rw / min(times) / 1e9, 2)}
+
+    cpu_model, numa_nodes = host_cpu()
     return {"value": round(rw / statistics.median(timesn) / 1e9, 2), "unit": "GB/s",
             "cores": cores, "kind": "oracle",
             "sample": f"gather + scatter of {m} of the {args.prefix_blocks} prefix blocks "
-                      f"({out.nbytes / 1e9:.2f} GB payload each way), median of 3; "
-                      f"{cores} threads each running the C oracle on a disjoint chunk range; "
-                      f"single thread: {one_core:.2f} GB/s"}
+                      f"({out.nbytes / 1e9:.2f} GB payload each way, GB/s of bytes read + "
+                      f"written), 3 repetitions; {cores} threads each running the C oracle on "
+                      f"a disjoint chunk range; single thread: {one_core:.2f} GB/s",
+            "rates_GBps": {"threads": rates(timesn), "single_thread": rates(times1)},
+            "affinity_cores": affinity, "omp_num_threads": share or None,
+            "cpu_model": cpu_model, "numa_nodes": numa_nodes}
+
+
+def host_cpu():
+    """The host's CPU model name and NUMA node count (None where unknown)."""
+    import glob
+
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    nodes = len(glob.glob("/sys/devices/system/node/node[0-9]*")) or None
+    return model, nodes
 
 
 # ---- 32k-token granularity sweep --------------------------------------------------------
@@ -633,32 +746,28 @@ def run_batch(args):
     s_r, s_o = torch.cuda.Stream(), torch.cuda.Stream()
 
     def one_step():
-        """The store of the new blocks runs deferred (kvx_offload_begin) while
-        the restore of the missing chunks runs on this thread."""
+        """Both transfers run on the rings' own threads (kvx_restore_begin,
+        kvx_offload_begin); this thread starts them and collects them. The
+        restore is timed to its last scatter, the offload by its ring (from
+        the start of its transfer until every destination holds its image)."""
         t = {}
-        done = {}
-
-        def collect():
-            kvx.kvx_offload_wait(o_ring)
-            done["offload"] = time.perf_counter()
-
         t0 = time.perf_counter()
+        kvx.kvx_restore_begin(r_ring, rbt, stream=s_r)
         kvx.kvx_offload_begin(o_ring, obt, stream=s_o)
-        waiter = threading.Thread(target=collect)
-        waiter.start()
-        kvx.kvx_restore_from_staging(r_ring, rbt, stream=s_r)
+        kvx.kvx_restore_wait(r_ring, stream=s_r)
         s_r.synchronize()
         t["restore"] = time.perf_counter() - t0
-        waiter.join()
-        t["offload"] = done["offload"] - t0
+        kvx.kvx_offload_wait(o_ring)
         t["step"] = time.perf_counter() - t0
+        t["offload"] = o_ring.stats()["enqueue_ms"] / 1e3
         return t
 
     for _ in range(args.warmup):
         one_step()
     torch.cuda.synchronize()
     recs = [one_step() for _ in range(args.steps)]
-    kvx.kvx_check()
+    kvx.kvx_check(s_r)
+    kvx.kvx_check(s_o)
     med = {k: statistics.median(r[k] for r in recs) for k in recs[0]}
     # each leg alone, for comparison with the concurrent step
     alone = {"restore": [], "offload": []}
@@ -670,6 +779,8 @@ def run_batch(args):
         t0 = time.perf_counter()
         kvx.kvx_offload_to_staging(o_ring, obt, stream=s_o)
         alone["offload"].append(time.perf_counter() - t0)
+    kvx.kvx_check(s_r)
+    kvx.kvx_check(s_o)
     alone = {k: min(v) for k, v in alone.items()}
     o_stats = o_ring.stats()
     r_stats = r_ring.stats()
@@ -682,7 +793,9 @@ def run_batch(args):
                        "restore_blocks": plan.restore_blocks,
                        "offload_blocks": plan.offload_blocks,
                        "resident_chunks": plan.resident_hits, "parallelism": "single GPU"})
-    out.update({"restore_GBps": round(rb / med["restore"] / 1e9, 2),
+    out.update({"step_calls": "kvx_restore_begin / kvx_offload_begin from one thread, then "
+                              "kvx_restore_wait / kvx_offload_wait",
+                "restore_GBps": round(rb / med["restore"] / 1e9, 2),
                 "restore_frac_of_h2d": round(rb / med["restore"] / 1e9 / (probe["h2d_GBps"]), 4),
                 "offload_GBps": round(ob / med["offload"] / 1e9, 2),
                 "offload_frac_of_d2h": round(ob / med["offload"] / 1e9 / probe["d2h_GBps"], 4),
