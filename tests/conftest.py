@@ -24,6 +24,12 @@ def _built():
 
 
 def pytest_sessionstart(session):
+    # KVX_TEST_LIB: run the tests against another build of libkvx (the
+    # sanitizer tests' host-only build); nothing outside tests/ reads it.
+    if os.environ.get("KVX_TEST_LIB"):
+        from paper_2609_11744_amd import _native
+
+        _native.LIB_PATH = os.environ["KVX_TEST_LIB"]
     # Build only when nothing is built; after a source change run
     # __graft_entry__.build() before pytest.
     if not _built() and not os.environ.get("KVX_NO_AUTOBUILD"):
