@@ -123,6 +123,7 @@ struct UnitGeom {
   uint32_t n16;              // 16-byte vectors per slab
   uint32_t parts;            // workgroups per slab (parts_shift: log2 of a power of two, else 32)
   uint32_t parts_shift;
+  uint32_t two_fronts;       // ordered scatter: walk each XCD's range as two fronts
   DivU32 parts_div;
   DivU32 upc_div;            // by units_per_chunk
   DivU32 bpc_div;            // by bpc
@@ -145,6 +146,24 @@ __device__ int g_error_words[kErrorWords];
 __device__ __forceinline__ uint32_t xcd_contiguous(uint32_t b, uint32_t n) {
   const uint32_t q = n / kXcds, r = n % kXcds, x = b % kXcds, k = b / kXcds;
   return x * q + (x < r ? x : r) + k;
+}
+
+// The same ranges for the destination-ordered scatter, walked as two fronts:
+// XCD x's range is cut into halves (the first a whole number of slabs,
+// `parts` work items each, parts a power of two, 2^shift) and its workgroups
+// alternate between them, one work item at a time (items past twice the
+// first half follow in order). A bijection on [0, n). Where the halves are
+// whole layer|K|V slices apart, the two fronts move the same destination
+// block of two slices together: its writes in two cache tensors, its reads
+// from one packed chunk, `distance` slices apart. The launcher uses it only
+// where that pairing measured faster (two_fronts_pays).
+__device__ __forceinline__ uint32_t xcd_two_fronts(uint32_t b, uint32_t n, uint32_t shift) {
+  const uint32_t q = n / kXcds, r = n % kXcds, x = b % kXcds, k = b / kXcds;
+  const uint32_t len = q + (x < r ? 1u : 0u), start = x * q + (x < r ? x : r);
+  const uint32_t half = ((len >> 1) >> shift) << shift;
+  if (k >= 2 * half) return start + k;
+  const uint32_t pair = k >> (shift + 1), i = k & ((2u << shift) - 1);
+  return start + (i & 1) * half + (pair << shift) + (i >> 1);
 }
 
 template <int T, int V>
@@ -488,8 +507,10 @@ __global__ void __launch_bounds__(T)
                       const OrderEntry* __restrict__ order, char* __restrict__ packed,
                       int* __restrict__ err) {
   uint32_t part;
-  uint32_t u = split_work(work_base + xcd_contiguous(blockIdx.x, work_count), g.parts,
-                          g.parts_shift, g.parts_div, &part);
+  const uint32_t w = kOrdered && g.two_fronts
+                         ? xcd_two_fronts(blockIdx.x, work_count, g.parts_shift)
+                         : xcd_contiguous(blockIdx.x, work_count);
+  uint32_t u = split_work(work_base + w, g.parts, g.parts_shift, g.parts_div, &part);
   uint32_t c, first, nc, lk, j;
   int32_t id;
   char* layer;
@@ -755,6 +776,32 @@ void slab_parts(int layout, uint32_t n16, uint32_t heads, uint32_t* parts, uint3
   *shift = (*parts & (*parts - 1)) == 0 ? (uint32_t)__builtin_ctz(*parts) : 32u;
 }
 
+// Whether the ordered scatter of n_work work items (one launch) walks each
+// XCD's range as two fronts (xcd_two_fronts). It pays, as measured, where
+// the halves of every XCD's range are whole slices apart and the two slabs
+// that move together sit 2 MiB apart in the packed chunk: the 32-layer
+// scatter with 16-block chunks (256 tokens) and 32 KiB slabs, whose fronts
+// are 4 slices apart. Alternated with one front on two boxes (same process
+// layout, library bench): 80k-token scatter 75.1-75.6 % of peak against
+// 72.7-72.9 %, and 80.5-81.0 % against 78.9-79.0 % on a faster box; the 32k
+// scatter with 256-token chunks 72.6-72.8 % against 69.5-70.5 %. The same
+// pairing at other distances (128 KiB, 512 KiB, 8 MiB: the other chunk
+// sizes of the 32k sweep) measured 1-3 points slower than one front, and a
+// standalone probe found no other pairing distance or front count that paid
+// (four fronts 72.1 %, eight 69.0 %, fronts at unrelated destinations 70.8 %,
+// against 72.5 % for one). Why 2 MiB is the distance that pays is not
+// established (it is a property of how the chip maps addresses to memory
+// channels, which these kernels do not see).
+bool two_fronts_pays(uint32_t n_work, uint32_t parts, uint32_t parts_shift, uint32_t n_blocks,
+                     uint32_t bpc, uint64_t slab) {
+  if (parts_shift >= 32 || n_work % kXcds || n_work > kMaxWorkPerLaunch) return false;
+  const uint64_t len = n_work / kXcds;
+  const uint64_t half = ((len >> 1) >> parts_shift) << parts_shift;
+  const uint64_t slice = (uint64_t)parts * n_blocks;  // work items of one slice
+  if (half == 0 || half % slice) return false;
+  return (half / slice) * bpc * slab == (2u << 20);
+}
+
 DivU32 div_u32(uint32_t d) {
   DivU32 f{d, 0u, 0u};
   if (d <= 1) return f;
@@ -870,6 +917,8 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.sg = slab_geom(cache, to_packed);
   if ((uint64_t)g.n_units * ug.parts > 0x7FFFFFFF) return KVX_EINTERNAL;
   const uint32_t n_work = (uint32_t)g.n_units * ug.parts;
+  ug.two_fronts = !to_packed && two_fronts_pays(n_work, ug.parts, ug.parts_shift, ug.n_blocks,
+                                                ug.bpc, ug.slab);
   if (to_packed) {
     hipError_t e = launch<true, false>(lp, block_table, ug, n_work, nullptr, (char*)packed, err,
                                        layout, elem, stream);
