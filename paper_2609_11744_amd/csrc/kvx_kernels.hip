@@ -123,7 +123,12 @@ struct UnitGeom {
   uint32_t n16;              // 16-byte vectors per slab
   uint32_t parts;            // workgroups per slab (parts_shift: log2 of a power of two, else 32)
   uint32_t parts_shift;
-  uint32_t two_fronts;       // ordered scatter: walk each XCD's range as two fronts
+  // Ordered scatter walked as two fronts per XCD (xcd_two_fronts) whose
+  // slices are paired pair_dist apart (paired_slice); pair_shift = log2 of
+  // pair_dist, or 32 for one front per XCD.
+  uint32_t pair_shift;
+  uint32_t half_slices;      // slices per half of an XCD's range
+  DivU32 xcd_slices_div;     // by slices per XCD range
   DivU32 parts_div;
   DivU32 upc_div;            // by units_per_chunk
   DivU32 bpc_div;            // by bpc
@@ -152,11 +157,11 @@ __device__ __forceinline__ uint32_t xcd_contiguous(uint32_t b, uint32_t n) {
 // XCD x's range is cut into halves (the first a whole number of slabs,
 // `parts` work items each, parts a power of two, 2^shift) and its workgroups
 // alternate between them, one work item at a time (items past twice the
-// first half follow in order). A bijection on [0, n). Where the halves are
-// whole layer|K|V slices apart, the two fronts move the same destination
-// block of two slices together: its writes in two cache tensors, its reads
-// from one packed chunk, `distance` slices apart. The launcher uses it only
-// where that pairing measured faster (two_fronts_pays).
+// first half follow in order). A bijection on [0, n). The launcher uses it
+// only where each XCD's range is a whole, even number of layer|K|V slices,
+// so that the two fronts move the same destination block of two slices
+// together (its writes in two cache tensors, its reads from one packed
+// chunk), and paired_slice chooses which two (scatter_pairing).
 __device__ __forceinline__ uint32_t xcd_two_fronts(uint32_t b, uint32_t n, uint32_t shift) {
   const uint32_t q = n / kXcds, r = n % kXcds, x = b % kXcds, k = b / kXcds;
   const uint32_t len = q + (x < r ? 1u : 0u), start = x * q + (x < r ? x : r);
@@ -164,6 +169,18 @@ __device__ __forceinline__ uint32_t xcd_two_fronts(uint32_t b, uint32_t n, uint3
   if (k >= 2 * half) return start + k;
   const uint32_t pair = k >> (shift + 1), i = k & ((2u << shift) - 1);
   return start + (i & 1) * half + (pair << shift) + (i >> 1);
+}
+
+// Slice of the ordered walk's slice r (r / S-th XCD range, S slices each,
+// halves of H = S / 2): slice t of the first half of XCD x's range and slice
+// t of its second half are pair j = H x + t, which moves slices a_j and a_j +
+// D (a_j: the j-th slice whose index has bit log2 D clear, D = 2^pair_shift).
+// A bijection on the slices when their count is a multiple of 2 D.
+__device__ __forceinline__ uint32_t paired_slice(uint32_t r, DivU32 sx, uint32_t half,
+                                                 uint32_t ds) {
+  const uint32_t x = divu(r, sx), rem = r - x * sx.d;
+  const uint32_t h = rem >= half ? 1u : 0u, jj = half * x + rem - h * half;
+  return ((jj >> ds) << (ds + 1)) + (jj & ((1u << ds) - 1)) + (h << ds);
 }
 
 template <int T, int V>
@@ -507,7 +524,7 @@ __global__ void __launch_bounds__(T)
                       const OrderEntry* __restrict__ order, char* __restrict__ packed,
                       int* __restrict__ err) {
   uint32_t part;
-  const uint32_t w = kOrdered && g.two_fronts
+  const uint32_t w = kOrdered && g.pair_shift < 32
                          ? xcd_two_fronts(blockIdx.x, work_count, g.parts_shift)
                          : xcd_contiguous(blockIdx.x, work_count);
   uint32_t u = split_work(work_base + w, g.parts, g.parts_shift, g.parts_div, &part);
@@ -515,8 +532,10 @@ __global__ void __launch_bounds__(T)
   int32_t id;
   char* layer;
   if (kOrdered) {
-    lk = divu(u, g.nb_div);
-    const OrderEntry e = order[u - lk * g.n_blocks];  // e.index < n_blocks (a permutation)
+    const uint32_t walk = divu(u, g.nb_div);  // slice in walk order
+    const OrderEntry e = order[u - walk * g.n_blocks];  // e.index < n_blocks (a permutation)
+    lk = g.pair_shift < 32 ? paired_slice(walk, g.xcd_slices_div, g.half_slices, g.pair_shift)
+                           : walk;
     layer = layers.p[lk];
     __asm__ volatile("" : : "s"(e.index), "s"(e.id), "s"(layer));
     const uint32_t i = e.index;
@@ -776,30 +795,31 @@ void slab_parts(int layout, uint32_t n16, uint32_t heads, uint32_t* parts, uint3
   *shift = (*parts & (*parts - 1)) == 0 ? (uint32_t)__builtin_ctz(*parts) : 32u;
 }
 
-// Whether the ordered scatter of n_work work items (one launch) walks each
-// XCD's range as two fronts (xcd_two_fronts). It pays, as measured, where
-// the halves of every XCD's range are whole slices apart and the two slabs
-// that move together sit 2 MiB apart in the packed chunk: the 32-layer
-// scatter with 16-block chunks (256 tokens) and 32 KiB slabs, whose fronts
-// are 4 slices apart. Alternated with one front on two boxes (same process
-// layout, library bench): 80k-token scatter 75.1-75.6 % of peak against
-// 72.7-72.9 %, and 80.5-81.0 % against 78.9-79.0 % on a faster box; the 32k
-// scatter with 256-token chunks 72.6-72.8 % against 69.5-70.5 %. The same
-// pairing at other distances (128 KiB, 512 KiB, 8 MiB: the other chunk
-// sizes of the 32k sweep) measured 1-3 points slower than one front, and a
-// standalone probe found no other pairing distance or front count that paid
-// (four fronts 72.1 %, eight 69.0 %, fronts at unrelated destinations 70.8 %,
-// against 72.5 % for one). Why 2 MiB is the distance that pays is not
-// established (it is a property of how the chip maps addresses to memory
-// channels, which these kernels do not see).
-bool two_fronts_pays(uint32_t n_work, uint32_t parts, uint32_t parts_shift, uint32_t n_blocks,
-                     uint32_t bpc, uint64_t slab) {
-  if (parts_shift >= 32 || n_work % kXcds || n_work > kMaxWorkPerLaunch) return false;
-  const uint64_t len = n_work / kXcds;
-  const uint64_t half = ((len >> 1) >> parts_shift) << parts_shift;
-  const uint64_t slice = (uint64_t)parts * n_blocks;  // work items of one slice
-  if (half == 0 || half % slice) return false;
-  return (half / slice) * bpc * slab == (2u << 20);
+// Pairing for the ordered scatter of n_work work items (one launch) over
+// n_slices layer|K|V slices: log2 of the distance D in slices between the two
+// slices its fronts move together, or 32 for one front per XCD. Two fronts
+// pay, as measured, where the paired slabs sit 2 MiB apart in the packed
+// chunk (D chunk layers apart) and D <= 4: on the 80k scatter pattern
+// (standalone probe, one allocation for the pool, two processes) pairs 2 MiB
+// apart beat one front by 2.2-2.3 points with 16-block chunks (D = 4) and by
+// 0.9-2.0 with 64-block chunks (D = 1), and lost 0.6-1.1 with 4-block chunks
+// (D = 16); pairs at any other distance (32 KiB to 64 MiB) lost 0.5-2 points
+// to one front in all but one process. In the library, alternated on three
+// boxes: the 80k scatter (D = 4) 75.1-75.6 % of peak against 72.7-72.9 %,
+// 80.5-83.0 % against 78.9-80.5 % on two faster boxes; the 32k scatter with
+// 256-token chunks 72.6-72.8 % against 69.5-70.5 %. Why 2 MiB is the
+// distance that pays is not established: it depends on how the chip maps
+// physical addresses to memory channels, which these kernels do not see.
+uint32_t scatter_pairing(uint32_t n_work, uint32_t parts_shift, uint32_t n_slices, uint32_t bpc,
+                         uint64_t slab) {
+  constexpr uint64_t kPairBytes = 2u << 20;
+  if (parts_shift >= 32 || n_work > kMaxWorkPerLaunch || n_slices % (2 * kXcds)) return 32;
+  const uint64_t run = (uint64_t)bpc * slab;  // one slice's run in a chunk
+  if (run == 0 || kPairBytes % run) return 32;
+  const uint64_t d = kPairBytes / run;
+  const uint32_t ds = d == 1 ? 0 : d == 2 ? 1 : d == 4 ? 2 : 32;
+  if (ds == 32 || n_slices % (2 * d)) return 32;
+  return ds;
 }
 
 DivU32 div_u32(uint32_t d) {
@@ -917,8 +937,11 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.sg = slab_geom(cache, to_packed);
   if ((uint64_t)g.n_units * ug.parts > 0x7FFFFFFF) return KVX_EINTERNAL;
   const uint32_t n_work = (uint32_t)g.n_units * ug.parts;
-  ug.two_fronts = !to_packed && two_fronts_pays(n_work, ug.parts, ug.parts_shift, ug.n_blocks,
-                                                ug.bpc, ug.slab);
+  const uint32_t n_slices = (uint32_t)(2 * g.lr);
+  ug.pair_shift = to_packed ? 32u
+                            : scatter_pairing(n_work, ug.parts_shift, n_slices, ug.bpc, ug.slab);
+  ug.half_slices = n_slices / kXcds / 2;
+  ug.xcd_slices_div = div_u32(n_slices / kXcds ? n_slices / kXcds : 1);
   if (to_packed) {
     hipError_t e = launch<true, false>(lp, block_table, ug, n_work, nullptr, (char*)packed, err,
                                        layout, elem, stream);
