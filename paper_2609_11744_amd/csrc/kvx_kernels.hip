@@ -125,8 +125,10 @@ struct UnitGeom {
   uint32_t parts_shift;
   // Ordered scatter walked as two fronts per XCD (xcd_two_fronts) whose
   // slices are paired pair_dist apart (paired_slice); pair_shift = log2 of
-  // pair_dist, or 32 for one front per XCD.
+  // pair_dist, or 32 for one front per XCD. Gather: each chunk's slices
+  // walked in pairs gather_pair_dist apart (see the unit decode), or 32.
   uint32_t pair_shift;
+  uint32_t gather_pair_shift;
   uint32_t half_slices;      // slices per half of an XCD's range
   DivU32 xcd_slices_div;     // by slices per XCD range
   DivU32 parts_div;
@@ -551,9 +553,26 @@ __global__ void __launch_bounds__(T)
     const uint32_t r = u - c * g.units_per_chunk;
     first = c * g.bpc;
     const uint32_t left = g.n_blocks - first;
-    nc = left < g.bpc ? left : g.bpc;                   // blocks in this chunk
-    lk = divu(r, nc == g.bpc ? g.bpc_div : g.last_div);  // 2 * (l - l0) + kv
-    j = r - lk * nc;
+    nc = left < g.bpc ? left : g.bpc;  // blocks in this chunk
+    const DivU32 ncd = nc == g.bpc ? g.bpc_div : g.last_div;
+    if (g.gather_pair_shift < 32) {
+      // Paired walk of the chunk: its work items in walk order are pair p of
+      // slices (a_p, a_p + D) (a_p: the p-th slice whose index has bit log2 D
+      // clear, D = 2^ds), then block j, then the two slices' part `part`
+      // alternately. A bijection on the chunk's items.
+      const uint32_t ps = g.parts_shift + 1, ds = g.gather_pair_shift;
+      const uint32_t wi = (r << g.parts_shift) + part;  // walk position within the chunk
+      const uint32_t p = divu(wi >> ps, ncd);            // 2 * nc * parts items per pair
+      const uint32_t r2 = wi - ((p * nc) << ps);
+      const uint32_t r3 = r2 & ((1u << ps) - 1);
+      j = r2 >> ps;
+      part = r3 >> 1;
+      lk = ((p >> ds) << (ds + 1)) + (p & ((1u << ds) - 1)) + ((r3 & 1) << ds);
+      u = c * g.units_per_chunk + lk * nc + j;  // image position of (lk, j)
+    } else {
+      lk = divu(r, ncd);  // 2 * (l - l0) + kv
+      j = r - lk * nc;
+    }
     id = block_table[first + j];
     layer = layers.p[lk];
     __asm__ volatile("" : : "s"(id), "s"(layer));
@@ -810,16 +829,31 @@ void slab_parts(int layout, uint32_t n16, uint32_t heads, uint32_t* parts, uint3
 // 256-token chunks 72.6-72.8 % against 69.5-70.5 %. Why 2 MiB is the
 // distance that pays is not established: it depends on how the chip maps
 // physical addresses to memory channels, which these kernels do not see.
-uint32_t scatter_pairing(uint32_t n_work, uint32_t parts_shift, uint32_t n_slices, uint32_t bpc,
-                         uint64_t slab) {
+uint32_t pairing_2mib(uint32_t parts_shift, uint32_t n_slices, uint32_t bpc, uint64_t slab) {
   constexpr uint64_t kPairBytes = 2u << 20;
-  if (parts_shift >= 32 || n_work > kMaxWorkPerLaunch || n_slices % (2 * kXcds)) return 32;
+  if (parts_shift >= 32) return 32;
   const uint64_t run = (uint64_t)bpc * slab;  // one slice's run in a chunk
   if (run == 0 || kPairBytes % run) return 32;
   const uint64_t d = kPairBytes / run;
   const uint32_t ds = d == 1 ? 0 : d == 2 ? 1 : d == 4 ? 2 : 32;
   if (ds == 32 || n_slices % (2 * d)) return 32;
   return ds;
+}
+
+uint32_t scatter_pairing(uint32_t n_work, uint32_t parts_shift, uint32_t n_slices, uint32_t bpc,
+                         uint64_t slab) {
+  if (n_work > kMaxWorkPerLaunch || n_slices % (2 * kXcds)) return 32;
+  return pairing_2mib(parts_shift, n_slices, bpc, slab);
+}
+
+// Pairing for the gather: each chunk's slices walked in pairs 2 MiB apart in
+// the chunk, D <= 4 slices (the packed-side writes then alternate between two
+// runs 2 MiB apart). On the 80k gather pattern (standalone probe, two
+// processes each) this measured 0.3-0.8 points above the plain walk with 16-
+// and 64-block chunks; pairs at other distances (512 KiB to 32 MiB) were
+// 0.5-4 points slower.
+uint32_t gather_pairing(uint32_t parts_shift, uint32_t n_slices, uint32_t bpc, uint64_t slab) {
+  return pairing_2mib(parts_shift, n_slices, bpc, slab);
 }
 
 DivU32 div_u32(uint32_t d) {
@@ -940,6 +974,8 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   const uint32_t n_slices = (uint32_t)(2 * g.lr);
   ug.pair_shift = to_packed ? 32u
                             : scatter_pairing(n_work, ug.parts_shift, n_slices, ug.bpc, ug.slab);
+  ug.gather_pair_shift =
+      to_packed ? gather_pairing(ug.parts_shift, n_slices, ug.bpc, ug.slab) : 32u;
   ug.half_slices = n_slices / kXcds / 2;
   ug.xcd_slices_div = div_u32(n_slices / kXcds ? n_slices / kXcds : 1);
   if (to_packed) {
