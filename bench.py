@@ -91,6 +91,9 @@ def parse():
     ap.add_argument("--io-depth", type=int, default=8, help="8b-files: storage I/O depth")
     ap.add_argument("--offload-reps", type=int, default=3,
                     help="reps of the staged offload leg (8b-80k), timed after the steps")
+    ap.add_argument("--trace-out", default="",
+                    help="8b-80k: write the traced restore's timeline (run after the timed "
+                         "steps) as Chrome trace-event JSON to this path")
     ap.add_argument("--sweep-reps", type=int, default=5,
                     help="reps of the 32k-token gather / scatter sweep (8b-80k), timed after "
                          "the steps; 0 skips it")
@@ -286,6 +289,7 @@ def run_80k(args):
     wall_ms = (time.perf_counter() - t_begin) * 1e3
     kvx.kvx_check()
     log("timed steps done")
+    timeline = restore_timeline(args, ring, bt_rst)
     offload = offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe)
     sweep = sweep_32k(args, cache, L, perm, packed, slab, args.sweep_reps) \
         if H == 8 and args.sweep_reps > 0 else None
@@ -330,6 +334,7 @@ def run_80k(args):
         "restore_breakdown_ms": {"fill_thread_sum": round(med["fill_ms"], 2),
                                  "enqueue_wait_for_fill": round(med["wait_fill_ms"], 2),
                                  "device_span": round(med["restore_dev_ms"], 2)},
+        "restore_timeline": timeline,
         "offload": offload,
         "sweep_32k": sweep,
         "gate": gate,
@@ -346,6 +351,80 @@ def run_80k(args):
     print(json.dumps(out), flush=True)
     ring.close()
     image.free()
+
+
+def restore_timeline(args, ring, bt_rst):
+    """One more restore, outside the timed steps, with the ring's timeline on
+    (kvx_ring_set_trace): the counters it yields (host-to-device busy time
+    and gaps, per-piece fill, copy and scatter times), and with --trace-out
+    the timeline itself as Chrome trace-event JSON."""
+    import torch
+
+    import paper_2609_11744_amd as kvx
+
+    ring.set_trace(True)
+    try:
+        t0 = time.perf_counter()
+        kvx.kvx_restore_from_staging(ring, bt_rst)
+        torch.cuda.synchronize()
+        wall_ms = (time.perf_counter() - t0) * 1e3
+        ev = ring.trace()
+    finally:
+        ring.set_trace(False)
+    if args.trace_out:
+        with open(args.trace_out, "w") as f:
+            json.dump(kvx.trace_chrome(ev, name="restore, 80k-token prefix"), f)
+    summary = timeline_summary(ev)
+    summary["restore_ms_traced"] = round(wall_ms, 3)
+    log(f"restore timeline: {summary}")
+    return summary
+
+
+def timeline_summary(ev):
+    """Counters of a restore timeline: pieces, the host-to-device copies' busy
+    time (union of their intervals), span and idle gaps, their rate while
+    busy, the median piece's fill (first fill start to last fill end), copy
+    and scatter times, and how long the first copy waited from the first fill
+    and the last scatter ran past the last copy."""
+    by = {}
+    for e in ev:
+        by.setdefault(e["kind"], []).append(e)
+    h2d = sorted(by.get("h2d", []), key=lambda e: e["t0_ns"])
+    if not h2d:
+        return {"pieces": 0}
+    busy, end, gaps = 0, None, []
+    for e in h2d:
+        if end is None or e["t0_ns"] >= end:
+            if end is not None:
+                gaps.append(e["t0_ns"] - end)
+            busy += e["t1_ns"] - e["t0_ns"]
+            end = e["t1_ns"]
+        elif e["t1_ns"] > end:
+            busy += e["t1_ns"] - end
+            end = e["t1_ns"]
+    fills = {}
+    for e in by.get("fill", []):
+        a, b = fills.get(e["piece"], (e["t0_ns"], e["t1_ns"]))
+        fills[e["piece"]] = (min(a, e["t0_ns"]), max(b, e["t1_ns"]))
+    scat = sorted(by.get("scatter", []), key=lambda e: e["t0_ns"])
+    first = min((a for a, _ in fills.values()), default=h2d[0]["t0_ns"])
+    return {
+        "pieces": len(h2d),
+        "h2d_busy_ms": round(busy / 1e6, 3),
+        "h2d_span_ms": round((h2d[-1]["t1_ns"] - h2d[0]["t0_ns"]) / 1e6, 3),
+        "h2d_idle_ms": round(sum(gaps) / 1e6, 3),
+        "h2d_max_gap_us": round(max(gaps, default=0) / 1e3, 1),
+        "h2d_GBps_while_busy": round(sum(e["bytes"] for e in h2d) / busy, 2) if busy else None,
+        "piece_fill_ms_median": round(statistics.median(b - a for a, b in fills.values()) / 1e6,
+                                      3) if fills else None,
+        "piece_h2d_ms_median": round(statistics.median(e["t1_ns"] - e["t0_ns"] for e in h2d)
+                                     / 1e6, 3),
+        "piece_scatter_us_median": round(statistics.median(e["t1_ns"] - e["t0_ns"] for e in scat)
+                                         / 1e3, 1) if scat else None,
+        "first_h2d_after_first_fill_ms": round((h2d[0]["t0_ns"] - first) / 1e6, 3),
+        "last_scatter_after_last_h2d_us": round((scat[-1]["t1_ns"] - h2d[-1]["t1_ns"]) / 1e3, 1)
+        if scat else None,
+    }
 
 
 def ms_stats(v):

@@ -420,6 +420,66 @@ typedef struct kvx_ring_stats {
 
 kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out);
 
+/* ---- transfer timeline ---------------------------------------------------------- *
+ *
+ * The paper traces its connector with a profiler whose timeline shows storage
+ * reads interleaved with GPU transfers (Sec. 4.1, the trace sample). A ring
+ * with tracing on records, for its transfers, one interval per:
+ *   KVX_TRACE_FILL     a fill thread copying its share of a piece into the
+ *                      piece's pinned slot (restore; lane = the thread);
+ *   KVX_TRACE_DRAIN    a drain thread copying its share out of the slot
+ *                      (offload; lane = the thread);
+ *   KVX_TRACE_WAIT     the enqueuing thread waiting for a piece's fill or
+ *                      drain threads;
+ *   KVX_TRACE_H2D      a piece's host-to-device copy (restore);
+ *   KVX_TRACE_D2H      a piece's device-to-host copy (offload);
+ *   KVX_TRACE_SCATTER  a piece's fused scatter launch (restore);
+ *   KVX_TRACE_GATHER   a piece's fused gather launch (offload).
+ * Times are nanoseconds of the host's monotonic clock (CLOCK_MONOTONIC, the
+ * clock of std::chrono::steady_clock and Python's time.monotonic_ns), so host
+ * events of the caller line up with them. Copies on the DMA engines carry the
+ * engine's own start and end (HSA async-copy timestamps, converted from the
+ * HSA system clock sampled at the transfer's start); copies through the HIP
+ * runtime and the launches carry timing events, placed on the host clock by a
+ * reference event that the transfer records and waits for before its first
+ * piece (so a traced transfer first waits for work already queued on its
+ * stream, and device intervals may be off by the few microseconds between
+ * that event completing and the host seeing it). A DMA copy issued as several
+ * copies (a piece of several host spans, no fill or drain threads) has no
+ * H2D / D2H interval. Transfers bound to chunk files record no fill or drain
+ * intervals (the reactor's reads and writes are not traced). */
+#define KVX_TRACE_FILL 1
+#define KVX_TRACE_DRAIN 2
+#define KVX_TRACE_WAIT 3
+#define KVX_TRACE_H2D 4
+#define KVX_TRACE_D2H 5
+#define KVX_TRACE_SCATTER 6
+#define KVX_TRACE_GATHER 7
+
+typedef struct kvx_trace_event {
+  int32_t kind;    /* KVX_TRACE_* */
+  int32_t piece;   /* piece index within the transfer */
+  int32_t lane;    /* fill / drain thread; 0 for the others */
+  int32_t slot;    /* staging slot of the piece */
+  int64_t bytes;   /* bytes the interval moved (0 for KVX_TRACE_WAIT) */
+  int64_t t0_ns;   /* start and end, host monotonic clock */
+  int64_t t1_ns;
+} kvx_trace_event;
+
+/* Turn recording of the timeline on (enable = 1) or off (0) for this ring's
+ * next transfers; each transfer replaces the previous one's record. While any
+ * ring in the process traces, copies on the DMA engines are profiled (HSA
+ * async-copy profiling, process-wide). KVX_EBUSY during an asynchronous
+ * transfer. */
+kvx_status kvx_ring_set_trace(kvx_ring* ring, int32_t enable);
+
+/* The last traced transfer's intervals, ordered by start: up to cap of them
+ * into out (caller-owned; out may be null with cap 0), their total count into
+ * *n. Waits until that transfer's traced launches and copies have finished.
+ * KVX_EBUSY during an asynchronous transfer; *n = 0 if the last transfer was
+ * not traced or failed. */
+kvx_status kvx_ring_trace_get(kvx_ring* ring, kvx_trace_event* out, int32_t cap, int32_t* n);
+
 /* Make a running or later restore on this ring return KVX_ECLOSED. Safe to
  * call from another thread. */
 kvx_status kvx_ring_abort(kvx_ring* ring);

@@ -283,6 +283,35 @@ def kvx_check(stream=None) -> None:
 
 KVX_RAMP_NONE, KVX_RAMP_FIRST, KVX_RAMP_LAST = 0, 1, 2
 
+# kvx_trace_event kinds (include/kvx.h)
+TRACE_KINDS = {1: "fill", 2: "drain", 3: "wait", 4: "h2d", 5: "d2h", 6: "scatter", 7: "gather"}
+
+
+def trace_chrome(events, name="ring") -> dict:
+    """A ring timeline (StagingRing.trace) as Chrome trace-event JSON: one
+    complete event per interval, one track per fill or drain thread and one
+    each for the enqueuing thread's waits, the host-link copies and the
+    launches; times in microseconds from the first interval."""
+    t0 = min((e["t0_ns"] for e in events), default=0)
+    tracks = {"wait": (1, "enqueue thread: waits for fill / drain"),
+              "h2d": (2, "host-to-device copies"), "d2h": (2, "device-to-host copies"),
+              "scatter": (3, "scatter launches"), "gather": (3, "gather launches")}
+    out, named = [], set()
+    for e in events:
+        if e["kind"] in ("fill", "drain"):
+            tid, label = 10 + e["lane"], f'{e["kind"]} thread {e["lane"]}'
+        else:
+            tid, label = tracks.get(e["kind"], (0, e["kind"]))
+        if tid not in named:
+            named.add(tid)
+            out.append({"ph": "M", "name": "thread_name", "pid": 1, "tid": tid,
+                        "args": {"name": label}})
+        out.append({"ph": "X", "name": f'{e["kind"]} piece {e["piece"]}', "pid": 1, "tid": tid,
+                    "ts": (e["t0_ns"] - t0) / 1e3, "dur": (e["t1_ns"] - e["t0_ns"]) / 1e3,
+                    "args": {"piece": e["piece"], "slot": e["slot"], "bytes": e["bytes"]}})
+    out.append({"ph": "M", "name": "process_name", "pid": 1, "args": {"name": name}})
+    return {"traceEvents": out, "displayTimeUnit": "ms"}
+
 
 def kvx_plan_pieces(cache, l0, l1, n_blocks, chunk_tokens, slot_bytes, ramp=KVX_RAMP_NONE):
     """Staging pieces as a list of dicts (pure host computation)."""
@@ -447,6 +476,25 @@ class StagingRing:
         s = KvxRingStats()
         _ok(_native.lib().kvx_ring_stats_get(self.handle, ctypes.byref(s)), "kvx_ring_stats_get")
         return {f: getattr(s, f) for f, _ in KvxRingStats._fields_}
+
+    def set_trace(self, enable=True):
+        """Record the next transfers' timeline (kvx_ring_set_trace)."""
+        _ok(_native.lib().kvx_ring_set_trace(self.handle, 1 if enable else 0),
+            "kvx_ring_set_trace")
+
+    def trace(self) -> list:
+        """The last traced transfer's intervals (kvx_ring_trace_get), ordered by
+        start: dicts with kind (a TRACE_KINDS name), piece, lane, slot, bytes,
+        t0_ns, t1_ns (host monotonic clock, as time.monotonic_ns)."""
+        n = ctypes.c_int32()
+        _ok(_native.lib().kvx_ring_trace_get(self.handle, None, 0, ctypes.byref(n)),
+            "kvx_ring_trace_get")
+        arr = (_native.KvxTraceEvent * max(n.value, 1))()
+        _ok(_native.lib().kvx_ring_trace_get(self.handle, arr, n.value, ctypes.byref(n)),
+            "kvx_ring_trace_get")
+        return [{"kind": TRACE_KINDS.get(e.kind, str(e.kind)), "piece": e.piece, "lane": e.lane,
+                 "slot": e.slot, "bytes": e.bytes, "t0_ns": e.t0_ns, "t1_ns": e.t1_ns}
+                for e in arr[:n.value]]
 
     def abort(self):
         _ok(_native.lib().kvx_ring_abort(self.handle), "kvx_ring_abort")
@@ -669,5 +717,5 @@ __all__ = [
     "kvx_read_files", "kvx_write_files", "KVX_EIO", "KVX_EBUSY", "kvx_offload_begin",
     "kvx_offload_wait", "kvx_restore_begin", "kvx_restore_wait", "kvx_chunk_stride",
     "KVX_RAMP_NONE", "KVX_RAMP_FIRST", "KVX_RAMP_LAST", "kvx_scatter_blocks_noalloc",
-    "KVX_NOALLOC_MAX_BLOCKS",
+    "KVX_NOALLOC_MAX_BLOCKS", "TRACE_KINDS", "trace_chrome",
 ]

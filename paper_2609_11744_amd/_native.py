@@ -37,6 +37,11 @@ class KvxRingStats(ctypes.Structure):
                 ("dma", c_i32), ("dma_engine", c_i32)]
 
 
+class KvxTraceEvent(ctypes.Structure):
+    _fields_ = [("kind", c_i32), ("piece", c_i32), ("lane", c_i32), ("slot", c_i32),
+                ("bytes", c_i64), ("t0_ns", c_i64), ("t1_ns", c_i64)]
+
+
 class KvxFileChunk(ctypes.Structure):
     _fields_ = [("path", ctypes.c_char_p), ("bt_offset", c_i32), ("n_blocks", c_i32)]
 
@@ -117,6 +122,9 @@ SIGNATURES = {
     "kvx_restore_begin": (ctypes.c_int, [c_vp, c_vp, c_vp]),
     "kvx_restore_wait": (ctypes.c_int, [c_vp, c_vp]),
     "kvx_ring_stats_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxRingStats)]),
+    "kvx_ring_set_trace": (ctypes.c_int, [c_vp, c_i32]),
+    "kvx_ring_trace_get": (ctypes.c_int, [c_vp, ctypes.POINTER(KvxTraceEvent), c_i32,
+                                          ctypes.POINTER(c_i32)]),
     "kvx_ring_abort": (ctypes.c_int, [c_vp]),
     "kvx_ring_set_test_hooks": (ctypes.c_int, [c_vp, c_i32, c_i32]),
     "kvx_ring_destroy": (ctypes.c_int, [c_vp]),

@@ -140,11 +140,46 @@ struct kvx_ring {
   std::vector<std::string> pre_paths;  // distinct files, in chunk order
   std::vector<int32_t> pre_file;       // per bound chunk
   std::vector<int64_t> pre_bytes;      // per distinct file: its image bytes
+
+  // timeline (kvx_ring_set_trace): the last traced transfer's intervals
+  bool trace = false;
+  bool traced = false;                    // the last transfer was traced and succeeded
+  bool trace_resolved = false;            // its device intervals are in trace_ev
+  bool trace_to_packed = false;
+  int64_t trace_pieces = 0;
+  std::vector<kvx_trace_event> trace_ev;  // host-clock intervals (guarded by mu)
+  std::vector<hipEvent_t> trace_k;        // per piece: timing events around its launch
+  std::vector<hipEvent_t> trace_c;        // per piece: around its runtime host-link copy
+  std::vector<uint8_t> trace_k_used, trace_c_used;
+  std::vector<int64_t> trace_k_bytes, trace_c_bytes;
+  std::vector<int64_t> trace_dma_piece;   // per slot: piece whose copy time is unread, or -1
+  std::vector<int64_t> trace_dma_bytes;
+  hipEvent_t trace_ref = nullptr;         // recorded and waited for at the transfer's start
+  int64_t trace_ref_ns = 0;               // host clock when it was seen complete
+  uint64_t trace_hsa0 = 0, trace_hsa_hz = 0;
+  int64_t trace_host0 = 0;                // host clock at HSA system time trace_hsa0
 };
 
 namespace {
 
 using clk = std::chrono::steady_clock;
+
+int64_t now_ns() {
+  return std::chrono::duration_cast<std::chrono::nanoseconds>(clk::now().time_since_epoch())
+      .count();
+}
+
+// HSA async-copy profiling is process-wide: on while any ring traces.
+void copy_profiling(bool on) {
+  static std::mutex mu;
+  static int users = 0;
+  std::lock_guard<std::mutex> lock(mu);
+  if (on) {
+    if (users++ == 0) (void)hsa_amd_profiling_async_copy_enable(true);
+  } else if (users > 0 && --users == 0) {
+    (void)hsa_amd_profiling_async_copy_enable(false);
+  }
+}
 
 double ms_since(clk::time_point t0) {
   return std::chrono::duration<double, std::milli>(clk::now() - t0).count();
@@ -204,6 +239,15 @@ void destroy_resources(kvx_ring* r) {
   r->copy_done.clear();
   for (hsa_signal_t sig : r->dma_done) (void)hsa_signal_destroy(sig);
   r->dma_done.clear();
+  for (hipEvent_t e : r->trace_k) (void)hipEventDestroy(e);
+  for (hipEvent_t e : r->trace_c) (void)hipEventDestroy(e);
+  r->trace_k.clear();
+  r->trace_c.clear();
+  if (r->trace_ref) (void)hipEventDestroy(r->trace_ref);
+  r->trace_ref = nullptr;
+  if (r->trace && r->hsa_up) copy_profiling(false);
+  r->trace = false;
+  r->traced = false;
   if (r->hsa_up) (void)hsa_shut_down();
   r->hsa_up = false;
   r->dma = false;
@@ -230,7 +274,7 @@ void destroy_resources(kvx_ring* r) {
 }
 
 // Copy share w of T of a piece between host slot s and its spans.
-void copy_share(kvx_ring* r, const kvx::Piece& p, int32_t s, int w, int T, bool to_slot) {
+int64_t copy_share(kvx_ring* r, const kvx::Piece& p, int32_t s, int w, int T, bool to_slot) {
   int64_t per = (p.bytes + T - 1) / T;
   per = (per + 4095) & ~(int64_t)4095;
   const int64_t a = std::min<int64_t>(p.bytes, per * w);
@@ -246,6 +290,7 @@ void copy_share(kvx_ring* r, const kvx::Piece& p, int32_t s, int w, int T, bool 
     else
       std::memcpy(h, slot + lo, (size_t)(hi - lo));
   }
+  return b - a;
 }
 
 void signal_stop(kvx_ring* r) {
@@ -294,10 +339,12 @@ void fill_worker(kvx_ring* r, int w) {
       if (b > a) std::memset(r->host + (int64_t)s * r->slot_bytes + a, 0xA5, (size_t)(b - a));
       hook_pause(r, &rng);
     }
-    auto t0 = clk::now();
-    copy_share(r, r->plan.pieces[(size_t)i], s, w, T, true);
-    busy += std::chrono::duration_cast<std::chrono::nanoseconds>(clk::now() - t0).count();
+    const int64_t t0 = now_ns();
+    const int64_t bytes = copy_share(r, r->plan.pieces[(size_t)i], s, w, T, true);
+    const int64_t t1 = now_ns();
+    busy += t1 - t0;
     std::lock_guard<std::mutex> lock(r->mu);
+    if (r->trace) r->trace_ev.push_back(kvx_trace_event{KVX_TRACE_FILL, (int32_t)i, w, s, bytes, t0, t1});
     if (++r->parts_done[(size_t)i] == T) r->cv_host.notify_all();
   }
   r->busy_ns.fetch_add(busy);
@@ -322,10 +369,12 @@ void drain_worker(kvx_ring* r, int w) {
       signal_stop(r);
       break;
     }
-    auto t0 = clk::now();
-    copy_share(r, r->plan.pieces[(size_t)i], s, w, T, false);
-    busy += std::chrono::duration_cast<std::chrono::nanoseconds>(clk::now() - t0).count();
+    const int64_t t0 = now_ns();
+    const int64_t bytes = copy_share(r, r->plan.pieces[(size_t)i], s, w, T, false);
+    const int64_t t1 = now_ns();
+    busy += t1 - t0;
     std::lock_guard<std::mutex> lock(r->mu);
+    if (r->trace) r->trace_ev.push_back(kvx_trace_event{KVX_TRACE_DRAIN, (int32_t)i, w, s, bytes, t0, t1});
     if (++r->parts_done[(size_t)i] == T) r->cv_host.notify_all();
   }
   r->busy_ns.fetch_add(busy);
@@ -548,6 +597,136 @@ kvx_status launch_piece(kvx_ring* r, bool to_packed, const kvx::Piece& p, const 
                                  r->slot_bytes, stream, r->err_word);
 }
 
+// ---- timeline (kvx_ring_set_trace) ----------------------------------------------
+
+bool grow_events(std::vector<hipEvent_t>* v, size_t n) {
+  while (v->size() < n) {
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return false;  // timing events
+    v->push_back(e);
+  }
+  return true;
+}
+
+// Start the record of a traced transfer of P pieces whose launches go to
+// `stream`: a reference event on it (waited for, so its time on the host
+// clock is known) and the HSA system clock against the host clock.
+kvx_status trace_begin(kvx_ring* r, hipStream_t stream, int64_t P, bool to_packed) {
+  {
+    std::lock_guard<std::mutex> lock(r->mu);
+    r->trace_ev.clear();
+  }
+  r->traced = false;
+  r->trace_resolved = false;
+  r->trace_pieces = P;
+  r->trace_to_packed = to_packed;
+  if (!grow_events(&r->trace_k, 2 * (size_t)P) || !grow_events(&r->trace_c, 2 * (size_t)P))
+    return KVX_EHIP;
+  if (!r->trace_ref && hipEventCreate(&r->trace_ref) != hipSuccess) return KVX_EHIP;
+  r->trace_k_used.assign((size_t)P, 0);
+  r->trace_c_used.assign((size_t)P, 0);
+  r->trace_k_bytes.assign((size_t)P, 0);
+  r->trace_c_bytes.assign((size_t)P, 0);
+  r->trace_dma_piece.assign((size_t)r->n_slots, -1);
+  r->trace_dma_bytes.assign((size_t)r->n_slots, 0);
+  if (hipEventRecord(r->trace_ref, stream) != hipSuccess ||
+      hipEventSynchronize(r->trace_ref) != hipSuccess)
+    return KVX_EHIP;
+  r->trace_ref_ns = now_ns();
+  r->trace_hsa_hz = 0;
+  uint64_t hz = 0, t = 0;
+  if (r->hsa_up &&
+      hsa_system_get_info(HSA_SYSTEM_INFO_TIMESTAMP_FREQUENCY, &hz) == HSA_STATUS_SUCCESS && hz) {
+    const int64_t a = now_ns();
+    if (hsa_system_get_info(HSA_SYSTEM_INFO_TIMESTAMP, &t) == HSA_STATUS_SUCCESS) {
+      const int64_t b = now_ns();
+      r->trace_host0 = a + (b - a) / 2;
+      r->trace_hsa0 = t;
+      r->trace_hsa_hz = hz;
+    }
+  }
+  return KVX_OK;
+}
+
+void trace_push(kvx_ring* r, const kvx_trace_event& e) {
+  std::lock_guard<std::mutex> lock(r->mu);
+  r->trace_ev.push_back(e);
+}
+
+// Record the DMA copy interval of the piece last copied through slot s (its
+// copies have finished); nothing if it had several copies or no timestamps.
+void trace_dma_read(kvx_ring* r, int32_t s, bool h2d) {
+  const int64_t i = r->trace_dma_piece[(size_t)s];
+  if (i < 0) return;
+  r->trace_dma_piece[(size_t)s] = -1;
+  hsa_amd_profiling_async_copy_time_t t{};
+  if (!r->trace_hsa_hz ||
+      hsa_amd_profiling_get_async_copy_time(r->dma_done[(size_t)s], &t) != HSA_STATUS_SUCCESS ||
+      t.end < t.start)
+    return;
+  auto host = [&](uint64_t v) {
+    const long double d = ((long double)v - (long double)r->trace_hsa0) * 1e9L /
+                          (long double)r->trace_hsa_hz;
+    return r->trace_host0 + (int64_t)d;
+  };
+  trace_push(r, kvx_trace_event{h2d ? KVX_TRACE_H2D : KVX_TRACE_D2H, (int32_t)i, 0, s,
+                                r->trace_dma_bytes[(size_t)s], host(t.start), host(t.end)});
+}
+
+// launch_piece for piece i, between two timing events when tracing.
+kvx_status launch_piece_traced(kvx_ring* r, bool to_packed, int64_t i, const kvx::Piece& p,
+                               const int32_t* bt, uint8_t* dslot, hipStream_t stream) {
+  const bool t = r->trace;
+  if (t && hipEventRecord(r->trace_k[2 * (size_t)i], stream) != hipSuccess) return KVX_EHIP;
+  const kvx_status st = launch_piece(r, to_packed, p, bt, dslot, stream);
+  if (st != KVX_OK) return st;
+  if (t) {
+    if (hipEventRecord(r->trace_k[2 * (size_t)i + 1], stream) != hipSuccess) return KVX_EHIP;
+    r->trace_k_used[(size_t)i] = 1;
+    r->trace_k_bytes[(size_t)i] = p.bytes;
+  }
+  return KVX_OK;
+}
+
+// The device intervals of the last traced transfer (launches, runtime copies)
+// onto the host clock, once; then every interval ordered by start.
+kvx_status trace_resolve(kvx_ring* r) {
+  if (r->trace_resolved) return KVX_OK;
+  std::vector<kvx_trace_event> dev;
+  const int32_t S = r->n_slots;
+  auto at = [&](hipEvent_t e, int64_t* ns) {
+    float ms = 0;
+    if (hipEventSynchronize(e) != hipSuccess ||
+        hipEventElapsedTime(&ms, r->trace_ref, e) != hipSuccess)
+      return false;
+    *ns = r->trace_ref_ns + (int64_t)((double)ms * 1e6);
+    return true;
+  };
+  for (int64_t i = 0; i < r->trace_pieces; ++i) {
+    int64_t a = 0, b = 0;
+    if (r->trace_k_used[(size_t)i]) {
+      if (!at(r->trace_k[2 * (size_t)i], &a) || !at(r->trace_k[2 * (size_t)i + 1], &b))
+        return KVX_EHIP;
+      dev.push_back(kvx_trace_event{r->trace_to_packed ? KVX_TRACE_GATHER : KVX_TRACE_SCATTER,
+                                    (int32_t)i, 0, (int32_t)(i % S), r->trace_k_bytes[(size_t)i], a,
+                                    b});
+    }
+    if (r->trace_c_used[(size_t)i]) {
+      if (!at(r->trace_c[2 * (size_t)i], &a) || !at(r->trace_c[2 * (size_t)i + 1], &b))
+        return KVX_EHIP;
+      dev.push_back(kvx_trace_event{r->trace_to_packed ? KVX_TRACE_D2H : KVX_TRACE_H2D,
+                                    (int32_t)i, 0, (int32_t)(i % S), r->trace_c_bytes[(size_t)i],
+                                    a, b});
+    }
+  }
+  std::lock_guard<std::mutex> lock(r->mu);
+  r->trace_ev.insert(r->trace_ev.end(), dev.begin(), dev.end());
+  std::stable_sort(r->trace_ev.begin(), r->trace_ev.end(),
+                   [](const kvx_trace_event& x, const kvx_trace_event& y) { return x.t0_ns < y.t0_ns; });
+  r->trace_resolved = true;
+  return KVX_OK;
+}
+
 // One async copy on a DMA engine (engine 0: the runtime's choice); the copy
 // decrements sig when it has finished.
 hsa_status_t engine_copy(void* dst, hsa_agent_t dst_agent, const void* src, hsa_agent_t src_agent,
@@ -562,12 +741,15 @@ hsa_status_t engine_copy(void* dst, hsa_agent_t dst_agent, const void* src, hsa_
 // device slot s, or D2H (offload) device slot s to host slot s; without fill
 // or drain threads, one copy per span between its host address and its place
 // in the device slot. dma_done[s] counts the piece's copies down to 0.
-kvx_status issue_dma(kvx_ring* r, const kvx::Piece& p, int32_t s, uint8_t* dslot, uint8_t* hslot,
-                     bool h2d) {
+kvx_status issue_dma(kvx_ring* r, int64_t piece, const kvx::Piece& p, int32_t s, uint8_t* dslot,
+                     uint8_t* hslot, bool h2d) {
   hsa_signal_t sig = r->dma_done[(size_t)s];
   const bool whole = r->threads > 0;
   const int64_t n = whole ? 1 : (int64_t)p.spans.size();
   if (n == 0) return KVX_OK;
+  // the slot's previous copies have finished (every caller waited for them):
+  // read their interval before the signal is reused
+  if (r->trace) trace_dma_read(r, s, h2d);
   hsa_signal_store_screlease(sig, n);
   int64_t issued = 0;
   for (int64_t k = 0; k < n; ++k) {
@@ -584,6 +766,10 @@ kvx_status issue_dma(kvx_ring* r, const kvx::Piece& p, int32_t s, uint8_t* dslot
     hsa_signal_subtract_screlease(sig, n - issued);
     return KVX_EHIP;
   }
+  if (r->trace) {
+    r->trace_dma_piece[(size_t)s] = n == 1 ? piece : -1;
+    r->trace_dma_bytes[(size_t)s] = p.bytes;
+  }
   return KVX_OK;
 }
 
@@ -592,8 +778,8 @@ kvx_status issue_dma(kvx_ring* r, const kvx::Piece& p, int32_t s, uint8_t* dslot
 kvx_status scatter_copied(kvx_ring* r, int64_t j, const int32_t* bt, hipStream_t stream) {
   const int32_t s = (int32_t)(j % r->n_slots);
   if (!wait_dma(r, s)) return KVX_EHIP;
-  kvx_status st = launch_piece(r, false, r->plan.pieces[(size_t)j], bt,
-                               r->landing + (int64_t)s * r->slot_bytes, stream);
+  kvx_status st = launch_piece_traced(r, false, j, r->plan.pieces[(size_t)j], bt,
+                                      r->landing + (int64_t)s * r->slot_bytes, stream);
   if (st != KVX_OK) return st;
   return hipEventRecord(r->dev_done[(size_t)s], stream) == hipSuccess ? KVX_OK : KVX_EHIP;
 }
@@ -647,6 +833,11 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
   r->worker_error.store(0);
   r->stop.store(false);
   r->busy_ns.store(0);
+  r->traced = false;
+  if (r->trace) {
+    const kvx_status ts = trace_begin(r, stream, P, dir == Dir::kOffload);
+    if (ts != KVX_OK) return ts;
+  }
   std::vector<std::thread> workers;
   kvx_status st = KVX_OK;
   double wait_ms = 0;
@@ -671,10 +862,13 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
     st = KVX_ENOMEM;
   }
   auto wait_parts = [&](int64_t i) {
-    auto t0 = clk::now();
+    const int64_t t0 = now_ns();
     std::unique_lock<std::mutex> lock(r->mu);
     r->cv_host.wait(lock, [&] { return r->parts_done[(size_t)i] == T || r->stop.load(); });
-    wait_ms += ms_since(t0);
+    const int64_t t1 = now_ns();
+    wait_ms += (double)(t1 - t0) / 1e6;
+    if (r->trace)
+      r->trace_ev.push_back(kvx_trace_event{KVX_TRACE_WAIT, (int32_t)i, 0, (int32_t)(i % S), 0, t0, t1});
   };
   int64_t copied = -1;  // restore on the DMA engines: the piece copied but not yet scattered
   for (int64_t i = 0; st == KVX_OK && i < P; ++i) {
@@ -718,7 +912,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         st = KVX_EHIP;
         break;
       }
-      st = issue_dma(r, *pp, s, dslot, hslot, true);
+      st = issue_dma(r, i, *pp, s, dslot, hslot, true);
       if (st != KVX_OK) break;
       {
         std::lock_guard<std::mutex> lock(r->mu);
@@ -736,6 +930,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         break;
       }
       bool ok = hipStreamWaitEvent(r->side, r->dev_done[s], 0) == hipSuccess;
+      if (r->trace) ok = ok && hipEventRecord(r->trace_c[2 * (size_t)i], r->side) == hipSuccess;
       if (T > 0) {
         ok = ok && hipMemcpyAsync(dslot, hslot, (size_t)p.bytes, hipMemcpyHostToDevice, r->side) ==
                        hipSuccess;
@@ -743,6 +938,11 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         for (const kvx::Span& sp : pp->spans)
           ok = ok && hipMemcpyAsync(dslot + sp.slot_off, sp.host, (size_t)sp.bytes,
                                     hipMemcpyHostToDevice, r->side) == hipSuccess;
+      }
+      if (r->trace && ok) {
+        ok = hipEventRecord(r->trace_c[2 * (size_t)i + 1], r->side) == hipSuccess;
+        r->trace_c_used[(size_t)i] = ok ? 1 : 0;
+        r->trace_c_bytes[(size_t)i] = p.bytes;
       }
       ok = ok && hipEventRecord(r->copy_done[s], r->side) == hipSuccess;
       if (!ok) {
@@ -758,7 +958,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         st = KVX_EHIP;
         break;
       }
-      st = launch_piece(r, false, p, bt, dslot, stream);
+      st = launch_piece_traced(r, false, i, p, bt, dslot, stream);
       if (st != KVX_OK) break;
       if (hipEventRecord(r->dev_done[s], stream) != hipSuccess) st = KVX_EHIP;
     } else if (use_dma(r)) {
@@ -771,7 +971,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         st = KVX_EHIP;
         break;
       }
-      st = launch_piece(r, true, p, bt, dslot, stream);
+      st = launch_piece_traced(r, true, i, p, bt, dslot, stream);
       if (st != KVX_OK) break;
       if (hipEventRecord(r->dev_done[s], stream) != hipSuccess) {
         st = KVX_EHIP;
@@ -788,7 +988,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         st = KVX_EHIP;
         break;
       }
-      st = issue_dma(r, p, s, dslot, hslot, false);
+      st = issue_dma(r, i, p, s, dslot, hslot, false);
       if (st != KVX_OK) break;
       {
         std::lock_guard<std::mutex> lock(r->mu);
@@ -804,7 +1004,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         st = KVX_EHIP;
         break;
       }
-      st = launch_piece(r, true, p, bt, dslot, stream);
+      st = launch_piece_traced(r, true, i, p, bt, dslot, stream);
       if (st != KVX_OK) break;
       if (hipEventRecord(r->dev_done[s], stream) != hipSuccess) {
         st = KVX_EHIP;
@@ -816,6 +1016,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         break;
       }
       bool ok = hipStreamWaitEvent(r->side, r->dev_done[s], 0) == hipSuccess;
+      if (r->trace) ok = ok && hipEventRecord(r->trace_c[2 * (size_t)i], r->side) == hipSuccess;
       if (T > 0) {
         ok = ok && hipMemcpyAsync(hslot, dslot, (size_t)p.bytes, hipMemcpyDeviceToHost, r->side) ==
                        hipSuccess;
@@ -823,6 +1024,11 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         for (const kvx::Span& sp : p.spans)
           ok = ok && hipMemcpyAsync(sp.host, dslot + sp.slot_off, (size_t)sp.bytes,
                                     hipMemcpyDeviceToHost, r->side) == hipSuccess;
+      }
+      if (r->trace && ok) {
+        ok = hipEventRecord(r->trace_c[2 * (size_t)i + 1], r->side) == hipSuccess;
+        r->trace_c_used[(size_t)i] = ok ? 1 : 0;
+        r->trace_c_bytes[(size_t)i] = p.bytes;
       }
       ok = ok && hipEventRecord(r->copy_done[s], r->side) == hipSuccess;
       if (!ok) {
@@ -849,6 +1055,17 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
     } else if (hipStreamSynchronize(r->side) != hipSuccess) {
       st = KVX_EHIP;
     }
+  }
+  if (st == KVX_OK && r->trace && use_dma(r)) {
+    // the last pieces' copies (finished: waited for above)
+    for (int32_t s = 0; s < S; ++s)
+      if (r->trace_dma_piece[(size_t)s] >= 0) {
+        if (!wait_dma(r, s)) {
+          st = KVX_EHIP;
+          break;
+        }
+        trace_dma_read(r, s, dir == Dir::kRestore);
+      }
   }
   if (st != KVX_OK) {
     signal_stop(r);
@@ -879,6 +1096,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
   r->stats.dma = use_dma(r) ? 1 : 0;
   r->stats.dma_engine =
       use_dma(r) ? (int32_t)(dir == Dir::kRestore ? r->h2d_engine : r->d2h_engine) : 0;
+  r->traced = r->trace && st == KVX_OK;
   return st;
 }
 
@@ -1584,6 +1802,36 @@ kvx_status kvx_ring_stats_get(const kvx_ring* ring, kvx_ring_stats* out) {
   if (ring->async_busy.load()) return KVX_EBUSY;
   *out = ring->stats;
   return KVX_OK;
+}
+
+kvx_status kvx_ring_set_trace(kvx_ring* ring, int32_t enable) {
+  if (!ring || (enable != 0 && enable != 1)) return KVX_EINVAL;
+  if (ring->async_busy.load()) return KVX_EBUSY;
+  const bool on = enable == 1;
+  if (on == ring->trace) return KVX_OK;
+  if (ring->hsa_up) copy_profiling(on);
+  ring->trace = on;
+  return KVX_OK;
+}
+
+kvx_status kvx_ring_trace_get(kvx_ring* ring, kvx_trace_event* out, int32_t cap, int32_t* n) {
+  if (!ring || !n || cap < 0 || (cap > 0 && !out)) return KVX_EINVAL;
+  *n = 0;
+  if (ring->async_busy.load()) return KVX_EBUSY;
+  if (!ring->traced) return KVX_OK;
+  try {
+    DeviceGuard dg(ring->device);
+    if (!dg.ok) return KVX_EHIP;
+    const kvx_status st = trace_resolve(ring);
+    if (st != KVX_OK) return st;
+    std::lock_guard<std::mutex> lock(ring->mu);
+    if (ring->trace_ev.size() > (size_t)INT32_MAX) return KVX_EINTERNAL;
+    *n = (int32_t)ring->trace_ev.size();
+    for (int32_t i = 0; i < cap && i < *n; ++i) out[i] = ring->trace_ev[(size_t)i];
+    return KVX_OK;
+  } catch (...) {
+    return KVX_EINTERNAL;
+  }
 }
 
 kvx_status kvx_ring_abort(kvx_ring* ring) {
