@@ -289,6 +289,49 @@ def test_ordered_scatter_bit_exact(n):
     _untouched_equal(cache, before, s, {0, 1}, bt_dst, "ordered scatter")
 
 
+# Geometries of the 2 MiB pairings: the gather walks a chunk's slices in pairs
+# D apart, and the ordered scatter walks each XCD's range as two fronts paired
+# D slices apart, where a slice's run in a chunk (blocks per chunk x slab) times
+# D is 2 MiB with D <= 4; the scatter also needs the slice count to be a
+# multiple of 16 (two halves per XCD range) and of 2 D, the gather of 2 D.
+PAIRED = [
+    # (layers, NB, BS, heads, dim, elem, l0, l1, n, chunk_tokens): pairing taken
+    (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 256),    # 32 KiB slabs x 16 blocks: D = 4, both
+    (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 1024),   # x 64 blocks: D = 1, both
+    (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 512),    # x 32 blocks: D = 2, both
+    (40, 2100, 16, 2, 128, 2, 0, 40, 1030, 1024), # 8 KiB x 64: D = 4; 80 slices, 10 per XCD
+    (12, 2300, 16, 8, 128, 2, 2, 10, 1100, 256),  # a partial layer range: 16 slices, D = 4
+    (12, 2300, 16, 8, 128, 2, 0, 12, 1100, 256),  # 24 slices: gather paired, scatter one front
+    (10, 2300, 16, 8, 128, 2, 0, 10, 1100, 256),  # 20 slices: neither
+]
+
+
+@pytest.mark.parametrize("case", PAIRED, ids=[f"p{i}" for i in range(len(PAIRED))])
+def test_paired_walks_bit_exact(case):
+    L, NB, BS, H, D, e, l0, l1, n, ct = case
+    s = oracle.Shape(L, NB, BS, H, D, e)
+    seed = 300 + L + ct
+    bt_src, bt_dst = seeded_ids(seed, NB, n, n)
+    cache = device_cache(s, SRC(seed, kvsynth.MODE_RAW), DEV)
+    mirror = host_mirror(s, SRC(seed, kvsynth.MODE_RAW), np.concatenate([bt_src, bt_dst]))
+    expect = oracle.gather(s, *mirror, l0, l1, bt_src, ct)
+    guard = 4096
+    dst = torch.full((expect.size + guard,), 0xA5, dtype=torch.uint8, device=DEV)
+    kvx.kvx_gather_blocks(cache, l0, l1, _bt(bt_src), n, ct, dst)
+    _sync_check()
+    got = to_host(dst)
+    bad = first_mismatch(got[:expect.size], expect)
+    assert bad is None, f"gather differs at byte {bad}"
+    assert (got[expect.size:] == 0xA5).all(), "gather wrote past the packed image"
+    del got
+    before = _clone(cache)
+    kvx.kvx_scatter_blocks(cache, l0, l1, _bt(bt_dst), n, ct, dst)
+    _sync_check()
+    oracle.scatter(s, *mirror, l0, l1, bt_dst, ct, expect)
+    _compare_paged(cache, s, mirror, range(l0, l1), bt_dst, "ordered scatter")
+    _untouched_equal(cache, before, s, set(range(l0, l1)), bt_dst, "ordered scatter")
+
+
 def test_ordered_scatter_with_bad_ids_skips_only_those():
     s = oracle.Shape(2, 6000, 16, 2, 64, 2)
     n = 2000
