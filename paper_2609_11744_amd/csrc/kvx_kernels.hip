@@ -35,6 +35,15 @@
 // stream-ordered scratch) and then visits units layer by layer in ascending
 // destination order; the packed side is then read out of order, which costs
 // less than unordered writes.
+//
+// Pairing at 2 MiB. Where a layer|K|V slice's run in a packed chunk (blocks
+// per chunk x slab) times a small D (1, 2 or 4) is 2 MiB, both directions move
+// two slices D apart together: the gather walks each chunk's slices in such
+// pairs (its packed-side writes alternate between two runs 2 MiB apart), and
+// the ordered scatter walks each XCD's range as two fronts that move the same
+// destination block of two such slices. Both measured faster than the plain
+// walks on this chip, and pairs at other distances slower (scatter_pairing,
+// gather_pairing).
 #include <hip/hip_runtime.h>
 
 #include <mutex>
