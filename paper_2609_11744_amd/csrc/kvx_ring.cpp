@@ -141,8 +141,11 @@ struct kvx_ring {
   std::vector<int32_t> pre_file;       // per bound chunk
   std::vector<int64_t> pre_bytes;      // per distinct file: its image bytes
 
-  // timeline (kvx_ring_set_trace): the last traced transfer's intervals
+  // timeline (kvx_ring_set_trace): the last traced transfer's intervals.
+  // trace is the switch; trace_run its value for the running transfer, read
+  // by its threads (set before they start).
   bool trace = false;
+  bool trace_run = false;
   bool traced = false;                    // the last transfer was traced and succeeded
   bool trace_resolved = false;            // its device intervals are in trace_ev
   bool trace_to_packed = false;
@@ -344,7 +347,7 @@ void fill_worker(kvx_ring* r, int w) {
     const int64_t t1 = now_ns();
     busy += t1 - t0;
     std::lock_guard<std::mutex> lock(r->mu);
-    if (r->trace) r->trace_ev.push_back(kvx_trace_event{KVX_TRACE_FILL, (int32_t)i, w, s, bytes, t0, t1});
+    if (r->trace_run) r->trace_ev.push_back(kvx_trace_event{KVX_TRACE_FILL, (int32_t)i, w, s, bytes, t0, t1});
     if (++r->parts_done[(size_t)i] == T) r->cv_host.notify_all();
   }
   r->busy_ns.fetch_add(busy);
@@ -374,7 +377,7 @@ void drain_worker(kvx_ring* r, int w) {
     const int64_t t1 = now_ns();
     busy += t1 - t0;
     std::lock_guard<std::mutex> lock(r->mu);
-    if (r->trace) r->trace_ev.push_back(kvx_trace_event{KVX_TRACE_DRAIN, (int32_t)i, w, s, bytes, t0, t1});
+    if (r->trace_run) r->trace_ev.push_back(kvx_trace_event{KVX_TRACE_DRAIN, (int32_t)i, w, s, bytes, t0, t1});
     if (++r->parts_done[(size_t)i] == T) r->cv_host.notify_all();
   }
   r->busy_ns.fetch_add(busy);
@@ -676,7 +679,7 @@ void trace_dma_read(kvx_ring* r, int32_t s, bool h2d) {
 // launch_piece for piece i, between two timing events when tracing.
 kvx_status launch_piece_traced(kvx_ring* r, bool to_packed, int64_t i, const kvx::Piece& p,
                                const int32_t* bt, uint8_t* dslot, hipStream_t stream) {
-  const bool t = r->trace;
+  const bool t = r->trace_run;
   if (t && hipEventRecord(r->trace_k[2 * (size_t)i], stream) != hipSuccess) return KVX_EHIP;
   const kvx_status st = launch_piece(r, to_packed, p, bt, dslot, stream);
   if (st != KVX_OK) return st;
@@ -749,7 +752,7 @@ kvx_status issue_dma(kvx_ring* r, int64_t piece, const kvx::Piece& p, int32_t s,
   if (n == 0) return KVX_OK;
   // the slot's previous copies have finished (every caller waited for them):
   // read their interval before the signal is reused
-  if (r->trace) trace_dma_read(r, s, h2d);
+  if (r->trace_run) trace_dma_read(r, s, h2d);
   hsa_signal_store_screlease(sig, n);
   int64_t issued = 0;
   for (int64_t k = 0; k < n; ++k) {
@@ -766,7 +769,7 @@ kvx_status issue_dma(kvx_ring* r, int64_t piece, const kvx::Piece& p, int32_t s,
     hsa_signal_subtract_screlease(sig, n - issued);
     return KVX_EHIP;
   }
-  if (r->trace) {
+  if (r->trace_run) {
     r->trace_dma_piece[(size_t)s] = n == 1 ? piece : -1;
     r->trace_dma_bytes[(size_t)s] = p.bytes;
   }
@@ -814,6 +817,7 @@ kvx_status resolve_piece(kvx_ring* r, const kvx::Piece& p, const std::vector<voi
 
 // Run the bound transfer, its kernels on `stream` reporting bad ids to err.
 kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int* err) {
+  r->traced = false;
   if (r->dir != dir) return KVX_EINVAL;
   if (r->closed.load()) return KVX_ECLOSED;
   if (r->plan.pieces.empty()) return KVX_OK;
@@ -833,8 +837,8 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
   r->worker_error.store(0);
   r->stop.store(false);
   r->busy_ns.store(0);
-  r->traced = false;
-  if (r->trace) {
+  r->trace_run = r->trace;
+  if (r->trace_run) {
     const kvx_status ts = trace_begin(r, stream, P, dir == Dir::kOffload);
     if (ts != KVX_OK) return ts;
   }
@@ -867,7 +871,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
     r->cv_host.wait(lock, [&] { return r->parts_done[(size_t)i] == T || r->stop.load(); });
     const int64_t t1 = now_ns();
     wait_ms += (double)(t1 - t0) / 1e6;
-    if (r->trace)
+    if (r->trace_run)
       r->trace_ev.push_back(kvx_trace_event{KVX_TRACE_WAIT, (int32_t)i, 0, (int32_t)(i % S), 0, t0, t1});
   };
   int64_t copied = -1;  // restore on the DMA engines: the piece copied but not yet scattered
@@ -930,7 +934,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         break;
       }
       bool ok = hipStreamWaitEvent(r->side, r->dev_done[s], 0) == hipSuccess;
-      if (r->trace) ok = ok && hipEventRecord(r->trace_c[2 * (size_t)i], r->side) == hipSuccess;
+      if (r->trace_run) ok = ok && hipEventRecord(r->trace_c[2 * (size_t)i], r->side) == hipSuccess;
       if (T > 0) {
         ok = ok && hipMemcpyAsync(dslot, hslot, (size_t)p.bytes, hipMemcpyHostToDevice, r->side) ==
                        hipSuccess;
@@ -939,7 +943,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
           ok = ok && hipMemcpyAsync(dslot + sp.slot_off, sp.host, (size_t)sp.bytes,
                                     hipMemcpyHostToDevice, r->side) == hipSuccess;
       }
-      if (r->trace && ok) {
+      if (r->trace_run && ok) {
         ok = hipEventRecord(r->trace_c[2 * (size_t)i + 1], r->side) == hipSuccess;
         r->trace_c_used[(size_t)i] = ok ? 1 : 0;
         r->trace_c_bytes[(size_t)i] = p.bytes;
@@ -1016,7 +1020,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
         break;
       }
       bool ok = hipStreamWaitEvent(r->side, r->dev_done[s], 0) == hipSuccess;
-      if (r->trace) ok = ok && hipEventRecord(r->trace_c[2 * (size_t)i], r->side) == hipSuccess;
+      if (r->trace_run) ok = ok && hipEventRecord(r->trace_c[2 * (size_t)i], r->side) == hipSuccess;
       if (T > 0) {
         ok = ok && hipMemcpyAsync(hslot, dslot, (size_t)p.bytes, hipMemcpyDeviceToHost, r->side) ==
                        hipSuccess;
@@ -1025,7 +1029,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
           ok = ok && hipMemcpyAsync(sp.host, dslot + sp.slot_off, (size_t)sp.bytes,
                                     hipMemcpyDeviceToHost, r->side) == hipSuccess;
       }
-      if (r->trace && ok) {
+      if (r->trace_run && ok) {
         ok = hipEventRecord(r->trace_c[2 * (size_t)i + 1], r->side) == hipSuccess;
         r->trace_c_used[(size_t)i] = ok ? 1 : 0;
         r->trace_c_bytes[(size_t)i] = p.bytes;
@@ -1056,7 +1060,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
       st = KVX_EHIP;
     }
   }
-  if (st == KVX_OK && r->trace && use_dma(r)) {
+  if (st == KVX_OK && r->trace_run && use_dma(r)) {
     // the last pieces' copies (finished: waited for above)
     for (int32_t s = 0; s < S; ++s)
       if (r->trace_dma_piece[(size_t)s] >= 0) {
@@ -1096,7 +1100,7 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
   r->stats.dma = use_dma(r) ? 1 : 0;
   r->stats.dma_engine =
       use_dma(r) ? (int32_t)(dir == Dir::kRestore ? r->h2d_engine : r->d2h_engine) : 0;
-  r->traced = r->trace && st == KVX_OK;
+  r->traced = r->trace_run && st == KVX_OK;
   return st;
 }
 
