@@ -133,9 +133,9 @@ struct UnitGeom {
   uint32_t parts;            // workgroups per slab (parts_shift: log2 of a power of two, else 32)
   uint32_t parts_shift;
   // Ordered scatter walked as two fronts per XCD (xcd_two_fronts) whose
-  // slices are paired pair_dist apart (paired_slice); pair_shift = log2 of
-  // pair_dist, or 32 for one front per XCD. Gather: each chunk's slices
-  // walked in pairs gather_pair_dist apart (see the unit decode), or 32.
+  // slices are paired D = 2^pair_shift apart (paired_slice); pair_shift = 32
+  // for one front per XCD. Gather: each chunk's slices walked in pairs
+  // 2^gather_pair_shift apart (see the unit decode), or 32 for the plain walk.
   uint32_t pair_shift;
   uint32_t gather_pair_shift;
   uint32_t half_slices;      // slices per half of an XCD's range
@@ -182,11 +182,12 @@ __device__ __forceinline__ uint32_t xcd_two_fronts(uint32_t b, uint32_t n, uint3
   return start + (i & 1) * half + (pair << shift) + (i >> 1);
 }
 
-// Slice of the ordered walk's slice r (r / S-th XCD range, S slices each,
-// halves of H = S / 2): slice t of the first half of XCD x's range and slice
-// t of its second half are pair j = H x + t, which moves slices a_j and a_j +
-// D (a_j: the j-th slice whose index has bit log2 D clear, D = 2^pair_shift).
-// A bijection on the slices when their count is a multiple of 2 D.
+// The layer|K|V slice moved at slice r of the ordered walk (XCD x's range is
+// walk slices [x S, (x + 1) S), halves of H = S / 2): slice t of the first
+// half of XCD x's range and slice t of its second half are pair j = H x + t,
+// which moves slices a_j and a_j + D (a_j: the j-th slice whose index has bit
+// log2 D clear, D = 2^ds). A bijection on the slices when their count is a
+// multiple of 2 D.
 __device__ __forceinline__ uint32_t paired_slice(uint32_t r, DivU32 sx, uint32_t half,
                                                  uint32_t ds) {
   const uint32_t x = divu(r, sx), rem = r - x * sx.d;
