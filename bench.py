@@ -50,13 +50,13 @@ KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
 # only for the kernel code they were taken on (kernels_sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "b46e6d4d83ac078ade8d91af6998b6c1f5720de4288f7b808d06bd4584859a43",
+    "kernels_sha256": "6b66c3fd4ce2b4d2e5e31500206176deb095229c4d919b0ee8313f080e3e8cf2",
     # cache layout -> (fetched, written) HBM bytes of one gather launch at the
     # default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy calibration;
     # x1.999989 in the paged-attention pass), WRITE_SIZE KiB x 1.0
-    "nhd": (10488856364, 10485760000),         # 5,121,543.4 / 10,240,000.0 KiB
-    "paged_attn": (10488997557, 10485760000),  # 5,121,609.9 / 10,240,000.0 KiB
-    "hnd": (10488889356, 10485760000),         # 5,121,557.8 / 10,240,000.0 KiB
+    "nhd": (10488799702, 10485760000),         # 5,121,515.0 / 10,240,000.0 KiB
+    "paged_attn": (10488993347, 10485760000),  # 5,121,607.6 / 10,240,000.0 KiB
+    "hnd": (10488854793, 10485760000),         # 5,121,541.9 / 10,240,000.0 KiB
 }
 
 

@@ -74,7 +74,8 @@ typedef enum kvx_status {
   KVX_ECLOSED = -5,    /* the ring was aborted while a restore was running */
   KVX_EINTERNAL = -6,  /* invariant violated inside the library */
   KVX_EIO = -7,        /* a storage-tier file could not be opened, read, written or published */
-  KVX_EBUSY = -8       /* the ring is running an offload started by kvx_offload_begin */
+  KVX_EBUSY = -8       /* the ring is running a transfer started by kvx_offload_begin or
+                          kvx_restore_begin */
 } kvx_status;
 
 /* Largest layer range a single call may cover. */
@@ -157,7 +158,8 @@ kvx_status kvx_scatter_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
 /* kvx_scatter_blocks for callers that cannot allocate device memory (code
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * allocation): the same arguments, validation, kernels and result, but the
- * destination order a scatter of 1,024 blocks or more computes first lives in
+ * destination order a scatter of 1,024 blocks or more in chunks of more than
+ * one block computes first lives in
  * a fixed device array of the library's (512 KiB, KVX_NOALLOC_MAX_BLOCKS
  * 8-byte entries; each GPU the library runs on holds one until the process
  * ends) instead of stream-ordered scratch. The call allocates nothing.

@@ -219,7 +219,7 @@ const char* kvx_strerror(kvx_status s) {
     case KVX_ECLOSED: return "ring aborted";
     case KVX_EINTERNAL: return "internal error";
     case KVX_EIO: return "storage-tier file I/O failed";
-    case KVX_EBUSY: return "ring busy with an offload started by kvx_offload_begin";
+    case KVX_EBUSY: return "ring busy with a transfer started by kvx_offload_begin or kvx_restore_begin";
   }
   return "unknown status";
 }

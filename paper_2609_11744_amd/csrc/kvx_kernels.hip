@@ -34,7 +34,10 @@
 // large scatter first buckets the destination ids (order_kernel, into
 // stream-ordered scratch) and then visits units layer by layer in ascending
 // destination order; the packed side is then read out of order, which costs
-// less than unordered writes.
+// less than unordered writes. The exception is a chunk of one block: image
+// order then reads each chunk as one sequential run and writes one
+// destination block of every layer in turn, which measured faster
+// (scatter_in_destination_order).
 //
 // Pairing at 2 MiB. Where a layer|K|V slice's run in a packed chunk (blocks
 // per chunk x slab) times a small D (1, 2 or 4) is 2 MiB, both directions move
@@ -729,6 +732,21 @@ constexpr uint32_t kPartThreads = 256;
 // Scatters of at least this many blocks run in destination order.
 constexpr int32_t kOrderedScatterMinBlocks = 1024;
 
+// Whether a scatter of n_blocks in chunks of bpc blocks runs in destination
+// order. The rate of one walk over the same ids moves by up to 8 points of
+// peak with where the cache and the packed buffer land in physical memory,
+// so the walks were compared over 12 placements (4 caches x 3 packed buffers
+// allocated in one process, each walk on each pair, alternated; 8B-shaped
+// cache, 20,000-block pool, mean % of 8 TB/s). With one-block chunks image
+// order averaged 76.8 against 73.6 in destination order at 2,048 blocks (at
+// least as fast on 11 of the 12 pairs) and 76.3 against 76.1 at 5,000; with
+// 4-block chunks the two were level (73.6 / 73.6), and destination order led
+// with 16 and 64 (74.6 against 71.8 and 75.0 against 70.8 at 2,048 blocks,
+// 76.9 against 71.9 at 5,000 with 16).
+bool scatter_in_destination_order(int64_t n_blocks, int64_t bpc) {
+  return n_blocks >= kOrderedScatterMinBlocks && bpc > 1;
+}
+
 // Dynamic LDS bytes for a reordering layout: the image of one head, rounded
 // up to whole swizzle groups of 16 vectors (gather) or with its pad vectors
 // (scatter); none for HND, which moves rows directly.
@@ -996,13 +1014,13 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
                                        layout, elem, stream);
     return e == hipSuccess ? KVX_OK : KVX_EHIP;
   }
-  // Destination-ordered scatter for large calls; the order lives in the
-  // caller's scratch (order_scratch, n_blocks entries) or else in
-  // stream-ordered scratch allocated here. If that allocation fails, fall
-  // back to image order (same result, slower).
+  // Destination-ordered scatter for large calls of multi-block chunks; the
+  // order lives in the caller's scratch (order_scratch, n_blocks entries) or
+  // else in stream-ordered scratch allocated here. If that allocation fails,
+  // fall back to image order (same result, slower).
   OrderEntry* order = nullptr;
   const bool own = order_scratch == nullptr;
-  if (g.n_blocks >= kOrderedScatterMinBlocks) {
+  if (scatter_in_destination_order(g.n_blocks, g.bpc)) {
     if (!own)
       order = static_cast<OrderEntry*>(order_scratch);
     else if (hipMallocAsync((void**)&order, (size_t)g.n_blocks * sizeof(OrderEntry), stream) !=

@@ -293,9 +293,9 @@ extern "C" kvx_status kvx_plan_step(const kvx_step_request* reqs, int32_t n_requ
     for (const StepChunk& c : ch)
       if (!resident(c)) load[(size_t)c.request] += c.n_blocks;
     // a request with nothing to load counts as loading
-  auto loads = [&](int32_t r) {
-    return load[(size_t)r] == 0 || load[(size_t)r] * block_size >= gate_tokens;
-  };
+    auto loads = [&](int32_t r) {
+      return load[(size_t)r] == 0 || load[(size_t)r] * block_size >= gate_tokens;
+    };
     // first pass: sizes and the restore order
     std::vector<int32_t> restore_of(ch.size(), -1);  // by first occurrence: restore index
     std::vector<int32_t> restore_src;                // restore index -> chunk that defines it

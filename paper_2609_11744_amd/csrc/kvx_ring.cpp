@@ -1532,23 +1532,28 @@ bool make_store_stream(kvx_ring* r) {
 // enqueued on the caller's stream, reporting bad ids to the caller's stream.
 kvx_status start_async(kvx_ring* ring, Dir dir, const int32_t* block_table, hipStream_t stream) {
   if (!ring) return KVX_EINVAL;
-  if (ring->async_busy.load()) return KVX_EBUSY;
   if (ring->dir != dir) return KVX_EINVAL;
   if (ring->closed.load()) return KVX_ECLOSED;
   if (!block_table && !ring->plan.pieces.empty()) return KVX_EINVAL;
+  // claim the ring: of two begins racing on it, one gets KVX_EBUSY
+  bool idle = false;
+  if (!ring->async_busy.compare_exchange_strong(idle, true)) return KVX_EBUSY;
+  auto release = [ring](kvx_status st) {
+    ring->async_busy.store(false);
+    return st;
+  };
   try {
     DeviceGuard dg(ring->device);
-    if (!dg.ok) return KVX_EHIP;
-    if (!ring->store_stream && !make_store_stream(ring)) return KVX_EHIP;
+    if (!dg.ok) return release(KVX_EHIP);
+    if (!ring->store_stream && !make_store_stream(ring)) return release(KVX_EHIP);
     int* err = kvx::stream_error_word(stream);
-    if (!err) return KVX_EHIP;
+    if (!err) return release(KVX_EHIP);
     if (hipEventRecord(ring->store_begin, stream) != hipSuccess ||
         hipStreamWaitEvent(ring->store_stream, ring->store_begin, 0) != hipSuccess)
-      return KVX_EHIP;
+      return release(KVX_EHIP);
     hipStream_t own = ring->store_stream;
     ring->async_status = KVX_OK;
     ring->async_dir = dir;
-    ring->async_busy.store(true);
     ring->async_th = std::thread([ring, dir, block_table, own, err] {
       kvx_status st;
       try {
@@ -1565,8 +1570,7 @@ kvx_status start_async(kvx_ring* ring, Dir dir, const int32_t* block_table, hipS
     });
     return KVX_OK;
   } catch (...) {
-    ring->async_busy.store(false);
-    return KVX_EINTERNAL;
+    return release(KVX_EINTERNAL);
   }
 }
 

@@ -79,6 +79,53 @@ def test_restore_begin_wait_bit_exact(threads):
         assert np.array_equal(to_host(snap_v[l]), mirror[1][l]), f"V layer {l}"
 
 
+def test_racing_begins_claim_the_ring_once():
+    """Two threads start a restore on one ring at the same moment: exactly one
+    claims it (the other gets KVX_EBUSY, whatever the timing), and the one
+    restore is bit-exact."""
+    import threading
+
+    s = oracle.Shape(2, 400, 16, 2, 64, 2)
+    n, ct, seed = 150, 32, 77
+    (bt,) = seeded_ids(seed, s.num_blocks, n)
+    fill = Filled(seed, kvsynth.ROLE_DST, kvsynth.MODE_RAW)
+    cache = device_cache(s, fill, DEV)
+    src, img = _image(oracle.packed_bytes(s, 0, 2, n), seed, pinned=False)
+    ring = kvx.StagingRing(DEV, 2, 64 << 10)
+    bt_d = _bt(bt)
+    stream = torch.cuda.Stream()
+    gate = threading.Barrier(2)
+    outcome = [None, None]
+
+    def begin(i):
+        gate.wait()
+        try:
+            kvx.kvx_restore_begin(ring, bt_d, stream=stream)
+            outcome[i] = kvx.KVX_OK
+        except kvx.KvxError as e:
+            outcome[i] = e.status
+
+    try:
+        ring.bind(cache, 0, 2, n, ct, src, fill_threads=2)
+        torch.cuda.synchronize()
+        th = [threading.Thread(target=begin, args=(i,)) for i in range(2)]
+        for t in th:
+            t.start()
+        for t in th:
+            t.join()
+        assert sorted(outcome) == sorted([kvx.KVX_OK, kvx.KVX_EBUSY]), outcome
+        kvx.kvx_restore_wait(ring, stream=stream)
+        stream.synchronize()
+        kvx.kvx_check(stream)
+    finally:
+        ring.close()
+    mirror = host_mirror(s, fill, range(s.num_blocks))
+    oracle.restore(s, *mirror, 0, 2, bt, ct, img)
+    for l in range(2):
+        assert np.array_equal(to_host(cache.k[l]), mirror[0][l]), f"K layer {l}"
+        assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
+
+
 def test_restore_and_offload_started_together():
     """One thread starts a restore on one ring and an offload on another, then
     collects both: the restored blocks and the offloaded images are the
