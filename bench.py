@@ -50,13 +50,13 @@ KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
 # only for the kernel code they were taken on (kernels_sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "6b66c3fd4ce2b4d2e5e31500206176deb095229c4d919b0ee8313f080e3e8cf2",
+    "kernels_sha256": "f3c9762bba0e72b5c48e4b11b77b268db085e46471d28e2e78ab411d77f546cf",
     # cache layout -> (fetched, written) HBM bytes of one gather launch at the
-    # default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy calibration;
-    # x1.999989 in the paged-attention pass), WRITE_SIZE KiB x 1.0
-    "nhd": (10488799702, 10485760000),         # 5,121,515.0 / 10,240,000.0 KiB
-    "paged_attn": (10488993347, 10485760000),  # 5,121,607.6 / 10,240,000.0 KiB
-    "hnd": (10488854793, 10485760000),         # 5,121,541.9 / 10,240,000.0 KiB
+    # default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy calibration),
+    # WRITE_SIZE KiB x 1.0
+    "nhd": (10488841659, 10485760000),         # 5,121,534.9 / 10,240,000.0 KiB
+    "paged_attn": (10488991733, 10485760000),  # 5,121,609.4 / 10,240,000.0 KiB
+    "hnd": (10488866550, 10485760000),         # 5,121,548.3 / 10,240,000.0 KiB
 }
 
 
@@ -182,12 +182,42 @@ def probes(dev, reps):
     return p
 
 
-def event_ms(fn, reps):
+_HOLD = {"cycles": None}
+HOLD_US = 200.0
+
+
+def hold_stream():
+    """Keep the current stream busy for about HOLD_US microseconds (a spin
+    kernel), so that the host-side launch of the call enqueued next overlaps
+    it and events recorded around that call time its device execution only.
+    With the GPU idle when a timed call starts, its events also count the
+    call's host-side launch: about 1 % of a 3.3 ms kernel, 4 % of the
+    0.46 ms one-head shard gather."""
+    import torch
+
+    if _HOLD["cycles"] is None:
+        torch.cuda._sleep(1000)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        n = 4_000_000
+        a.record()
+        torch.cuda._sleep(n)
+        b.record()
+        b.synchronize()
+        per_us = n / max(a.elapsed_time(b) * 1e3, 1.0)
+        _HOLD["cycles"] = max(int(per_us * HOLD_US), 1)
+    torch.cuda._sleep(_HOLD["cycles"])
+
+
+def event_ms(fn, reps, hold=True):
+    """Device time of fn() per call (ms), HIP events on the current stream;
+    with hold, the stream is busy while fn is enqueued (hold_stream)."""
     import torch
 
     out = []
     for _ in range(reps):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        if hold:
+            hold_stream()
         a.record()
         fn()
         b.record()
@@ -253,6 +283,10 @@ def run_80k(args):
 
     def step(record):
         e = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        # the gather is enqueued while the stream is busy, so the events time
+        # the device work of both calls (the scatter is enqueued while the
+        # gather runs)
+        hold_stream()
         e[0].record()
         kvx.kvx_gather_blocks(cache, 0, L, bt_src, n, ct, packed)
         e[1].record()
@@ -289,6 +323,13 @@ def run_80k(args):
     wall_ms = (time.perf_counter() - t_begin) * 1e3
     kvx.kvx_check()
     log("timed steps done")
+    # the same calls timed from an idle GPU: the events then also count each
+    # call's host-side launch
+    launch_g = event_ms(lambda: kvx.kvx_gather_blocks(cache, 0, L, bt_src, n, ct, packed), 3,
+                        hold=False)
+    launch_s = event_ms(lambda: kvx.kvx_scatter_blocks(cache, 0, L, bt_dst, n, ct, packed), 3,
+                        hold=False)
+    kvx.kvx_check()
     timeline = restore_timeline(args, ring, bt_rst)
     offload = offload_leg(args, dev, cache, L, ct, n, bt_src, image, probe)
     sweep = sweep_32k(args, cache, L, perm, packed, slab, args.sweep_reps) \
@@ -327,6 +368,10 @@ def run_80k(args):
         "scatter_ms": round(mean_s, 4),
         "gather_ms_stats": ms_stats(rec["gather_ms"]),
         "scatter_ms_stats": ms_stats(rec["scatter_ms"]),
+        "timing": f"device time of each call: HIP events on its stream, the call enqueued "
+                  f"behind a {HOLD_US:.0f} us spin kernel so that its host-side launch is "
+                  f"not counted; launch_inclusive: the same calls timed from an idle GPU",
+        "launch_inclusive": {"gather_ms": ms_stats(launch_g), "scatter_ms": ms_stats(launch_s)},
         "restore_ms": round(med["restore_ms"], 3),
         "restore_GBps": round(restore_GBps, 2),
         "restore_frac_of_h2d": round(restore_GBps / probe["h2d_GBps"], 4),

@@ -40,13 +40,13 @@
 // (scatter_in_destination_order).
 //
 // Pairing at 2 MiB. Where a layer|K|V slice's run in a packed chunk (blocks
-// per chunk x slab) times a small D (1, 2 or 4) is 2 MiB, both directions move
+// per chunk x slab) times a power of two D is 2 MiB, both directions can move
 // two slices D apart together: the gather walks each chunk's slices in such
-// pairs (its packed-side writes alternate between two runs 2 MiB apart), and
-// the ordered scatter walks each XCD's range as two fronts that move the same
-// destination block of two such slices. Both measured faster than the plain
-// walks on this chip, and pairs at other distances slower (scatter_pairing,
-// gather_pairing).
+// pairs (its packed-side writes alternate between two runs 2 MiB apart; D up
+// to 32), and the ordered scatter walks each XCD's range as two fronts that
+// move the same destination block of two such slices (D up to 4). Both
+// measured faster than the plain walks on this chip, and pairs at other
+// distances slower (scatter_pairing, gather_pairing).
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -860,31 +860,43 @@ void slab_parts(int layout, uint32_t n16, uint32_t heads, uint32_t* parts, uint3
 // 256-token chunks 72.6-72.8 % against 69.5-70.5 %. Why 2 MiB is the
 // distance that pays is not established: it depends on how the chip maps
 // physical addresses to memory channels, which these kernels do not see.
-uint32_t pairing_2mib(uint32_t parts_shift, uint32_t n_slices, uint32_t bpc, uint64_t slab) {
+// log2 of D, the distance in slices at which two slices' runs in a packed
+// chunk sit 2 MiB apart, where D is a power of two of at most 2^max_ds and
+// the slice count a multiple of 2 D; else 32.
+uint32_t pairing_2mib(uint32_t parts_shift, uint32_t n_slices, uint32_t bpc, uint64_t slab,
+                      uint32_t max_ds) {
   constexpr uint64_t kPairBytes = 2u << 20;
   if (parts_shift >= 32) return 32;
   const uint64_t run = (uint64_t)bpc * slab;  // one slice's run in a chunk
   if (run == 0 || kPairBytes % run) return 32;
   const uint64_t d = kPairBytes / run;
-  const uint32_t ds = d == 1 ? 0 : d == 2 ? 1 : d == 4 ? 2 : 32;
-  if (ds == 32 || n_slices % (2 * d)) return 32;
-  return ds;
+  if ((d & (d - 1)) || d > (1ull << max_ds) || n_slices % (2 * d)) return 32;
+  return (uint32_t)__builtin_ctzll(d);
 }
 
 uint32_t scatter_pairing(uint32_t n_work, uint32_t parts_shift, uint32_t n_slices, uint32_t bpc,
                          uint64_t slab) {
   if (n_work > kMaxWorkPerLaunch || n_slices % (2 * kXcds)) return 32;
-  return pairing_2mib(parts_shift, n_slices, bpc, slab);
+  return pairing_2mib(parts_shift, n_slices, bpc, slab, 2);
 }
 
 // Pairing for the gather: each chunk's slices walked in pairs 2 MiB apart in
-// the chunk, D <= 4 slices (the packed-side writes then alternate between two
+// the chunk, D <= 32 slices (the packed-side writes then alternate between two
 // runs 2 MiB apart). On the 80k gather pattern (standalone probe, two
 // processes each) this measured 0.3-0.8 points above the plain walk with 16-
-// and 64-block chunks; pairs at other distances (512 KiB to 32 MiB) were
-// 0.5-4 points slower.
+// and 64-block chunks (D = 4, 1); pairs at other distances (512 KiB to 32 MiB)
+// were 0.5-4 points slower. Farther apart in slices, compared over 12 (cache,
+// packed buffer) allocation pairs in one process (8B shape, 20,000-block
+// pool; the rate of one walk moves by several points with where the
+// allocations land): with 4- and 8-block chunks of 32 KiB slabs (D = 16, 8)
+// 80.8 / 80.6 % of peak against 79.6 / 79.3 % for the plain walk at 2,048
+// blocks, 81.2 / 81.1 against 80.7 / 80.5 at 5,000; at the tensor-parallel
+// shard shapes (4 and 8 KiB slabs, 16-block chunks: D = 32, 16) 77.3 / 77.4
+// against 75.5 / 75.6 over 16 pairs, faster on every pair. (The ordered
+// scatter's two fronts that far apart lost 1.3-1.4 points at the shard
+// shapes, so it keeps D <= 4.)
 uint32_t gather_pairing(uint32_t parts_shift, uint32_t n_slices, uint32_t bpc, uint64_t slab) {
-  return pairing_2mib(parts_shift, n_slices, bpc, slab);
+  return pairing_2mib(parts_shift, n_slices, bpc, slab, 5);
 }
 
 DivU32 div_u32(uint32_t d) {
