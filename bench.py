@@ -50,13 +50,13 @@ KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
 # only for the kernel code they were taken on (kernels_sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "f3c9762bba0e72b5c48e4b11b77b268db085e46471d28e2e78ab411d77f546cf",
-    # cache layout -> (fetched, written) HBM bytes of one gather launch at the
-    # default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy calibration),
-    # WRITE_SIZE KiB x 1.0
-    "nhd": (10488841659, 10485760000),         # 5,121,534.9 / 10,240,000.0 KiB
-    "paged_attn": (10488991733, 10485760000),  # 5,121,609.4 / 10,240,000.0 KiB
-    "hnd": (10488866550, 10485760000),         # 5,121,548.3 / 10,240,000.0 KiB
+    "kernels_sha256": "594f2e3b490f8b363d72faf26fe995f7c200e3eac00970d6b2fe99d883409f1e",
+    # cache layout -> (fetched, written) HBM bytes of the timed gather launch
+    # at the default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy
+    # calibration), WRITE_SIZE KiB x 1.0
+    "nhd": (10488797686, 10485760000),         # 5,121,514.7 / 10,240,000.0 KiB
+    "paged_attn": (10488978520, 10485760000),  # 5,121,602.4 / 10,240,000.0 KiB
+    "hnd": (10488845996, 10485760000),         # 5,121,536.8 / 10,240,000.0 KiB
 }
 
 

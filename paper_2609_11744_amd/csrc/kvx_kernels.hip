@@ -34,10 +34,12 @@
 // large scatter first buckets the destination ids (order_kernel, into
 // stream-ordered scratch) and then visits units layer by layer in ascending
 // destination order; the packed side is then read out of order, which costs
-// less than unordered writes. The exception is a chunk of one block: image
-// order then reads each chunk as one sequential run and writes one
-// destination block of every layer in turn, which measured faster
-// (scatter_in_destination_order).
+// less than unordered writes. The exceptions measured faster in image order:
+// a chunk of one block (each chunk is then one sequential read, and the
+// writes go to one destination block of every layer in turn;
+// scatter_in_destination_order), and slabs of at most 8 KiB, walked with no
+// XCD ranges so that the whole chip reads the packed image front to back
+// (scatter_linear).
 //
 // Pairing at 2 MiB. Where a layer|K|V slice's run in a packed chunk (blocks
 // per chunk x slab) times a power of two D is 2 MiB, both directions can move
@@ -142,6 +144,7 @@ struct UnitGeom {
   uint32_t pair_shift;
   uint32_t gather_pair_shift;
   uint32_t half_slices;      // slices per half of an XCD's range
+  uint32_t linear_walk;      // 1: workgroup b moves work item b (no XCD ranges)
   DivU32 xcd_slices_div;     // by slices per XCD range
   DivU32 parts_div;
   DivU32 upc_div;            // by units_per_chunk
@@ -542,9 +545,10 @@ __global__ void __launch_bounds__(T)
                       const OrderEntry* __restrict__ order, char* __restrict__ packed,
                       int* __restrict__ err) {
   uint32_t part;
-  const uint32_t w = kOrdered && g.pair_shift < 32
-                         ? xcd_two_fronts(blockIdx.x, work_count, g.parts_shift)
-                         : xcd_contiguous(blockIdx.x, work_count);
+  const uint32_t w = g.linear_walk                  ? blockIdx.x
+                     : kOrdered && g.pair_shift < 32 ? xcd_two_fronts(blockIdx.x, work_count,
+                                                                      g.parts_shift)
+                                                     : xcd_contiguous(blockIdx.x, work_count);
   uint32_t u = split_work(work_base + w, g.parts, g.parts_shift, g.parts_div, &part);
   uint32_t c, first, nc, lk, j;
   int32_t id;
@@ -732,6 +736,19 @@ constexpr uint32_t kPartThreads = 256;
 // Scatters of at least this many blocks run in destination order.
 constexpr int32_t kOrderedScatterMinBlocks = 1024;
 
+// Whether a large scatter of small slabs walks the image in order with no
+// XCD ranges (workgroup b moves work item b: the whole chip reads the packed
+// image front to back). Compared over 9-16 (cache, packed buffer) allocation
+// pairs in one process at the tensor-parallel shard shapes of the 8B cache
+// (80k prefix, 16-block chunks, default layout), against the destination-
+// ordered walk: 4 KiB slabs 71.6-72.1 % of peak against 68.0-68.3 %, 8 KiB
+// 70.8 against 69.3-69.8 %, 16 KiB level (73.7 / 73.6 %, a wider spread), and
+// 32 KiB 71.1 against 75.3 % (image order with XCD ranges: 69.3 / 69.1 % at 4
+// and 8 KiB). Measured with the default layout only.
+bool scatter_linear(int64_t n_blocks, int64_t slab, int layout) {
+  return layout == KVX_LAYOUT_NHD && n_blocks >= kOrderedScatterMinBlocks && slab <= 8192;
+}
+
 // Whether a scatter of n_blocks in chunks of bpc blocks runs in destination
 // order. The rate of one walk over the same ids moves by up to 8 points of
 // peak with where the cache and the packed buffer land in physical memory,
@@ -743,8 +760,8 @@ constexpr int32_t kOrderedScatterMinBlocks = 1024;
 // 4-block chunks the two were level (73.6 / 73.6), and destination order led
 // with 16 and 64 (74.6 against 71.8 and 75.0 against 70.8 at 2,048 blocks,
 // 76.9 against 71.9 at 5,000 with 16).
-bool scatter_in_destination_order(int64_t n_blocks, int64_t bpc) {
-  return n_blocks >= kOrderedScatterMinBlocks && bpc > 1;
+bool scatter_in_destination_order(int64_t n_blocks, int64_t bpc, int64_t slab, int layout) {
+  return n_blocks >= kOrderedScatterMinBlocks && bpc > 1 && !scatter_linear(n_blocks, slab, layout);
 }
 
 // Dynamic LDS bytes for a reordering layout: the image of one head, rounded
@@ -1020,6 +1037,7 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.gather_pair_shift =
       to_packed ? gather_pairing(ug.parts_shift, n_slices, ug.bpc, ug.slab) : 32u;
   ug.half_slices = n_slices / kXcds / 2;
+  ug.linear_walk = 0u;
   ug.xcd_slices_div = div_u32(n_slices / kXcds ? n_slices / kXcds : 1);
   if (to_packed) {
     hipError_t e = launch<true, false>(lp, block_table, ug, n_work, nullptr, (char*)packed, err,
@@ -1032,7 +1050,8 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   // fall back to image order (same result, slower).
   OrderEntry* order = nullptr;
   const bool own = order_scratch == nullptr;
-  if (scatter_in_destination_order(g.n_blocks, g.bpc)) {
+  ug.linear_walk = scatter_linear(g.n_blocks, g.slab, layout) ? 1u : 0u;
+  if (scatter_in_destination_order(g.n_blocks, g.bpc, g.slab, layout)) {
     if (!own)
       order = static_cast<OrderEntry*>(order_scratch);
     else if (hipMallocAsync((void**)&order, (size_t)g.n_blocks * sizeof(OrderEntry), stream) !=

@@ -267,12 +267,16 @@ def test_aborted_ring_reports_closed():
         ring.close()
 
 
-# ---- destination-ordered scatter (1024..8192 blocks) --------------------------
+# ---- large scatters (1024..8192 blocks) ----------------------------------------
 
+@pytest.mark.parametrize("heads", [8, 2], ids=["ordered_16k_slabs", "linear_4k_slabs"])
 @pytest.mark.parametrize("n", [1024, 1500, 8192])
-def test_ordered_scatter_bit_exact(n):
-    s = oracle.Shape(2, 3 * 8192, 16, 2, 64, 2)  # 4 KiB slabs
-    seed = 40 + n
+def test_ordered_scatter_bit_exact(n, heads):
+    """Scatters of 1,024 blocks or more: in destination order with 16 KiB
+    slabs, in image order on a linear walk with 4 KiB slabs (48-token chunks,
+    three blocks each)."""
+    s = oracle.Shape(2, 3 * 8192, 16, heads, 64, 2)
+    seed = 40 + n + heads
     bt_src, bt_dst = seeded_ids(seed, s.num_blocks, n, n)
     cache = device_cache(s, SRC(seed, kvsynth.MODE_RAW), DEV)
     mirror = host_mirror(s, SRC(seed, kvsynth.MODE_RAW), np.concatenate([bt_src, bt_dst]))
@@ -338,8 +342,9 @@ def test_paired_walks_bit_exact(case):
     _untouched_equal(cache, before, s, set(range(l0, l1)), bt_dst, "ordered scatter")
 
 
-def test_ordered_scatter_with_bad_ids_skips_only_those():
-    s = oracle.Shape(2, 6000, 16, 2, 64, 2)
+@pytest.mark.parametrize("heads", [8, 2], ids=["ordered_16k_slabs", "linear_4k_slabs"])
+def test_ordered_scatter_with_bad_ids_skips_only_those(heads):
+    s = oracle.Shape(2, 6000, 16, heads, 64, 2)
     n = 2000
     bt, spare = seeded_ids(9, s.num_blocks, n, 3)
     bad_pos = [5, 777, 1999]

@@ -31,7 +31,7 @@ def _call(fn, cache, L, bt, n, ct, src):
 
 def test_noalloc_scatter_matches_scatter_twice_smaller_second():
     lib = _native.lib()
-    s = oracle.Shape(2, 7000, 16, 2, 64, 2)
+    s = oracle.Shape(2, 7000, 16, 8, 64, 2)  # 16 KiB slabs: scatters of 1,024+ blocks ordered
     L, ct, seed = 2, 256, 91
     fill = Filled(seed, kvsynth.ROLE_DST, kvsynth.MODE_RAW)
     ref = device_cache(s, fill, DEV)
