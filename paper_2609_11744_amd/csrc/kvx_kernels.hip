@@ -46,7 +46,8 @@
 // two slices D apart together: the gather walks each chunk's slices in such
 // pairs (its packed-side writes alternate between two runs 2 MiB apart; D up
 // to 32), and the ordered scatter walks each XCD's range as two fronts that
-// move the same destination block of two such slices (D up to 4). Both
+// move the same destination block of two such slices (D up to 16 for slabs
+// above 8 KiB, else 4). Both
 // measured faster than the plain walks on this chip, and pairs at other
 // distances slower (scatter_pairing, gather_pairing).
 #include <hip/hip_runtime.h>
@@ -891,10 +892,17 @@ uint32_t pairing_2mib(uint32_t parts_shift, uint32_t n_slices, uint32_t bpc, uin
   return (uint32_t)__builtin_ctzll(d);
 }
 
+// Farther apart (D = 8, 16) the fronts paid with slabs above 8 KiB, compared
+// over 9-12 (cache, packed buffer) allocation pairs in one process: 32 KiB
+// slabs in 8-block chunks (D = 8) 77.0 % of peak against 76.0 % for one front
+// at 5,000 blocks and 74.6 against 73.8 % at 2,048, in 4-block chunks (D = 16)
+// 76.6 against 76.0 % and 74.4 against 73.7 %; 16 KiB slabs in 16-block chunks
+// (D = 8) 74.4 against 73.3 %. With 4 and 8 KiB slabs (D = 32, 16) they lost
+// 1.3-1.4 points, so smaller slabs keep D <= 4.
 uint32_t scatter_pairing(uint32_t n_work, uint32_t parts_shift, uint32_t n_slices, uint32_t bpc,
                          uint64_t slab) {
   if (n_work > kMaxWorkPerLaunch || n_slices % (2 * kXcds)) return 32;
-  return pairing_2mib(parts_shift, n_slices, bpc, slab, 2);
+  return pairing_2mib(parts_shift, n_slices, bpc, slab, slab > 8192 ? 4 : 2);
 }
 
 // Pairing for the gather: each chunk's slices walked in pairs 2 MiB apart in
@@ -909,9 +917,7 @@ uint32_t scatter_pairing(uint32_t n_work, uint32_t parts_shift, uint32_t n_slice
 // 80.8 / 80.6 % of peak against 79.6 / 79.3 % for the plain walk at 2,048
 // blocks, 81.2 / 81.1 against 80.7 / 80.5 at 5,000; at the tensor-parallel
 // shard shapes (4 and 8 KiB slabs, 16-block chunks: D = 32, 16) 77.3 / 77.4
-// against 75.5 / 75.6 over 16 pairs, faster on every pair. (The ordered
-// scatter's two fronts that far apart lost 1.3-1.4 points at the shard
-// shapes, so it keeps D <= 4.)
+// against 75.5 / 75.6 over 16 pairs, faster on every pair.
 uint32_t gather_pairing(uint32_t parts_shift, uint32_t n_slices, uint32_t bpc, uint64_t slab) {
   return pairing_2mib(parts_shift, n_slices, bpc, slab, 5);
 }

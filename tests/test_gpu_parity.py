@@ -296,22 +296,26 @@ def test_ordered_scatter_bit_exact(n, heads):
 # Geometries of the 2 MiB pairings: the gather walks a chunk's slices in pairs
 # D apart, and the ordered scatter walks each XCD's range as two fronts paired
 # D slices apart, where a slice's run in a chunk (blocks per chunk x slab) times
-# D is 2 MiB, D a power of two (gather D <= 32, scatter D <= 4); the scatter
-# also needs the slice count to be a multiple of 16 (two halves per XCD range)
-# and of 2 D, the gather of 2 D.
+# D is 2 MiB, D a power of two (gather D <= 32, scatter D <= 16 for slabs above
+# 8 KiB, else 4); the scatter also needs the slice count to be a multiple of 16
+# (two halves per XCD range) and of 2 D, the gather of 2 D. (Scatters of slabs
+# of at most 8 KiB in the default layout walk the image instead.)
 PAIRED = [
     # (layers, NB, BS, heads, dim, elem, l0, l1, n, chunk_tokens): pairing taken
     (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 256),    # 32 KiB slabs x 16 blocks: D = 4, both
     (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 1024),   # x 64 blocks: D = 1, both
     (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 512),    # x 32 blocks: D = 2, both
-    (40, 2100, 16, 2, 128, 2, 0, 40, 1030, 1024), # 8 KiB x 64: D = 4; 80 slices, 10 per XCD
+    (40, 2100, 16, 2, 128, 2, 0, 40, 1030, 1024), # 8 KiB x 64: gather D = 4; linear scatter
+    (40, 2100, 16, 4, 128, 2, 0, 40, 1030, 1024), # 16 KiB x 64: D = 2; 80 slices, 10 per XCD
     (12, 2300, 16, 8, 128, 2, 2, 10, 1100, 256),  # a partial layer range: 16 slices, D = 4
     (12, 2300, 16, 8, 128, 2, 0, 12, 1100, 256),  # 24 slices: gather paired, scatter one front
     (10, 2300, 16, 8, 128, 2, 0, 10, 1100, 256),  # 20 slices: neither
-    (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 128),    # 32 KiB x 8 blocks: D = 8, gather only
-    (16, 2300, 16, 8, 128, 2, 0, 16, 1101, 64),   # x 4 blocks: D = 16, gather only; ragged last chunk
-    (32, 2300, 16, 1, 128, 2, 0, 32, 1100, 256),  # 4 KiB x 16 blocks: D = 32, gather only
-    (16, 2300, 16, 2, 128, 2, 0, 16, 1103, 256),  # 8 KiB x 16 blocks: D = 16, gather only; ragged
+    (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 128),    # 32 KiB x 8 blocks: D = 8, both
+    (16, 2300, 16, 8, 128, 2, 0, 16, 1101, 64),   # x 4 blocks: D = 16, both; ragged last chunk
+    (16, 2300, 16, 4, 128, 2, 0, 16, 1100, 256),  # 16 KiB x 16 blocks: D = 8, both
+    (4, 2300, 16, 8, 128, 2, 0, 4, 1100, 64),     # D = 16 but 8 slices: neither
+    (32, 2300, 16, 1, 128, 2, 0, 32, 1100, 256),  # 4 KiB x 16 blocks: D = 32, gather; linear scatter
+    (16, 2300, 16, 2, 128, 2, 0, 16, 1103, 256),  # 8 KiB x 16 blocks: D = 16, gather; linear scatter
     (24, 2300, 16, 1, 128, 2, 0, 24, 1100, 256),  # D = 32 but 48 slices: neither
 ]
 
