@@ -50,13 +50,13 @@ KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
 # only for the kernel code they were taken on (kernels_sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "cbd8a5f3dc2730371debcb7b78f3ded49559c25cb9dedddfe0a04ce5f35caf00",
+    "kernels_sha256": "94b632d1eabba63deba6f0d29c99212ab1598896361d8812c15a0ef514a50173",
     # cache layout -> (fetched, written) HBM bytes of the timed gather launch
     # at the default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy
     # calibration), WRITE_SIZE KiB x 1.0
-    "nhd": (10488809615, 10485760000),         # 5,121,518.4 / 10,240,000.0 KiB
-    "paged_attn": (10488991221, 10485760000),  # 5,121,609.2 / 10,240,000.0 KiB
-    "hnd": (10488859549, 10485760000),         # 5,121,543.1 / 10,240,000.0 KiB
+    "nhd": (10488823537, 10485760000),         # 5,121,524.6 / 10,240,000.0 KiB
+    "paged_attn": (10488982374, 10485760000),  # 5,121,604.6 / 10,240,000.0 KiB
+    "hnd": (10488845174, 10485760000),         # 5,121,537.9 / 10,240,000.0 KiB
 }
 
 

@@ -159,8 +159,8 @@ kvx_status kvx_scatter_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * allocation): the same arguments, validation, kernels and result, but the
  * destination order that a scatter of 1,024 blocks or more computes first (in
- * chunks of more than one block, and with the default layout only for slabs
- * above 8 KiB) lives in
+ * chunks of more than one block, and with the default layout, or HND with one
+ * KV head, only for slabs above 8 KiB) lives in
  * a fixed device array of the library's (512 KiB, KVX_NOALLOC_MAX_BLOCKS
  * 8-byte entries; each GPU the library runs on holds one until the process
  * ends) instead of stream-ordered scratch. The call allocates nothing.

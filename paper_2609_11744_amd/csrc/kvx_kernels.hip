@@ -745,9 +745,14 @@ constexpr int32_t kOrderedScatterMinBlocks = 1024;
 // ordered walk: 4 KiB slabs 71.6-72.1 % of peak against 68.0-68.3 %, 8 KiB
 // 70.8 against 69.3-69.8 %, 16 KiB level (73.7 / 73.6 %, a wider spread), and
 // 32 KiB 71.1 against 75.3 % (image order with XCD ranges: 69.3 / 69.1 % at 4
-// and 8 KiB). Measured with the default layout only.
-bool scatter_linear(int64_t n_blocks, int64_t slab, int layout) {
-  return layout == KVX_LAYOUT_NHD && n_blocks >= kOrderedScatterMinBlocks && slab <= 8192;
+// and 8 KiB). An HND cache with one KV head is the default layout byte for
+// byte, and measured the same way (4 KiB slabs: 73.7 against 70.4 %); with
+// two heads in 8 KiB it lost 1.8 points, and the paged-attention layout was
+// level at 4 KiB and 2.6 points slower at 8 KiB, so those keep destination
+// order.
+bool scatter_linear(int64_t n_blocks, int64_t slab, int layout, int32_t heads) {
+  const bool rows = layout == KVX_LAYOUT_NHD || (layout == KVX_LAYOUT_HND && heads == 1);
+  return rows && n_blocks >= kOrderedScatterMinBlocks && slab <= 8192;
 }
 
 // Whether a scatter of n_blocks in chunks of bpc blocks runs in destination
@@ -761,8 +766,10 @@ bool scatter_linear(int64_t n_blocks, int64_t slab, int layout) {
 // 4-block chunks the two were level (73.6 / 73.6), and destination order led
 // with 16 and 64 (74.6 against 71.8 and 75.0 against 70.8 at 2,048 blocks,
 // 76.9 against 71.9 at 5,000 with 16).
-bool scatter_in_destination_order(int64_t n_blocks, int64_t bpc, int64_t slab, int layout) {
-  return n_blocks >= kOrderedScatterMinBlocks && bpc > 1 && !scatter_linear(n_blocks, slab, layout);
+bool scatter_in_destination_order(int64_t n_blocks, int64_t bpc, int64_t slab, int layout,
+                                  int32_t heads) {
+  return n_blocks >= kOrderedScatterMinBlocks && bpc > 1 &&
+         !scatter_linear(n_blocks, slab, layout, heads);
 }
 
 // Dynamic LDS bytes for a reordering layout: the image of one head, rounded
@@ -1056,8 +1063,8 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   // fall back to image order (same result, slower).
   OrderEntry* order = nullptr;
   const bool own = order_scratch == nullptr;
-  ug.linear_walk = scatter_linear(g.n_blocks, g.slab, layout) ? 1u : 0u;
-  if (scatter_in_destination_order(g.n_blocks, g.bpc, g.slab, layout)) {
+  ug.linear_walk = scatter_linear(g.n_blocks, g.slab, layout, cache->num_kv_heads) ? 1u : 0u;
+  if (scatter_in_destination_order(g.n_blocks, g.bpc, g.slab, layout, cache->num_kv_heads)) {
     if (!own)
       order = static_cast<OrderEntry*>(order_scratch);
     else if (hipMallocAsync((void**)&order, (size_t)g.n_blocks * sizeof(OrderEntry), stream) !=

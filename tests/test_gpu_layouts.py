@@ -82,13 +82,15 @@ def test_layout_gather_scatter_bit_exact(case):
         assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
 
 
-@pytest.mark.parametrize("layout", [HND, PA])
-def test_layout_ordered_scatter_and_chunk_lists(layout):
-    """Destination-ordered scatter (>= 1024 blocks) and the chunk-list path
-    (ring restore and offload) in a transposing layout."""
-    s = oracle.Shape(2, 4000, 16, 2, 64, 2, layout)
+@pytest.mark.parametrize("layout,heads,dim", [(HND, 2, 64), (PA, 2, 64), (HND, 1, 128)],
+                         ids=["hnd", "paged_attn", "hnd_one_head"])
+def test_layout_ordered_scatter_and_chunk_lists(layout, heads, dim):
+    """Large scatters (>= 1024 blocks: destination order, or with one head in
+    HND the default layout's linear image-order walk) and the chunk-list path
+    (ring restore and offload) in a reordering layout."""
+    s = oracle.Shape(2, 4000, 16, heads, dim, 2, layout)
     n = 1300
-    seed = 210 + layout
+    seed = 210 + layout + heads
     bt_src, bt_dst = seeded_ids(seed, s.num_blocks, n, n)
     fill = Filled(seed, kvsynth.ROLE_SRC, kvsynth.MODE_RAW)
     cache = device_cache(s, fill, DEV)
