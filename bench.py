@@ -24,7 +24,11 @@ Other workloads print one JSON line each with their own metric:
   --workload 70b-batch     64 requests on a seeded prefix tree over a
                            70B-shaped cache (80 layers): the distinct missing
                            chunks restored through one ring while the new
-                           blocks are offloaded through another.
+                           blocks are offloaded through another;
+  --workload 8b-placements the default gather and scatter on every pair of
+                           several caches and packed buffers alive at once
+                           (--caches, --packed): how much of a run-to-run
+                           spread is where the allocations land in memory.
 """
 from __future__ import annotations
 
@@ -70,7 +74,11 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="8b-80k",
-                    choices=["8b-80k", "8b-32k-sweep", "70b-batch", "8b-files", "8b-preload"])
+                    choices=["8b-80k", "8b-32k-sweep", "70b-batch", "8b-files", "8b-preload",
+                             "8b-placements"])
+    ap.add_argument("--caches", type=int, default=4, help="8b-placements: caches allocated")
+    ap.add_argument("--packed", type=int, default=3,
+                    help="8b-placements: packed buffers allocated")
     ap.add_argument("--num-blocks", type=int, default=20000)
     ap.add_argument("--prefix-blocks", type=int, default=5000)
     ap.add_argument("--kv-heads", type=int, default=8,
@@ -1167,6 +1175,76 @@ def run_preload(args):
     print(json.dumps(out), flush=True)
 
 
+# ---- allocation placement -------------------------------------------------------------
+
+def run_placements(args):
+    """The default workload's gather and scatter (80k-token prefix, 256-token
+    chunks, the same seeded ids) on every (cache, packed buffer) pair of
+    --caches caches and --packed packed buffers, all allocated up front and
+    alive together: each pair sits at other physical addresses, and the spread
+    of the rates over the pairs is the placement's share of a run-to-run
+    spread (the code and the ids are the same for every pair)."""
+    import numpy as np
+    import torch
+
+    import kvsynth
+    import paper_2609_11744_amd as kvx
+
+    dev = torch.device("cuda:0")
+    L, BS, H, D, E = 32, 16, args.kv_heads, 128, 2
+    NB, n, ct = args.num_blocks, args.prefix_blocks, args.chunk_tokens
+    slab = BS * H * D * E
+    payload = n * L * 2 * slab
+    need = args.caches * NB * L * 2 * slab + args.packed * payload
+    free, _ = torch.cuda.mem_get_info()
+    if need > 0.9 * free:
+        raise SystemExit(f"{need / 1e9:.0f} GB of caches and packed buffers do not fit")
+    perm = np.random.default_rng(args.seed).permutation(NB).astype(np.int32)
+    bt_src = torch.from_numpy(perm[:n].copy()).to(dev)
+    bt_dst = torch.from_numpy(perm[n:2 * n].copy()).to(dev)
+    caches, packs = [], []
+    for i in range(max(args.caches, args.packed)):
+        if i < args.caches:
+            c = kvx.PagedKVCache.allocate(L, NB, BS, H, D, torch.bfloat16, dev)
+            fill_cache(c, args.seed, kvsynth.ROLE_SRC)
+            caches.append(c)
+        if i < args.packed:
+            packs.append(torch.empty(payload, dtype=torch.uint8, device=dev))
+    torch.cuda.synchronize()
+    reps = max(args.steps, 3)
+    pct = lambda ms: 100 * 2 * payload / ms / 1e6 / HBM_PEAK_GBPS
+    rows = []
+    for ci, c in enumerate(caches):
+        for pi, p in enumerate(packs):
+            g = event_ms(lambda: kvx.kvx_gather_blocks(c, 0, L, bt_src, n, ct, p), reps)
+            sc = event_ms(lambda: kvx.kvx_scatter_blocks(c, 0, L, bt_dst, n, ct, p), reps)
+            rows.append({"cache": ci, "packed": pi,
+                         "gather_pct_hbm_peak": round(pct(statistics.median(g)), 2),
+                         "scatter_pct_hbm_peak": round(pct(statistics.median(sc)), 2)})
+    kvx.kvx_check()
+    log(f"placements: {[(r['cache'], r['packed'], r['gather_pct_hbm_peak'], r['scatter_pct_hbm_peak']) for r in rows]}")
+
+    def spread(key):
+        v = [r[key] for r in rows]
+        return {"mean": round(statistics.mean(v), 2), "min": min(v), "max": max(v)}
+
+    gs = spread("gather_pct_hbm_peak")
+    ss = spread("scatter_pct_hbm_peak")
+    mean_rate = (gs["mean"] + ss["mean"]) / 2 * HBM_PEAK_GBPS / 100
+    out = base_record(
+        args, "KV gather/scatter GB/s & % HBM peak over allocation placements", "GB/s",
+        round(mean_rate, 1), None,
+        {"workload": "llama-3-8b-shaped paged KV, 80k-token prefix (5000 blocks), 256-token "
+                     f"chunks, on each of {args.caches} caches x {args.packed} packed buffers",
+         "num_blocks": NB, "prefix_tokens": n * BS, "chunk_tokens": ct, "kv_heads": H,
+         "caches": args.caches, "packed": args.packed, "parallelism": "single GPU"})
+    out.update({"gather_pct_hbm_peak": gs, "scatter_pct_hbm_peak": ss, "pairs": rows,
+                "reps_per_pair": reps,
+                "note": "value: mean of the gather and scatter rates over the pairs; each "
+                        "call timed as in the default workload (median of reps_per_pair)"})
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -1177,7 +1255,8 @@ def main():
 
     torch.cuda.set_device(torch.device("cuda:0"))
     {"8b-80k": run_80k, "8b-32k-sweep": run_sweep, "70b-batch": run_batch,
-     "8b-files": run_files, "8b-preload": run_preload}[args.workload](args)
+     "8b-files": run_files, "8b-preload": run_preload,
+     "8b-placements": run_placements}[args.workload](args)
 
 
 if __name__ == "__main__":
