@@ -44,9 +44,10 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0  # MI355X HBM3E, vendor figure
-# The copy kernels' sources: the kernels and the store they issue.
+# The copy kernels' sources: the kernels, the store they issue, the walk
+# selection and the launch constants they share.
 KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
-               for f in ("kvx_kernels.hip", "kvx_store.h")]
+               for f in ("kvx_kernels.hip", "kvx_store.h", "kvx_walk.cpp", "kvx_internal.h")]
 
 # HBM bytes of one gather launch on the 80k workload, from two rocprofv3 --pmc
 # runs (FETCH_SIZE, then WRITE_SIZE; profiles/copy_units_8b_80k_pmc.md), each
@@ -54,13 +55,13 @@ KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
 # only for the kernel code they were taken on (kernels_sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "94b632d1eabba63deba6f0d29c99212ab1598896361d8812c15a0ef514a50173",
+    "kernels_sha256": "a6c713560f24862291985b5983b8410eccc9b3c6f9b6e7d2a02f8de45cf853d0",
     # cache layout -> (fetched, written) HBM bytes of the timed gather launch
     # at the default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy
     # calibration), WRITE_SIZE KiB x 1.0
-    "nhd": (10488823537, 10485760000),         # 5,121,524.6 / 10,240,000.0 KiB
-    "paged_attn": (10488982374, 10485760000),  # 5,121,604.6 / 10,240,000.0 KiB
-    "hnd": (10488845174, 10485760000),         # 5,121,537.9 / 10,240,000.0 KiB
+    "nhd": (10488806774, 10485760000),         # 5,121,519.1 / 10,240,000.0 KiB
+    "paged_attn": (10488988105, 10485760000),  # 5,121,606.8 / 10,240,000.0 KiB
+    "hnd": (10488852824, 10485760000),         # 5,121,541.0 / 10,240,000.0 KiB
 }
 
 
@@ -380,6 +381,8 @@ def run_80k(args):
                   f"behind a {HOLD_US:.0f} us spin kernel so that its host-side launch is "
                   f"not counted; launch_inclusive: the same calls timed from an idle GPU",
         "launch_inclusive": {"gather_ms": ms_stats(launch_g), "scatter_ms": ms_stats(launch_s)},
+        "walks": {"gather": kvx.kvx_copy_walk(cache, 0, L, n, ct, True),
+                  "scatter": kvx.kvx_copy_walk(cache, 0, L, n, ct, False)},
         "restore_ms": round(med["restore_ms"], 3),
         "restore_GBps": round(restore_GBps, 2),
         "restore_frac_of_h2d": round(restore_GBps / probe["h2d_GBps"], 4),
@@ -510,7 +513,9 @@ def sweep_32k(args, cache, L, perm, packed, slab, reps=5):
                                                   / HBM_PEAK_GBPS, 2),
                      "scatter_pct_hbm_peak": round(100 * 2 * payload / statistics.median(sc) / 1e6
                                                    / HBM_PEAK_GBPS, 2),
-                     "gather_ms": ms_stats(g), "scatter_ms": ms_stats(sc)})
+                     "gather_ms": ms_stats(g), "scatter_ms": ms_stats(sc),
+                     "walks": {"gather": kvx.kvx_copy_walk(cache, 0, L, n, ct, True),
+                               "scatter": kvx.kvx_copy_walk(cache, 0, L, n, ct, False)}})
     kvx.kvx_check()
     log(f"32k sweep: {[(r['chunk_tokens'], r['gather_pct_hbm_peak'], r['scatter_pct_hbm_peak']) for r in rows]}")
     return {"prefix_tokens": n * 16, "payload_bytes": payload, "reps": reps, "rows": rows}

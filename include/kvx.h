@@ -152,6 +152,34 @@ kvx_status kvx_scatter_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
                               const int32_t* block_table, int32_t n_blocks, int32_t chunk_tokens,
                               const void* src, hipStream_t stream);
 
+/* How kvx_gather_blocks (to_packed = 1) or kvx_scatter_blocks (0) with these
+ * arguments walks its work: the launcher's own choice, reported for tests and
+ * measurement records. Pure host code: the cache's tensor pointers may be
+ * NULL. A call moves work_items workgroups; each moves one part of a slab
+ * (parts per slab: 4 KiB pieces with the default layout, heads with the
+ * others). A scatter of 1,024 blocks or more in chunks of more than one block
+ * runs in ascending destination order (ordered = 1; block ids bucketed by a
+ * small kernel first), except with slabs of at most 8 KiB in the default
+ * layout (or HND with one KV head): those, like every smaller scatter, walk
+ * the packed image in order, with linear = 1 when workgroup b moves work item
+ * b rather than each XCD taking one contiguous range. pair_slices = D > 0:
+ * slices D apart, whose runs sit 2 MiB apart in a packed chunk, are moved
+ * together (the gather's paired walk, or an ordered scatter's two fronts per
+ * XCD: fronts = 2). For an empty call every field is 0. KVX_EINVAL for the
+ * arguments the copy calls reject on the host (except pointers). */
+typedef struct kvx_walk {
+  int64_t work_items;
+  int32_t parts;
+  int32_t ordered;
+  int32_t linear;
+  int32_t pair_slices;
+  int32_t fronts;
+  int32_t reserved;
+} kvx_walk;
+
+kvx_status kvx_copy_walk(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t n_blocks,
+                         int32_t chunk_tokens, int32_t to_packed, kvx_walk* out);
+
 /* Largest n_blocks of kvx_scatter_blocks_noalloc. */
 #define KVX_NOALLOC_MAX_BLOCKS 65536
 

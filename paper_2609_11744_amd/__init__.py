@@ -313,6 +313,16 @@ def trace_chrome(events, name="ring") -> dict:
     return {"traceEvents": out, "displayTimeUnit": "ms"}
 
 
+def kvx_copy_walk(cache, l0, l1, n_blocks, chunk_tokens, to_packed: bool) -> dict:
+    """The walk a gather (to_packed) or scatter of these arguments takes (pure
+    host computation, kvx_copy_walk)."""
+    c = _cstruct(cache)
+    w = _native.KvxWalk()
+    _ok(_native.lib().kvx_copy_walk(ctypes.byref(c), l0, l1, n_blocks, chunk_tokens,
+                                    1 if to_packed else 0, ctypes.byref(w)), "kvx_copy_walk")
+    return {f: getattr(w, f) for f, _ in _native.KvxWalk._fields_ if f != "reserved"}
+
+
 def kvx_plan_pieces(cache, l0, l1, n_blocks, chunk_tokens, slot_bytes, ramp=KVX_RAMP_NONE):
     """Staging pieces as a list of dicts (pure host computation)."""
     c = _cstruct(cache)
@@ -717,5 +727,5 @@ __all__ = [
     "kvx_read_files", "kvx_write_files", "KVX_EIO", "KVX_EBUSY", "kvx_offload_begin",
     "kvx_offload_wait", "kvx_restore_begin", "kvx_restore_wait", "kvx_chunk_stride",
     "KVX_RAMP_NONE", "KVX_RAMP_FIRST", "KVX_RAMP_LAST", "kvx_scatter_blocks_noalloc",
-    "KVX_NOALLOC_MAX_BLOCKS", "TRACE_KINDS", "trace_chrome",
+    "KVX_NOALLOC_MAX_BLOCKS", "TRACE_KINDS", "trace_chrome", "kvx_copy_walk",
 ]

@@ -57,6 +57,11 @@ class KvxPreloadStats(ctypes.Structure):
                                      "staged", "held")]
 
 
+class KvxWalk(ctypes.Structure):
+    _fields_ = [("work_items", c_i64), ("parts", c_i32), ("ordered", c_i32), ("linear", c_i32),
+                ("pair_slices", c_i32), ("fronts", c_i32), ("reserved", c_i32)]
+
+
 class KvxCurve(ctypes.Structure):
     _fields_ = [("tokens", ctypes.POINTER(ctypes.c_double)),
                 ("seconds", ctypes.POINTER(ctypes.c_double)), ("n", c_i32)]
@@ -103,6 +108,8 @@ SIGNATURES = {
                                          c_vp, c_i32, c_i32, c_vp, c_i64, c_vp]),
     "kvx_scatter_chunks": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_vp, c_i32,
                                           c_vp, c_i32, c_i32, c_vp, c_i64, c_vp]),
+    "kvx_copy_walk": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32, c_i32, c_i32,
+                                     ctypes.POINTER(KvxWalk)]),
     "kvx_check": (ctypes.c_int, [c_vp]),
     "kvx_strerror": (ctypes.c_char_p, [ctypes.c_int]),
     "kvx_plan_pieces": (ctypes.c_int, [ctypes.POINTER(KvxCache), c_i32, c_i32, c_i32, c_i32,

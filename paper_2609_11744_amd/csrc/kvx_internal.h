@@ -31,6 +31,42 @@ struct Geometry {
   int32_t num_blocks = 0;    // pool size, for the kernel's id check
 };
 
+// MI355X: 8 XCDs; a launch's workgroups are dispatched to them round-robin.
+constexpr unsigned kXcds = 8;
+
+// A dispatch's grid is counted in work-items in 32 bits, so one launch covers
+// at most kMaxWorkPerLaunch workgroups (of at most 256 threads: 2^30
+// work-items); larger calls are split.
+constexpr uint32_t kMaxWorkPerLaunch = 1u << 22;
+
+// Default-layout copy shape: one workgroup of kPartThreads threads moves
+// kPartThreads 16-byte vectors of a slab.
+constexpr uint32_t kPartThreads = 256;
+
+// Scatters of at least this many blocks run in destination order.
+constexpr int32_t kOrderedScatterMinBlocks = 1024;
+
+// Workgroups per slab for the layout (4 KiB pieces with the default layout,
+// heads with the reordering ones), and log2 of that count when it is a power
+// of two (else 32: the kernels divide).
+void slab_parts(int layout, uint32_t n16, uint32_t heads, uint32_t* parts, uint32_t* shift);
+
+// How a gather or scatter walks its work items: the launcher's choice, also
+// reported by kvx_copy_walk (kvx_walk.cpp).
+struct Walk {
+  uint32_t parts = 0, parts_shift = 32;  // workgroups per slab (slab_parts)
+  uint32_t n_work = 0;                    // work items (workgroups) of the call
+  uint32_t pair_shift = 32;               // ordered scatter: fronts 2^pair_shift slices apart
+  uint32_t gather_pair_shift = 32;        // gather: slices paired 2^gather_pair_shift apart
+  bool linear = false;                    // workgroup b moves work item b
+  bool ordered = false;                   // scatter in destination order
+};
+
+// The walk of a validated gather (to_packed) or scatter: KVX_EINTERNAL when
+// its work items do not fit 31 bits.
+kvx_status choose_walk(bool to_packed, const kvx_cache* cache, const Geometry& g, Walk* w);
+
+
 // Host-side validation shared by every entry point. `packed` may be null only
 // when no copy follows (plan-only callers). Fills *g on success.
 kvx_status validate(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t n_blocks,

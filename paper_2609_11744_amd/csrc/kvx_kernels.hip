@@ -37,9 +37,9 @@
 // less than unordered writes. The exceptions measured faster in image order:
 // a chunk of one block (each chunk is then one sequential read, and the
 // writes go to one destination block of every layer in turn;
-// scatter_in_destination_order), and slabs of at most 8 KiB, walked with no
-// XCD ranges so that the whole chip reads the packed image front to back
-// (scatter_linear).
+// scatter_in_destination_order in kvx_walk.cpp), and slabs of at most 8 KiB,
+// walked with no XCD ranges so that the whole chip reads the packed image
+// front to back (scatter_linear).
 //
 // Pairing at 2 MiB. Where a layer|K|V slice's run in a packed chunk (blocks
 // per chunk x slab) times a power of two D is 2 MiB, both directions can move
@@ -49,7 +49,7 @@
 // move the same destination block of two such slices (D up to 16 for slabs
 // above 8 KiB, else 4). Both
 // measured faster than the plain walks on this chip, and pairs at other
-// distances slower (scatter_pairing, gather_pairing).
+// distances slower (scatter_pairing, gather_pairing in kvx_walk.cpp).
 #include <hip/hip_runtime.h>
 
 #include <mutex>
@@ -68,7 +68,6 @@ using kvx_dev::v4u;
 constexpr int kErrBadBlock = 1;
 constexpr int kErrBadChunk = 2;
 constexpr int kErrorWords = 1024;  // word 0: the null stream, and streams beyond the table
-constexpr unsigned kXcds = 8;  // MI355X: 8 XCDs, workgroups dispatched round-robin
 
 // One entry of a scatter's destination order: a block-table index and the
 // block id found there (read once by the ordering kernel).
@@ -179,7 +178,7 @@ __device__ __forceinline__ uint32_t xcd_contiguous(uint32_t b, uint32_t n) {
 // only where each XCD's range is a whole, even number of layer|K|V slices,
 // so that the two fronts move the same destination block of two slices
 // together (its writes in two cache tensors, its reads from one packed
-// chunk), and paired_slice chooses which two (scatter_pairing).
+// chunk), and paired_slice chooses which two (scatter_pairing, kvx_walk.cpp).
 __device__ __forceinline__ uint32_t xcd_two_fronts(uint32_t b, uint32_t n, uint32_t shift) {
   const uint32_t q = n / kXcds, r = n % kXcds, x = b % kXcds, k = b / kXcds;
   const uint32_t len = q + (x < r ? 1u : 0u), start = x * q + (x < r ? x : r);
@@ -725,53 +724,6 @@ __global__ void __launch_bounds__(kOrderThreads)
   }
 }
 
-// A dispatch's grid is counted in work-items in 32 bits, so one launch covers
-// at most kMaxWorkPerLaunch workgroups (of at most 256 threads: 2^30
-// work-items); larger calls are split.
-constexpr uint32_t kMaxWorkPerLaunch = 1u << 22;
-
-// Default-layout copy shape: one workgroup of kPartThreads threads moves
-// kPartThreads 16-byte vectors of a slab.
-constexpr uint32_t kPartThreads = 256;
-
-// Scatters of at least this many blocks run in destination order.
-constexpr int32_t kOrderedScatterMinBlocks = 1024;
-
-// Whether a large scatter of small slabs walks the image in order with no
-// XCD ranges (workgroup b moves work item b: the whole chip reads the packed
-// image front to back). Compared over 9-16 (cache, packed buffer) allocation
-// pairs in one process at the tensor-parallel shard shapes of the 8B cache
-// (80k prefix, 16-block chunks, default layout), against the destination-
-// ordered walk: 4 KiB slabs 71.6-72.1 % of peak against 68.0-68.3 %, 8 KiB
-// 70.8 against 69.3-69.8 %, 16 KiB level (73.7 / 73.6 %, a wider spread), and
-// 32 KiB 71.1 against 75.3 % (image order with XCD ranges: 69.3 / 69.1 % at 4
-// and 8 KiB). An HND cache with one KV head is the default layout byte for
-// byte, and measured the same way (4 KiB slabs: 73.7 against 70.4 %); with
-// two heads in 8 KiB it lost 1.8 points, and the paged-attention layout was
-// level at 4 KiB and 2.6 points slower at 8 KiB, so those keep destination
-// order.
-bool scatter_linear(int64_t n_blocks, int64_t slab, int layout, int32_t heads) {
-  const bool rows = layout == KVX_LAYOUT_NHD || (layout == KVX_LAYOUT_HND && heads == 1);
-  return rows && n_blocks >= kOrderedScatterMinBlocks && slab <= 8192;
-}
-
-// Whether a scatter of n_blocks in chunks of bpc blocks runs in destination
-// order. The rate of one walk over the same ids moves by up to 8 points of
-// peak with where the cache and the packed buffer land in physical memory,
-// so the walks were compared over 12 placements (4 caches x 3 packed buffers
-// allocated in one process, each walk on each pair, alternated; 8B-shaped
-// cache, 20,000-block pool, mean % of 8 TB/s). With one-block chunks image
-// order averaged 76.8 against 73.6 in destination order at 2,048 blocks (at
-// least as fast on 11 of the 12 pairs) and 76.3 against 76.1 at 5,000; with
-// 4-block chunks the two were level (73.6 / 73.6), and destination order led
-// with 16 and 64 (74.6 against 71.8 and 75.0 against 70.8 at 2,048 blocks,
-// 76.9 against 71.9 at 5,000 with 16).
-bool scatter_in_destination_order(int64_t n_blocks, int64_t bpc, int64_t slab, int layout,
-                                  int32_t heads) {
-  return n_blocks >= kOrderedScatterMinBlocks && bpc > 1 &&
-         !scatter_linear(n_blocks, slab, layout, heads);
-}
-
 // Dynamic LDS bytes for a reordering layout: the image of one head, rounded
 // up to whole swizzle groups of 16 vectors (gather) or with its pad vectors
 // (scatter); none for HND, which moves rows directly.
@@ -860,73 +812,6 @@ hipError_t launch_chunks(const LayerPtrs& lp, const int32_t* bt, const kvx_chunk
     if (e != hipSuccess) return e;
   }
   return hipSuccess;
-}
-
-// Workgroups per slab for the layout (4 KiB pieces with the default layout,
-// heads with the reordering ones), and log2 of that count when it is a power
-// of two (else 32: the kernels divide).
-void slab_parts(int layout, uint32_t n16, uint32_t heads, uint32_t* parts, uint32_t* shift) {
-  *parts = layout == KVX_LAYOUT_NHD ? (n16 + kPartThreads - 1) / kPartThreads : heads;
-  *shift = (*parts & (*parts - 1)) == 0 ? (uint32_t)__builtin_ctz(*parts) : 32u;
-}
-
-// Pairing for the ordered scatter of n_work work items (one launch) over
-// n_slices layer|K|V slices: log2 of the distance D in slices between the two
-// slices its fronts move together, or 32 for one front per XCD. Two fronts
-// pay, as measured, where the paired slabs sit 2 MiB apart in the packed
-// chunk (D chunk layers apart) and D <= 4: on the 80k scatter pattern
-// (standalone probe, one allocation for the pool, two processes) pairs 2 MiB
-// apart beat one front by 2.2-2.3 points with 16-block chunks (D = 4) and by
-// 0.9-2.0 with 64-block chunks (D = 1), and lost 0.6-1.1 with 4-block chunks
-// (D = 16); pairs at any other distance (32 KiB to 64 MiB) lost 0.5-2 points
-// to one front in all but one process. In the library, alternated on three
-// boxes: the 80k scatter (D = 4) 75.1-75.6 % of peak against 72.7-72.9 %,
-// 80.5-83.0 % against 78.9-80.5 % on two faster boxes; the 32k scatter with
-// 256-token chunks 72.6-72.8 % against 69.5-70.5 %. Why 2 MiB is the
-// distance that pays is not established: it depends on how the chip maps
-// physical addresses to memory channels, which these kernels do not see.
-// log2 of D, the distance in slices at which two slices' runs in a packed
-// chunk sit 2 MiB apart, where D is a power of two of at most 2^max_ds and
-// the slice count a multiple of 2 D; else 32.
-uint32_t pairing_2mib(uint32_t parts_shift, uint32_t n_slices, uint32_t bpc, uint64_t slab,
-                      uint32_t max_ds) {
-  constexpr uint64_t kPairBytes = 2u << 20;
-  if (parts_shift >= 32) return 32;
-  const uint64_t run = (uint64_t)bpc * slab;  // one slice's run in a chunk
-  if (run == 0 || kPairBytes % run) return 32;
-  const uint64_t d = kPairBytes / run;
-  if ((d & (d - 1)) || d > (1ull << max_ds) || n_slices % (2 * d)) return 32;
-  return (uint32_t)__builtin_ctzll(d);
-}
-
-// Farther apart (D = 8, 16) the fronts paid with slabs above 8 KiB, compared
-// over 9-12 (cache, packed buffer) allocation pairs in one process: 32 KiB
-// slabs in 8-block chunks (D = 8) 77.0 % of peak against 76.0 % for one front
-// at 5,000 blocks and 74.6 against 73.8 % at 2,048, in 4-block chunks (D = 16)
-// 76.6 against 76.0 % and 74.4 against 73.7 %; 16 KiB slabs in 16-block chunks
-// (D = 8) 74.4 against 73.3 %. With 4 and 8 KiB slabs (D = 32, 16) they lost
-// 1.3-1.4 points, so smaller slabs keep D <= 4.
-uint32_t scatter_pairing(uint32_t n_work, uint32_t parts_shift, uint32_t n_slices, uint32_t bpc,
-                         uint64_t slab) {
-  if (n_work > kMaxWorkPerLaunch || n_slices % (2 * kXcds)) return 32;
-  return pairing_2mib(parts_shift, n_slices, bpc, slab, slab > 8192 ? 4 : 2);
-}
-
-// Pairing for the gather: each chunk's slices walked in pairs 2 MiB apart in
-// the chunk, D <= 32 slices (the packed-side writes then alternate between two
-// runs 2 MiB apart). On the 80k gather pattern (standalone probe, two
-// processes each) this measured 0.3-0.8 points above the plain walk with 16-
-// and 64-block chunks (D = 4, 1); pairs at other distances (512 KiB to 32 MiB)
-// were 0.5-4 points slower. Farther apart in slices, compared over 12 (cache,
-// packed buffer) allocation pairs in one process (8B shape, 20,000-block
-// pool; the rate of one walk moves by several points with where the
-// allocations land): with 4- and 8-block chunks of 32 KiB slabs (D = 16, 8)
-// 80.8 / 80.6 % of peak against 79.6 / 79.3 % for the plain walk at 2,048
-// blocks, 81.2 / 81.1 against 80.7 / 80.5 at 5,000; at the tensor-parallel
-// shard shapes (4 and 8 KiB slabs, 16-block chunks: D = 32, 16) 77.3 / 77.4
-// against 75.5 / 75.6 over 16 pairs, faster on every pair.
-uint32_t gather_pairing(uint32_t parts_shift, uint32_t n_slices, uint32_t bpc, uint64_t slab) {
-  return pairing_2mib(parts_shift, n_slices, bpc, slab, 5);
 }
 
 DivU32 div_u32(uint32_t d) {
@@ -1027,6 +912,9 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
     lp.p[2 * (l - l0)] = static_cast<char*>(cache->k[l]);
     lp.p[2 * (l - l0) + 1] = static_cast<char*>(cache->v[l]);
   }
+  Walk walk;
+  const kvx_status ws = choose_walk(to_packed, cache, g, &walk);
+  if (ws != KVX_OK) return ws;
   UnitGeom ug;
   ug.units_per_chunk = (uint32_t)(2 * g.lr * g.bpc);
   ug.bpc = (uint32_t)g.bpc;
@@ -1034,7 +922,8 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.num_blocks = (uint32_t)g.num_blocks;
   ug.n16 = (uint32_t)(g.slab / 16);
   const int layout = cache->layout, elem = cache->elem_bytes;
-  slab_parts(layout, ug.n16, (uint32_t)cache->num_kv_heads, &ug.parts, &ug.parts_shift);
+  ug.parts = walk.parts;
+  ug.parts_shift = walk.parts_shift;
   ug.parts_div = div_u32(ug.parts);
   ug.upc_div = div_u32(ug.units_per_chunk);
   ug.bpc_div = div_u32(ug.bpc);
@@ -1042,15 +931,12 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   ug.nb_div = div_u32(ug.n_blocks);
   ug.slab = (uint64_t)g.slab;
   ug.sg = slab_geom(cache, to_packed);
-  if ((uint64_t)g.n_units * ug.parts > 0x7FFFFFFF) return KVX_EINTERNAL;
-  const uint32_t n_work = (uint32_t)g.n_units * ug.parts;
+  const uint32_t n_work = walk.n_work;
   const uint32_t n_slices = (uint32_t)(2 * g.lr);
-  ug.pair_shift = to_packed ? 32u
-                            : scatter_pairing(n_work, ug.parts_shift, n_slices, ug.bpc, ug.slab);
-  ug.gather_pair_shift =
-      to_packed ? gather_pairing(ug.parts_shift, n_slices, ug.bpc, ug.slab) : 32u;
+  ug.pair_shift = walk.pair_shift;
+  ug.gather_pair_shift = walk.gather_pair_shift;
   ug.half_slices = n_slices / kXcds / 2;
-  ug.linear_walk = 0u;
+  ug.linear_walk = walk.linear ? 1u : 0u;
   ug.xcd_slices_div = div_u32(n_slices / kXcds ? n_slices / kXcds : 1);
   if (to_packed) {
     hipError_t e = launch<true, false>(lp, block_table, ug, n_work, nullptr, (char*)packed, err,
@@ -1063,8 +949,7 @@ kvx_status launch_copy(bool to_packed, const kvx_cache* cache, int32_t l0, int32
   // fall back to image order (same result, slower).
   OrderEntry* order = nullptr;
   const bool own = order_scratch == nullptr;
-  ug.linear_walk = scatter_linear(g.n_blocks, g.slab, layout, cache->num_kv_heads) ? 1u : 0u;
-  if (scatter_in_destination_order(g.n_blocks, g.bpc, g.slab, layout, cache->num_kv_heads)) {
+  if (walk.ordered) {
     if (!own)
       order = static_cast<OrderEntry*>(order_scratch);
     else if (hipMallocAsync((void**)&order, (size_t)g.n_blocks * sizeof(OrderEntry), stream) !=
@@ -1187,3 +1072,4 @@ extern "C" kvx_status kvx_scatter_blocks_noalloc(const kvx_cache* cache, int32_t
     return KVX_EINTERNAL;
   }
 }
+

@@ -264,3 +264,54 @@ def test_layer_range_limit_on_the_host():
     assert kvx.kvx_packed_bytes(c, 1, 129, 10) == 128 * 2 * 10 * 16 * 8 * 128 * 2
     assert kvx.kvx_packed_bytes(c, 0, 129, 10) == -1
     assert kvx.kvx_packed_bytes(c, 0, 131, 10) == -1
+
+
+# ---- the walk a copy takes (kvx_copy_walk: the launcher's choice, host only) ----------
+
+HND_, PA_ = kvx.KVX_LAYOUT_HND, kvx.KVX_LAYOUT_PAGED_ATTN
+# (layers, heads, layout, n_blocks, chunk_tokens, to_packed) -> (parts, ordered, linear,
+# pair_slices, fronts); block size 16, head dim 128, 2-byte words, 20,000-block pool
+WALKS = [
+    ((32, 8, 0, 5000, 256, True), (8, 0, 0, 4, 1)),     # 80k gather: slices 4 apart (2 MiB)
+    ((32, 8, 0, 5000, 256, False), (8, 1, 0, 4, 2)),    # 80k scatter: ordered, two fronts
+    ((32, 8, 0, 2048, 16, False), (8, 0, 0, 0, 1)),     # one-block chunks: image order
+    ((32, 8, 0, 2048, 16, True), (8, 0, 0, 0, 1)),      # D = 64 > 32: plain walk
+    ((32, 8, 0, 2048, 64, False), (8, 1, 0, 16, 2)),    # 32 KiB x 4 blocks: fronts 16 apart
+    ((32, 8, 0, 2048, 64, True), (8, 0, 0, 16, 1)),
+    ((32, 8, 0, 2048, 128, False), (8, 1, 0, 8, 2)),
+    ((32, 8, 0, 2048, 1024, False), (8, 1, 0, 1, 2)),
+    ((32, 8, 0, 1023, 256, False), (8, 0, 0, 0, 1)),    # below 1,024 blocks: image order
+    ((32, 1, 0, 5000, 256, True), (1, 0, 0, 32, 1)),    # tp = 8 shard: gather 32 apart
+    ((32, 1, 0, 5000, 256, False), (1, 0, 1, 0, 1)),    # 4 KiB slabs: linear image order
+    ((32, 2, 0, 5000, 256, False), (2, 0, 1, 0, 1)),    # 8 KiB slabs: linear image order
+    ((32, 2, 0, 5000, 256, True), (2, 0, 0, 16, 1)),
+    ((32, 4, 0, 5000, 256, False), (4, 1, 0, 8, 2)),    # 16 KiB slabs: fronts 8 apart
+    ((32, 1, HND_, 5000, 256, False), (1, 0, 1, 0, 1)), # one-head HND = the default layout
+    ((32, 2, HND_, 5000, 256, False), (2, 1, 0, 0, 1)), # two heads: ordered, D = 16 > 4
+    ((32, 1, PA_, 5000, 256, False), (1, 1, 0, 0, 1)),  # paged attention keeps the order
+    ((32, 8, PA_, 5000, 256, True), (8, 0, 0, 4, 1)),
+    ((80, 8, 0, 3000, 256, False), (8, 1, 0, 4, 2)),    # 70B shape: 160 slices
+    ((80, 8, 0, 4000, 256, False), (8, 1, 0, 0, 1)),    # over 2^22 work items: one front
+    ((10, 8, 0, 1100, 256, False), (8, 1, 0, 0, 1)),    # 20 slices: one front
+    ((10, 8, 0, 1100, 256, True), (8, 0, 0, 0, 1)),     # 20 slices: not a multiple of 8
+]
+
+
+@pytest.mark.parametrize("case,want", WALKS, ids=[f"w{i}" for i in range(len(WALKS))])
+def test_copy_walk_rules(case, want):
+    L, H, layout, n, ct, to_packed = case
+    c = kvx.shape_only_cache(L, 20000, 16, H, 128, 2, layout)
+    w = kvx.kvx_copy_walk(c, 0, L, n, ct, to_packed)
+    assert (w["parts"], w["ordered"], w["linear"], w["pair_slices"], w["fronts"]) == want
+    assert w["work_items"] == n * L * 2 * w["parts"]
+
+
+def test_copy_walk_empty_and_invalid():
+    c = kvx.shape_only_cache(4, 100, 16, 2, 64, 2)
+    assert kvx.kvx_copy_walk(c, 0, 4, 0, 16, True) == \
+        {"work_items": 0, "parts": 0, "ordered": 0, "linear": 0, "pair_slices": 0, "fronts": 0}
+    with pytest.raises(kvx.KvxError) as ei:
+        kvx.kvx_copy_walk(c, 0, 4, 10, 24, False)  # not a multiple of the block size
+    assert ei.value.status == kvx.KVX_EINVAL
+    with pytest.raises(kvx.KvxError):
+        kvx.kvx_copy_walk(c, 0, 5, 10, 16, False)  # layer range beyond the cache

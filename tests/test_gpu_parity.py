@@ -301,29 +301,36 @@ def test_ordered_scatter_bit_exact(n, heads):
 # (two halves per XCD range) and of 2 D, the gather of 2 D. (Scatters of slabs
 # of at most 8 KiB in the default layout walk the image instead.)
 PAIRED = [
-    # (layers, NB, BS, heads, dim, elem, l0, l1, n, chunk_tokens): pairing taken
-    (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 256),    # 32 KiB slabs x 16 blocks: D = 4, both
-    (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 1024),   # x 64 blocks: D = 1, both
-    (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 512),    # x 32 blocks: D = 2, both
-    (40, 2100, 16, 2, 128, 2, 0, 40, 1030, 1024), # 8 KiB x 64: gather D = 4; linear scatter
-    (40, 2100, 16, 4, 128, 2, 0, 40, 1030, 1024), # 16 KiB x 64: D = 2; 80 slices, 10 per XCD
-    (12, 2300, 16, 8, 128, 2, 2, 10, 1100, 256),  # a partial layer range: 16 slices, D = 4
-    (12, 2300, 16, 8, 128, 2, 0, 12, 1100, 256),  # 24 slices: gather paired, scatter one front
-    (10, 2300, 16, 8, 128, 2, 0, 10, 1100, 256),  # 20 slices: neither
-    (8, 2300, 16, 8, 128, 2, 0, 8, 1100, 128),    # 32 KiB x 8 blocks: D = 8, both
-    (16, 2300, 16, 8, 128, 2, 0, 16, 1101, 64),   # x 4 blocks: D = 16, both; ragged last chunk
-    (16, 2300, 16, 4, 128, 2, 0, 16, 1100, 256),  # 16 KiB x 16 blocks: D = 8, both
-    (4, 2300, 16, 8, 128, 2, 0, 4, 1100, 64),     # D = 16 but 8 slices: neither
-    (32, 2300, 16, 1, 128, 2, 0, 32, 1100, 256),  # 4 KiB x 16 blocks: D = 32, gather; linear scatter
-    (16, 2300, 16, 2, 128, 2, 0, 16, 1103, 256),  # 8 KiB x 16 blocks: D = 16, gather; linear scatter
-    (24, 2300, 16, 1, 128, 2, 0, 24, 1100, 256),  # D = 32 but 48 slices: neither
+    # (layers, NB, BS, heads, dim, elem, l0, l1, n, chunk_tokens), then the walks taken:
+    # gather pair distance D, scatter (ordered, linear, fronts' D, fronts)
+    ((8, 2300, 16, 8, 128, 2, 0, 8, 1100, 256), 4, (1, 0, 4, 2)),    # 32 KiB slabs x 16 blocks
+    ((8, 2300, 16, 8, 128, 2, 0, 8, 1100, 1024), 1, (1, 0, 1, 2)),   # x 64 blocks
+    ((8, 2300, 16, 8, 128, 2, 0, 8, 1100, 512), 2, (1, 0, 2, 2)),    # x 32 blocks
+    ((40, 2100, 16, 2, 128, 2, 0, 40, 1030, 1024), 4, (0, 1, 0, 1)), # 8 KiB x 64: linear scatter
+    ((40, 2100, 16, 4, 128, 2, 0, 40, 1030, 1024), 2, (1, 0, 2, 2)), # 16 KiB x 64: 10 slices per XCD
+    ((12, 2300, 16, 8, 128, 2, 2, 10, 1100, 256), 4, (1, 0, 4, 2)),  # a partial layer range: 16 slices
+    ((12, 2300, 16, 8, 128, 2, 0, 12, 1100, 256), 4, (1, 0, 0, 1)),  # 24 slices: scatter one front
+    ((10, 2300, 16, 8, 128, 2, 0, 10, 1100, 256), 0, (1, 0, 0, 1)),  # 20 slices: neither paired
+    ((8, 2300, 16, 8, 128, 2, 0, 8, 1100, 128), 8, (1, 0, 8, 2)),    # 32 KiB x 8 blocks
+    ((16, 2300, 16, 8, 128, 2, 0, 16, 1101, 64), 16, (1, 0, 16, 2)), # x 4 blocks; ragged last chunk
+    ((16, 2300, 16, 4, 128, 2, 0, 16, 1100, 256), 8, (1, 0, 8, 2)),  # 16 KiB x 16 blocks
+    ((4, 2300, 16, 8, 128, 2, 0, 4, 1100, 64), 0, (1, 0, 0, 1)),     # D = 16 but 8 slices
+    ((32, 2300, 16, 1, 128, 2, 0, 32, 1100, 256), 32, (0, 1, 0, 1)), # 4 KiB x 16 blocks
+    ((16, 2300, 16, 2, 128, 2, 0, 16, 1103, 256), 16, (0, 1, 0, 1)), # 8 KiB x 16 blocks; ragged
+    ((24, 2300, 16, 1, 128, 2, 0, 24, 1100, 256), 0, (0, 1, 0, 1)),  # D = 32 but 48 slices
 ]
 
 
-@pytest.mark.parametrize("case", PAIRED, ids=[f"p{i}" for i in range(len(PAIRED))])
-def test_paired_walks_bit_exact(case):
+@pytest.mark.parametrize("case,gather_d,scatter_walk", PAIRED,
+                         ids=[f"p{i}" for i in range(len(PAIRED))])
+def test_paired_walks_bit_exact(case, gather_d, scatter_walk):
     L, NB, BS, H, D, e, l0, l1, n, ct = case
     s = oracle.Shape(L, NB, BS, H, D, e)
+    # the geometry takes the walk it is here for (kvx_copy_walk reports the launcher's choice)
+    c = kvx.shape_only_cache(L, NB, BS, H, D, e)
+    assert kvx.kvx_copy_walk(c, l0, l1, n, ct, True)["pair_slices"] == gather_d
+    w = kvx.kvx_copy_walk(c, l0, l1, n, ct, False)
+    assert (w["ordered"], w["linear"], w["pair_slices"], w["fronts"]) == scatter_walk
     seed = 300 + L + ct
     bt_src, bt_dst = seeded_ids(seed, NB, n, n)
     cache = device_cache(s, SRC(seed, kvsynth.MODE_RAW), DEV)

@@ -25,7 +25,7 @@ pytestmark = pytest.mark.slow
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2609_11744_amd", "csrc")
 HOST_SOURCES = ["kvx_api.cpp", "kvx_gate.cpp", "kvx_io.cpp", "kvx_plan.cpp", "kvx_preload.cpp",
-                "kvx_ring.cpp"]
+                "kvx_ring.cpp", "kvx_walk.cpp"]
 INC = ["-D__HIP_PLATFORM_AMD__", "-I/opt/rocm/include", "-I" + os.path.join(ROOT, "include"),
        "-I" + CSRC]
 ASAN = ["-O1", "-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined",
