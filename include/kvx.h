@@ -260,7 +260,8 @@ const char* kvx_strerror(kvx_status status);
  * bytes) hold the packed image of blocks block_table[bt_first ..
  * bt_first + n_blocks) over layers [l_begin, l_end) with chunk size
  * chunk_tokens (a piece is either a run of whole chunks or a layer range of
- * one chunk). */
+ * one chunk). chunk_tokens is the call's, or the prefix's length where the
+ * prefix is shorter than one chunk (the two images are the same bytes). */
 typedef struct kvx_piece {
   int64_t src_offset;
   int64_t bytes;

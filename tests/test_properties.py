@@ -1,0 +1,197 @@
+"""Property-based checks of the library's host logic on random shapes (CPU):
+
+  * the ring's piece planner tiles a packed image exactly once, within each
+    piece's size limit, in chunk order, for every ramp, and scattering the
+    pieces one by one equals the oracle's scatter of the whole image;
+  * the walk a gather or scatter takes (kvx_copy_walk) keeps the invariants its
+    kernels rely on: work items = units x parts, 2 MiB pairs whose slice count
+    divides evenly, destination order only for large multi-block scatters and
+    never together with the linear walk;
+  * the library's step plan equals the oracle's exact-key plan on random prefix
+    trees whose shared prefixes end anywhere, at random residency and gates.
+"""
+import numpy as np
+import pytest
+
+hypothesis = pytest.importorskip("hypothesis")
+from hypothesis import HealthCheck, given, settings, strategies as st  # noqa: E402
+
+import kvsynth  # noqa: E402
+import oracle  # noqa: E402
+import oracle.prefix as op  # noqa: E402
+import paper_2609_11744_amd as kvx  # noqa: E402
+from test_step_plan import _exact_of_hash, _library_plan  # noqa: E402
+
+SETTINGS = dict(deadline=None, derandomize=True, database=None,
+                suppress_health_check=[HealthCheck.too_slow, HealthCheck.data_too_large])
+
+
+# ---- piece planner ---------------------------------------------------------------
+
+@st.composite
+def plans(draw):
+    L = draw(st.integers(1, 8))
+    H = draw(st.integers(1, 3))
+    D = draw(st.sampled_from([8, 16, 32]))
+    BS = draw(st.integers(1, 8))
+    n = draw(st.integers(1, 90))
+    bpc = draw(st.integers(1, 12))
+    layer = min(bpc, n) * 2 * BS * H * D * 2  # one layer of a full chunk
+    slot = layer * draw(st.integers(1, 3 * L + 2)) + draw(st.integers(0, layer - 1))
+    ramp = draw(st.sampled_from([kvx.KVX_RAMP_NONE, kvx.KVX_RAMP_FIRST, kvx.KVX_RAMP_LAST]))
+    return L, H, D, BS, n, bpc * BS, slot, ramp
+
+
+def _caps(n_pieces, slot, ramp):
+    caps = [slot] * n_pieces
+    first = [slot >> 3, slot >> 2, slot >> 1]
+    for k in range(min(3, n_pieces)):
+        if ramp == kvx.KVX_RAMP_FIRST:
+            caps[k] = first[k]
+        elif ramp == kvx.KVX_RAMP_LAST:
+            caps[n_pieces - 1 - k] = first[k]
+    return caps
+
+
+@settings(max_examples=150, **SETTINGS)
+@given(plans())
+def test_pieces_tile_the_image_within_limits(case):
+    L, H, D, BS, n, ct, slot, ramp = case
+    slab = BS * H * D * 2
+    c = kvx.shape_only_cache(L, n + 1, BS, H, D, 2)
+    pieces = kvx.kvx_plan_pieces(c, 0, L, n, ct, slot, ramp)
+    bpc = ct // BS
+    layer = min(bpc, n) * 2 * slab
+    spans = []
+    for p, cap in zip(pieces, _caps(len(pieces), slot, ramp)):
+        lr = p["l_end"] - p["l_begin"]
+        assert 0 <= p["l_begin"] < p["l_end"] <= L
+        assert p["bytes"] == p["n_blocks"] * lr * 2 * slab > 0
+        assert p["bytes"] <= max(cap, layer if lr == 1 else 0)
+        assert p["bt_first"] % bpc == 0 and p["bt_first"] + p["n_blocks"] <= n
+        assert p["chunk_tokens"] == min(bpc, n) * BS  # a chunk past the prefix is the prefix
+        spans.append((p["src_offset"], p["bytes"]))
+    at = 0
+    for off, b in sorted(spans):
+        assert off == at
+        at += b
+    assert at == kvx.kvx_packed_bytes(c, 0, L, n)
+    if ramp != kvx.KVX_RAMP_LAST:  # the restore's pieces run front to back
+        assert spans == sorted(spans)
+
+
+@settings(max_examples=40, **SETTINGS)
+@given(plans(), st.integers(0, 2**31 - 1))
+def test_scattering_the_pieces_equals_scattering_the_image(case, seed):
+    L, H, D, BS, n, ct, slot, ramp = case
+    NB = 2 * n + 3
+    s = oracle.Shape(L, NB, BS, H, D, 2)
+    c = kvx.shape_only_cache(L, NB, BS, H, D, 2)
+    bt = np.random.default_rng(seed).permutation(NB)[:n].astype(np.int32)
+    img = kvsynth.host_bytes(oracle.packed_bytes(s, 0, L, n), seed % 1000, 7, mode=kvsynth.MODE_RAW)
+    whole = oracle.new_mirror(s)
+    oracle.scatter(s, *whole, 0, L, bt, ct, img)
+    by_piece = oracle.new_mirror(s)
+    for p in kvx.kvx_plan_pieces(c, 0, L, n, ct, slot, ramp):
+        oracle.scatter(s, *by_piece, p["l_begin"], p["l_end"],
+                       bt[p["bt_first"]:p["bt_first"] + p["n_blocks"]], p["chunk_tokens"],
+                       img[p["src_offset"]:p["src_offset"] + p["bytes"]])
+    for a, b in zip(whole[0] + whole[1], by_piece[0] + by_piece[1]):
+        assert np.array_equal(a, b)
+
+
+# ---- the walk of a copy ----------------------------------------------------------
+
+@st.composite
+def walks(draw):
+    layout = draw(st.sampled_from([kvx.KVX_LAYOUT_NHD, kvx.KVX_LAYOUT_HND,
+                                   kvx.KVX_LAYOUT_PAGED_ATTN]))
+    BS = draw(st.sampled_from([1, 4, 8, 16, 32]))
+    H = draw(st.integers(1, 16))
+    D = draw(st.sampled_from([64, 128, 256]))
+    if layout != kvx.KVX_LAYOUT_NHD:
+        D = 64 if BS * H * D * 2 > 48 * 1024 else D
+        H = max(1, min(H, (48 * 1024) // (BS * D * 2)))
+    L = draw(st.integers(1, 128))
+    l0 = draw(st.integers(0, L - 1))
+    l1 = draw(st.integers(l0 + 1, L))
+    n = draw(st.integers(1, 40000))
+    bpc = draw(st.sampled_from([1, 2, 4, 8, 16, 32, 64, 3, 5]))
+    to_packed = draw(st.booleans())
+    return layout, L, l0, l1, BS, H, D, n, bpc * BS, to_packed
+
+
+@settings(max_examples=400, **SETTINGS)
+@given(walks())
+def test_walk_invariants(case):
+    layout, L, l0, l1, BS, H, D, n, ct, to_packed = case
+    slab = BS * H * D * 2
+    parts = (slab + 4095) // 4096 if layout == kvx.KVX_LAYOUT_NHD else H
+    if n * (l1 - l0) * 2 * parts > 2**31 - 1:
+        return  # beyond one call's work-item range
+    c = kvx.shape_only_cache(L, n + 1, BS, H, D, 2, layout)
+    w = kvx.kvx_copy_walk(c, l0, l1, n, ct, to_packed)
+    assert w["parts"] == parts
+    assert w["work_items"] == n * (l1 - l0) * 2 * parts
+    bpc = min(ct // BS, n)
+    slices = 2 * (l1 - l0)
+    if w["pair_slices"]:
+        D_ = w["pair_slices"]
+        assert D_ & (D_ - 1) == 0 and D_ * bpc * slab == 2 << 20
+        assert slices % (2 * D_) == 0 and parts & (parts - 1) == 0
+    if to_packed:
+        assert (w["ordered"], w["linear"], w["fronts"]) == (0, 0, 1)
+        assert w["pair_slices"] <= 32
+        return
+    assert not (w["ordered"] and w["linear"])
+    if w["ordered"]:
+        assert n >= 1024 and bpc > 1
+    if w["linear"]:
+        assert n >= 1024 and slab <= 8192
+    if not w["ordered"]:
+        assert w["pair_slices"] == 0 and w["fronts"] == 1
+    assert (w["fronts"] == 2) == (w["ordered"] == 1 and w["pair_slices"] > 0)
+    if w["fronts"] == 2:
+        assert slices % 16 == 0 and w["work_items"] <= 1 << 22
+        assert w["pair_slices"] <= (16 if slab > 8192 else 4)
+
+
+# ---- step plan against the oracle ------------------------------------------------
+
+class _Req:
+    def __init__(self, tokens, resident, new_blocks):
+        self.tokens = np.asarray(tokens, dtype=np.int32)
+        self.resident = resident
+        self.new_blocks = new_blocks
+
+
+@st.composite
+def steps(draw):
+    bs = draw(st.sampled_from([1, 2, 4, 16]))
+    bpc = draw(st.sampled_from([1, 2, 3, 4, 16]))
+    n_req = draw(st.integers(1, 12))
+    fresh = iter(range(1, 10**9))
+    toks = []
+    reqs = []
+    for r in range(n_req):
+        parent = draw(st.integers(-1, r - 1)) if r else -1
+        shared = draw(st.integers(0, len(toks[parent]) // bs)) * bs if parent >= 0 else 0
+        extra = draw(st.integers(0 if shared else 1, 3 * bpc + 2)) * bs
+        t = (toks[parent][:shared] if parent >= 0 else []) + [next(fresh) for _ in range(extra)]
+        toks.append(t)
+        n_chunks = -(-(len(t) // bs) // bpc)
+        resident = [draw(st.booleans()) for _ in range(n_chunks)]
+        reqs.append(_Req(t, resident, draw(st.integers(0, 2 * bpc + 1))))
+    gate = draw(st.integers(0, 4 * bpc * bs + 1))
+    return reqs, bs, bpc * bs, gate
+
+
+@settings(max_examples=150, **SETTINGS)
+@given(steps())
+def test_library_step_plan_equals_oracle(case):
+    reqs, bs, ct, gate = case
+    exact = _exact_of_hash(reqs, bs, ct)
+    want = op.plan_step(reqs, bs, ct, gate)
+    got = _library_plan(reqs, bs, ct, gate)
+    got["restore"] = [(exact[k], nb, o, bt) for k, nb, o, bt in got["restore"]]
+    assert got == want
