@@ -696,8 +696,8 @@ def cpu_baseline(args, L, BS, H, D, E, perm):
         one(0, m)
         times1.append(time.perf_counter() - t0)
     # every core of the process's affinity mask, unless OMP_NUM_THREADS says
-    # the process's CPU share is smaller (on the GPU machine it is set to the one
-    # GPU's share of the host, 16 threads)
+    # the process's CPU share is smaller (on a machine shared by several GPUs it
+    # is set to one GPU's share of the host, 16 threads)
     affinity = len(os.sched_getaffinity(0))
     share = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
     cores = max(1, min(affinity, share) if share > 0 else affinity)

@@ -742,7 +742,7 @@ inline size_t lds_bytes(int layout, const SlabGeom& sg, bool to_packed) {
 // head fits, else kVecPerThread. A paged-attention scatter of such a head runs
 // on half as many threads with two vectors each: twice as many of its
 // workgroups fit a compute unit, which keeps more loads in flight across its
-// LDS phases (71.6 % of peak against 68.9 % on the 80k workload, same box; the
+// LDS phases (71.6 % of peak against 68.9 % on the 80k workload, same machine; the
 // gather and the HND layout were no faster that way). PREFIX is the kernel's
 // parenthesized leading template arguments; kToPacked is the enclosing
 // launcher's direction.

@@ -14,7 +14,7 @@ typedef unsigned int v4u __attribute__((ext_vector_type(4)));
 // sc1, which together stream the line to memory at device scope. On the 80k
 // gather and scatter patterns this measured 78.8 % and 74.0 % of the 8 TB/s
 // peak against 77.0 % and 72.6 % with the plain non-temporal store (same
-// kernel shape, same box); the load's policy bits made no difference.
+// kernel shape, same machine); the load's policy bits made no difference.
 constexpr int kStorePolicy = 2 | 16;
 
 // Buffer-resource word 3 of a raw (untyped, unswizzled) buffer on gfx9-family

@@ -61,8 +61,8 @@ bool scatter_in_destination_order(int64_t n_blocks, int64_t bpc, int64_t slab, i
 // 0.9-2.0 with 64-block chunks (D = 1), and lost 0.6-1.1 with 4-block chunks
 // (D = 16); pairs at any other distance (32 KiB to 64 MiB) lost 0.5-2 points
 // to one front in all but one process. In the library, alternated on three
-// boxes: the 80k scatter (D = 4) 75.1-75.6 % of peak against 72.7-72.9 %,
-// 80.5-83.0 % against 78.9-80.5 % on two faster boxes; the 32k scatter with
+// machines: the 80k scatter (D = 4) 75.1-75.6 % of peak against 72.7-72.9 %,
+// 80.5-83.0 % against 78.9-80.5 % on two faster machines; the 32k scatter with
 // 256-token chunks 72.6-72.8 % against 69.5-70.5 %. Why 2 MiB is the
 // distance that pays is not established: it depends on how the chip maps
 // physical addresses to memory channels, which these kernels do not see.

@@ -93,7 +93,7 @@ def test_asan_ubsan_host_builds(tmp_path):
              "tests/test_kvtest_util.py"]
     r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-m", "not gpu",
                         "-p", "no:cacheprovider", *tests,
-                        # kvx_probe_stream is a stub in this build
+                        # kvx_probe_stream is a stub in the host-only library
                         "--deselect", "tests/test_abi.py::test_probe_rejects_bad_arguments_on_the_host"],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=900)
     assert r.returncode == 0, f"tests under ASan/UBSan failed:\n{r.stdout[-4000:]}\n{r.stderr[-4000:]}"
