@@ -137,8 +137,10 @@ int64_t kvx_chunk_stride(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t
  * n_blocks == 0 or l0 == l1 is a no-op returning KVX_OK.
  * Errors: KVX_EINVAL for a null or misaligned pointer, l0 < 0, l1 < l0,
  * l1 > num_layers, l1 - l0 > KVX_MAX_LAYERS, chunk_tokens not a positive
- * multiple of block_size, slab not a multiple of 16 bytes, or dst overlapping
- * the cache; KVX_EHIP if the launch fails. Bad block ids: see kvx_check. */
+ * multiple of block_size, slab not a multiple of 16 bytes, dst overlapping
+ * the cache, or a call of more than 2^31 - 1 slabs or workgroups (slabs x
+ * parts per slab: its 4 KiB pieces with the default layout, its heads with
+ * the others); KVX_EHIP if the launch fails. Bad block ids: see kvx_check. */
 kvx_status kvx_gather_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
                              const int32_t* block_table, int32_t n_blocks, int32_t chunk_tokens,
                              void* dst, hipStream_t stream);

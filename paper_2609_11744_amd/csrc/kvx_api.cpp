@@ -43,6 +43,11 @@ kvx_status validate(const kvx_cache* c, int32_t l0, int32_t l1, int32_t n_blocks
   const int64_t lr = l1 - l0;
   const int64_t n_units = lr * 2 * (int64_t)n_blocks;
   if (n_units > INT32_MAX) return KVX_EINVAL;
+  // one workgroup per part of a slab (4 KiB pieces with the default layout,
+  // heads with the others): the launch counts them in 31 bits
+  const int64_t parts = c->layout == KVX_LAYOUT_NHD ? (slab / 16 + kPartThreads - 1) / kPartThreads
+                                                    : (int64_t)c->num_kv_heads;
+  if (n_units * parts > INT32_MAX) return KVX_EINVAL;
   int64_t packed = 0;
   if (!mul_ok(n_units, slab, &packed)) return KVX_EINVAL;
   if (need_pointers && n_units > 0) {
@@ -113,7 +118,10 @@ static kvx_status chunks_entry(bool to_packed, const kvx_cache* cache, int32_t l
     if (((uintptr_t)cache->k[l] | (uintptr_t)cache->v[l]) & 15) return KVX_EINVAL;
   }
   const int64_t units = (int64_t)n_chunks * (l1 - l0) * 2 * (chunk_tokens / cache->block_size);
-  if (units > INT32_MAX) return KVX_EINVAL;
+  const int64_t parts = cache->layout == KVX_LAYOUT_NHD
+                            ? (g.slab / 16 + kPartThreads - 1) / kPartThreads
+                            : (int64_t)cache->num_kv_heads;
+  if (units > INT32_MAX || units * parts > INT32_MAX) return KVX_EINVAL;
   if (overlaps_cache(cache, l0, l1, packed, packed_bytes)) return KVX_EINVAL;
   return launch_copy_chunks(to_packed, cache, l0, l1, block_table, table_len, chunks, n_chunks,
                             chunk_tokens, const_cast<void*>(packed), packed_bytes, stream,

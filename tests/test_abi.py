@@ -315,3 +315,17 @@ def test_copy_walk_empty_and_invalid():
     assert ei.value.status == kvx.KVX_EINVAL
     with pytest.raises(kvx.KvxError):
         kvx.kvx_copy_walk(c, 0, 5, 10, 16, False)  # layer range beyond the cache
+
+
+def test_calls_beyond_the_workgroup_range_are_invalid():
+    """A call's workgroups (slabs x parts per slab) are counted in 31 bits: one
+    more is rejected on the host as an invalid argument, not launched."""
+    c = kvx.shape_only_cache(128, 16, 16, 64, 64, 2)  # 128 KiB slabs: 32 parts each
+    n_ok = (2**31 - 1) // (256 * 32)                    # 128 layers x K|V = 256 slabs per block
+    assert kvx.kvx_copy_walk(c, 0, 128, n_ok, 16, True)["work_items"] == n_ok * 256 * 32
+    for fn in (lambda n: kvx.kvx_copy_walk(c, 0, 128, n, 16, True),
+               lambda n: kvx.kvx_copy_walk(c, 0, 128, n, 16, False)):
+        with pytest.raises(kvx.KvxError) as ei:
+            fn(n_ok + 1)
+        assert ei.value.status == kvx.KVX_EINVAL
+    assert kvx.kvx_packed_bytes(c, 0, 128, n_ok + 1) == -1
