@@ -315,6 +315,11 @@ def test_copy_walk_empty_and_invalid():
     assert ei.value.status == kvx.KVX_EINVAL
     with pytest.raises(kvx.KvxError):
         kvx.kvx_copy_walk(c, 0, 5, 10, 16, False)  # layer range beyond the cache
+    lib = _native.lib()
+    w = _native.KvxWalk()
+    assert lib.kvx_copy_walk(ctypes.byref(c), 0, 4, 10, 16, 2, ctypes.byref(w)) == kvx.KVX_EINVAL
+    assert lib.kvx_copy_walk(ctypes.byref(c), 0, 4, 10, 16, 1, None) == kvx.KVX_EINVAL
+    assert lib.kvx_copy_walk(None, 0, 4, 10, 16, 1, ctypes.byref(w)) == kvx.KVX_EINVAL
 
 
 def test_calls_beyond_the_workgroup_range_are_invalid():
