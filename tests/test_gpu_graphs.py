@@ -1,8 +1,10 @@
 """The copy kernels under HIP graph capture: a gather + scatter + chunk-list
 gather step (sizes that take no scratch allocation: scatters below the
-destination-ordering threshold) captured once and replayed several times,
-with eager work and synchronizations between replays, and every replay
-checked bit-exact against the oracle of what it computes."""
+destination-ordering threshold), and a destination-ordered scatter through
+kvx_scatter_blocks_noalloc (its order table in the library's fixed array),
+each captured once and replayed several times with eager work and
+synchronizations between replays, and every replay checked bit-exact against
+the oracle of what it computes."""
 import numpy as np
 import pytest
 
@@ -65,3 +67,53 @@ def test_captured_step_replays_bit_exact():
         for l in range(L):
             assert np.array_equal(to_host(cache.k[l]), m[0][l]), f"replay {rep}: K layer {l}"
             assert np.array_equal(to_host(cache.v[l]), m[1][l]), f"replay {rep}: V layer {l}"
+
+
+def test_captured_noalloc_ordered_scatter_replays_bit_exact():
+    """kvx_scatter_blocks_noalloc under graph capture: a scatter large enough to
+    run in destination order (its order table in the library's fixed array,
+    nothing allocated), captured once and replayed with a new packed image
+    loaded into the same buffer before each replay; every replay against the
+    oracle's scatter of that image."""
+    import ctypes
+
+    from paper_2609_11744_amd import _native
+
+    s = oracle.Shape(2, 4000, 16, 8, 64, 2)  # 16 KiB slabs
+    n, ct, L = 1500, 64, 2
+    seed = 73
+    assert kvx.kvx_copy_walk(kvx.shape_only_cache(2, 4000, 16, 8, 64, 2), 0, L, n, ct,
+                             False)["ordered"] == 1
+    (bt_dst,) = seeded_ids(seed, s.num_blocks, n)
+    fill = Filled(seed, kvsynth.ROLE_DST, kvsynth.MODE_RAW)
+    cache = device_cache(s, fill, DEV)
+    mirror = host_mirror(s, fill, range(s.num_blocks))
+    t_dst = torch.from_numpy(bt_dst.astype(np.int32)).to(DEV)
+    nbytes = oracle.packed_bytes(s, 0, L, n)
+    packed = torch.empty(nbytes, dtype=torch.uint8, device=DEV)
+    lib = _native.lib()
+
+    def step():
+        st = lib.kvx_scatter_blocks_noalloc(ctypes.byref(cache.c_struct()), 0, L, t_dst.data_ptr(), n,
+                                            ct, packed.data_ptr(),
+                                            torch.cuda.current_stream().cuda_stream)
+        assert st == kvx.KVX_OK
+
+    packed.copy_(torch.from_numpy(kvsynth.host_bytes(nbytes, seed, 500, mode=kvsynth.MODE_RAW)))
+    step()  # eager first: the scratch array's address is resolved outside the capture
+    torch.cuda.synchronize()
+    kvx.kvx_check()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    for rep in range(4):
+        img = kvsynth.host_bytes(nbytes, seed, 501 + rep, mode=kvsynth.MODE_RAW)
+        packed.copy_(torch.from_numpy(img))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        kvx.kvx_check()
+        oracle.scatter(s, *mirror, 0, L, bt_dst, ct, img)
+        for l in range(L):
+            assert np.array_equal(to_host(cache.k[l]), mirror[0][l]), f"replay {rep}: K layer {l}"
+            assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"replay {rep}: V layer {l}"
