@@ -204,6 +204,10 @@ def hold_stream():
     0.46 ms one-head shard gather."""
     import torch
 
+    sleep = getattr(torch.cuda, "_sleep", None)
+    if sleep is None:  # no spin kernel in this torch: calls are timed from idle
+        _HOLD["cycles"] = 0
+        return
     if _HOLD["cycles"] is None:
         torch.cuda._sleep(1000)
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -377,9 +381,11 @@ def run_80k(args):
         "scatter_ms": round(mean_s, 4),
         "gather_ms_stats": ms_stats(rec["gather_ms"]),
         "scatter_ms_stats": ms_stats(rec["scatter_ms"]),
-        "timing": f"device time of each call: HIP events on its stream, the call enqueued "
-                  f"behind a {HOLD_US:.0f} us spin kernel so that its host-side launch is "
-                  f"not counted; launch_inclusive: the same calls timed from an idle GPU",
+        "timing": (f"device time of each call: HIP events on its stream, the call enqueued "
+                   f"behind a {HOLD_US:.0f} us spin kernel so that its host-side launch is "
+                   f"not counted; launch_inclusive: the same calls timed from an idle GPU"
+                   if _HOLD["cycles"] else "HIP events on each call's stream from an idle GPU "
+                   "(no spin kernel in this torch): the host-side launch is counted"),
         "launch_inclusive": {"gather_ms": ms_stats(launch_g), "scatter_ms": ms_stats(launch_s)},
         "walks": {"gather": kvx.kvx_copy_walk(cache, 0, L, n, ct, True),
                   "scatter": kvx.kvx_copy_walk(cache, 0, L, n, ct, False)},
