@@ -55,13 +55,13 @@ KERNELS_SRC = [os.path.join(ROOT, "paper_2609_11744_amd", "csrc", f)
 # only for the kernel code they were taken on (kernels_sha256 below); otherwise the
 # bench reports traffic as null.
 GATHER_TRAFFIC = {
-    "kernels_sha256": "a6c713560f24862291985b5983b8410eccc9b3c6f9b6e7d2a02f8de45cf853d0",
+    "kernels_sha256": "96ab12857d16c71ee4cd3fc6458b23157b570131f84e23a98ea96daadf762bfa",
     # cache layout -> (fetched, written) HBM bytes of the timed gather launch
     # at the default 80k-token workload: FETCH_SIZE KiB x 1.999988 (copy
     # calibration), WRITE_SIZE KiB x 1.0
-    "nhd": (10488806774, 10485760000),         # 5,121,519.1 / 10,240,000.0 KiB
-    "paged_attn": (10488988105, 10485760000),  # 5,121,606.8 / 10,240,000.0 KiB
-    "hnd": (10488852824, 10485760000),         # 5,121,541.0 / 10,240,000.0 KiB
+    "nhd": (10488814621, 10485760000),         # 5,121,521.1 / 10,240,000.0 KiB
+    "paged_attn": (10488986766, 10485760000),  # 5,121,604.9 / 10,240,000.0 KiB
+    "hnd": (10488843210, 10485760000),         # 5,121,536.0 / 10,240,000.0 KiB
 }
 
 

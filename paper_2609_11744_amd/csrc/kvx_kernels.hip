@@ -738,11 +738,22 @@ inline size_t lds_bytes(int layout, const SlabGeom& sg, bool to_packed) {
 // one head per workgroup of 256 threads (paged attention through LDS).
 #define KVX_UNPAREN(...) __VA_ARGS__
 
+// Whether a paged-attention scatter of heads that fit one vector per thread
+// runs them on half as many threads with two vectors each. Twice as many of
+// its workgroups then fit a compute unit, which keeps more loads in flight
+// across its LDS phases. Measured over 12-18 (cache, packed buffer)
+// allocation pairs in one process at the 80k prefix of the 8B shape, against
+// one vector on each of 256 threads: 81.2 against 78.9 % of peak with 8
+// heads, level with 4 (75.3 / 75.2 %), 69.4 against 69.9 % with 2 and, with
+// the linear walk a one-head scatter takes (kvx_walk.cpp), 69.6 against
+// 73.2 % with 1. So only slabs of four heads or more take it.
+inline bool pa_scatter_on_half_threads(const SlabGeom& sg) {
+  return sg.nh <= (uint32_t)kTransposeThreads && sg.prow >= 4u * sg.v16.d;
+}
+
 // One head per workgroup of kTransposeThreads: one vector per thread when the
-// head fits, else kVecPerThread. A paged-attention scatter of such a head runs
-// on half as many threads with two vectors each: twice as many of its
-// workgroups fit a compute unit, which keeps more loads in flight across its
-// LDS phases (71.6 % of peak against 68.9 % on the 80k workload, same machine; the
+// head fits, else kVecPerThread; a paged-attention scatter of four or more
+// such heads per slab on half the threads (pa_scatter_on_half_threads; the
 // gather and the HND layout were no faster that way). PREFIX is the kernel's
 // parenthesized leading template arguments; kToPacked is the enclosing
 // launcher's direction.
@@ -750,7 +761,7 @@ inline size_t lds_bytes(int layout, const SlabGeom& sg, bool to_packed) {
   do {                                                                                 \
     const dim3 tb(kTransposeThreads);                                                  \
     if constexpr (LAYOUT == KVX_LAYOUT_PAGED_ATTN && !kToPacked) {                     \
-      if (sg.nh <= (uint32_t)kTransposeThreads) {                                      \
+      if (pa_scatter_on_half_threads(sg)) {                                            \
         hipLaunchKernelGGL(                                                            \
             (KERNEL<KVX_UNPAREN PREFIX, LAYOUT, ELEM, kTransposeThreads / 2, 2>), grid, \
             dim3(kTransposeThreads / 2), lds_bytes(layout, sg, kToPacked), stream, __VA_ARGS__);  \

@@ -26,11 +26,14 @@ namespace {
 // 32 KiB 71.1 against 75.3 % (image order with XCD ranges: 69.3 / 69.1 % at 4
 // and 8 KiB). An HND cache with one KV head is the default layout byte for
 // byte, and measured the same way (4 KiB slabs: 73.7 against 70.4 %); with
-// two heads in 8 KiB it lost 1.8 points, and the paged-attention layout was
-// level at 4 KiB and 2.6 points slower at 8 KiB, so those keep destination
-// order.
+// two heads in 8 KiB it lost 1.8 points, so it keeps destination order. The
+// paged-attention layout with one head takes the linear walk too, with its
+// heads on 256 threads (kvx_kernels.hip): over 18 allocation pairs 73.2 %
+// against 68.3 % for destination order on 128 threads, and about 1 point
+// with either change alone; with two heads the linear walk lost 0.2 points.
 bool scatter_linear(int64_t n_blocks, int64_t slab, int layout, int32_t heads) {
-  const bool rows = layout == KVX_LAYOUT_NHD || (layout == KVX_LAYOUT_HND && heads == 1);
+  const bool rows = layout == KVX_LAYOUT_NHD ||
+                    ((layout == KVX_LAYOUT_HND || layout == KVX_LAYOUT_PAGED_ATTN) && heads == 1);
   return rows && n_blocks >= kOrderedScatterMinBlocks && slab <= 8192;
 }
 

@@ -288,7 +288,8 @@ WALKS = [
     ((32, 4, 0, 5000, 256, False), (4, 1, 0, 8, 2)),    # 16 KiB slabs: fronts 8 apart
     ((32, 1, HND_, 5000, 256, False), (1, 0, 1, 0, 1)), # one-head HND = the default layout
     ((32, 2, HND_, 5000, 256, False), (2, 1, 0, 0, 1)), # two heads: ordered, D = 16 > 4
-    ((32, 1, PA_, 5000, 256, False), (1, 1, 0, 0, 1)),  # paged attention keeps the order
+    ((32, 1, PA_, 5000, 256, False), (1, 0, 1, 0, 1)),  # one-head paged attention: linear
+    ((32, 2, PA_, 5000, 256, False), (2, 1, 0, 0, 1)),  # two heads keep destination order
     ((32, 8, PA_, 5000, 256, True), (8, 0, 0, 4, 1)),
     ((80, 8, 0, 3000, 256, False), (8, 1, 0, 4, 2)),    # 70B shape: 160 slices
     ((80, 8, 0, 4000, 256, False), (8, 1, 0, 0, 1)),    # over 2^22 work items: one front

@@ -82,15 +82,21 @@ def test_layout_gather_scatter_bit_exact(case):
         assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
 
 
-@pytest.mark.parametrize("layout,heads,dim", [(HND, 2, 64), (PA, 2, 64), (HND, 1, 128)],
-                         ids=["hnd", "paged_attn", "hnd_one_head"])
+@pytest.mark.parametrize("layout,heads,dim", [(HND, 2, 64), (PA, 2, 64), (HND, 1, 128),
+                                              (PA, 1, 128), (PA, 4, 32)],
+                         ids=["hnd", "paged_attn", "hnd_one_head", "paged_attn_one_head",
+                              "paged_attn_four_heads"])
 def test_layout_ordered_scatter_and_chunk_lists(layout, heads, dim):
-    """Large scatters (>= 1024 blocks: destination order, or with one head in
-    HND the default layout's linear image-order walk) and the chunk-list path
-    (ring restore and offload) in a reordering layout."""
+    """Large scatters (>= 1024 blocks: destination order, or with one head
+    the default layout's linear image-order walk; paged-attention heads on 256
+    threads, or on 128 threads x 2 vectors with four heads or more) and the
+    chunk-list path (ring restore and offload) in a reordering layout."""
     s = oracle.Shape(2, 4000, 16, heads, dim, 2, layout)
     n = 1300
     seed = 210 + layout + heads
+    walk = kvx.kvx_copy_walk(kvx.shape_only_cache(2, 4000, 16, heads, dim, 2, layout), 0, 2, n,
+                             64, False)
+    assert (walk["ordered"], walk["linear"]) == ((0, 1) if heads == 1 else (1, 0))
     bt_src, bt_dst = seeded_ids(seed, s.num_blocks, n, n)
     fill = Filled(seed, kvsynth.ROLE_SRC, kvsynth.MODE_RAW)
     cache = device_cache(s, fill, DEV)
