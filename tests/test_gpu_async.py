@@ -189,6 +189,43 @@ def test_abort_during_async_restore():
         ring.close()
 
 
+def test_destroy_with_an_async_restore_running():
+    """kvx_ring_destroy while a restore started by kvx_restore_begin runs: it
+    waits for the transfer (the ring's thread, its copies and its stream),
+    then frees the ring; the cache then holds the oracle's restore of the
+    image, every other block unchanged."""
+    import threading
+
+    s = oracle.Shape(2, 3000, 16, 2, 64, 2)
+    n = 1200
+    (bt,) = seeded_ids(79, s.num_blocks, n)
+    fill = Filled(79, kvsynth.ROLE_DST)
+    cache = device_cache(s, fill, DEV)
+    mirror = host_mirror(s, fill, range(s.num_blocks))
+    src, img = _image(oracle.packed_bytes(s, 0, 2, n), 79, pinned=False)
+    ring = kvx.StagingRing(DEV, 2, 64 << 10)
+    ring.bind(cache, 0, 2, n, 64, src, fill_threads=2)
+    table = _bt(bt)
+    torch.cuda.synchronize()
+    kvx.kvx_restore_begin(ring, table)
+    done = threading.Event()
+
+    def close():
+        ring.close()  # waits for the restore to finish, then frees the ring
+        done.set()
+
+    th = threading.Thread(target=close)
+    th.start()
+    th.join(timeout=60)
+    assert done.is_set()
+    torch.cuda.synchronize()
+    kvx.kvx_check()
+    oracle.restore(s, *mirror, 0, 2, bt, 64, img)
+    for l in range(2):
+        assert np.array_equal(to_host(cache.k[l]), mirror[0][l]), f"K layer {l}"
+        assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
+
+
 # ---- error words, one per stream ----------------------------------------------------
 
 def test_error_words_are_per_stream():
