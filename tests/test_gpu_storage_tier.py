@@ -33,20 +33,24 @@ def _chunks(root, n, bpc, tag="m"):
     return out
 
 
+PA, HND = oracle.LAYOUT_PAGED_ATTN, oracle.LAYOUT_HND
 CASES = [
-    # (shape args, n, chunk_tokens, slots, slot_bytes, io_depth, hip_copies)
+    # (shape args, n, chunk_tokens, slots, slot_bytes, io_depth, hip_copies[, (l0, l1)])
     ((4, 400, 16, 2, 64, 2), 150, 64, 2, 256 << 10, 4, False),   # several chunks per slot
     ((4, 400, 16, 2, 64, 2), 150, 64, 3, 48 << 10, 2, False),    # chunks split by layers
     ((4, 400, 16, 2, 64, 2), 150, 64, 2, 256 << 10, 1, True),    # copies through the runtime
     ((3, 300, 5, 2, 16, 2), 70, 15, 2, 64 << 10, 8, False),      # 320-byte slabs: buffered I/O
+    ((4, 400, 16, 2, 64, 2, PA), 150, 64, 2, 64 << 10, 4, False),  # paged-attention cache
+    ((5, 300, 16, 1, 128, 2, HND), 90, 48, 3, 128 << 10, 2, False, (1, 4)),  # HND, layers 1..3
 ]
 
 
 @pytest.mark.parametrize("case", CASES, ids=[f"c{i}" for i in range(len(CASES))])
 def test_offload_to_files_then_restore_from_files(tmp_path, case):
-    shape_args, n, ct, slots, slot_bytes, depth, hip_copies = case
+    shape_args, n, ct, slots, slot_bytes, depth, hip_copies = case[:7]
     s = oracle.Shape(*shape_args)
     L, BS = s.num_layers, s.block_size
+    l0, l1 = case[7] if len(case) > 7 else (0, L)
     seed = 300 + n + depth
     bt_src, bt_dst = seeded_ids(seed, s.num_blocks, n, n)
     fill = Filled(seed, kvsynth.ROLE_NEW, kvsynth.MODE_RAW)
@@ -56,16 +60,16 @@ def test_offload_to_files_then_restore_from_files(tmp_path, case):
     ring = kvx.StagingRing(DEV, slots, slot_bytes)
     try:
         ring.set_test_hooks(hip_copies=hip_copies)
-        ring.bind_offload_files(cache, 0, L, ct, chunks, io_depth=depth)
+        ring.bind_offload_files(cache, l0, l1, ct, chunks, io_depth=depth)
         kvx.kvx_offload_to_staging(ring, _bt(bt_src))
         kvx.kvx_check()
         for path, b0, nb in chunks:  # every file holds its chunk's image, published
-            exp = oracle.gather(s, *mirror, 0, L, bt_src[b0:b0 + nb], ct)
+            exp = oracle.gather(s, *mirror, l0, l1, bt_src[b0:b0 + nb], ct)
             got = np.fromfile(path, dtype=np.uint8)
             assert np.array_equal(got, exp), f"chunk file {path} differs"
         assert not [f for d, _, fs in os.walk(tmp_path) for f in fs if ".tmp." in f]
         # restore the files into fresh blocks
-        ring.bind_files(cache, 0, L, ct, chunks, io_depth=depth)
+        ring.bind_files(cache, l0, l1, ct, chunks, io_depth=depth)
         for _ in range(2):
             kvx.kvx_restore_from_staging(ring, _bt(bt_dst))
         torch.cuda.synchronize()
@@ -73,7 +77,7 @@ def test_offload_to_files_then_restore_from_files(tmp_path, case):
     finally:
         ring.close()
     for path, b0, nb in chunks:
-        oracle.scatter(s, *mirror, 0, L, bt_dst[b0:b0 + nb], ct, np.fromfile(path, np.uint8))
+        oracle.scatter(s, *mirror, l0, l1, bt_dst[b0:b0 + nb], ct, np.fromfile(path, np.uint8))
     for l in range(L):
         assert np.array_equal(to_host(cache.k[l]), mirror[0][l]), f"K layer {l}"
         assert np.array_equal(to_host(cache.v[l]), mirror[1][l]), f"V layer {l}"
