@@ -29,6 +29,10 @@ Other workloads print one JSON line each with their own metric:
                            several caches and packed buffers alive at once
                            (--caches, --packed): how much of a run-to-run
                            spread is where the allocations land in memory.
+  --workload 8b-layouts    the default gather and scatter with the cache read
+                           as each of the three layouts, on the same
+                           allocations (--caches x --packed pairs): what a
+                           layout costs, with placement held fixed.
 """
 from __future__ import annotations
 
@@ -76,8 +80,9 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="8b-80k",
                     choices=["8b-80k", "8b-32k-sweep", "70b-batch", "8b-files", "8b-preload",
-                             "8b-placements"])
-    ap.add_argument("--caches", type=int, default=4, help="8b-placements: caches allocated")
+                             "8b-placements", "8b-layouts"])
+    ap.add_argument("--caches", type=int, default=4,
+                    help="8b-placements: caches allocated (8b-layouts: at most 2)")
     ap.add_argument("--packed", type=int, default=3,
                     help="8b-placements: packed buffers allocated")
     ap.add_argument("--num-blocks", type=int, default=20000)
@@ -1256,6 +1261,91 @@ def run_placements(args):
     print(json.dumps(out), flush=True)
 
 
+def run_layouts(args):
+    """The default workload's gather and scatter with each cache read as the
+    default (NHD), HND and paged-attention layouts. A layout only decides
+    where a cache tensor's bytes belong, so one allocation serves all three
+    (views of the same tensors, holding random data): on every (cache, packed
+    buffer) pair the three layouts move equal bytes at equal addresses, and
+    their difference is the layout's own cost, with the placement share of a
+    run-to-run spread held fixed."""
+    import numpy as np
+    import torch
+
+    import kvsynth
+    import paper_2609_11744_amd as kvx
+
+    dev = torch.device("cuda:0")
+    L, BS, H, D, E = 32, 16, args.kv_heads, 128, 2
+    NB, n, ct = args.num_blocks, args.prefix_blocks, args.chunk_tokens
+    slab = BS * H * D * E
+    payload = n * L * 2 * slab
+    caches_n, packed_n = min(args.caches, 2), min(args.packed, 2)
+    need = caches_n * NB * L * 2 * slab + packed_n * payload
+    free, _ = torch.cuda.mem_get_info()
+    if need > 0.9 * free:
+        raise SystemExit(f"{need / 1e9:.0f} GB of caches and packed buffers do not fit")
+    perm = np.random.default_rng(args.seed).permutation(NB).astype(np.int32)
+    bt_src = torch.from_numpy(perm[:n].copy()).to(dev)
+    bt_dst = torch.from_numpy(perm[n:2 * n].copy()).to(dev)
+    x = 16 // E
+    views = []
+    for _ in range(caches_n):
+        c = kvx.PagedKVCache.allocate(L, NB, BS, H, D, torch.bfloat16, dev)
+        fill_cache(c, args.seed, kvsynth.ROLE_SRC)
+        views.append({
+            "nhd": c,
+            "hnd": kvx.PagedKVCache([t.view(NB, H, BS, D) for t in c.k],
+                                    [t.view(NB, H, BS, D) for t in c.v], kvx.KVX_LAYOUT_HND),
+            "paged_attn": kvx.PagedKVCache([t.view(NB, H, D // x, BS, x) for t in c.k],
+                                           [t.view(NB, H, D, BS) for t in c.v],
+                                           kvx.KVX_LAYOUT_PAGED_ATTN)})
+    packs = [torch.empty(payload, dtype=torch.uint8, device=dev) for _ in range(packed_n)]
+    torch.cuda.synchronize()
+    reps = max(args.steps, 3)
+    pct = lambda ms: 100 * 2 * payload / ms / 1e6 / HBM_PEAK_GBPS
+    layouts = ("nhd", "hnd", "paged_attn")
+    rows = []
+    for ci, cv in enumerate(views):
+        for pi, p in enumerate(packs):
+            row = {"cache": ci, "packed": pi}
+            for lay in layouts:
+                c = cv[lay]
+                g = event_ms(lambda: kvx.kvx_gather_blocks(c, 0, L, bt_src, n, ct, p), reps)
+                sc = event_ms(lambda: kvx.kvx_scatter_blocks(c, 0, L, bt_dst, n, ct, p), reps)
+                row[f"{lay}_gather_pct"] = round(pct(statistics.median(g)), 2)
+                row[f"{lay}_scatter_pct"] = round(pct(statistics.median(sc)), 2)
+            rows.append(row)
+    kvx.kvx_check()
+    log(f"layouts: {rows}")
+    summary = {}
+    for lay in layouts:
+        for d in ("gather", "scatter"):
+            v = [r[f"{lay}_{d}_pct"] for r in rows]
+            s = {"mean": round(statistics.mean(v), 2), "min": min(v), "max": max(v)}
+            if lay != "nhd":
+                diff = [r[f"{lay}_{d}_pct"] - r[f"nhd_{d}_pct"] for r in rows]
+                s["minus_nhd"] = {"mean": round(statistics.mean(diff), 2),
+                                  "min": round(min(diff), 2), "max": round(max(diff), 2)}
+            summary[f"{lay}_{d}_pct_hbm_peak"] = s
+    mean_rate = statistics.mean([summary[f"{lay}_{d}_pct_hbm_peak"]["mean"] for lay in layouts
+                                 for d in ("gather", "scatter")]) * HBM_PEAK_GBPS / 100
+    out = base_record(
+        args, "KV gather/scatter GB/s & % HBM peak per cache layout, same allocations", "GB/s",
+        round(mean_rate, 1), None,
+        {"workload": "llama-3-8b-shaped paged KV, 80k-token prefix (5000 blocks), 256-token "
+                     "chunks, the cache read as NHD, HND and paged attention on each of "
+                     f"{caches_n} caches x {packed_n} packed buffers",
+         "num_blocks": NB, "prefix_tokens": n * BS, "chunk_tokens": ct, "kv_heads": H,
+         "caches": caches_n, "packed": packed_n, "parallelism": "single GPU"})
+    out.update(summary)
+    out.update({"pairs": rows, "reps_per_pair": reps,
+                "note": "value: mean of the six rates (three layouts, two directions) over "
+                        "the pairs; minus_nhd: each pair's rate less the NHD rate on the "
+                        "same pair, in points of peak"})
+    print(json.dumps(out), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -1267,7 +1357,7 @@ def main():
     torch.cuda.set_device(torch.device("cuda:0"))
     {"8b-80k": run_80k, "8b-32k-sweep": run_sweep, "70b-batch": run_batch,
      "8b-files": run_files, "8b-preload": run_preload,
-     "8b-placements": run_placements}[args.workload](args)
+     "8b-placements": run_placements, "8b-layouts": run_layouts}[args.workload](args)
 
 
 if __name__ == "__main__":
