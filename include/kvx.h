@@ -162,7 +162,8 @@ kvx_status kvx_scatter_blocks(const kvx_cache* cache, int32_t l0, int32_t l1,
  * others). A scatter of 1,024 blocks or more in chunks of more than one block
  * runs in ascending destination order (ordered = 1; block ids bucketed by a
  * small kernel first), except with slabs of at most 8 KiB in the default
- * layout (or HND with one KV head): those, like every smaller scatter, walk
+ * layout (or a reordering layout with one KV head): those, like every smaller
+ * scatter, walk
  * the packed image in order, with linear = 1 when workgroup b moves work item
  * b rather than each XCD taking one contiguous range. pair_slices = D > 0:
  * slices D apart, whose runs sit 2 MiB apart in a packed chunk, are moved
@@ -189,8 +190,8 @@ kvx_status kvx_copy_walk(const kvx_cache* cache, int32_t l0, int32_t l1, int32_t
  * under HIP graph capture, tight serving loops, harnesses that forbid
  * allocation): the same arguments, validation, kernels and result, but the
  * destination order that a scatter of 1,024 blocks or more computes first (in
- * chunks of more than one block, and with the default layout, or HND with one
- * KV head, only for slabs above 8 KiB) lives in
+ * chunks of more than one block, and with the default layout, or a
+ * reordering layout with one KV head, only for slabs above 8 KiB) lives in
  * a fixed device array of the library's (512 KiB, KVX_NOALLOC_MAX_BLOCKS
  * 8-byte entries; each GPU the library runs on holds one until the process
  * ends) instead of stream-ordered scratch. The call allocates nothing.
