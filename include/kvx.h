@@ -278,12 +278,15 @@ typedef struct kvx_piece {
 
 /* Where a plan's piece sizes ramp up to the slot size. */
 #define KVX_RAMP_NONE 0   /* every piece up to slot_bytes */
-#define KVX_RAMP_FIRST 1  /* the first three pieces at most 1/8, 1/4 and 1/2 of a slot
-                             (a restore: its first copy starts after a small fill) */
-#define KVX_RAMP_LAST 2   /* the last three at most 1/2, 1/4 and 1/8 of a slot (an
-                             offload: its last copy and drain are short); the pieces
-                             of the first-ramp plan of the reversed chunk list, in
-                             reverse order, each carrying its chunks in image order */
+#define KVX_RAMP_FIRST 1  /* the first piece at most 1/8 of a slot, each next one at
+                             most twice the piece before it, until a piece may fill a
+                             slot (a restore: its first copy starts after a small
+                             fill, and each fill finishes while the copy before it
+                             still runs) */
+#define KVX_RAMP_LAST 2   /* the same ramp from the last piece backwards (an offload:
+                             its last copy and drain are short); the pieces of the
+                             first-ramp plan of the reversed chunk list, in reverse
+                             order, each carrying its chunks in image order */
 
 /* Split the packed image of (cache shape, [l0, l1), n_blocks, chunk_tokens)
  * into pieces: as many consecutive whole chunks per piece as fit its size
@@ -323,9 +326,10 @@ kvx_status kvx_ring_create(int device, int32_t n_slots, int64_t slot_bytes, void
  * into staging slots. fill_threads == 0 skips staging: the H2D copies then
  * read the image directly, which must be pinned (the preloaded case, where
  * the data already sits in pinned memory). Plans the pieces as
- * kvx_plan_pieces does with KVX_RAMP_FIRST: a restore's first three pieces
- * hold at most 1/8, 1/4 and 1/2 of a slot (larger chunks cut into layer
- * ranges), so its first host-to-device copy starts after a small first fill;
+ * kvx_plan_pieces does with KVX_RAMP_FIRST: a restore's first piece holds at
+ * most 1/8 of a slot and each next one at most twice the piece before it
+ * (larger chunks cut into layer ranges) until a piece may fill a slot, so its
+ * first host-to-device copy starts after a small first fill;
  * offloads (kvx_ring_bind_offload) plan with KVX_RAMP_LAST. */
 kvx_status kvx_ring_bind(kvx_ring* ring, const kvx_cache* cache, int32_t l0, int32_t l1,
                          int32_t n_blocks, int32_t chunk_tokens, const void* host_source,

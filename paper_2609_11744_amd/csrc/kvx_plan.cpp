@@ -32,16 +32,32 @@ struct Group {
 // Cut the list into groups: as many consecutive whole chunks per piece as
 // fit its size limit; a chunk larger than its piece's limit is cut into
 // layer ranges, each as many layers as the piece it becomes allows (at
-// least one). With the ramp, the limits of the first three pieces are 1/8,
-// 1/4 and 1/2 of a slot.
+// least one). With the ramp, the first piece holds at most 1/8 of a slot and
+// each next one at most twice the piece before it, until a piece's limit
+// reaches the slot; from there on every piece may fill a slot. Doubling from
+// the previous piece, not from a fixed 1/8, 1/4, 1/2 of a slot, keeps the
+// short tail of a chunk cut into layer ranges from being followed by a whole
+// slot, whose fill the tail's copy cannot hide. Measured on the 8B shape
+// (4 x 64 MiB ring, one process, alternated with the fixed ramp): restores of
+// 1k, 2k, 4k and 8k tokens 3.8, 1.1, 0.2 and 1.3 % faster, 80k level.
 kvx_status plan_groups(const std::vector<HostChunk>& chunks, int32_t l0, int32_t l1, int64_t slab,
                        int64_t slot_bytes, bool ramp, std::vector<Group>* out) {
   const int64_t lr = l1 - l0;
+  bool ramping = ramp;
+  int64_t prev = 0;  // bytes of the last group
   auto cap = [&]() -> int64_t {
-    const size_t k = out->size();
-    if (!ramp || k >= 3) return slot_bytes;
-    const int64_t c = slot_bytes >> (3 - k);
-    return c > 0 ? c : slot_bytes;
+    if (!ramping) return slot_bytes;
+    const int64_t first = slot_bytes >> 3;
+    int64_t c = out->empty() ? first : std::max(first, 2 * prev);
+    if (c <= 0 || c >= slot_bytes) {
+      ramping = false;
+      return slot_bytes;
+    }
+    return c;
+  };
+  auto push = [&](const Group& g, int64_t bytes) {
+    out->push_back(g);
+    prev = bytes;
   };
   bool open = false;
   int64_t cur_bytes = 0, cur_cap = 0;
@@ -54,14 +70,14 @@ kvx_status plan_groups(const std::vector<HostChunk>& chunks, int32_t l0, int32_t
       cur_bytes += chunk_bytes;
       continue;
     }
-    if (open) out->push_back(cur);
+    if (open) push(cur, cur_bytes);
     open = false;
     if (chunk_bytes > cap()) {
       if (layer_bytes > slot_bytes) return KVX_EINVAL;
       for (int64_t a = l0; a < l1;) {
         const int64_t fit = cap() / layer_bytes;
         const int64_t b = std::min<int64_t>(a + (fit > 0 ? fit : 1), l1);
-        out->push_back(Group{i, i + 1, (int32_t)a, (int32_t)b});
+        push(Group{i, i + 1, (int32_t)a, (int32_t)b}, (b - a) * layer_bytes);
         a = b;
       }
       continue;
@@ -71,7 +87,7 @@ kvx_status plan_groups(const std::vector<HostChunk>& chunks, int32_t l0, int32_t
     cur_cap = cap();
     open = true;
   }
-  if (open) out->push_back(cur);
+  if (open) push(cur, cur_bytes);
   return KVX_OK;
 }
 

@@ -148,14 +148,24 @@ def test_plan_rejects_slot_smaller_than_one_layer():
         kvx.kvx_plan_pieces(c, 0, 4, 16, 256, (1 << 20) - 4096)
 
 
-def _ramp_caps(n_pieces, slot, ramp):
-    caps = [slot] * n_pieces
-    first = [slot >> 3, slot >> 2, slot >> 1]
-    for k in range(min(3, n_pieces)):
-        if ramp == kvx.KVX_RAMP_FIRST:
-            caps[k] = first[k]
-        elif ramp == kvx.KVX_RAMP_LAST:
-            caps[n_pieces - 1 - k] = first[k]
+def _ramp_caps(sizes, slot, ramp):
+    """Each piece's size limit under a ramp, from the pieces' own sizes: in
+    ramp order (from the first piece, or from the last one backwards), the
+    first at most slot / 8 and each next at most twice the piece before it,
+    until a limit reaches the slot, and the slot from there on."""
+    if ramp == kvx.KVX_RAMP_NONE:
+        return [slot] * len(sizes)
+    order = list(range(len(sizes)))
+    if ramp == kvx.KVX_RAMP_LAST:
+        order.reverse()
+    caps = [slot] * len(sizes)
+    prev = None
+    for k in order:
+        c = slot >> 3 if prev is None else max(slot >> 3, 2 * prev)
+        if c >= slot:
+            break
+        caps[k] = c
+        prev = sizes[k]
     return caps
 
 
@@ -170,7 +180,7 @@ def test_ramped_plan_tiles_image_within_limits(case, ramp):
     c = kvx.shape_only_cache(L, 4 * n + 8, BS, H, D, 2)
     slab = BS * H * D * 2
     pieces = kvx.kvx_plan_pieces(c, 0, L, n, ct, slot, ramp)
-    caps = _ramp_caps(len(pieces), slot, ramp)
+    caps = _ramp_caps([p["bytes"] for p in pieces], slot, ramp)
     bpc = ct // BS
     covered = []
     for p, cap in zip(pieces, caps):
@@ -191,16 +201,20 @@ def test_ramped_plan_tiles_image_within_limits(case, ramp):
 
 def test_ramped_80k_restore_plan():
     """The restore's first-piece ramp at 80k: the first 32 MiB chunk is cut
-    into 8, 16 and 8 MiB layer ranges, then 156 two-chunk pieces."""
+    into 8, 16 and 8 MiB layer ranges; after the 8 MiB tail the next chunk
+    goes as two 16 MiB halves (at most twice the piece before), the next
+    whole (32 MiB), and from there two-chunk pieces of a full slot."""
     c = kvx.shape_only_cache(32, 20000, 16, 8, 128, 2)
     pieces = kvx.kvx_plan_pieces(c, 0, 32, 5000, 256, 64 << 20, kvx.KVX_RAMP_FIRST)
-    assert len(pieces) == 159
-    assert [p["bytes"] >> 20 for p in pieces[:4]] == [8, 16, 8, 64]
-    assert [(p["l_begin"], p["l_end"]) for p in pieces[:3]] == [(0, 8), (8, 24), (24, 32)]
+    assert len(pieces) == 161
+    assert [p["bytes"] >> 20 for p in pieces[:8]] == [8, 16, 8, 16, 16, 32, 64, 64]
+    assert [(p["l_begin"], p["l_end"]) for p in pieces[:5]] == \
+        [(0, 8), (8, 24), (24, 32), (0, 16), (16, 32)]
     # the end ramp starts from the compact 16 MiB last chunk: 8 + 8 MiB
-    # layer halves, the 32 MiB chunk before it alone
+    # layer halves, the 32 MiB chunk before it in 16 MiB halves, the one
+    # before that alone
     end = kvx.kvx_plan_pieces(c, 0, 32, 5000, 256, 64 << 20, kvx.KVX_RAMP_LAST)
-    assert [p["bytes"] >> 20 for p in end[-3:]] == [32, 8, 8]
+    assert [p["bytes"] >> 20 for p in end[-6:]] == [64, 32, 16, 16, 8, 8]
     assert [(p["l_begin"], p["l_end"]) for p in end[-2:]] == [(16, 32), (0, 16)]
     with pytest.raises(kvx.KvxError):
         kvx.kvx_plan_pieces(c, 0, 32, 5000, 256, 64 << 20, 3)

@@ -25,7 +25,7 @@ DEV = "cuda:0"
 NB = 20000
 SLOT = 64 << 20
 # Pieces of the ramped 80k restore plan (also checked on the CPU, test_abi).
-RAMPED_80K_PIECES = 159
+RAMPED_80K_PIECES = 161
 
 
 def _bt(ids):
@@ -121,9 +121,9 @@ def test_80k_staged_restore_4x64MiB(w80k):
         ring.bind(w.cache, 0, 32, 5000, 256, image, fill_threads=8)
         kvx.kvx_restore_from_staging(ring, _bt(w.bt_rst))
         _check()
-        # the plain plan's 157 pieces, with the restore's ramp cutting the
-        # first 32 MiB chunk into 8, 16 and 8 MiB pieces (at most 1/8, 1/4,
-        # 1/2 slot): 3 + 156 two-chunk pieces (the last one 32 + 16 MiB)
+        # the restore's ramp (each piece at most twice the one before, from
+        # 1/8 slot): 8, 16, 8 MiB of the first chunk, 16 + 16 of the second,
+        # the third whole, then 155 two-chunk pieces (the last 32 + 16 MiB)
         assert ring.stats()["pieces"] == RAMPED_80K_PIECES
     finally:
         ring.close()

@@ -42,14 +42,21 @@ def plans(draw):
     return L, H, D, BS, n, bpc * BS, slot, ramp
 
 
-def _caps(n_pieces, slot, ramp):
-    caps = [slot] * n_pieces
-    first = [slot >> 3, slot >> 2, slot >> 1]
-    for k in range(min(3, n_pieces)):
-        if ramp == kvx.KVX_RAMP_FIRST:
-            caps[k] = first[k]
-        elif ramp == kvx.KVX_RAMP_LAST:
-            caps[n_pieces - 1 - k] = first[k]
+def _caps(sizes, slot, ramp):
+    """Each piece's size limit under a ramp (from the first piece, or from
+    the last backwards): slot / 8 first, then at most twice the piece before,
+    until a limit reaches the slot."""
+    caps = [slot] * len(sizes)
+    if ramp == kvx.KVX_RAMP_NONE:
+        return caps
+    order = list(range(len(sizes)))[::-1 if ramp == kvx.KVX_RAMP_LAST else 1]
+    prev = None
+    for k in order:
+        c = slot >> 3 if prev is None else max(slot >> 3, 2 * prev)
+        if c >= slot:
+            break
+        caps[k] = c
+        prev = sizes[k]
     return caps
 
 
@@ -63,7 +70,7 @@ def test_pieces_tile_the_image_within_limits(case):
     bpc = ct // BS
     layer = min(bpc, n) * 2 * slab
     spans = []
-    for p, cap in zip(pieces, _caps(len(pieces), slot, ramp)):
+    for p, cap in zip(pieces, _caps([q["bytes"] for q in pieces], slot, ramp)):
         lr = p["l_end"] - p["l_begin"]
         assert 0 <= p["l_begin"] < p["l_end"] <= L
         assert p["bytes"] == p["n_blocks"] * lr * 2 * slab > 0
