@@ -315,7 +315,11 @@ typedef struct kvx_ring kvx_ring;
  * candidates, on 32 MiB device and 32 MiB pinned buffers of its own, freed
  * afterwards). device_landing is the
  * device buffer that H2D copies land in (n_slots * slot_bytes bytes, 16-byte
- * aligned, owned by the caller); NULL makes the ring allocate its own. */
+ * aligned, owned by the caller); NULL makes the ring allocate its own. The
+ * ring's fill (restore) or drain (offload) threads are started by the first
+ * transfer that needs them and kept, parked between transfers, until
+ * kvx_ring_destroy (a bind that changes their direction or count replaces
+ * them at the next transfer). */
 kvx_status kvx_ring_create(int device, int32_t n_slots, int64_t slot_bytes, void* device_landing,
                            kvx_ring** out);
 

@@ -105,6 +105,19 @@ struct kvx_ring {
   std::atomic<int64_t> busy_ns{0};
   kvx_ring_stats stats{};
 
+  // fill (restore) or drain (offload) threads, kept from one transfer to the
+  // next: started by the first transfer that needs them (or again when a
+  // bind changes their direction or count), parked on cv_pool in between,
+  // joined by kvx_ring_destroy. Creating them per transfer put their start-up
+  // on every transfer's path: the first piece's fill shares began 0-130 us
+  // apart, one thread created at a time.
+  std::vector<std::thread> pool;
+  Dir pool_dir = Dir::kNone;
+  uint64_t pool_gen = 0;   // transfers handed to the pool (guarded by mu)
+  int32_t pool_done = 0;   // workers done with the current one (guarded by mu)
+  bool pool_quit = false;  // guarded by mu
+  std::condition_variable cv_pool, cv_pool_done;
+
   // test hooks (kvx_ring_set_test_hooks)
   int32_t hook_max_delay_us = 0;
   bool hook_poison = false;
@@ -232,7 +245,12 @@ void drain_device(kvx_ring* r) {
     if (e) (void)hipEventSynchronize(e);
 }
 
+void signal_stop(kvx_ring* r);
+void stop_pool(kvx_ring* r);
+
 void destroy_resources(kvx_ring* r) {
+  signal_stop(r);  // pool threads blocked inside a transfer return to the pool
+  stop_pool(r);
   drain_device(r);
   for (hipEvent_t e : r->dev_done)
     if (e) (void)hipEventDestroy(e);
@@ -381,6 +399,70 @@ void drain_worker(kvx_ring* r, int w) {
     if (++r->parts_done[(size_t)i] == T) r->cv_host.notify_all();
   }
   r->busy_ns.fetch_add(busy);
+}
+
+// A pool thread: runs worker w of every transfer handed to the pool (a new
+// pool_gen) until told to quit. `seen` starts at the generation current when
+// the thread is created, before the transfer it is created for is handed
+// over, so that it cannot miss that transfer.
+void pool_worker(kvx_ring* r, Dir dir, int w, uint64_t seen) {
+  for (;;) {
+    {
+      std::unique_lock<std::mutex> lock(r->mu);
+      r->cv_pool.wait(lock, [&] { return r->pool_quit || r->pool_gen != seen; });
+      if (r->pool_quit) return;
+      seen = r->pool_gen;
+    }
+    if (dir == Dir::kRestore)
+      fill_worker(r, w);
+    else
+      drain_worker(r, w);
+    std::lock_guard<std::mutex> lock(r->mu);
+    if (++r->pool_done == (int32_t)r->pool.size()) r->cv_pool_done.notify_all();
+  }
+}
+
+// Join the pool's threads (none may be running a transfer).
+void stop_pool(kvx_ring* r) {
+  {
+    std::lock_guard<std::mutex> lock(r->mu);
+    r->pool_quit = true;
+  }
+  r->cv_pool.notify_all();
+  for (auto& th : r->pool) th.join();
+  r->pool.clear();
+  r->pool_dir = Dir::kNone;
+  std::lock_guard<std::mutex> lock(r->mu);
+  r->pool_quit = false;
+}
+
+// Hand the transfer about to run to T pool threads of direction dir, starting
+// them first where the pool has another direction or count. Called by the
+// transfer's own thread, the only one that changes pool_gen. Throws if a
+// thread cannot be created (the pool is then empty).
+void start_pool(kvx_ring* r, Dir dir, int32_t T) {
+  if (r->pool_dir != dir || (int32_t)r->pool.size() != T) {
+    stop_pool(r);
+    r->pool_dir = dir;
+    try {
+      for (int w = 0; w < T; ++w) r->pool.emplace_back(pool_worker, r, dir, w, r->pool_gen);
+    } catch (...) {
+      stop_pool(r);
+      throw;
+    }
+  }
+  {
+    std::lock_guard<std::mutex> lock(r->mu);
+    r->pool_done = 0;
+    ++r->pool_gen;
+  }
+  r->cv_pool.notify_all();
+}
+
+// Wait until every pool thread is done with the current transfer.
+void wait_pool(kvx_ring* r) {
+  std::unique_lock<std::mutex> lock(r->mu);
+  r->cv_pool_done.wait(lock, [&] { return r->pool_done == (int32_t)r->pool.size(); });
 }
 
 // ---- storage tier -----------------------------------------------------------
@@ -856,12 +938,26 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
     if (st != KVX_OK) return st;
     imgs.assign(r->pre_paths.size(), nullptr);
   }
+  bool pooled = false;  // the pool's threads run this transfer
+  // Whatever way this function is left, the pool is done with the transfer
+  // first (on an exception: told to stop, then waited for).
+  struct PoolGuard {
+    kvx_ring* r;
+    bool* pooled;
+    ~PoolGuard() {
+      if (*pooled) {
+        signal_stop(r);
+        wait_pool(r);
+      }
+    }
+  } pool_guard{r, &pooled};
   try {
-    if (r->files_mode)
+    if (r->files_mode) {
       workers.emplace_back(dir == Dir::kRestore ? file_fill_worker : file_drain_worker, r);
-    else
-      for (int w = 0; w < T; ++w)
-        workers.emplace_back(dir == Dir::kRestore ? fill_worker : drain_worker, r, w);
+    } else if (T > 0) {
+      start_pool(r, dir, T);
+      pooled = true;
+    }
   } catch (...) {
     st = KVX_ENOMEM;
   }
@@ -1084,6 +1180,10 @@ kvx_status run(kvx_ring* r, Dir dir, const int32_t* bt, hipStream_t stream, int*
     }
   }
   for (auto& th : workers) th.join();
+  if (pooled) {
+    wait_pool(r);
+    pooled = false;
+  }
   if (!holds.empty()) {
     // the images may be evicted once released: the copies out of them first
     if (!use_dma(r) && hipStreamSynchronize(r->side) != hipSuccess && st == KVX_OK) st = KVX_EHIP;
