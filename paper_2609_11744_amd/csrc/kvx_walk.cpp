@@ -26,7 +26,8 @@ namespace {
 // 32 KiB 71.1 against 75.3 % (image order with XCD ranges: 69.3 / 69.1 % at 4
 // and 8 KiB). An HND cache with one KV head is the default layout byte for
 // byte, and measured the same way (4 KiB slabs: 73.7 against 70.4 %); with
-// two heads in 8 KiB it lost 1.8 points, so it keeps destination order. The
+// two heads in 8 KiB it lost 1.8 points (1.4 on the current kernels, over 18
+// pairs), so it keeps destination order. The
 // paged-attention layout with one head takes the linear walk too, with its
 // heads on 256 threads (kvx_kernels.hip): over 18 allocation pairs 73.2 %
 // against 68.3 % for destination order on 128 threads, and about 1 point
