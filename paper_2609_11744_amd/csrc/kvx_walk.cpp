@@ -27,11 +27,11 @@ namespace {
 // and 8 KiB). An HND cache with one KV head is the default layout byte for
 // byte, and measured the same way (4 KiB slabs: 73.7 against 70.4 %); with
 // two heads in 8 KiB it lost 1.8 points (1.4 on the current kernels, over 18
-// pairs), so it keeps destination order. The
-// paged-attention layout with one head takes the linear walk too, with its
-// heads on 256 threads (kvx_kernels.hip): over 18 allocation pairs 73.2 %
-// against 68.3 % for destination order on 128 threads, and about 1 point
-// with either change alone; with two heads the linear walk lost 0.2 points.
+// pairs), so it keeps destination order. The paged-attention layout with one
+// head takes the linear walk too, with its heads on 256 threads
+// (kvx_kernels.hip): over 18 allocation pairs 73.2 % against 68.3 % for
+// destination order on 128 threads, and about 1 point with either change
+// alone; with two heads the linear walk lost 0.2 points.
 bool scatter_linear(int64_t n_blocks, int64_t slab, int layout, int32_t heads) {
   const bool rows = layout == KVX_LAYOUT_NHD ||
                     ((layout == KVX_LAYOUT_HND || layout == KVX_LAYOUT_PAGED_ATTN) && heads == 1);
