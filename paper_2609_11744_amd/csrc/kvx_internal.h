@@ -131,9 +131,10 @@ struct Plan {
 };
 
 // Where a plan's pieces ramp up to the slot size: nowhere, over the first
-// three pieces (1/8, 1/4, 1/2 of a slot; a restore's first copy then starts
-// after a small fill) or, mirrored, over the last three (an offload's last
-// copy and drain are then short).
+// pieces (the first at most 1/8 of a slot, each next at most twice the piece
+// before it; a restore's first copy then starts after a small fill) or,
+// mirrored, over the last pieces (an offload's last copy and drain are then
+// short).
 enum class Ramp { kNone, kFirst, kLast };
 
 // Cut a chunk list into staging pieces of at most slot_bytes (see kvx_plan.cpp);
