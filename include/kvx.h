@@ -426,7 +426,8 @@ kvx_status kvx_offload_wait(kvx_ring* ring);
 
 /* Asynchronous restore (Sec. 6.4: the worker turns load plans into transfers
  * without blocking the engine; Sec. 6.2): start the restore of the bound
- * transfer into the blocks named by block_table on a thread the ring owns,
+ * transfer into the blocks named by block_table on a thread the ring owns
+ * (started by the first begin on the ring and kept until kvx_ring_destroy),
  * and return at once. Its scatters run after the work already enqueued on
  * `stream`, on a stream the ring owns; fills, host-link copies and slot reuse
  * are those of kvx_restore_from_staging. Until kvx_restore_wait has returned,

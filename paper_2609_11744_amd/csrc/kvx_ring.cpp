@@ -134,10 +134,20 @@ struct kvx_ring {
   hipStream_t store_stream = nullptr;
   hipEvent_t store_begin = nullptr;
   hipEvent_t restore_end = nullptr;
-  std::thread async_th;
   std::atomic<bool> async_busy{false};
   Dir async_dir = Dir::kNone;
   kvx_status async_status = KVX_OK;
+  // The thread that runs them, kept from one call to the next: started by
+  // the first begin, parked on cv_async in between, joined by
+  // kvx_ring_destroy once a posted transfer has run. A begin posts the
+  // transfer (async_posted) and its wait waits for async_done.
+  std::thread async_th;
+  std::mutex async_mu;
+  std::condition_variable cv_async;
+  bool async_posted = false, async_done = false, async_quit = false;  // guarded by async_mu
+  const int32_t* async_bt = nullptr;
+  hipStream_t async_own = nullptr;
+  int* async_err = nullptr;
 
   // storage tier: the bound chunks live in files (kvx_ring_bind_files /
   // kvx_ring_bind_offload_files); a reactor thread replaces the fill / drain
@@ -1627,9 +1637,61 @@ bool make_store_stream(kvx_ring* r) {
   return true;
 }
 
-// kvx_offload_begin / kvx_restore_begin: the bound transfer on a thread of
-// the ring's own, its kernels on the ring's stream after the work already
-// enqueued on the caller's stream, reporting bad ids to the caller's stream.
+// The ring's asynchronous thread: runs each posted transfer, then reports
+// its status (an asynchronous restore also records restore_end on the
+// ring's stream, after a failure too, so that the caller's stream never
+// waits on an event that was not recorded). Returns once told to quit with
+// nothing posted.
+void async_worker(kvx_ring* r) {
+  std::unique_lock<std::mutex> lock(r->async_mu);
+  for (;;) {
+    r->cv_async.wait(lock, [&] { return r->async_posted || r->async_quit; });
+    if (!r->async_posted) return;
+    r->async_posted = false;
+    const Dir dir = r->async_dir;
+    const int32_t* bt = r->async_bt;
+    hipStream_t own = r->async_own;
+    int* err = r->async_err;
+    lock.unlock();
+    kvx_status st;
+    try {
+      st = run(r, dir, bt, own, err);
+    } catch (...) {
+      st = KVX_EINTERNAL;
+    }
+    if (dir == Dir::kRestore) {
+      DeviceGuard g(r->device);
+      if ((!g.ok || hipEventRecord(r->restore_end, own) != hipSuccess) && st == KVX_OK)
+        st = KVX_EHIP;
+    }
+    lock.lock();
+    r->async_status = st;
+    r->async_done = true;
+    r->cv_async.notify_all();
+  }
+}
+
+// Wait for the posted transfer and return its status.
+kvx_status wait_async(kvx_ring* r) {
+  std::unique_lock<std::mutex> lock(r->async_mu);
+  r->cv_async.wait(lock, [&] { return r->async_done; });
+  return r->async_status;
+}
+
+// Stop the asynchronous thread (after a posted transfer has run).
+void stop_async(kvx_ring* r) {
+  {
+    std::lock_guard<std::mutex> lock(r->async_mu);
+    r->async_quit = true;
+  }
+  r->cv_async.notify_all();
+  if (r->async_th.joinable()) r->async_th.join();
+}
+
+// kvx_offload_begin / kvx_restore_begin: the bound transfer on the ring's
+// asynchronous thread, its kernels on the ring's stream after the work
+// already enqueued on the caller's stream, reporting bad ids to the caller's
+// stream.
 kvx_status start_async(kvx_ring* ring, Dir dir, const int32_t* block_table, hipStream_t stream) {
   if (!ring) return KVX_EINVAL;
   if (ring->dir != dir) return KVX_EINVAL;
@@ -1651,23 +1713,18 @@ kvx_status start_async(kvx_ring* ring, Dir dir, const int32_t* block_table, hipS
     if (hipEventRecord(ring->store_begin, stream) != hipSuccess ||
         hipStreamWaitEvent(ring->store_stream, ring->store_begin, 0) != hipSuccess)
       return release(KVX_EHIP);
-    hipStream_t own = ring->store_stream;
-    ring->async_status = KVX_OK;
-    ring->async_dir = dir;
-    ring->async_th = std::thread([ring, dir, block_table, own, err] {
-      kvx_status st;
-      try {
-        st = run(ring, dir, block_table, own, err);
-      } catch (...) {
-        st = KVX_EINTERNAL;
-      }
-      if (dir == Dir::kRestore) {
-        DeviceGuard g(ring->device);
-        if ((!g.ok || hipEventRecord(ring->restore_end, own) != hipSuccess) && st == KVX_OK)
-          st = KVX_EHIP;
-      }
-      ring->async_status = st;
-    });
+    if (!ring->async_th.joinable()) ring->async_th = std::thread(async_worker, ring);
+    {
+      std::lock_guard<std::mutex> lock(ring->async_mu);
+      ring->async_status = KVX_OK;
+      ring->async_dir = dir;
+      ring->async_bt = block_table;
+      ring->async_own = ring->store_stream;
+      ring->async_err = err;
+      ring->async_done = false;
+      ring->async_posted = true;
+    }
+    ring->cv_async.notify_all();
     return KVX_OK;
   } catch (...) {
     return release(KVX_EINTERNAL);
@@ -1853,8 +1910,7 @@ kvx_status kvx_offload_wait(kvx_ring* ring) {
   if (!ring) return KVX_EINVAL;
   if (!ring->async_busy.load()) return KVX_OK;
   if (ring->async_dir != Dir::kOffload) return KVX_EINVAL;
-  if (ring->async_th.joinable()) ring->async_th.join();
-  const kvx_status st = ring->async_status;
+  const kvx_status st = wait_async(ring);
   ring->async_busy.store(false);
   return st;
 }
@@ -1867,8 +1923,7 @@ kvx_status kvx_restore_wait(kvx_ring* ring, hipStream_t stream) {
   if (!ring) return KVX_EINVAL;
   if (!ring->async_busy.load()) return KVX_OK;
   if (ring->async_dir != Dir::kRestore) return KVX_EINVAL;
-  if (ring->async_th.joinable()) ring->async_th.join();
-  kvx_status st = ring->async_status;
+  kvx_status st = wait_async(ring);
   try {
     // the caller's stream continues after the last scatter (restore_end was
     // recorded on the ring's stream after it, also after a failure, so that
@@ -1951,7 +2006,7 @@ kvx_status kvx_ring_abort(kvx_ring* ring) {
 
 kvx_status kvx_ring_destroy(kvx_ring* ring) {
   if (!ring) return KVX_OK;
-  if (ring->async_th.joinable()) ring->async_th.join();  // a deferred store still running
+  stop_async(ring);  // after a deferred store or restore still running
   try {
     DeviceGuard dg(ring->device);
     destroy_resources(ring);
