@@ -79,6 +79,46 @@ def test_restore_begin_wait_bit_exact(threads):
         assert np.array_equal(to_host(snap_v[l]), mirror[1][l]), f"V layer {l}"
 
 
+def test_repeated_begins_on_one_ring():
+    """The ring's asynchronous thread is kept from one begin to the next: three
+    asynchronous restores into different blocks, a blocking restore between
+    them, then a bind with another chunk size and one more asynchronous
+    restore, each waited on the caller's stream; the whole cache against the
+    oracle applying the same restores in the same order."""
+    s = oracle.Shape(3, 900, 16, 2, 64, 2)
+    n, seed = 120, 83
+    tables = seeded_ids(seed, s.num_blocks, n, n, n, n, n)
+    fill = Filled(seed, kvsynth.ROLE_DST, kvsynth.MODE_RAW)
+    cache = device_cache(s, fill, DEV)
+    src, img = _image(oracle.packed_bytes(s, 0, 3, n), seed, pinned=False)
+    mirror = host_mirror(s, fill, range(s.num_blocks))
+    ring = kvx.StagingRing(DEV, 2, 64 << 10)
+    stream = torch.cuda.Stream()
+    try:
+        ring.bind(cache, 0, 3, n, 48, src, fill_threads=2)
+        for i, bt in enumerate(tables[:4]):
+            if i == 2:
+                kvx.kvx_restore_from_staging(ring, _bt(bt), stream=stream)
+            else:
+                kvx.kvx_restore_begin(ring, _bt(bt), stream=stream)
+                kvx.kvx_restore_wait(ring, stream=stream)
+            oracle.restore(s, *mirror, 0, 3, bt, 48, img)
+        ring.bind(cache, 0, 3, n, 80, src, fill_threads=3)
+        kvx.kvx_restore_begin(ring, _bt(tables[4]), stream=stream)
+        kvx.kvx_restore_wait(ring, stream=stream)
+        oracle.restore(s, *mirror, 0, 3, tables[4], 80, img)
+        with torch.cuda.stream(stream):
+            snap_k = [t.clone() for t in cache.k]
+            snap_v = [t.clone() for t in cache.v]
+        stream.synchronize()
+        kvx.kvx_check(stream)
+    finally:
+        ring.close()
+    for l in range(3):
+        assert np.array_equal(to_host(snap_k[l]), mirror[0][l]), f"K layer {l}"
+        assert np.array_equal(to_host(snap_v[l]), mirror[1][l]), f"V layer {l}"
+
+
 def test_racing_begins_claim_the_ring_once():
     """Two threads start a restore on one ring at the same moment: exactly one
     claims it (the other gets KVX_EBUSY, whatever the timing), and the one
